@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark of the KVLink hot path on one MI355X.
+
+One step is one pass of the whole path over one request batch: the index maps
+of the batch are already on the device; the step re-encodes the cached keys
+of every layer (one launch) and then, layer by layer, rotates and appends the
+new tokens and runs their attention over the concatenated cache.  Inputs are
+resident in HBM before the timed region starts.
+
+Prints one JSON line.  The metric is microseconds per layer of the path
+(re-encode + new-token attention) at the Llama-3.1-8B attention shape, with
+the algorithmic HBM GB/s, TFLOP/s and the roofline fraction of the dominant
+kernel, and the CPU oracle timed on a bounded sample as a reported baseline.
+"""
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16
+VALU_F32_PEAK_TFLOPS = 157.3
+
+METRIC = "µs/layer and HBM GB/s for re-encode+new-token attention at 8B shape; % roofline"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b-32layer-10doc")
+    ap.add_argument("--split-keys", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-iters", type=int, default=20)
+    return ap.parse_args()
+
+
+def to_torch(w, x, device):
+    import torch
+    if w.dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
+
+
+class Setup:
+    """Device buffers of a single-request workload (documents stored back to
+    back, concatenated cache with room for the new tokens)."""
+
+    def __init__(self, w, split_keys, device="cuda"):
+        import torch
+        import workloads
+        from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
+        self.w = w
+        L, H, d = w.n_layers, w.n_kv_heads, w.head_dim
+        row0 = workloads.doc_row0(w)
+        docs = w.docs[0]
+        self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
+                               [0, len(docs)], w.doc_len(0), w.link_count[0], w.n_query,
+                               doc_src_row=[int(row0[j]) for j in docs], split_keys=split_keys,
+                               device=device)
+        R = int(sum(w.doc_table_len))
+        self.cap = cap = b.max_total
+        self.k_src, self.k_dst = [], []
+        self.v_dst = torch.zeros((L, H, 1, cap, d), dtype=b.torch_dtype, device=device)
+        ksrc = torch.empty((L, H, R, d), dtype=b.torch_dtype, device=device)
+        self.q, self.kn, self.vn = [], [], []
+        for l in range(L):
+            ld = workloads.layer_data(w, l)
+            ksrc[l] = to_torch(w, ld.k_store, device)
+            kc, vc = workloads.request_cache(w, ld, 0)
+            self.v_dst[l, :, 0, :kc.shape[1]] = to_torch(w, vc, device)
+            self.q.append(to_torch(w, ld.q_new, device))
+            self.kn.append(to_torch(w, ld.k_new, device))
+            self.vn.append(to_torch(w, ld.v_new, device))
+        # two source/destination pairs, used alternately by the isolated
+        # re-encode timing so that back-to-back launches do not hit the LLC
+        for copy in range(2):
+            self.k_src.append(ksrc if copy == 0 else ksrc.clone())
+            self.k_dst.append(torch.zeros((L, H, 1, cap, d), dtype=b.torch_dtype, device=device))
+        self.src_views = [contiguous_view(t, H, 1, R, d) for t in self.k_src]
+        self.dst_views = [contiguous_view(t, H, 1, cap, d) for t in self.k_dst]
+        self.v_view = contiguous_view(self.v_dst, H, 1, cap, d)
+        self.out = b.new_out()
+        self.lse = b.new_lse()
+
+    def reencode(self, i=0):
+        self.batch.reencode(self.src_views[i], self.dst_views[i])
+
+    def attend(self, l, i=0):
+        self.batch.attend(l, self.q[l], self.kn[l], self.vn[l], self.dst_views[i], self.v_view,
+                          self.out, self.lse)
+
+    def step(self):
+        self.reencode(0)
+        for l in range(self.w.n_layers):
+            self.attend(l, 0)
+
+
+def algorithmic(w, batch):
+    """Bytes and flops the method itself moves (per the closed forms)."""
+    es = 2 if w.dtype == "bf16" else 4
+    Tc = int(batch.layout["seq_cached"][0])
+    n_new = batch.n_new
+    H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
+    re_bytes = 2 * w.n_layers * H * Tc * d * es
+    pairs = int((batch.layout["new_pos"].astype(np.int64) + 1).sum())
+    at_bytes = (2 * H * Tc * d + n_new * (Hq + 2 * H) * d + n_new * Hq * d) * es
+    at_flops = 4 * d * Hq * pairs
+    return dict(reencode_bytes=re_bytes, attend_bytes=at_bytes, attend_flops=at_flops,
+                pairs_per_qhead=pairs, cached_tokens=Tc, new_tokens=n_new)
+
+
+def time_region(fn, iters):
+    import torch
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for i in range(iters):
+        fn(i)
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / iters
+
+
+def cpu_baseline(w, alg):
+    """The oracle, untouched, on layer 0: re-encode of every document and the
+    attention of a sample of new tokens, scaled to one full layer."""
+    import oracle
+    import workloads
+    ld = workloads.layer_data(w, 0)
+    kc, vc = workloads.request_cache(w, ld, 0)
+    q, kn, vn = workloads.request_new(w, ld, 0)
+    f = lambda x: workloads.as_f64(w, x)
+    kc, vc, q, kn, vn = f(kc), f(vc), f(q), f(kn), f(vn)
+    t0 = time.perf_counter()
+    r0 = 0
+    g = 0
+    for j, L in enumerate(w.doc_len(0)):
+        oracle.reencode(kc[:, r0:r0 + L], g, w.rope_theta)
+        r0 += L
+        g += L + w.link_count[0][j]
+    t_re = time.perf_counter() - t0
+    n_new = alg["new_tokens"]
+    n_rows = min(n_new, 32)
+    rows = np.linspace(0, n_new - 1, n_rows).round().astype(np.int32)
+    t0 = time.perf_counter()
+    oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, kc, vc, w.rope_theta,
+                  w.scale, rows=rows)
+    t_at = time.perf_counter() - t0
+    us_layer = (t_re + t_at * n_new / n_rows) * 1e6
+    return {"value": us_layer, "unit": "us/layer", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"layer 0 of {w.n_layers}: re-encode of all {len(w.doc_len(0))} documents "
+                      f"({t_re:.2f} s) + attention of {n_rows} of {n_new} new tokens x "
+                      f"{w.n_q_heads} heads ({t_at:.2f} s), scaled to all new tokens",
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the path is single-GPU; see the sharding notes)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = workloads.get(args.workload)
+    if w.pool:
+        raise SystemExit("paged workloads are parity cases, not bench lines")
+    st = Setup(w, args.split_keys)
+    alg = algorithmic(w, st.batch)
+    print(f"# setup done: {w.name} cached={alg['cached_tokens']} new={alg['new_tokens']} "
+          f"splits={st.batch.split_keys}", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+    ms_step = time_region(lambda i: st.step(), args.steps)
+
+    # isolated kernels, on the stream they are launched on (torch's current)
+    it = args.kernel_iters
+    for i in range(2):
+        st.reencode(i)
+    re_ms = time_region(lambda i: st.reencode(i % 2), it)
+    at_ms = time_region(lambda i: [st.attend(l) for l in range(w.n_layers)], it) / w.n_layers
+
+    L = w.n_layers
+    us_layer = ms_step * 1000.0 / L
+    step_bytes = alg["reencode_bytes"] + L * alg["attend_bytes"]
+    step_flops = L * alg["attend_flops"]
+    re_gbps = alg["reencode_bytes"] / (re_ms * 1e-3) / 1e9
+    at_gbps = alg["attend_bytes"] / (at_ms * 1e-3) / 1e9
+    at_tflops = alg["attend_flops"] / (at_ms * 1e-3) / 1e12
+    ai = alg["attend_flops"] / alg["attend_bytes"]
+    peak_flops = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
+    at_bound = "mfma" if ai > peak_flops * 1e12 / (HBM_PEAK_GBPS * 1e9) else "hbm"
+    re_roof = {"kernel": "reencode_kernel", "bound": "hbm", "achieved": round(re_gbps, 1),
+               "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(re_gbps / HBM_PEAK_GBPS, 4),
+               "traffic": None, "us_per_launch": round(re_ms * 1000, 2),
+               "bytes_per_launch": alg["reencode_bytes"]}
+    if at_bound == "hbm":
+        at_roof = {"kernel": "attend (rope_new + attention + combine)", "bound": "hbm",
+                   "achieved": round(at_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                   "frac": round(at_gbps / HBM_PEAK_GBPS, 4), "traffic": None}
+    else:
+        at_roof = {"kernel": "attend (rope_new + attention + combine)", "bound": "mfma",
+                   "achieved": round(at_tflops, 2), "peak": peak_flops, "unit": "TFLOP/s",
+                   "frac": round(at_tflops / peak_flops, 4), "traffic": None}
+    at_roof.update({"us_per_launch": round(at_ms * 1000, 2),
+                    "bytes_per_launch": alg["attend_bytes"],
+                    "flops_per_launch": alg["attend_flops"],
+                    "hbm_gbps": round(at_gbps, 1), "tflops": round(at_tflops, 2)})
+    dominant_attend = L * at_ms > re_ms
+    res = {
+        "metric": METRIC,
+        "value": round(us_layer, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded, Llama-shaped caches; no weights or datasets)",
+        "config": {"workload": w.name, "n_layers": L, "n_q_heads": w.n_q_heads,
+                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "rope_theta": w.rope_theta, "documents": len(w.docs[0]),
+                   "link_tokens_per_doc": w.link_count[0][0], "query_tokens": w.n_query[0],
+                   "cached_tokens": alg["cached_tokens"], "new_tokens": alg["new_tokens"],
+                   "split_keys": st.batch.split_keys},
+        "hbm_gbps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 3),
+        "roofline": at_roof if dominant_attend else re_roof,
+        "roofline_other": re_roof if dominant_attend else at_roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, alg)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,253 @@
+/*
+ * kvlink.h — C ABI of the MI355X (gfx950) KVLink inference hot path.
+ *
+ * KVLink (arXiv 2502.16002) precomputes the KV cache of every document on its
+ * own, concatenates the caches of the retrieved documents at inference time,
+ * moves their keys to their global positions (Sec. 2.2, positional
+ * re-encoding) and runs one forward pass over the link tokens placed after
+ * each document and the query tokens (Sec. 2.3).  This library implements the
+ * per-layer parts of that path that touch the cache:
+ *
+ *   kvlink_build_layout       index maps of the concatenated sequence (host)
+ *   kvlink_reencode_keys      K' = R(delta_i) K for every cached key (GPU)
+ *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
+ *                             append of their keys/values to the cache and
+ *                             split-K GQA attention over the cache (GPU)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Every function returns a kvlink_status, never aborts, and lets no C++
+ *    exception cross the ABI.  On a non-OK status kvlink_last_error() returns a
+ *    message (thread-local, valid until the next call on that thread).
+ *  * Host-side validation happens before any HIP call: a call that returns
+ *    KVLINK_ERR_INVALID_ARG, KVLINK_ERR_UNSUPPORTED, KVLINK_ERR_LAYOUT or
+ *    KVLINK_ERR_WORKSPACE has launched nothing.  KVLINK_ERR_HIP means a launch
+ *    failed; the message holds HIP's error string.
+ *  * GPU calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL means the null stream).  The library allocates no device memory and
+ *    keeps no state between calls; the caller owns every buffer, including
+ *    the workspace.  Host arrays are only read during the call.
+ *  * Positions are 0-based.  RoPE (Sec. 2.2) rotates each pair
+ *    (x_j, x_{j + d/2}), j < d/2, by pos * theta^(-2j/d): the half-split
+ *    pairing of the Llama family the paper fine-tunes (Sec. 3.1).  Angles are
+ *    formed in double precision on the device and the cos/sin values rounded
+ *    to float before the rotation, which runs in float.
+ *  * bf16 values are rounded from float with round-to-nearest-even.
+ *  * Device descriptor arrays (d_* arguments) are not re-validated on the
+ *    device; they must be the uploaded outputs of kvlink_build_layout for the
+ *    same request batch.
+ */
+#ifndef KVLINK_H
+#define KVLINK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KVLINK_OK = 0,
+    KVLINK_ERR_INVALID_ARG = 1, /* null pointer, bad scalar, misaligned buffer */
+    KVLINK_ERR_UNSUPPORTED = 2, /* head_dim, dtype or GQA group not built      */
+    KVLINK_ERR_LAYOUT = 3,      /* inconsistent lengths, counts or positions    */
+    KVLINK_ERR_WORKSPACE = 4,   /* workspace missing or too small               */
+    KVLINK_ERR_HIP = 5          /* a HIP launch failed                          */
+} kvlink_status;
+
+typedef enum { KVLINK_F32 = 0, KVLINK_BF16 = 1 } kvlink_dtype;
+
+/*
+ * A K or V tensor covering all layers, on the device.  Element j (0 <= j <
+ * head_dim, always unit stride) of row `row` of KV head `head` of sequence
+ * `seq` in layer `layer` is at
+ *
+ *   contiguous (block_table == NULL):
+ *     base + layer*layer_stride + head*head_stride + seq*seq_stride
+ *          + row*row_stride + j
+ *   paged (block_table != NULL):
+ *     base + layer*layer_stride + head*head_stride
+ *          + block_table[seq*max_pages + row/page_size]*page_stride
+ *          + (row % page_size)*row_stride + j
+ *
+ * Strides are in elements.  base must be 16-byte aligned and every stride a
+ * multiple of 16 bytes.  The block table is a device array of int32 physical
+ * page numbers.
+ */
+typedef struct {
+    void* base;
+    int64_t layer_stride;
+    int64_t head_stride;
+    int64_t row_stride;
+    int64_t seq_stride;
+    int64_t page_stride;
+    const int32_t* block_table;
+    int32_t page_size;
+    int32_t max_pages;
+} kvlink_kv_view;
+
+/*
+ * One stored document cache to re-encode (Sec. 2.2): `len` rows starting at
+ * row src_row of sequence src_seq of the source view go, rotated by
+ * R(delta), to rows dst_row.. of sequence dst_seq of the destination view.
+ * delta = g_i - src_pos0_i, the document's global offset after
+ * concatenation minus the position its keys were rotated at when cached.
+ */
+typedef struct {
+    int32_t src_seq;
+    int32_t src_row;
+    int32_t dst_seq;
+    int32_t dst_row;
+    int32_t len;
+    int32_t delta;
+} kvlink_span;
+
+/*
+ * kvlink_build_layout — index maps of a batch of requests (host, integer,
+ * bit-exact).  Follows the layout of Sec. 2.1 and Sec. 2.3: in request s the
+ * retrieved documents come in retrieval order, each as
+ * (c_1..c_L, link_1..link_K), and the query tokens follow.  The link tokens
+ * of the n-th document are link_n-1..link_n-K (Appendix A.2).
+ *
+ * Inputs (host arrays):
+ *   n_seqs                 number of requests (>= 1)
+ *   seq_doc_ptr[n_seqs+1]  request s owns documents seq_doc_ptr[s]..seq_doc_ptr[s+1]-1
+ *                          (non-decreasing, seq_doc_ptr[0] == 0)
+ *   doc_len[n_docs]        L_i >= 1, rows of each document's stored cache
+ *   link_count[n_docs]     K_i >= 0, link tokens after each document
+ *   n_query[n_seqs]        query tokens of each request, >= 0
+ *   doc_src_seq[n_docs]    source sequence of each stored cache (NULL: 0)
+ *   doc_src_row[n_docs]    first row of it in that sequence (NULL: the
+ *                          documents of each request stored back to back,
+ *                          i.e. the same rows as in the destination)
+ *   doc_src_pos0[n_docs]   position its keys were rotated at (NULL: 0)
+ *
+ * Outputs (host arrays sized by the caller; any may be NULL to skip it):
+ *   spans[n_docs]          re-encode descriptors (dst_seq = s, dst_row = first
+ *                          row of the document in the request's concatenated
+ *                          cache, rows of a request's documents back to back
+ *                          in retrieval order)
+ *   doc_pos0[n_docs]       global position g_i of each document's first token
+ *   seq_cached[n_seqs]     T_c: cached rows of each request
+ *   seq_new_ptr[n_seqs+1]  request s owns new tokens seq_new_ptr[s]..seq_new_ptr[s+1]-1
+ *   new_pos[n_new]         global position of each new token; within a
+ *                          request the new tokens are the link tokens in
+ *                          document order, then the query tokens, so the
+ *                          positions increase
+ *   new_visible[n_new]     cached rows visible to the new token: the rows of
+ *                          every document at or before its own (all T_c for
+ *                          query tokens); the token also sees the new tokens
+ *                          of its request up to and including itself
+ *   new_doc[n_new]         document index within the request, -1 for queries
+ *   new_slot[n_new]        link index k (0-based) or query index
+ *   totals[6]              n_docs, n_new, max doc_len, max T_c, max new
+ *                          tokens per request, max total positions per request
+ *
+ * Errors: KVLINK_ERR_INVALID_ARG for a null required input or n_seqs < 1;
+ * KVLINK_ERR_LAYOUT for a length < 1, a negative count, a non-monotone
+ * seq_doc_ptr, or a position that would not fit in int32.
+ */
+kvlink_status kvlink_build_layout(int32_t n_seqs, const int32_t* seq_doc_ptr,
+                                  const int32_t* doc_len, const int32_t* link_count,
+                                  const int32_t* n_query, const int32_t* doc_src_seq,
+                                  const int32_t* doc_src_row, const int32_t* doc_src_pos0,
+                                  kvlink_span* spans, int32_t* doc_pos0, int32_t* seq_cached,
+                                  int32_t* seq_new_ptr, int32_t* new_pos, int32_t* new_visible,
+                                  int32_t* new_doc, int32_t* new_slot, int64_t* totals);
+
+/*
+ * kvlink_reencode_keys — positional re-encoding of cached keys (Sec. 2.2):
+ * for every layer l < n_layers, KV head h < n_kv_heads, span i and row
+ * t < len_i:
+ *     dst(l, h, dst_seq_i, dst_row_i + t) = R(delta_i) src(l, h, src_seq_i, src_row_i + t)
+ * Values are never touched.  One launch covers all layers (delta does not
+ * depend on the layer).  src and dst may be the same view (in place) as long
+ * as every span maps its rows onto themselves; otherwise they must not
+ * overlap.
+ *
+ *   d_spans       device array of n_spans kvlink_span
+ *   max_span_len  an upper bound of every span's len (sizes the grid)
+ *   head_dim      64 or 128; dtype KVLINK_F32 or KVLINK_BF16
+ *
+ * Errors: KVLINK_ERR_INVALID_ARG (null pointers, n_layers/n_kv_heads < 1,
+ * n_spans < 0, rope_theta <= 0, misaligned base or stride),
+ * KVLINK_ERR_UNSUPPORTED (head_dim, dtype), KVLINK_ERR_HIP.
+ * n_spans == 0 or max_span_len == 0 launches nothing and returns KVLINK_OK.
+ */
+kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
+                                   int32_t head_dim, double rope_theta, int32_t n_spans,
+                                   const kvlink_span* d_spans, int32_t max_span_len,
+                                   kvlink_kv_view src, kvlink_kv_view dst, void* stream);
+
+/*
+ * Workspace bytes kvlink_attend_new_tokens needs for these sizes (same
+ * meaning as its arguments, including split_keys).  Returns 0 for invalid
+ * sizes.
+ */
+size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                     int32_t head_dim, int32_t n_seqs, int32_t n_new_total,
+                                     int32_t max_new, int32_t max_cached, int32_t split_keys);
+
+/*
+ * kvlink_attend_new_tokens — one layer of the forward pass over the new
+ * tokens (Sec. 2.3, last paragraph: the link tokens are appended after the
+ * reused caches and run with the customised attention map; Sec. 2.1: the
+ * query follows).  For every request s and new token r of it, at global
+ * position p_r:
+ *
+ *   1. q_r, k_r are rotated by R(p_r) (they arrive before RoPE);
+ *   2. the rotated k_r and v_r are appended to the cache of `layer` at row
+ *      seq_cached[s] + r (right after the request's cached rows);
+ *   3. for every query head hq (KV head hk = hq / (n_q_heads / n_kv_heads)):
+ *        out[r][hq] = sum_b softmax_b(scale * <q_r, k_b>) v_b
+ *      over the keys b the attention map of Sec. 2.3 lets a link or query
+ *      token see: every position at or before p_r, i.e. the first
+ *      new_visible[r] cached rows and the new tokens 0..r of the request.
+ *      lse[r][hq] (if lse != NULL) = log sum_b exp(scale * <q_r, k_b>).
+ *
+ * Arguments:
+ *   n_seqs, n_new_total        requests and new tokens in the batch
+ *   max_new, max_cached        max over requests of new tokens and of T_c
+ *   d_seq_new_ptr[n_seqs+1], d_seq_cached[n_seqs], d_new_pos[n_new_total],
+ *   d_new_visible[n_new_total] device copies of kvlink_build_layout outputs
+ *   q_new  [n_new_total][n_q_heads][head_dim]   device, dtype, pre-RoPE
+ *   k_new, v_new [n_new_total][n_kv_heads][head_dim]  device, dtype
+ *   k_cache, v_cache           views (see kvlink_kv_view) whose rows
+ *                              0..T_c-1 of request s hold its re-encoded keys
+ *                              and its values, with room for the new rows
+ *   out   [n_new_total][n_q_heads][head_dim]    device, dtype
+ *   lse   [n_new_total][n_q_heads] float, or NULL
+ *   split_keys                 keys per split of the split-K schedule: 0 lets
+ *                              the library choose from the sizes; otherwise a
+ *                              positive multiple of 128 (the result does not
+ *                              depend on it beyond float rounding order)
+ *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
+ *                              device bytes, 256-byte aligned
+ *
+ * Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in {1, 2, 4, 8};
+ * dtype KVLINK_F32 or KVLINK_BF16 (float accumulation and softmax either way).
+ *
+ * Errors: KVLINK_ERR_INVALID_ARG, KVLINK_ERR_UNSUPPORTED,
+ * KVLINK_ERR_WORKSPACE, KVLINK_ERR_HIP, as listed above.  n_new_total == 0
+ * launches nothing and returns KVLINK_OK.
+ */
+kvlink_status kvlink_attend_new_tokens(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Message of the last non-OK status on the calling thread ("" if none). */
+const char* kvlink_last_error(void);
+
+/* Library version string. */
+const char* kvlink_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

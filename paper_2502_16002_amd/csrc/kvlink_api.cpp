@@ -1,0 +1,286 @@
+// kvlink_api.cpp — the C ABI of include/kvlink.h: host-side layout, argument
+// validation (before any HIP call) and the launches.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "kvlink_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+kvlink_status fail(kvlink_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+kvlink_status ok() {
+    g_error.clear();
+    return KVLINK_OK;
+}
+
+size_t elem_size(kvlink_dtype dt) { return dt == KVLINK_BF16 ? 2 : 4; }
+
+bool dtype_ok(kvlink_dtype dt) { return dt == KVLINK_F32 || dt == KVLINK_BF16; }
+
+// A view must be usable with 16-byte vector accesses.
+kvlink_status check_view(const kvlink_kv_view& v, kvlink_dtype dt, const char* name) {
+    const size_t es = elem_size(dt);
+    const int64_t q = (int64_t)(16 / es);
+    if (!v.base) return fail(KVLINK_ERR_INVALID_ARG, "%s: base is NULL", name);
+    if (reinterpret_cast<uintptr_t>(v.base) % 16)
+        return fail(KVLINK_ERR_INVALID_ARG, "%s: base is not 16-byte aligned", name);
+    if (v.layer_stride % q || v.head_stride % q || v.row_stride % q || v.seq_stride % q ||
+        v.page_stride % q)
+        return fail(KVLINK_ERR_INVALID_ARG, "%s: a stride is not a multiple of 16 bytes", name);
+    if (v.layer_stride < 0 || v.head_stride < 0 || v.row_stride < 0 || v.seq_stride < 0 ||
+        v.page_stride < 0)
+        return fail(KVLINK_ERR_INVALID_ARG, "%s: negative stride", name);
+    if (v.block_table && (v.page_size < 1 || v.max_pages < 1))
+        return fail(KVLINK_ERR_INVALID_ARG, "%s: paged view needs page_size and max_pages >= 1",
+                    name);
+    return KVLINK_OK;
+}
+
+kvlink::View to_view(const kvlink_kv_view& v) {
+    kvlink::View d;
+    d.base = reinterpret_cast<char*>(v.base);
+    d.layer_stride = v.layer_stride;
+    d.head_stride = v.head_stride;
+    d.row_stride = v.row_stride;
+    d.seq_stride = v.seq_stride;
+    d.page_stride = v.page_stride;
+    d.block_table = v.block_table;
+    d.page_size = v.block_table ? v.page_size : 1;
+    d.max_pages = v.max_pages;
+    return d;
+}
+
+}  // namespace
+
+extern "C" {
+
+kvlink_status kvlink_build_layout(int32_t n_seqs, const int32_t* seq_doc_ptr,
+                                  const int32_t* doc_len, const int32_t* link_count,
+                                  const int32_t* n_query, const int32_t* doc_src_seq,
+                                  const int32_t* doc_src_row, const int32_t* doc_src_pos0,
+                                  kvlink_span* spans, int32_t* doc_pos0, int32_t* seq_cached,
+                                  int32_t* seq_new_ptr, int32_t* new_pos, int32_t* new_visible,
+                                  int32_t* new_doc, int32_t* new_slot, int64_t* totals) {
+    try {
+        if (n_seqs < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_seqs must be >= 1");
+        if (!seq_doc_ptr || !n_query)
+            return fail(KVLINK_ERR_INVALID_ARG, "seq_doc_ptr and n_query are required");
+        if (seq_doc_ptr[0] != 0) return fail(KVLINK_ERR_LAYOUT, "seq_doc_ptr[0] must be 0");
+        for (int s = 0; s < n_seqs; ++s)
+            if (seq_doc_ptr[s + 1] < seq_doc_ptr[s])
+                return fail(KVLINK_ERR_LAYOUT, "seq_doc_ptr decreases at request %d", s);
+        const int64_t n_docs = seq_doc_ptr[n_seqs];
+        if (n_docs > 0 && (!doc_len || !link_count))
+            return fail(KVLINK_ERR_INVALID_ARG, "doc_len and link_count are required");
+        for (int64_t i = 0; i < n_docs; ++i) {
+            if (doc_len[i] < 1) return fail(KVLINK_ERR_LAYOUT, "doc_len[%lld] < 1", (long long)i);
+            if (link_count[i] < 0)
+                return fail(KVLINK_ERR_LAYOUT, "link_count[%lld] < 0", (long long)i);
+        }
+        int64_t n_new = 0, max_doc = 0, max_cached = 0, max_new_s = 0, max_total = 0;
+        for (int s = 0; s < n_seqs; ++s) {
+            if (n_query[s] < 0) return fail(KVLINK_ERR_LAYOUT, "n_query[%d] < 0", s);
+            int64_t tc = 0, nn = n_query[s];
+            for (int64_t i = seq_doc_ptr[s]; i < seq_doc_ptr[s + 1]; ++i) {
+                tc += doc_len[i];
+                nn += link_count[i];
+                max_doc = std::max<int64_t>(max_doc, doc_len[i]);
+            }
+            if (tc + nn > INT32_MAX)
+                return fail(KVLINK_ERR_LAYOUT, "request %d has more than 2^31-1 positions", s);
+            n_new += nn;
+            max_cached = std::max(max_cached, tc);
+            max_new_s = std::max(max_new_s, nn);
+            max_total = std::max(max_total, tc + nn);
+        }
+        if (n_new > INT32_MAX) return fail(KVLINK_ERR_LAYOUT, "more than 2^31-1 new tokens");
+
+        // Sec. 2.3: each document is followed by its K link tokens; the query
+        // tokens come after the last document (Sec. 2.1).
+        int64_t nidx = 0;
+        for (int s = 0; s < n_seqs; ++s) {
+            if (seq_new_ptr) seq_new_ptr[s] = (int32_t)nidx;
+            int64_t pos = 0, row = 0;
+            const int64_t d0 = seq_doc_ptr[s], d1 = seq_doc_ptr[s + 1];
+            for (int64_t i = d0; i < d1; ++i) {
+                const int64_t g = pos;              // global offset of the document
+                if (doc_pos0) doc_pos0[i] = (int32_t)g;
+                if (spans) {
+                    kvlink_span sp;
+                    sp.src_seq = doc_src_seq ? doc_src_seq[i] : 0;
+                    sp.src_row = doc_src_row ? doc_src_row[i] : (int32_t)row;
+                    sp.dst_seq = s;
+                    sp.dst_row = (int32_t)row;
+                    sp.len = doc_len[i];
+                    sp.delta = (int32_t)(g - (doc_src_pos0 ? doc_src_pos0[i] : 0));
+                    spans[i] = sp;
+                }
+                pos += doc_len[i];
+                row += doc_len[i];
+                for (int k = 0; k < link_count[i]; ++k, ++pos, ++nidx) {
+                    // a link token sees every cached row up to its own document
+                    if (new_pos) new_pos[nidx] = (int32_t)pos;
+                    if (new_visible) new_visible[nidx] = (int32_t)row;
+                    if (new_doc) new_doc[nidx] = (int32_t)(i - d0);
+                    if (new_slot) new_slot[nidx] = k;
+                }
+            }
+            if (seq_cached) seq_cached[s] = (int32_t)row;
+            for (int q = 0; q < n_query[s]; ++q, ++pos, ++nidx) {
+                if (new_pos) new_pos[nidx] = (int32_t)pos;
+                if (new_visible) new_visible[nidx] = (int32_t)row;
+                if (new_doc) new_doc[nidx] = -1;
+                if (new_slot) new_slot[nidx] = q;
+            }
+        }
+        if (seq_new_ptr) seq_new_ptr[n_seqs] = (int32_t)nidx;
+        if (totals) {
+            totals[0] = n_docs;
+            totals[1] = n_new;
+            totals[2] = max_doc;
+            totals[3] = max_cached;
+            totals[4] = max_new_s;
+            totals[5] = max_total;
+        }
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_INVALID_ARG, "unexpected exception in kvlink_build_layout");
+    }
+}
+
+kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
+                                   int32_t head_dim, double rope_theta, int32_t n_spans,
+                                   const kvlink_span* d_spans, int32_t max_span_len,
+                                   kvlink_kv_view src, kvlink_kv_view dst, void* stream) {
+    try {
+        if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (n_layers < 1 || n_kv_heads < 1)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_layers and n_kv_heads must be >= 1");
+        if (n_spans < 0 || max_span_len < 0)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_spans and max_span_len must be >= 0");
+        if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+            return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+        if (n_spans > 65535) return fail(KVLINK_ERR_UNSUPPORTED, "more than 65535 spans");
+        if ((int64_t)n_layers * n_kv_heads > (int64_t)8 * 65535)
+            return fail(KVLINK_ERR_UNSUPPORTED, "too many layers x heads");
+        if (n_spans == 0 || max_span_len == 0) return ok();
+        if (!d_spans) return fail(KVLINK_ERR_INVALID_ARG, "d_spans is NULL");
+        kvlink_status st = check_view(src, dtype, "src");
+        if (st != KVLINK_OK) return st;
+        if ((st = check_view(dst, dtype, "dst")) != KVLINK_OK) return st;
+        hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads, rope_theta,
+                                               n_spans, d_spans, max_span_len, to_view(src),
+                                               to_view(dst), reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "re-encode launch: %s", hipGetErrorString(e));
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_reencode_keys");
+    }
+}
+
+size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                     int32_t head_dim, int32_t n_seqs, int32_t n_new_total,
+                                     int32_t max_new, int32_t max_cached, int32_t split_keys) {
+    if (!dtype_ok(dtype)) return 0;
+    kvlink::AttendPlan p;
+    if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs, n_new_total,
+                                  max_new, max_cached, split_keys, &p))
+        return 0;
+    return p.total_bytes;
+}
+
+kvlink_status kvlink_attend_new_tokens(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    void* workspace, size_t workspace_bytes, void* stream) {
+    try {
+        if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_q_heads must be a positive multiple of n_kv_heads");
+        const int group = n_q_heads / n_kv_heads;
+        if (group != 1 && group != 2 && group != 4 && group != 8)
+            return fail(KVLINK_ERR_UNSUPPORTED, "GQA group %d (built: 1, 2, 4, 8)", group);
+        if (n_seqs < 1 || n_new_total < 0 || max_new < 0 || max_cached < 0 || layer < 0)
+            return fail(KVLINK_ERR_INVALID_ARG, "negative size or layer");
+        if (n_new_total > 0 && max_new < 1)
+            return fail(KVLINK_ERR_INVALID_ARG, "max_new must be >= 1 when there are new tokens");
+        if ((int64_t)max_new > n_new_total)
+            return fail(KVLINK_ERR_INVALID_ARG, "max_new exceeds n_new_total");
+        if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+            return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+        if (!std::isfinite(softmax_scale))
+            return fail(KVLINK_ERR_INVALID_ARG, "softmax_scale must be finite");
+        if (split_keys < 0 || split_keys % 128)
+            return fail(KVLINK_ERR_INVALID_ARG, "split_keys must be 0 or a positive multiple of 128");
+        if (n_seqs > 65535 / n_kv_heads)
+            return fail(KVLINK_ERR_UNSUPPORTED, "n_seqs * n_kv_heads above 65535");
+        if (n_new_total == 0) return ok();
+        if (!d_seq_new_ptr || !d_seq_cached || !d_new_pos || !d_new_visible)
+            return fail(KVLINK_ERR_INVALID_ARG, "a layout descriptor pointer is NULL");
+        if (!q_new || !k_new || !v_new || !out)
+            return fail(KVLINK_ERR_INVALID_ARG, "q_new, k_new, v_new and out are required");
+        kvlink_status st = check_view(k_cache, dtype, "k_cache");
+        if (st != KVLINK_OK) return st;
+        if ((st = check_view(v_cache, dtype, "v_cache")) != KVLINK_OK) return st;
+        kvlink::AttendPlan plan;
+        if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs, n_new_total,
+                                      max_new, max_cached, split_keys, &plan))
+            return fail(KVLINK_ERR_INVALID_ARG, "invalid attention sizes");
+        if (!workspace) return fail(KVLINK_ERR_WORKSPACE, "workspace is NULL");
+        if (reinterpret_cast<uintptr_t>(workspace) % 256)
+            return fail(KVLINK_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+        if (workspace_bytes < plan.total_bytes)
+            return fail(KVLINK_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes,
+                        plan.total_bytes);
+        kvlink::AttendArgs a;
+        a.q_new = q_new;
+        a.k_new = k_new;
+        a.v_new = v_new;
+        a.k = to_view(k_cache);
+        a.v = to_view(v_cache);
+        a.layer = layer;
+        a.seq_new_ptr = d_seq_new_ptr;
+        a.seq_cached = d_seq_cached;
+        a.new_pos = d_new_pos;
+        a.new_visible = d_new_visible;
+        a.theta = rope_theta;
+        a.scale = softmax_scale;
+        a.out = out;
+        a.lse = lse;
+        a.workspace = workspace;
+        hipError_t e = kvlink::launch_attend(dtype, plan, a, reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_attend_new_tokens");
+    }
+}
+
+const char* kvlink_last_error(void) { return g_error.c_str(); }
+
+const char* kvlink_version(void) { return "kvlink-gfx950 0.1"; }
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// kvlink_internal.h — shared device helpers and launcher declarations of the
+// gfx950 KVLink library.  Not part of the public ABI (see include/kvlink.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvlink.h"
+
+namespace kvlink {
+
+// ------------------------------------------------------------ element types
+
+struct bf16_t {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float((uint32_t)x.bits << 16); }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
+    // IEEE conversion: round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
+    __bf16 h = (__bf16)x;
+    return bf16_t{__builtin_bit_cast(uint16_t, h)};
+}
+
+// ------------------------------------------------------------------- views
+
+// Device copy of kvlink_kv_view, with the base typed by the caller.
+struct View {
+    char* base;  // bytes
+    int64_t layer_stride, head_stride, row_stride, seq_stride, page_stride;  // elements
+    const int32_t* block_table;
+    int32_t page_size, max_pages;
+};
+
+// Element offset of (layer, head, seq, row, 0) in a view.
+__device__ __forceinline__ int64_t view_offset(const View& v, int layer, int head, int seq,
+                                               int row) {
+    int64_t off = (int64_t)layer * v.layer_stride + (int64_t)head * v.head_stride;
+    if (v.block_table) {
+        const int page = v.block_table[(int64_t)seq * v.max_pages + row / v.page_size];
+        off += (int64_t)page * v.page_stride + (int64_t)(row % v.page_size) * v.row_stride;
+    } else {
+        off += (int64_t)seq * v.seq_stride + (int64_t)row * v.row_stride;
+    }
+    return off;
+}
+
+// cos and sin of pos * theta^(-2j/d): the angle is formed and reduced in
+// double precision, then rounded to float.
+__device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, int d, double theta,
+                                             float* c, float* s) {
+    const double w = pow(theta, -2.0 * (double)j / (double)d);
+    double sd, cd;
+    sincos((double)pos * w, &sd, &cd);
+    *c = (float)cd;
+    *s = (float)sd;
+}
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                           double theta, int n_spans, const kvlink_span* spans,
+                           int max_span_len, const View& src, const View& dst,
+                           hipStream_t stream);
+
+struct AttendPlan {
+    int n_q_heads, n_kv_heads, group, head_dim;
+    int n_seqs, n_new_total, max_new, max_cached;
+    int split_keys, n_splits;
+    int row_block;          // GQA rows per workgroup
+    bool use_mfma;
+    size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
+};
+
+// Fills every field from the sizes; returns false on invalid sizes.
+bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
+                      int n_seqs, int n_new_total, int max_new, int max_cached, int split_keys,
+                      AttendPlan* p);
+
+struct AttendArgs {
+    const void* q_new;
+    const void* k_new;
+    const void* v_new;
+    View k, v;
+    int layer;
+    const int32_t* seq_new_ptr;
+    const int32_t* seq_cached;
+    const int32_t* new_pos;
+    const int32_t* new_visible;
+    double theta;
+    float scale;
+    void* out;
+    float* lse;
+    void* workspace;
+};
+
+hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,
+                         hipStream_t stream);
+
+}  // namespace kvlink

@@ -1,0 +1,167 @@
+// reencode.hip — positional re-encoding of cached keys (KVLink Sec. 2.2).
+//
+// Keys of a document were stored with RoPE at the positions they had when the
+// document was encoded alone.  After concatenation the document starts at
+// global offset g_i, so every stored key is rotated once more, by
+// R(delta_i) with delta_i = g_i - (its stored start position); rotations
+// compose, R(delta) R(t) = R(delta + t).  Values are not touched.
+//
+// The pass is bound by HBM bandwidth (about 1.5 flop per byte moved):
+//   * one launch covers every layer and KV head, since delta does not depend
+//     on them;
+//   * a workgroup owns up to kRows rows of one document for kLH (layer, head)
+//     pairs, so the document's cos/sin table is built once (double-precision
+//     angles, in LDS) and then held in registers: each thread always handles
+//     the same slice of the rotation pairs;
+//   * each thread moves 16-byte vectors: the slice [j0, j0+E) and its partner
+//     slice [j0+d/2, j0+d/2+E), consecutive threads cover one row, then the
+//     next row, so a wavefront reads and writes whole contiguous rows;
+//   * kUnroll vectors are loaded before any is stored, to keep enough bytes in
+//     flight per wavefront.
+#include "kvlink_internal.h"
+
+namespace kvlink {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRows = 64;
+constexpr int kLH = 8;
+constexpr int kUnroll = 4;
+
+template <typename T>
+__device__ __forceinline__ void unpack16(const uint4& v, float* f);
+template <>
+__device__ __forceinline__ void unpack16<float>(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x);
+    f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z);
+    f[3] = __uint_as_float(v.w);
+}
+template <>
+__device__ __forceinline__ void unpack16<bf16_t>(const uint4& v, float* f) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ uint4 pack16(const float* f);
+template <>
+__device__ __forceinline__ uint4 pack16<float>(const float* f) {
+    return uint4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                 __float_as_uint(f[3])};
+}
+template <>
+__device__ __forceinline__ uint4 pack16<bf16_t>(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)from_f32<bf16_t>(f[2 * i]).bits |
+               ((uint32_t)from_f32<bf16_t>(f[2 * i + 1]).bits << 16);
+    return uint4{w[0], w[1], w[2], w[3]};
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
+                                                            const kvlink_span* __restrict__ spans,
+                                                            int n_lh, int n_kv_heads,
+                                                            double theta) {
+    constexpr int H = D / 2;                 // rotation pairs per vector
+    constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte access
+    constexpr int TPV = H / E;               // threads per vector
+    constexpr int VPP = kThreads / TPV;      // vectors per pass of the workgroup
+    __shared__ float s_cos[H], s_sin[H];
+
+    const kvlink_span sp = spans[blockIdx.y];
+    const int r0 = blockIdx.x * kRows;
+    if (r0 >= sp.len) return;
+    const int rows = min(kRows, sp.len - r0);
+    const int lh0 = blockIdx.z * kLH;
+    const int nlh = min(kLH, n_lh - lh0);
+
+    for (int j = threadIdx.x; j < H; j += kThreads)
+        rope_cos_sin(sp.delta, j, D, theta, &s_cos[j], &s_sin[j]);
+    __syncthreads();
+
+    const int sub = threadIdx.x % TPV;
+    float c[E], s[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        c[e] = s_cos[sub * E + e];
+        s[e] = s_sin[sub * E + e];
+    }
+
+    const int n_vec = rows * nlh;
+    for (int v0 = threadIdx.x / TPV; v0 < n_vec; v0 += VPP * kUnroll) {
+        uint4 lo[kUnroll], hi[kUnroll];
+        int64_t doff[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int v = v0 + u * VPP;
+            if (v < n_vec) {
+                const int lh = lh0 + v / rows;
+                const int row = v % rows;
+                const int layer = lh / n_kv_heads, head = lh % n_kv_heads;
+                const int64_t so =
+                    view_offset(src, layer, head, sp.src_seq, sp.src_row + r0 + row) + sub * E;
+                const T* p = reinterpret_cast<const T*>(src.base) + so;
+                lo[u] = *reinterpret_cast<const uint4*>(p);
+                hi[u] = *reinterpret_cast<const uint4*>(p + H);
+                doff[u] = view_offset(dst, layer, head, sp.dst_seq, sp.dst_row + r0 + row) + sub * E;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int v = v0 + u * VPP;
+            if (v < n_vec) {
+                float a[E], b[E], x[E], y[E];
+                unpack16<T>(lo[u], a);
+                unpack16<T>(hi[u], b);
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    x[e] = a[e] * c[e] - b[e] * s[e];
+                    y[e] = a[e] * s[e] + b[e] * c[e];
+                }
+                T* q = reinterpret_cast<T*>(dst.base) + doff[u];
+                *reinterpret_cast<uint4*>(q) = pack16<T>(x);
+                *reinterpret_cast<uint4*>(q + H) = pack16<T>(y);
+            }
+        }
+    }
+}
+
+template <typename T, int D>
+hipError_t launch(int n_layers, int n_kv_heads, double theta, int n_spans,
+                  const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
+                  hipStream_t stream) {
+    const int n_lh = n_layers * n_kv_heads;
+    dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
+    hipLaunchKernelGGL((reencode_kernel<T, D>), grid, dim3(kThreads), 0, stream, src, dst, spans,
+                       n_lh, n_kv_heads, theta);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                           double theta, int n_spans, const kvlink_span* spans,
+                           int max_span_len, const View& src, const View& dst,
+                           hipStream_t stream) {
+    if (dt == KVLINK_BF16) {
+        if (head_dim == 128)
+            return launch<bf16_t, 128>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len,
+                                       src, dst, stream);
+        return launch<bf16_t, 64>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src,
+                                  dst, stream);
+    }
+    if (head_dim == 128)
+        return launch<float, 128>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src,
+                                  dst, stream);
+    return launch<float, 64>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src, dst,
+                             stream);
+}
+
+}  // namespace kvlink

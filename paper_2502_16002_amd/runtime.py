@@ -1,0 +1,101 @@
+"""Device-side request batches for the KVLink hot path.
+
+A batch owns the device buffers of one request batch: the uploaded index maps
+from ``kvlink_build_layout``, the destination K/V caches (contiguous or paged)
+and the attention workspace.  Running the path is two library calls:
+``reencode`` (all layers, one launch) and ``attend`` (one layer).  Everything
+here is buffer management and argument marshalling; the work runs in
+libkvlink.so.
+
+Storage layouts used here (all elements of the workload dtype, head_dim
+innermost):
+
+* contiguous stored caches:  [n_layers][H_kv][R][d], documents back to back;
+* contiguous request caches: [n_layers][H_kv][n_seqs][cap][d] with
+  cap >= max over requests of (cached rows + new tokens);
+* paged caches: [n_layers][n_pages][H_kv][page][d]: one page holds all KV
+  heads of `page` consecutive rows; a block table per sequence maps logical
+  pages to physical pages.
+"""
+import numpy as np
+import torch
+
+from . import (KVLINK_BF16, KVLINK_F32, SPAN_FIELDS, kv_view, kvlink_attend_new_tokens,
+               kvlink_attend_workspace_bytes, kvlink_build_layout, kvlink_reencode_keys)
+
+TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
+
+
+def dtype_code(name):
+    return {"f32": KVLINK_F32, "bf16": KVLINK_BF16}[name]
+
+
+def contiguous_view(t, n_kv_heads, n_seqs, cap, d):
+    """View of a [L][H][S][cap][d] tensor."""
+    return kv_view(t, n_kv_heads * n_seqs * cap * d, n_seqs * cap * d, d, seq_stride=cap * d)
+
+
+def paged_view(t, n_pages, n_kv_heads, page, d, block_table, max_pages):
+    """View of a [L][n_pages][H][page][d] tensor through a block table."""
+    return kv_view(t, n_pages * n_kv_heads * page * d, page * d, d, page_stride=n_kv_heads * page * d,
+                   block_table=block_table, page_size=page, max_pages=max_pages)
+
+
+class Batch:
+    """Index maps and workspace of one request batch on the device."""
+
+    def __init__(self, dtype, n_layers, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
+                 seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq=None, doc_src_row=None,
+                 doc_src_pos0=None, split_keys=0, device="cuda"):
+        self.dtype = dtype
+        self.torch_dtype = TORCH_DTYPE[dtype]
+        self.n_layers, self.n_q_heads, self.n_kv_heads = n_layers, n_q_heads, n_kv_heads
+        self.head_dim, self.rope_theta, self.softmax_scale = head_dim, rope_theta, softmax_scale
+        self.device = device
+        self.layout = kvlink_build_layout(seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq,
+                                          doc_src_row, doc_src_pos0)
+        t = self.layout["totals"]
+        self.n_docs, self.n_new = int(t[0]), int(t[1])
+        self.max_doc_len, self.max_cached = int(t[2]), int(t[3])
+        self.max_new, self.max_total = int(t[4]), int(t[5])
+        self.n_seqs = len(n_query)
+
+        def up(a):
+            return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+        self.d_spans = up(self.layout["spans"].reshape(-1, SPAN_FIELDS))
+        self.d_seq_new_ptr = up(self.layout["seq_new_ptr"])
+        self.d_seq_cached = up(self.layout["seq_cached"])
+        self.d_new_pos = up(self.layout["new_pos"])
+        self.d_new_visible = up(self.layout["new_visible"])
+        self.set_split_keys(split_keys)
+
+    def set_split_keys(self, split_keys):
+        self.split_keys = split_keys
+        self.ws_bytes = kvlink_attend_workspace_bytes(self.dtype, self.n_q_heads, self.n_kv_heads,
+                                                      self.head_dim, self.n_seqs, self.n_new,
+                                                      self.max_new, self.max_cached, split_keys)
+        if self.ws_bytes == 0:
+            raise ValueError("invalid attention sizes")
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def reencode(self, src_view, dst_view, stream=None):
+        """Re-encode every cached key of the batch, all layers (one launch)."""
+        kvlink_reencode_keys(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                             self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
+                             src_view, dst_view, stream)
+
+    def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None):
+        """RoPE + append of the new tokens and their attention, one layer."""
+        kvlink_attend_new_tokens(self.dtype, self.n_q_heads, self.n_kv_heads, self.head_dim,
+                                 self.rope_theta, self.softmax_scale, self.n_seqs, self.n_new,
+                                 self.max_new, self.max_cached, self.d_seq_new_ptr,
+                                 self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
+                                 k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys,
+                                 self.workspace, self.ws_bytes, stream)
+
+    def new_out(self):
+        return torch.empty((self.n_new, self.n_q_heads, self.head_dim), dtype=self.torch_dtype,
+                           device=self.device)
+
+    def new_lse(self):
+        return torch.empty((self.n_new, self.n_q_heads), dtype=torch.float32, device=self.device)

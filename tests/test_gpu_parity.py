@@ -1,0 +1,214 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs, at the workload sizes the benchmark uses, plus the
+invariants of the method (delta = 0 is a copy, values untouched, split-count
+invariance, in-place = out-of-place, run-to-run determinism)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from harness import ContiguousRun, check_bf16_rounding, check_close, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_2502_16002_amd  # noqa: F401  (raises if the library is missing)
+
+
+def _print(*a):
+    print(*a, flush=True)
+
+
+# ------------------------------------------------------------------ re-encode
+
+
+def _check_reencode(run, layers, rows_sample=None):
+    w = run.w
+    k_dst = run.k_dst
+    b = run.batch
+    spans = b.layout["spans"]
+    worst = 0.0
+    for l in layers:
+        kc, _ = workloads.request_cache(w, run.lds[l], 0)
+        kc = workloads.as_f64(w, kc)                              # [H][T_c][d]
+        got = to_f64(k_dst[l, :, 0, :kc.shape[1]])
+        for i, sp in enumerate(spans):
+            r0, n, delta = int(sp[3]), int(sp[4]), int(sp[5])
+            rows = np.arange(r0, r0 + n) if rows_sample is None else \
+                np.unique(np.clip(r0 + rows_sample % n, r0, r0 + n - 1))
+            ref = oracle.reencode(kc[:, rows], delta, w.rope_theta)
+            worst = max(worst, check_close(w, got[:, rows], ref, f"re-encode layer {l} doc {i}"))
+            if w.dtype == "bf16":
+                check_bf16_rounding(got[:, rows], ref, f"re-encode layer {l} doc {i}")
+    return worst
+
+
+def test_reencode_tiny_f32():
+    w = workloads.tiny_f32()
+    run = ContiguousRun(w, layers=[])
+    run.batch.reencode(run.src_view, run.k_view)
+    _print("tiny re-encode worst", _check_reencode(run, [0]))
+
+
+def test_reencode_llama1b():
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[])
+    run.batch.reencode(run.src_view, run.k_view)
+    _print("1b re-encode worst", _check_reencode(run, [0]))
+
+
+def test_reencode_llama8b_all_layers():
+    w = workloads.llama8b_10doc()
+    run = ContiguousRun(w, layers=[])
+    run.batch.reencode(run.src_view, run.k_view)
+    _print("8b re-encode worst", _check_reencode(run, range(w.n_layers)))
+
+
+def test_reencode_long_sampled_layers():
+    w = workloads.llama8b_long()
+    run = ContiguousRun(w, layers=[])
+    run.batch.reencode(run.src_view, run.k_view)
+    worst = _check_reencode(run, [0, 15, 31])
+    rng = np.random.default_rng(5)
+    worst = max(worst, _check_reencode(run, [3, 22], rows_sample=rng.integers(0, 512, 48)))
+    _print("long re-encode worst", worst)
+
+
+def test_reencode_first_document_is_bitwise_copy_and_in_place_matches():
+    import torch
+    from paper_2502_16002_amd.runtime import contiguous_view
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[])
+    run.batch.reencode(run.src_view, run.k_view)
+    sp = run.batch.layout["spans"]
+    assert sp[0][5] == 0
+    n0 = int(sp[0][4])
+    torch.cuda.synchronize()
+    assert torch.equal(run.k_dst[0, :, 0, :n0].view(torch.int16),
+                       run.k_src[0, :, :n0].view(torch.int16))
+    # in place: load the stored keys into the concatenated buffer, rotate there
+    inplace = torch.zeros_like(run.k_dst)
+    inplace[:, :, 0, :run.R] = run.k_src
+    view = contiguous_view(inplace, w.n_kv_heads, 1, run.cap, w.head_dim)
+    run.batch.reencode(view, view)
+    torch.cuda.synchronize()
+    assert torch.equal(inplace.view(torch.int16), run.k_dst.view(torch.int16))
+
+
+# ------------------------------------------------------------------ attention
+
+
+def _check_attend(run, l, rows=None, tag=""):
+    w = run.w
+    kc, vc, q, kn, vn = run.oracle_inputs(l)
+    ref, ref_lse = oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, kc, vc,
+                                 w.rope_theta, w.scale, rows=rows)
+    got = to_f64(run.out[l])
+    lse = to_f64(run.lse[l])
+    if rows is not None:
+        got, lse = got[rows], lse[rows]
+    worst = check_close(w, got, ref, f"{tag} attention layer {l}")
+    lse_err = float(np.max(np.abs(lse - ref_lse)))
+    assert lse_err <= (1e-5 if w.dtype == "f32" else 2e-2), f"{tag} lse err {lse_err}"
+    return worst, lse_err
+
+
+def _check_append(run, l):
+    """The new tokens' keys (rotated at their positions) and values were
+    appended after the cached rows."""
+    w, b = run.w, run.batch
+    Tc = int(b.layout["seq_cached"][0])
+    _, _, _, kn, vn = run.oracle_inputs(l)
+    pos = b.layout["new_pos"]
+    got_k = to_f64(run.k_dst[l, :, 0, Tc:Tc + b.n_new])      # [H][n_new][d]
+    got_v = to_f64(run.v_dst[l, :, 0, Tc:Tc + b.n_new])
+    ref_k = np.stack([[oracle.rope(kn[r, h], int(pos[r]), w.rope_theta) for r in range(b.n_new)]
+                      for h in range(w.n_kv_heads)])
+    check_close(w, got_k, ref_k, "appended keys")
+    assert np.array_equal(got_v, vn.transpose(1, 0, 2))
+
+
+def test_attend_tiny_f32():
+    w = workloads.tiny_f32()
+    run = ContiguousRun(w, layers=[0])
+    run.run()
+    _print("tiny attend", _check_attend(run, 0, tag="tiny"))
+    _check_append(run, 0)
+
+
+def test_attend_llama1b():
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[0])
+    run.run()
+    _print("1b attend", _check_attend(run, 0, tag="1b"))
+    _check_append(run, 0)
+
+
+def test_attend_llama8b_32_layers():
+    w = workloads.llama8b_10doc()
+    run = ContiguousRun(w, layers=list(range(w.n_layers)))
+    run.run()
+    rng = np.random.default_rng(3)
+    for l in [0, 31]:
+        _print("8b attend layer", l, _check_attend(run, l, tag="8b"))
+    for l in [7, 15, 24]:
+        rows = np.sort(rng.choice(run.batch.n_new, 16, replace=False))
+        _print("8b attend layer", l, "sampled", _check_attend(run, l, rows=rows, tag="8b"))
+    _check_append(run, 31)
+
+
+def test_attend_long_sampled():
+    w = workloads.llama8b_long()
+    run = ContiguousRun(w, layers=list(range(w.n_layers)))
+    run.run()
+    n_new = run.batch.n_new
+    # early and late link tokens, and first / last queries
+    rows = np.array([0, 1, 4, 5, 99, 100, 199, 200, 201, n_new - 2, n_new - 1])
+    for l in [0, 15, 31]:
+        _print("long attend layer", l, _check_attend(run, l, rows=rows, tag="long"))
+
+
+@pytest.mark.parametrize("split", [128, 256, 4096])
+def test_split_count_invariance(split):
+    w = workloads.llama1b_layer()
+    base = ContiguousRun(w, layers=[0])
+    base.run()
+    other = ContiguousRun(w, layers=[0], split_keys=split)
+    other.run()
+    a, b = to_f64(base.out[0]), to_f64(other.out[0])
+    rowmax = np.maximum(np.max(np.abs(a), axis=-1), 1e-30)
+    assert float(np.max(np.max(np.abs(a - b), axis=-1) / rowmax)) <= 1e-2
+    _check_attend(other, 0, tag=f"split{split}")
+
+
+@pytest.mark.parametrize("doc_len,link_count,n_query", [
+    ([], [], 9),                            # no documents: plain causal queries
+    ([37], [0], 20),                        # one document, K = 0
+    ([1, 1, 3, 1], [3, 0, 2, 1], 0),        # ragged, no queries
+    ([130, 5, 260], [5, 5, 5], 33),         # lengths crossing tile edges
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_attend_edge_layouts(doc_len, link_count, n_query, dtype):
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2,
+                         head_dim=128 if dtype == "bf16" else 64, dtype=dtype,
+                         rope_theta=5e5, seed=17)
+    for split in [0, 128]:
+        run = ContiguousRun(w, layers=[0], split_keys=split)
+        run.run()
+        _check_attend(run, 0, tag=f"edge{doc_len}/{split}")
+        if doc_len:
+            _check_reencode(run, [0])
+
+
+def test_run_twice_is_bitwise_identical():
+    import torch
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[0])
+    run.run()
+    first = run.out[0].clone()
+    run.run()
+    assert torch.equal(first.view(torch.int16), run.out[0].view(torch.int16))
