@@ -130,37 +130,36 @@ def time_region(fn, iters):
     return s.elapsed_time(e) / iters
 
 
-def cpu_baseline(w, alg):
-    """The oracle, untouched, on layer 0: re-encode of every document and the
-    attention of a sample of new tokens, scaled to one full layer."""
+def cpu_baseline(w, alg, budget_s=15.0):
+    """The oracle, untouched, on whole layers of the same workload: the
+    re-encode of every document and the attention of every new token and
+    head, layer after layer until about budget_s seconds have run."""
     import oracle
     import workloads
-    ld = workloads.layer_data(w, 0)
-    kc, vc = workloads.request_cache(w, ld, 0)
-    q, kn, vn = workloads.request_new(w, ld, 0)
     f = lambda x: workloads.as_f64(w, x)
-    kc, vc, q, kn, vn = f(kc), f(vc), f(q), f(kn), f(vn)
-    t0 = time.perf_counter()
-    r0 = 0
-    g = 0
-    for j, L in enumerate(w.doc_len(0)):
-        oracle.reencode(kc[:, r0:r0 + L], g, w.rope_theta)
-        r0 += L
-        g += L + w.link_count[0][j]
-    t_re = time.perf_counter() - t0
-    n_new = alg["new_tokens"]
-    n_rows = min(n_new, 32)
-    rows = np.linspace(0, n_new - 1, n_rows).round().astype(np.int32)
-    t0 = time.perf_counter()
-    oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, kc, vc, w.rope_theta,
-                  w.scale, rows=rows)
-    t_at = time.perf_counter() - t0
-    us_layer = (t_re + t_at * n_new / n_rows) * 1e6
-    return {"value": us_layer, "unit": "us/layer", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"layer 0 of {w.n_layers}: re-encode of all {len(w.doc_len(0))} documents "
-                      f"({t_re:.2f} s) + attention of {n_rows} of {n_new} new tokens x "
-                      f"{w.n_q_heads} heads ({t_at:.2f} s), scaled to all new tokens",
+    total, layers = 0.0, 0
+    for l in range(w.n_layers):
+        ld = workloads.layer_data(w, l)
+        kc, vc = workloads.request_cache(w, ld, 0)
+        q, kn, vn = workloads.request_new(w, ld, 0)
+        kc, vc, q, kn, vn = f(kc), f(vc), f(q), f(kn), f(vn)
+        t0 = time.perf_counter()
+        r0, g = 0, 0
+        for j, L in enumerate(w.doc_len(0)):
+            oracle.reencode(kc[:, r0:r0 + L], g, w.rope_theta)
+            r0 += L
+            g += L + w.link_count[0][j]
+        oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, kc, vc,
+                      w.rope_theta, w.scale)
+        total += time.perf_counter() - t0
+        layers += 1
+        if total >= budget_s:
+            break
+    return {"value": round(total / layers * 1e6, 1), "unit": "us/layer",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{layers} of {w.n_layers} layers in full (re-encode of all "
+                      f"{len(w.doc_len(0))} documents + attention of all {alg['new_tokens']} "
+                      f"new tokens x {w.n_q_heads} heads), {total:.1f} s",
             "cpu": platform.processor() or platform.machine()}
 
 

@@ -225,7 +225,8 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
  *                              device bytes, 256-byte aligned
  *
- * Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in {1, 2, 4, 8};
+ * softmax_scale must be positive and finite (1/sqrt(head_dim) for the Llama
+ * family).  Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in {1, 2, 4, 8};
  * dtype KVLINK_F32 or KVLINK_BF16 (float accumulation and softmax either way).
  *
  * Errors: KVLINK_ERR_INVALID_ARG, KVLINK_ERR_UNSUPPORTED,

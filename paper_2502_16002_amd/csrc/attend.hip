@@ -23,99 +23,70 @@
 // the new rows up to its last token; each key is masked per row.
 #include <algorithm>
 
-#include "kvlink_internal.h"
+#include "attend_common.h"
 
 namespace kvlink {
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-    return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
-}
-
-// Request of global new token n (binary search over seq_new_ptr).
-__device__ __forceinline__ int seq_of(const int32_t* seq_new_ptr, int n_seqs, int n) {
-    int lo = 0, hi = n_seqs - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (seq_new_ptr[mid] <= n) lo = mid; else hi = mid - 1;
-    }
-    return lo;
-}
-
-// Key range of a row block: cached rows seen by its last token (cmax) and
-// the virtual key count cmax + (last token + 1).
-struct BlockKeys {
-    int cmax, nvirt, r_last;
-};
-__device__ __forceinline__ BlockKeys block_keys(const int32_t* new_visible, int n0, int rows_s,
-                                                int rho0, int row_block, int group) {
-    const int rho_end = min(rho0 + row_block, rows_s);
-    BlockKeys b;
-    b.r_last = (rho_end - 1) / group;
-    b.cmax = new_visible[n0 + b.r_last];
-    b.nvirt = b.cmax + b.r_last + 1;
-    return b;
-}
-
-struct KParams {
-    const void* q_rot;
-    View k, v;
-    int layer, n_seqs, n_q_heads, n_kv_heads, group;
-    const int32_t* seq_new_ptr;
-    const int32_t* seq_cached;
-    const int32_t* new_visible;
-    float scale_log2;
-    int split_keys, n_splits, row_block;
-    float* part_o;
-    float* part_ml;
-    void* out;
-    float* lse;
-};
+using namespace attn;
 
 // --------------------------------------------------------------- prologue
 
+// One workgroup per new token: the token's cos/sin table (double-precision
+// angles) goes to LDS, then every q head and every k head is rotated with
+// 16-byte accesses (q to the workspace, k to the cache row T_c + r) and the v
+// heads are copied to the same cache row.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_new_kernel(
     const T* __restrict__ q_new, const T* __restrict__ k_new, const T* __restrict__ v_new,
-    T* __restrict__ q_rot, View k, View v, int layer, int n_seqs, int n_new_total, int n_q_heads,
-    int n_kv_heads, const int32_t* __restrict__ seq_new_ptr,
-    const int32_t* __restrict__ seq_cached, const int32_t* __restrict__ new_pos, double theta) {
+    T* __restrict__ q_rot, View k, View v, int layer, int n_seqs, int n_q_heads, int n_kv_heads,
+    const int32_t* __restrict__ seq_new_ptr, const int32_t* __restrict__ seq_cached,
+    const int32_t* __restrict__ new_pos, double theta) {
     constexpr int H = D / 2;
-    const int idx = blockIdx.x * 256 + threadIdx.x;
-    if (idx >= n_new_total * H) return;
-    const int n = idx / H, j = idx % H;
+    constexpr int E = 16 / (int)sizeof(T);
+    constexpr int TPV = H / E;               // threads per head vector
+    __shared__ float s_cos[H], s_sin[H];
+    const int n = blockIdx.x;
     const int s = seq_of(seq_new_ptr, n_seqs, n);
-    const int r = n - seq_new_ptr[s];
-    const int row = seq_cached[s] + r;
-    float c, sn;
-    rope_cos_sin(new_pos[n], j, D, theta, &c, &sn);
-    for (int h = 0; h < n_q_heads; ++h) {
-        const int64_t o = ((int64_t)n * n_q_heads + h) * D;
-        const float a = to_f32(q_new[o + j]), b = to_f32(q_new[o + j + H]);
-        q_rot[o + j] = from_f32<T>(a * c - b * sn);
-        q_rot[o + j + H] = from_f32<T>(a * sn + b * c);
+    const int row = seq_cached[s] + (n - seq_new_ptr[s]);
+    for (int j = threadIdx.x; j < H; j += 256) rope_cos_sin(new_pos[n], j, D, theta, &s_cos[j], &s_sin[j]);
+    __syncthreads();
+    const int sub = threadIdx.x % TPV;
+    float c[E], sn[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        c[e] = s_cos[sub * E + e];
+        sn[e] = s_sin[sub * E + e];
     }
     T* kb = reinterpret_cast<T*>(k.base);
     T* vb = reinterpret_cast<T*>(v.base);
-    for (int h = 0; h < n_kv_heads; ++h) {
-        const int64_t o = ((int64_t)n * n_kv_heads + h) * D;
-        const float a = to_f32(k_new[o + j]), b = to_f32(k_new[o + j + H]);
-        const int64_t ko = view_offset(k, layer, h, s, row);
-        kb[ko + j] = from_f32<T>(a * c - b * sn);
-        kb[ko + j + H] = from_f32<T>(a * sn + b * c);
-        const int64_t vo = view_offset(v, layer, h, s, row);
-        vb[vo + j] = v_new[o + j];
-        vb[vo + j + H] = v_new[o + j + H];
+    for (int hv = threadIdx.x / TPV; hv < n_q_heads + n_kv_heads; hv += 256 / TPV) {
+        const T* src;
+        T* dst;
+        if (hv < n_q_heads) {
+            src = q_new + ((int64_t)n * n_q_heads + hv) * D;
+            dst = q_rot + ((int64_t)n * n_q_heads + hv) * D;
+        } else {
+            const int hk = hv - n_q_heads;
+            src = k_new + ((int64_t)n * n_kv_heads + hk) * D;
+            dst = kb + view_offset(k, layer, hk, s, row);
+        }
+        float a[E], b[E], x[E], y[E];
+        unpack16<T>(*reinterpret_cast<const uint4*>(src + sub * E), a);
+        unpack16<T>(*reinterpret_cast<const uint4*>(src + H + sub * E), b);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            x[e] = a[e] * c[e] - b[e] * sn[e];
+            y[e] = a[e] * sn[e] + b[e] * c[e];
+        }
+        *reinterpret_cast<uint4*>(dst + sub * E) = pack16<T>(x);
+        *reinterpret_cast<uint4*>(dst + H + sub * E) = pack16<T>(y);
+    }
+    constexpr int VPH = D / E;               // 16-byte vectors per v head
+    for (int i = threadIdx.x; i < n_kv_heads * VPH; i += 256) {
+        const int hk = i / VPH, cch = i % VPH;
+        *reinterpret_cast<uint4*>(vb + view_offset(v, layer, hk, s, row) + cch * E) =
+            *reinterpret_cast<const uint4*>(v_new + ((int64_t)n * n_kv_heads + hk) * D + cch * E);
     }
 }
 
@@ -305,19 +276,22 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.out = a.out;
     p.lse = a.lse;
 
-    const int n_pairs = pl.n_new_total * (D / 2);
-    hipLaunchKernelGGL((rope_new_kernel<T, D>), dim3((n_pairs + 255) / 256), dim3(256), 0, stream,
+    hipLaunchKernelGGL((rope_new_kernel<T, D>), dim3(pl.n_new_total), dim3(256), 0, stream,
                        reinterpret_cast<const T*>(a.q_new), reinterpret_cast<const T*>(a.k_new),
                        reinterpret_cast<const T*>(a.v_new), q_rot, a.k, a.v, a.layer, pl.n_seqs,
-                       pl.n_new_total, pl.n_q_heads, pl.n_kv_heads, a.seq_new_ptr, a.seq_cached,
-                       a.new_pos, a.theta);
+                       pl.n_q_heads, pl.n_kv_heads, a.seq_new_ptr, a.seq_cached, a.new_pos,
+                       a.theta);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
     const int n_rb = (pl.max_new * pl.group + pl.row_block - 1) / pl.row_block;
     dim3 grid(pl.n_splits, n_rb, pl.n_seqs * pl.n_kv_heads);
-    hipLaunchKernelGGL((attend_valu_kernel<T, D>), grid, dim3(256), 0, stream, p);
-    e = hipGetLastError();
+    if (pl.use_mfma) {
+        e = launch_attend_mfma(D, p, grid, stream);
+    } else {
+        hipLaunchKernelGGL((attend_valu_kernel<T, D>), grid, dim3(256), 0, stream, p);
+        e = hipGetLastError();
+    }
     if (e != hipSuccess || pl.n_splits == 1) return e;
 
     const int64_t n_rows = (int64_t)pl.n_new_total * pl.n_q_heads;
@@ -344,14 +318,17 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->n_new_total = n_new_total;
     p->max_new = max_new;
     p->max_cached = max_cached;
-    p->use_mfma = false;
-    p->row_block = 16;
+    // matrix cores where the GQA-packed rows of a KV head form a real dense
+    // contraction; the VALU schedule for fp32 and for thin row counts
+    p->use_mfma = dt == KVLINK_BF16 && (int64_t)max_new * p->group >= 32;
+    p->row_block = p->use_mfma ? 64 : 16;
     const int64_t max_keys = (int64_t)max_cached + max_new;
     if (split_keys == 0) {
-        // aim at about 1024 workgroups in total, splits of at least 256 keys
+        // aim at a few workgroups per compute unit, splits of at least 256 keys
+        const int64_t target = p->use_mfma ? 512 : 1024;
         const int64_t n_rb = (int64_t)n_seqs * n_kv_heads *
                              (((int64_t)max_new * p->group + p->row_block - 1) / p->row_block);
-        const int64_t want_splits = n_rb > 0 ? (1024 + n_rb - 1) / n_rb : 1;
+        const int64_t want_splits = n_rb > 0 ? (target + n_rb - 1) / n_rb : 1;
         int64_t sk = (max_keys + want_splits - 1) / std::max<int64_t>(want_splits, 1);
         sk = (sk + 127) / 128 * 128;
         split_keys = (int)std::max<int64_t>(256, sk);

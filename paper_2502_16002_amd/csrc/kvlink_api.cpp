@@ -231,8 +231,8 @@ kvlink_status kvlink_attend_new_tokens(
             return fail(KVLINK_ERR_INVALID_ARG, "max_new exceeds n_new_total");
         if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
             return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
-        if (!std::isfinite(softmax_scale))
-            return fail(KVLINK_ERR_INVALID_ARG, "softmax_scale must be finite");
+        if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+            return fail(KVLINK_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
         if (split_keys < 0 || split_keys % 128)
             return fail(KVLINK_ERR_INVALID_ARG, "split_keys must be 0 or a positive multiple of 128");
         if (n_seqs > 65535 / n_kv_heads)

@@ -29,6 +29,43 @@ __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
     return bf16_t{__builtin_bit_cast(uint16_t, h)};
 }
 
+// 16 bytes of T <-> floats (8 bf16 or 4 f32 per 16-byte access)
+template <typename T>
+__device__ __forceinline__ void unpack16(const uint4& v, float* f);
+template <>
+__device__ __forceinline__ void unpack16<float>(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x);
+    f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z);
+    f[3] = __uint_as_float(v.w);
+}
+template <>
+__device__ __forceinline__ void unpack16<bf16_t>(const uint4& v, float* f) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ uint4 pack16(const float* f);
+template <>
+__device__ __forceinline__ uint4 pack16<float>(const float* f) {
+    return uint4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                 __float_as_uint(f[3])};
+}
+template <>
+__device__ __forceinline__ uint4 pack16<bf16_t>(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)from_f32<bf16_t>(f[2 * i]).bits |
+               ((uint32_t)from_f32<bf16_t>(f[2 * i + 1]).bits << 16);
+    return uint4{w[0], w[1], w[2], w[3]};
+}
+
 // ------------------------------------------------------------------- views
 
 // Device copy of kvlink_kv_view, with the base typed by the caller.
@@ -50,6 +87,41 @@ __device__ __forceinline__ int64_t view_offset(const View& v, int layer, int hea
         off += (int64_t)seq * v.seq_stride + (int64_t)row * v.row_stride;
     }
     return off;
+}
+
+// Rows of one (layer, head, seq) slice of a view, with the slice's part of
+// the address hoisted: the per-row cost is one multiply-add (contiguous) or a
+// block-table lookup (paged).
+struct RowPtr {
+    const char* base;          // bytes: contiguous: row 0 of the slice; paged: (layer, head)
+    int64_t row_bytes;         // row stride in bytes
+    const int32_t* table;      // paged: this sequence's block-table row, else NULL
+    int64_t page_bytes;        // paged: page stride in bytes
+    int32_t page_size;
+    __device__ __forceinline__ const char* row(int r) const {
+        if (!table) return base + (int64_t)r * row_bytes;
+        const int pg = table[r / page_size];
+        return base + (int64_t)pg * page_bytes + (int64_t)(r % page_size) * row_bytes;
+    }
+};
+
+template <typename T>
+__device__ __forceinline__ RowPtr row_ptr(const View& v, int layer, int head, int seq) {
+    RowPtr r;
+    const int64_t es = sizeof(T);
+    r.base = v.base + ((int64_t)layer * v.layer_stride + (int64_t)head * v.head_stride) * es;
+    r.row_bytes = v.row_stride * es;
+    if (v.block_table) {
+        r.table = v.block_table + (int64_t)seq * v.max_pages;
+        r.page_bytes = v.page_stride * es;
+        r.page_size = v.page_size;
+    } else {
+        r.base += (int64_t)seq * v.seq_stride * es;
+        r.table = nullptr;
+        r.page_bytes = 0;
+        r.page_size = 1;
+    }
+    return r;
 }
 
 // cos and sin of pos * theta^(-2j/d): the angle is formed and reduced in

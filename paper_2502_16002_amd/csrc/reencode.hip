@@ -28,42 +28,6 @@ constexpr int kRows = 64;
 constexpr int kLH = 8;
 constexpr int kUnroll = 4;
 
-template <typename T>
-__device__ __forceinline__ void unpack16(const uint4& v, float* f);
-template <>
-__device__ __forceinline__ void unpack16<float>(const uint4& v, float* f) {
-    f[0] = __uint_as_float(v.x);
-    f[1] = __uint_as_float(v.y);
-    f[2] = __uint_as_float(v.z);
-    f[3] = __uint_as_float(v.w);
-}
-template <>
-__device__ __forceinline__ void unpack16<bf16_t>(const uint4& v, float* f) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        f[2 * i] = __uint_as_float(w[i] << 16);
-        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
-}
-
-template <typename T>
-__device__ __forceinline__ uint4 pack16(const float* f);
-template <>
-__device__ __forceinline__ uint4 pack16<float>(const float* f) {
-    return uint4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
-                 __float_as_uint(f[3])};
-}
-template <>
-__device__ __forceinline__ uint4 pack16<bf16_t>(const float* f) {
-    uint32_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        w[i] = (uint32_t)from_f32<bf16_t>(f[2 * i]).bits |
-               ((uint32_t)from_f32<bf16_t>(f[2 * i + 1]).bits << 16);
-    return uint4{w[0], w[1], w[2], w[3]};
-}
-
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                                                             const kvlink_span* __restrict__ spans,

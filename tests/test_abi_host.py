@@ -198,6 +198,8 @@ def _call_attend(kv, a):
     (dict(max_new=11), 1),
     (dict(theta=-1.0), 1),
     (dict(scale=float("inf")), 1),
+    (dict(scale=0.0), 1),
+    (dict(scale=-0.1), 1),
     (dict(split=100), 1),
     (dict(snp=None), 1),
     (dict(q=None), 1),
