@@ -321,7 +321,7 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     // matrix cores where the GQA-packed rows of a KV head form a real dense
     // contraction; the VALU schedule for fp32 and for thin row counts
     p->use_mfma = dt == KVLINK_BF16 && (int64_t)max_new * p->group >= 32;
-    p->row_block = p->use_mfma ? 64 : 16;
+    p->row_block = p->use_mfma ? attn::attend_mfma_row_block() : 16;
     const int64_t max_keys = (int64_t)max_cached + max_new;
     if (split_keys == 0) {
         // aim at a few workgroups per compute unit, splits of at least 256 keys

@@ -63,6 +63,8 @@ struct KParams {
 
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, dim3 grid, hipStream_t stream);
+// GQA rows per workgroup of the MFMA kernel
+int attend_mfma_row_block();
 
 }  // namespace attn
 }  // namespace kvlink

@@ -1,35 +1,38 @@
 // attend_mfma.hip — bf16 split-K attention of the new tokens on gfx950 matrix
 // cores (v_mfma_f32_16x16x32_bf16, float accumulation).
 //
-// A workgroup owns one KV head, 64 GQA-packed rows (16 tokens x 4 heads for
-// a group of 4) and one split of the block's virtual key range.  Its eight
-// wavefronts form two row groups of 32 rows times four key waves; each is an
-// independent online-softmax worker over 32-key chunks (key wave w takes
-// chunks w, w+4, ...) for its 32 rows.  The two waves that take the same
-// chunk read it at about the same time, so the second read is served by the
-// L1 cache.  Per-wave state fits two wavefronts per SIMD, so one wave's
-// softmax overlaps the other's matrix products:
+// A workgroup owns one KV head, kRB = 256 GQA-packed rows (64 tokens x 4
+// heads for a group of 4) and one split of the block's virtual key range.
+// Each of its eight wavefronts owns 32 of the rows and walks every key of
+// the split (two wavefronts per SIMD, so one's softmax overlaps the other's
+// matrix products); K and V tiles of 64 keys are brought into LDS once per
+// workgroup and shared by the eight waves:
 //
-//   S^T = K Q^T     A = 16 keys x 32 dims of K, straight from global memory
-//                   into registers (row-major K is already the A layout);
-//                   B = Q^T, loaded once (rows x dims, again row-major).
-//                   The accumulator holds, per lane, 4 keys of one row.
-//   P   = exp2(S*scale*log2e - m)   in float, per lane, then packed to bf16:
-//                   the 8 keys a lane holds for its row are exactly the 8
-//                   k-elements the B operand of the next product needs, so
-//                   P goes from accumulator to operand without a shuffle.
-//   O^T += V^T P^T  A = V^T (16 dims x 32 keys): V is row-major in memory, so
-//                   each wave transposes its 32 x d V chunk through a
-//                   wave-private LDS tile (rows of 32 keys, 80-byte stride:
-//                   the 8-byte operand reads are bank-conflict free).
+//   * the tiles are loaded straight from global memory into a four-stage
+//     LDS ring with 16-byte direct-to-LDS loads (each wave issues an eighth
+//     of a tile), so the loads of the next three tiles are in flight while the
+//     current one is used, at no register cost;
+//   * K is stored in MFMA operand order (for each 16-key x 32-dim block,
+//     lane l's 16 bytes at l*16): the A operand of S^T = K Q^T is one
+//     conflict-free ds_read_b128 per lane;
+//   * V is stored row-major with the 16-byte chunks of row k XOR-swizzled by
+//     k, and read with ds_read_b64_tr_b16, which hands each lane four keys of
+//     one dim: exactly the A operand of O^T = V^T P^T, with no transpose on
+//     the vector ALUs.
 //
-// The key order inside the 32-key contraction is permuted the same way in
-// both operands (lane group g holds keys 4g..4g+3 and 16+4g..16+4g+3), which
-// leaves the sum unchanged.  The row max is reduced across the four lane
-// groups that hold a row; the row sum stays per lane until the end.  After
-// the loop the key waves of a row group merge their (m, l, O) in LDS and key
-// wave 0 writes the group's result (final output, or a split partial for the
-// combine).
+// Per wave and 32-key sub-tile:
+//   S^T = K Q^T     B = Q^T (32 rows, loaded once into registers); the
+//                   accumulator holds, per lane, 4 keys of one row;
+//   P   = 2^(S*scale*log2e - m)  per lane in float, packed to bf16: the 8
+//                   keys a lane holds for its row are the 8 k-elements the B
+//                   operand of the next product needs (lane group g holds
+//                   keys 4g..4g+3 and 16+4g..16+4g+3; the A operand uses the
+//                   same key order, which leaves the contraction unchanged);
+//   O^T += V^T P^T
+//
+// The running row maximum is raised lazily (only when a score exceeds it by
+// more than 2^kTau), so the rescale of O and l and the cross-lane reduction
+// are off the common path.
 #include <algorithm>
 
 #include "attend_common.h"
@@ -39,25 +42,32 @@ namespace attn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 
 namespace {
 
-constexpr int kRB = 64;         // GQA rows per workgroup
-constexpr int kRG = 2;          // row groups (of kRB / kRG rows) per workgroup
-constexpr int kKW = 4;          // key waves per row group
-constexpr int kWaves = kRG * kKW;
-constexpr int kRT = kRB / kRG / 16;   // 16-row tiles per wave
-constexpr int kChunk = 32;      // keys per wave step
-constexpr int kVtStride = 80;   // bytes per dim row of the transposed V tile
+constexpr int kWaves = 8;
+constexpr int kRT = 2;                    // 16-row tiles per wave
+constexpr int kRB = kWaves * kRT * 16;    // GQA rows per workgroup
+constexpr int kTile = 64;                 // keys per LDS stage
+constexpr int kStages = 4;
+// Rescale threshold of the online softmax, in log2 units: p = 2^(s - m)
+// stays below 2^kTau (exact in float, representable in bf16).
+constexpr float kTau = 8.0f;
+// Finite stand-in for "no score seen yet": any real score exceeds it by more
+// than kTau, and masked scores (-inf) still give p = 0 without NaN.
+constexpr float kNoMax = -1.0e30f;
 
 template <int D>
 struct Smem {
-    static constexpr int vt_wave = D * kVtStride;
-    static constexpr int vt_all = kWaves * vt_wave;
-    static constexpr int slot = (D / 16) * kRT * 4 * 64 * 4;   // one wave's O^T registers
-    static constexpr int merge = kRG * 2 * slot;
-    static constexpr int ml_off = vt_all > merge ? vt_all : merge;
-    static constexpr int bytes = ml_off + 2 * kWaves * (kRB / kRG) * 4;
+    static constexpr int k_bytes = kTile * D * 2;
+    static constexpr int v_bytes = kTile * D * 2;
+    static constexpr int stage = k_bytes + v_bytes;
+    // direct-to-LDS loads need a non-zero LDS address: keep the first bytes
+    // of the allocation out of the ring
+    static constexpr int base = 1024;
+    static constexpr int bytes = base + kStages * stage;
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
@@ -68,28 +78,106 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
     return (uint32_t)from_f32<bf16_t>(a).bits | ((uint32_t)from_f32<bf16_t>(b).bits << 16);
 }
 
-__device__ __forceinline__ void wave_lds_fence() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+// Transposed reads of the V^T operands of one 32-key sub-tile: r[dt][h] for
+// dt < DT (16-dim tiles) and h in {0, 1} (keys 4g.. and 16+4g..), from the
+// LDS byte addresses a[dt][h].  Issued as one block followed by a single
+// wait on the LDS counter; the results are early-clobber outputs, since a
+// read's data may return while later reads of the block still need their
+// address registers.  The V tile was written by direct-to-LDS loads
+// whose completion the caller has already waited for (vector-memory counter
+// and a workgroup barrier), so no further wait on those loads is needed.
+template <int DT>
+__device__ __forceinline__ void read_vt(const uint32_t (&a)[DT][2], uint2 (&r)[DT][2]);
+
+// (The host compilation pass sees only the declarations: the register
+// constraints exist for the GPU target alone.)
+template <>
+__device__ __forceinline__ void read_vt<8>(const uint32_t (&a)[8][2], uint2 (&r)[8][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %16\n\t"
+        "ds_read_b64_tr_b16 %1, %17\n\t"
+        "ds_read_b64_tr_b16 %2, %18\n\t"
+        "ds_read_b64_tr_b16 %3, %19\n\t"
+        "ds_read_b64_tr_b16 %4, %20\n\t"
+        "ds_read_b64_tr_b16 %5, %21\n\t"
+        "ds_read_b64_tr_b16 %6, %22\n\t"
+        "ds_read_b64_tr_b16 %7, %23\n\t"
+        "ds_read_b64_tr_b16 %8, %24\n\t"
+        "ds_read_b64_tr_b16 %9, %25\n\t"
+        "ds_read_b64_tr_b16 %10, %26\n\t"
+        "ds_read_b64_tr_b16 %11, %27\n\t"
+        "ds_read_b64_tr_b16 %12, %28\n\t"
+        "ds_read_b64_tr_b16 %13, %29\n\t"
+        "ds_read_b64_tr_b16 %14, %30\n\t"
+        "ds_read_b64_tr_b16 %15, %31\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
+          "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1]), "=&v"(r[4][0]), "=&v"(r[4][1]),
+          "=&v"(r[5][0]), "=&v"(r[5][1]), "=&v"(r[6][0]), "=&v"(r[6][1]), "=&v"(r[7][0]),
+          "=&v"(r[7][1])
+        : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]),
+          "v"(a[3][0]), "v"(a[3][1]), "v"(a[4][0]), "v"(a[4][1]), "v"(a[5][0]), "v"(a[5][1]),
+          "v"(a[6][0]), "v"(a[6][1]), "v"(a[7][0]), "v"(a[7][1])
+        : "memory");
+#endif
 }
 
-// Rescale threshold of the online softmax, in log2 units: the running row
-// maximum m is only raised (and O, l rescaled) when a score exceeds it by
-// more than kTau, so probabilities p = 2^(s - m) stay below 2^kTau (exact in
-// float, representable in bf16) and the rescale is rare after the first
-// chunks.
-constexpr float kTau = 8.0f;
-// Finite stand-in for "no score seen yet": any real score exceeds it by more
-// than kTau, and masked scores (-inf) still give p = 0 without NaN.
-constexpr float kNoMax = -1.0e30f;
+template <>
+__device__ __forceinline__ void read_vt<4>(const uint32_t (&a)[4][2], uint2 (&r)[4][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8\n\t"
+        "ds_read_b64_tr_b16 %1, %9\n\t"
+        "ds_read_b64_tr_b16 %2, %10\n\t"
+        "ds_read_b64_tr_b16 %3, %11\n\t"
+        "ds_read_b64_tr_b16 %4, %12\n\t"
+        "ds_read_b64_tr_b16 %5, %13\n\t"
+        "ds_read_b64_tr_b16 %6, %14\n\t"
+        "ds_read_b64_tr_b16 %7, %15\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
+          "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1])
+        : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]),
+          "v"(a[3][0]), "v"(a[3][1])
+        : "memory");
+#endif
+}
+
+// LDS byte address of a pointer into a __shared__ array (the low 32 bits of
+// its generic address).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+
+// 16-byte direct load from global memory into LDS: lane i's bytes land at
+// lds + 16 i (lds must be wave-uniform and not LDS address 0).  Device pass
+// only, like the register-constrained asm above.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+#endif
+}
+
+// Wait until at most n of this wave's vector-memory loads are outstanding.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    // vmcnt is split over bits [3:0] and [15:14]; expcnt (bits [6:4]) and
+    // lgkmcnt (bits [11:8]) are left at their maxima, i.e. not waited on
+    __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
 template <int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
-    constexpr int DT = D / 16;   // 16-dim tiles of O^T
-    constexpr int DS = D / 32;   // 32-dim steps of S^T = K Q^T
-    constexpr int VCH = D / 64;  // 16-byte V chunks a lane loads per key
-    __shared__ __attribute__((aligned(16))) unsigned char smem[Smem<D>::bytes];
+    constexpr int DT = D / 16;         // 16-dim tiles of O^T
+    constexpr int DS = D / 32;         // 32-dim steps of S^T = K Q^T
+    constexpr int KB = 4 * DS;         // 1 KB operand blocks of a K tile
+    constexpr int VI = kTile * D * 2 / 1024;   // 1 KB direct loads of a V tile
+    constexpr int CH = D / 8;          // 16-byte chunks per V row
+    constexpr int LPW = (KB + VI) / kWaves;    // direct loads per wave per tile
+    static_assert((KB % kWaves) == 0 && (VI % kWaves) == 0, "tile split");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
 
     const int split = blockIdx.x;
     const int s = blockIdx.z / p.n_kv_heads, h = blockIdx.z % p.n_kv_heads;
@@ -103,17 +191,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     if (kbeg >= bk.nvirt) return;
     const int kend = min(kbeg + p.split_keys, bk.nvirt);
     const int Tc = p.seq_cached[s];
-    const int vis_min = p.new_visible[n0 + rho0 / G];
     const float c2 = p.scale_log2;   // > 0
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int rg = wave / kKW, kw = wave % kKW;     // row group, key wave
     const int lr = lane & 15, lg = lane >> 4;
-    const int rho_w = rho0 + rg * (kRB / kRG);      // first row of this wave
+    const int rho_w = rho0 + wave * kRT * 16;      // first row of this wave
 
-    // The rows of this lane (one per row tile).  Row r may see virtual
-    // key v iff v < lo[rt] (cached rows up to its document, within the split)
-    // or cmax <= v <= hi[rt] (new rows up to its own, within the split).
+    // Rows of this lane (one per row tile).  Row r may see virtual key v iff
+    // v < lo (cached rows up to its document, within the split) or
+    // cmax <= v <= hi (new rows up to its own, within the split).
     int tok[kRT], lo[kRT], hi[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
@@ -123,6 +209,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         lo[rt] = min(vis, kend);
         hi[rt] = tok[rt] >= 0 ? min(bk.cmax + tok[rt], kend - 1) : -1;
     }
+    // keys below this bound are visible to every row of the wave (its
+    // first token sees the fewest cached rows)
+    const int wave_vis_min = p.new_visible[n0 + min(rho_w, rows_s - 1) / G];
 
     // Q^T operand, loaded once
     const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
@@ -145,173 +234,225 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) o[dt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m[kRT], lsum[kRT];
+    float m[kRT], lsum[kRT], thr[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         m[rt] = kNoMax;
         lsum[rt] = 0.f;
+        thr[rt] = -3.0e38f;   // the first finite score takes the slow path
     }
 
     const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
     const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
-    unsigned char* vt = smem + wave * Smem<D>::vt_wave;
-    const int kg = lane & 7, cc = lane >> 3;      // V loader: keys 4kg..4kg+3, dims 8cc..
-    const int n_chunks = (kend - kbeg + kChunk - 1) / kChunk;
+    const int n_tiles = (kend - kbeg + kTile - 1) / kTile;
 
-    // virtual key -> cache row (clamped into the split so that every load is
-    // of a real row; out-of-range keys are masked)
+    // virtual key -> cache row, clamped into the split so that every load
+    // reads a real row (keys past the split end are masked)
     auto key_row = [&](int v) {
         v = min(v, kend - 1);
         return v < bk.cmax ? v : Tc + (v - bk.cmax);
     };
-    auto load_k = [&](int c, uint4 (&ka)[2][DS]) {
-        const int v0 = kbeg + c * kChunk;
+    // Per-lane parts of the direct-load addresses, fixed for the whole
+    // split: this wave loads K blocks wave + kWaves*i and V slots
+    // (wave + kWaves*i)*64 + lane of every tile.
+    constexpr int KI = KB / kWaves, VJ = VI / kWaves;
+    int k_key[KI], k_off[KI], v_key[VJ], v_off[VJ];
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            const char* kr = kp.row(key_row(v0 + 16 * kt + lr)) + 16 * lg;
+    for (int i = 0; i < KI; ++i) {
+        const int b = wave + kWaves * i;                  // K block (sc, kt, ds)
+        const int ds = b % DS, kt = (b / DS) % 2, sc = b / (2 * DS);
+        k_key[i] = 32 * sc + 16 * kt + lr;
+        k_off[i] = 64 * ds + 16 * lg;
+    }
 #pragma unroll
-            for (int ds = 0; ds < DS; ++ds) ka[kt][ds] = *reinterpret_cast<const uint4*>(kr + 64 * ds);
+    for (int i = 0; i < VJ; ++i) {
+        const int pos = (wave + kWaves * i) * 64 + lane;  // 16-byte slot of the V tile
+        const int key = pos / CH, pc = pos % CH;
+        v_key[i] = key;
+        v_off[i] = 16 * (pc ^ (key & (CH - 1)));          // logical chunk stored at slot pc
+    }
+    const bool contiguous = kp.table == nullptr && vp.table == nullptr;
+    const int fast_end = min(kend, bk.cmax);              // rows here are the keys themselves
+
+    // this wave's share of tile t, straight into LDS stage t % kStages
+    auto issue_tile = [&](int t) {
+        unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
+        const int tb = kbeg + t * kTile;
+        if (contiguous && tb + kTile <= fast_end) {
+            // the whole tile is cached rows tb.., one 64-bit add per load
+            const char* kt0 = kp.base + (int64_t)tb * kp.row_bytes;
+            const char* vt0 = vp.base + (int64_t)tb * vp.row_bytes;
+#pragma unroll
+            for (int i = 0; i < KI; ++i)
+                load_lds16(kt0 + k_key[i] * kp.row_bytes + k_off[i], st + (wave + kWaves * i) * 1024);
+#pragma unroll
+            for (int i = 0; i < VJ; ++i)
+                load_lds16(vt0 + v_key[i] * vp.row_bytes + v_off[i],
+                           st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
+        } else {
+#pragma unroll
+            for (int i = 0; i < KI; ++i)
+                load_lds16(kp.row(key_row(tb + k_key[i])) + k_off[i], st + (wave + kWaves * i) * 1024);
+#pragma unroll
+            for (int i = 0; i < VJ; ++i)
+                load_lds16(vp.row(key_row(tb + v_key[i])) + v_off[i],
+                           st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
         }
     };
-    auto load_v = [&](int c, uint4 (&va)[4][VCH]) {
-        const int v0 = kbeg + c * kChunk;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const char* vr = vp.row(key_row(v0 + 4 * kg + i)) + 16 * cc;
-#pragma unroll
-            for (int j = 0; j < VCH; ++j) va[i][j] = *reinterpret_cast<const uint4*>(vr + 128 * j);
-        }
-    };
 
-    // K of the next chunk is prefetched into registers one iteration ahead;
-    // V of the current chunk is requested at the top of the iteration and
-    // lands while the K Q^T products run
-    uint4 ka[2][DS];
-    if (kw < n_chunks) load_k(kw, ka);
+#pragma unroll
+    for (int t = 0; t < kStages - 1; ++t)
+        if (t < n_tiles) issue_tile(t);
 
-    for (int c = kw; c < n_chunks; c += kKW) {
-        const int v0 = kbeg + c * kChunk;
-        uint4 va[4][VCH];
-        load_v(c, va);
-        uint4 kn[2][DS];
-        const bool has_next = c + kKW < n_chunks;
-        if (has_next) load_k(c + kKW, kn);
+    for (int t = 0; t < n_tiles; ++t) {
+        // this wave's loads of tile t are done when at most those of the
+        // next kStages-2 tiles are still outstanding; the barrier makes every
+        // wave's part visible and frees the stage of tile t-1 for tile
+        // t+kStages-1
+        const int ahead = min(kStages - 2, n_tiles - 1 - t);
+        if (ahead >= 2) wait_vm<2 * LPW>(); else if (ahead == 1) wait_vm<LPW>(); else wait_vm<0>();
+        __syncthreads();
+        if (t + kStages - 1 < n_tiles) issue_tile(t + kStages - 1);
 
-        // S^T = K Q^T
-        floatx4 sacc[2][kRT];
+        const unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
+        const unsigned char* vt = st + Smem<D>::k_bytes;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) {
-                floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ds = 0; ds < DS; ++ds)
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[kt][ds]), qB[rt][ds],
-                                                                  acc, 0, 0, 0);
-                sacc[kt][rt] = acc;
-            }
+        for (int sc = 0; sc < 2; ++sc) {
+            const int v0 = kbeg + t * kTile + 32 * sc;
+            if (v0 >= kend) break;
 
-        // transpose V through the wave's LDS tile: row d holds the 32 keys of
-        // dim d; a lane writes keys 4kg..4kg+3 of 8 dims.  The fence orders
-        // these writes after the previous chunk's reads of the tile.
-        wave_lds_fence();
+            // S^T = K Q^T
+            floatx4 sacc[2][kRT];
 #pragma unroll
-        for (int j = 0; j < VCH; ++j) {
-            const uint32_t w0[4] = {va[0][j].x, va[0][j].y, va[0][j].z, va[0][j].w};
-            const uint32_t w1[4] = {va[1][j].x, va[1][j].y, va[1][j].z, va[1][j].w};
-            const uint32_t w2[4] = {va[2][j].x, va[2][j].y, va[2][j].z, va[2][j].w};
-            const uint32_t w3[4] = {va[3][j].x, va[3][j].y, va[3][j].z, va[3][j].w};
+            for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int wi = e >> 1;
-                uint32_t a, b;
-                if (e & 1) {
-                    a = __builtin_amdgcn_perm(w1[wi], w0[wi], 0x07060302u);
-                    b = __builtin_amdgcn_perm(w3[wi], w2[wi], 0x07060302u);
-                } else {
-                    a = __builtin_amdgcn_perm(w1[wi], w0[wi], 0x05040100u);
-                    b = __builtin_amdgcn_perm(w3[wi], w2[wi], 0x05040100u);
+                for (int rt = 0; rt < kRT; ++rt) sacc[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ds = 0; ds < DS; ++ds) {
+                    const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(
+                        st + ((sc * 2 + kt) * DS + ds) * 1024 + lane * 16));
+#pragma unroll
+                    for (int rt = 0; rt < kRT; ++rt)
+                        sacc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qB[rt][ds],
+                                                                               sacc[kt][rt], 0, 0, 0);
                 }
-                const int d = 8 * cc + 64 * j + e;
-                *reinterpret_cast<uint2*>(vt + d * kVtStride + 8 * kg) = uint2{a, b};
             }
-        }
 
-        // mask (only chunks that reach past what every row of the block sees)
-        if (v0 + kChunk > vis_min) {
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int v = v0 + 16 * kt + 4 * lg + i;
+            // mask, by the kind of sub-tile (wave-uniform): keys below every
+            // row's visible prefix need none; keys in the cached region need
+            // v < lo; keys in the new-token region need v <= hi; a sub-tile
+            // across cmax needs both tests.  Lane group g holds key offsets
+            // 16kt + 4g + i of the sub-tile.
+            const int vb = v0 + 4 * lg;
+            if (v0 + 32 > wave_vis_min) {
+                if (v0 + 32 <= bk.cmax) {
 #pragma unroll
                     for (int rt = 0; rt < kRT; ++rt) {
-                        const bool ok = v < lo[rt] || (v >= bk.cmax && v <= hi[rt]);
-                        sacc[kt][rt][i] = ok ? sacc[kt][rt][i] : -INFINITY;
+                        const int t_lo = lo[rt] - vb;
+#pragma unroll
+                        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                sacc[kt][rt][i] = 16 * kt + i < t_lo ? sacc[kt][rt][i] : -INFINITY;
+                    }
+                } else if (v0 >= bk.cmax) {
+#pragma unroll
+                    for (int rt = 0; rt < kRT; ++rt) {
+                        const int t_hi = hi[rt] - vb;
+#pragma unroll
+                        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                sacc[kt][rt][i] = 16 * kt + i <= t_hi ? sacc[kt][rt][i] : -INFINITY;
+                    }
+                } else {
+#pragma unroll
+                    for (int rt = 0; rt < kRT; ++rt) {
+                        const int t_lo = lo[rt] - vb, t_c = bk.cmax - vb, t_hi = hi[rt] - vb;
+#pragma unroll
+                        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const int o = 16 * kt + i;
+                                const bool ok = o < t_lo || (o >= t_c && o <= t_hi);
+                                sacc[kt][rt][i] = ok ? sacc[kt][rt][i] : -INFINITY;
+                            }
                     }
                 }
-        }
+            }
 
-        // online softmax in base 2 with a lazily raised maximum
-        float mx[kRT];
-        bool over = false;
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            mx[rt] = fmaxf(fmaxf(fmaxf(sacc[0][rt][0], sacc[0][rt][1]), fmaxf(sacc[0][rt][2], sacc[0][rt][3])),
-                           fmaxf(fmaxf(sacc[1][rt][0], sacc[1][rt][1]), fmaxf(sacc[1][rt][2], sacc[1][rt][3])));
-            over |= mx[rt] * c2 > m[rt] + kTau;
-        }
-        if (__builtin_amdgcn_ballot_w64(over)) {
+            // online softmax in base 2 with a lazily raised maximum: the
+            // slow path runs only if some raw score exceeds thr = (m + kTau)
+            // / scale_log2
+            float mx[kRT];
+            bool over = false;
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt) {
-                float r = mx[rt];
-                r = fmaxf(r, __shfl_xor(r, 16));
-                r = fmaxf(r, __shfl_xor(r, 32));
-                const float m_new = fmaxf(m[rt], r * c2);
-                const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
-                m[rt] = m_new;
-                lsum[rt] *= alpha;
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+                mx[rt] = fmaxf(fmaxf(fmaxf(sacc[0][rt][0], sacc[0][rt][1]),
+                                     fmaxf(sacc[0][rt][2], sacc[0][rt][3])),
+                               fmaxf(fmaxf(sacc[1][rt][0], sacc[1][rt][1]),
+                                     fmaxf(sacc[1][rt][2], sacc[1][rt][3])));
+                over |= mx[rt] > thr[rt];
             }
-        }
-        uint32_t pk[kRT][4];
+            if (__builtin_amdgcn_ballot_w64(over)) {
 #pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            float pr[2][4];
+                for (int rt = 0; rt < kRT; ++rt) {
+                    float r = mx[rt];
+                    r = fmaxf(r, __shfl_xor(r, 16));
+                    r = fmaxf(r, __shfl_xor(r, 32));
+                    const float m_new = fmaxf(m[rt], r * c2);
+                    const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
+                    m[rt] = m_new;
+                    thr[rt] = (m_new + kTau) / c2;
+                    lsum[rt] *= alpha;
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
+                    for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+                }
+            }
+            uint32_t pk[kRT][4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    pr[kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][rt][i], c2, -m[rt]));
-            lsum[rt] += ((pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3])) +
-                        ((pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]));
-            pk[rt][0] = pack_bf16(pr[0][0], pr[0][1]);
-            pk[rt][1] = pack_bf16(pr[0][2], pr[0][3]);
-            pk[rt][2] = pack_bf16(pr[1][0], pr[1][1]);
-            pk[rt][3] = pack_bf16(pr[1][2], pr[1][3]);
-        }
+            for (int rt = 0; rt < kRT; ++rt) {
+                float pr[2][4];
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        pr[kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][rt][i], c2, -m[rt]));
+                lsum[rt] += ((pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3])) +
+                            ((pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]));
+                pk[rt][0] = pack_bf16(pr[0][0], pr[0][1]);
+                pk[rt][1] = pack_bf16(pr[0][2], pr[0][3]);
+                pk[rt][2] = pack_bf16(pr[1][0], pr[1][1]);
+                pk[rt][3] = pack_bf16(pr[1][2], pr[1][3]);
+            }
 
-        // O^T += V^T P^T
-        wave_lds_fence();
+            // O^T += V^T P^T.  For a 16-lane block, the transpose read gives
+            // lane i element i%4 of the 4-element rows supplied by lanes
+            // 4k + i/4 (k = 0..3); lane j therefore supplies key
+            // 32sc + 16h + 4lg + j/4, dims 16dt + 4(j%4).., so that lane i
+            // receives keys 4lg+k (k = 0..3) of dim 16dt + i.
+            uint32_t va[DT][2];
+            uint2 vr[DT][2];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const unsigned char* row = vt + (16 * dt + lr) * kVtStride + 8 * lg;
-            const uint2 lo8 = *reinterpret_cast<const uint2*>(row);
-            const uint2 hi8 = *reinterpret_cast<const uint2*>(row + 32);
-            const bf16x8 a = as_bf16x8(uint4{lo8.x, lo8.y, hi8.x, hi8.y});
+            for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int rt = 0; rt < kRT; ++rt)
-                o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
-                    0, 0, 0);
-        }
-
-        if (has_next) {
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int key = 32 * sc + 16 * hh + 4 * lg + (lr >> 2);
+                    const int c = 2 * dt + ((lr >> 1) & 1);
+                    va[dt][hh] = lds_addr(vt + key * (2 * D) + 16 * (c ^ (key & (CH - 1))) +
+                                          8 * (lr & 1));
+                }
+            read_vt<DT>(va, vr);
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
+            for (int dt = 0; dt < DT; ++dt) {
+                const uint2* half = vr[dt];
+                const bf16x8 a = as_bf16x8(uint4{half[0].x, half[0].y, half[1].x, half[1].y});
 #pragma unroll
-                for (int ds = 0; ds < DS; ++ds) ka[kt][ds] = kn[kt][ds];
+                for (int rt = 0; rt < kRT; ++rt)
+                    o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
+                        0, 0, 0);
+            }
         }
     }
 
@@ -322,63 +463,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         lsum[rt] += __shfl_xor(lsum[rt], 32);
     }
 
-    // merge the key waves of each row group
-    constexpr int RW = kRB / kRG;                   // rows per row group
-    float* s_m = reinterpret_cast<float*>(smem + Smem<D>::ml_off);
-    float* s_l = s_m + kWaves * RW;
-    __syncthreads();                                // every wave is done with its V^T tile
-    if (lg == 0) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            s_m[wave * RW + 16 * rt + lr] = m[rt];
-            s_l[wave * RW + 16 * rt + lr] = lsum[rt];
-        }
-    }
-    __syncthreads();
-    float Mrow[kRT], Lrow[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        const int row = 16 * rt + lr;
-        float M = kNoMax;
-#pragma unroll
-        for (int w = 0; w < kKW; ++w) M = fmaxf(M, s_m[(rg * kKW + w) * RW + row]);
-        float L = 0.f;
-#pragma unroll
-        for (int w = 0; w < kKW; ++w)
-            L += s_l[(rg * kKW + w) * RW + row] *
-                 __builtin_amdgcn_exp2f(s_m[(rg * kKW + w) * RW + row] - M);
-        const float f = __builtin_amdgcn_exp2f(m[rt] - M);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= f;
-        Mrow[rt] = M;
-        Lrow[rt] = L;
-    }
-    constexpr int SLOT = Smem<D>::slot / 4;         // floats
-    float* slot = reinterpret_cast<float*>(smem) + rg * 2 * SLOT;
-    auto store_slot = [&](float* sl) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt)
-                *reinterpret_cast<floatx4*>(sl + ((dt * kRT + rt) * 64 + lane) * 4) = o[dt][rt];
-    };
-    auto add_slot = [&](const float* sl) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt)
-                o[dt][rt] += *reinterpret_cast<const floatx4*>(sl + ((dt * kRT + rt) * 64 + lane) * 4);
-    };
-    if (kw >= 2) store_slot(slot + (kw - 2) * SLOT);
-    __syncthreads();
-    if (kw < 2) add_slot(slot + kw * SLOT);
-    __syncthreads();
-    if (kw == 1) store_slot(slot);
-    __syncthreads();
-    if (kw != 0) return;
-    add_slot(slot);
-
-    // key wave 0 of each row group writes the group's rows
+    // each wave writes its own rows
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         if (tok[rt] < 0) continue;
@@ -386,14 +471,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         const int64_t orow = (int64_t)(n0 + tok[rt]) * p.n_q_heads + h * G + rho % G;
         if (p.n_splits == 1) {
             bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + orow * D;
-            const float inv = 1.f / Lrow[rt];
+            const float inv = 1.f / lsum[rt];
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
                 const floatx4 v = o[dt][rt];
                 *reinterpret_cast<uint2*>(out + 16 * dt + 4 * lg) =
                     uint2{pack_bf16(v[0] * inv, v[1] * inv), pack_bf16(v[2] * inv, v[3] * inv)};
             }
-            if (p.lse && lg == 0) p.lse[orow] = (Mrow[rt] + log2f(Lrow[rt])) * kLn2;
+            if (p.lse && lg == 0) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
         } else {
             const int64_t pi = orow * p.n_splits + split;
             float* po = p.part_o + pi * D;
@@ -401,14 +486,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
             for (int dt = 0; dt < DT; ++dt)
                 *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = o[dt][rt];
             if (lg == 0) {
-                p.part_ml[pi * 2] = Mrow[rt];
-                p.part_ml[pi * 2 + 1] = Lrow[rt];
+                p.part_ml[pi * 2] = m[rt];
+                p.part_ml[pi * 2 + 1] = lsum[rt];
             }
         }
     }
 }
 
 }  // namespace
+
+int attend_mfma_row_block() { return kRB; }
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, dim3 grid, hipStream_t stream) {
     if (head_dim == 128)
