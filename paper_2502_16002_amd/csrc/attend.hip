@@ -41,7 +41,7 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
     const T* __restrict__ q_new, const T* __restrict__ k_new, const T* __restrict__ v_new,
     T* __restrict__ q_rot, View k, View v, int layer, int n_seqs, int n_q_heads, int n_kv_heads,
     const int32_t* __restrict__ seq_new_ptr, const int32_t* __restrict__ seq_cached,
-    const int32_t* __restrict__ new_pos, double theta) {
+    const int32_t* __restrict__ new_pos, RopeFreqs freqs) {
     constexpr int H = D / 2;
     constexpr int E = 16 / (int)sizeof(T);
     constexpr int TPV = H / E;               // threads per head vector
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
     const int n = blockIdx.x;
     const int s = seq_of(seq_new_ptr, n_seqs, n);
     const int row = seq_cached[s] + (n - seq_new_ptr[s]);
-    for (int j = threadIdx.x; j < H; j += 256) rope_cos_sin(new_pos[n], j, D, theta, &s_cos[j], &s_sin[j]);
+    for (int j = threadIdx.x; j < H; j += 256) rope_cos_sin(new_pos[n], j, freqs, &s_cos[j], &s_sin[j]);
     __syncthreads();
     const int sub = threadIdx.x % TPV;
     float c[E], sn[E];
@@ -213,9 +213,13 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 
 // ------------------------------------------------------------- combine
 
+// One wavefront per (new token, query head) row.  The maximum over the
+// splits is taken first (lane-strided), then the splits are accumulated four
+// at a time with all their loads issued together, so the row costs a few
+// memory round trips instead of two per split.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total) {
-    constexpr int DPL = D / 64;
+    constexpr int DPL = D / 64;   // consecutive dims per lane
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int64_t orow = (int64_t)blockIdx.x * 4 + wave;   // (n, hq) flattened
     if (orow >= (int64_t)n_new_total * p.n_q_heads) return;
@@ -227,25 +231,44 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     const int rho0 = rho / p.row_block * p.row_block;
     const BlockKeys bk = block_keys(p.new_visible, n0, rows_s, rho0, p.row_block, p.group);
     const int nsp = (bk.nvirt + p.split_keys - 1) / p.split_keys;
+    const float* ml = p.part_ml + orow * p.n_splits * 2;
+    const float* po = p.part_o + orow * p.n_splits * D + lane * DPL;
 
     float M = -INFINITY;
-    for (int c = 0; c < nsp; ++c) M = fmaxf(M, p.part_ml[(orow * p.n_splits + c) * 2]);
+    for (int c = lane; c < nsp; c += 64) M = fmaxf(M, ml[2 * c]);
+    M = wave_max(M);
+
     float L = 0.f, acc[DPL];
 #pragma unroll
-    for (int dd = 0; dd < DPL; ++dd) acc[dd] = 0.f;
-    for (int c = 0; c < nsp; ++c) {
-        const int64_t pi = orow * p.n_splits + c;
-        const float mc = p.part_ml[pi * 2];
-        if (mc == -INFINITY) continue;
-        const float w = exp2f(mc - M);
-        L += w * p.part_ml[pi * 2 + 1];
+    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+    int c = 0;
+    for (; c + 4 <= nsp; c += 4) {
+        float mc[4], lc[4], oc[4][DPL];
 #pragma unroll
-        for (int dd = 0; dd < DPL; ++dd) acc[dd] += w * p.part_o[pi * D + lane + 64 * dd];
+        for (int u = 0; u < 4; ++u) {
+            mc[u] = ml[2 * (c + u)];
+            lc[u] = ml[2 * (c + u) + 1];
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) oc[u][e] = po[(c + u) * D + e];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float w = __builtin_amdgcn_exp2f(mc[u] - M);   // 0 for an empty split
+            L += w * lc[u];
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) acc[e] += w * oc[u][e];
+        }
     }
-    T* out = reinterpret_cast<T*>(p.out);
+    for (; c < nsp; ++c) {
+        const float w = __builtin_amdgcn_exp2f(ml[2 * c] - M);
+        L += w * ml[2 * c + 1];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[e] += w * po[c * D + e];
+    }
+    T* out = reinterpret_cast<T*>(p.out) + orow * D + lane * DPL;
     const float inv = 1.f / L;
 #pragma unroll
-    for (int dd = 0; dd < DPL; ++dd) out[orow * D + lane + 64 * dd] = from_f32<T>(acc[dd] * inv);
+    for (int e = 0; e < DPL; ++e) out[e] = from_f32<T>(acc[e] * inv);
     if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * kLn2;
 }
 
@@ -280,7 +303,7 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
                        reinterpret_cast<const T*>(a.q_new), reinterpret_cast<const T*>(a.k_new),
                        reinterpret_cast<const T*>(a.v_new), q_rot, a.k, a.v, a.layer, pl.n_seqs,
                        pl.n_q_heads, pl.n_kv_heads, a.seq_new_ptr, a.seq_cached, a.new_pos,
-                       a.theta);
+                       a.freqs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 

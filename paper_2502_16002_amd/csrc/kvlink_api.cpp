@@ -67,6 +67,31 @@ kvlink::View to_view(const kvlink_kv_view& v) {
 
 }  // namespace
 
+namespace kvlink {
+
+RopeFreqs make_rope_freqs(double theta, int head_dim) {
+    RopeFreqs f;
+    for (int j = 0; j < 64; ++j)
+        f.w[j] = j < head_dim / 2
+                     ? (double)powl((long double)theta, -2.0L * j / (long double)head_dim)
+                     : 0.0;
+    // pi/2 = p0 + p1 + p2 with p0, p1 of 22 significant bits each
+    const long double pio2 = acosl(0.0L);
+    auto trunc22 = [](long double v) {
+        int e;
+        const long double m = frexpl(v, &e);
+        return ldexpl(floorl(ldexpl(m, 22)), e - 22);
+    };
+    const long double p0 = trunc22(pio2);
+    const long double p1 = trunc22(pio2 - p0);
+    f.pio2[0] = (double)p0;
+    f.pio2[1] = (double)p1;
+    f.pio2[2] = (double)(pio2 - p0 - p1);
+    return f;
+}
+
+}  // namespace kvlink
+
 extern "C" {
 
 kvlink_status kvlink_build_layout(int32_t n_seqs, const int32_t* seq_doc_ptr,
@@ -185,7 +210,8 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
         kvlink_status st = check_view(src, dtype, "src");
         if (st != KVLINK_OK) return st;
         if ((st = check_view(dst, dtype, "dst")) != KVLINK_OK) return st;
-        hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads, rope_theta,
+        hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads,
+                                               kvlink::make_rope_freqs(rope_theta, head_dim),
                                                n_spans, d_spans, max_span_len, to_view(src),
                                                to_view(dst), reinterpret_cast<hipStream_t>(stream));
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "re-encode launch: %s", hipGetErrorString(e));
@@ -266,7 +292,7 @@ kvlink_status kvlink_attend_new_tokens(
         a.seq_cached = d_seq_cached;
         a.new_pos = d_new_pos;
         a.new_visible = d_new_visible;
-        a.theta = rope_theta;
+        a.freqs = kvlink::make_rope_freqs(rope_theta, head_dim);
         a.scale = softmax_scale;
         a.out = out;
         a.lse = lse;

@@ -124,21 +124,60 @@ __device__ __forceinline__ RowPtr row_ptr(const View& v, int layer, int head, in
     return r;
 }
 
-// cos and sin of pos * theta^(-2j/d): the angle is formed and reduced in
-// double precision, then rounded to float.
-__device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, int d, double theta,
-                                             float* c, float* s) {
-    const double w = pow(theta, -2.0 * (double)j / (double)d);
-    double sd, cd;
-    sincos((double)pos * w, &sd, &cd);
-    *c = (float)cd;
-    *s = (float)sd;
+// RoPE frequencies of one (theta, head_dim): w[j] = theta^(-2j/d) for
+// j < d/2, and pi/2 split into three parts for the argument reduction
+// (pio2[0] and pio2[1] carry 22 significant bits each, so n * pio2[k] is
+// exact for |n| < 2^31; the sum matches pi/2 to about 64 bits).  Built on the
+// host in long double (make_rope_freqs) and passed by value to the kernels.
+struct RopeFreqs {
+    double w[64];
+    double pio2[3];
+};
+
+RopeFreqs make_rope_freqs(double theta, int head_dim);
+
+// cos and sin of the RoPE angle pos * w[j] (Sec. 2.2), computed in double
+// precision in registers, then rounded to float: Cody-Waite reduction of the
+// angle by pi/2, Taylor series of sin and cos on the reduced argument
+// (|r| <= pi/4, truncation error below 1e-17), and the quadrant.
+__device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, const RopeFreqs& f, float* c,
+                                             float* s) {
+    const double x = (double)pos * f.w[j];
+    const double n = rint(x * 0.63661977236758134308);   // x / (pi/2), rounded
+    double r = fma(-n, f.pio2[0], x);
+    r = fma(-n, f.pio2[1], r);
+    r = fma(-n, f.pio2[2], r);
+    const double r2 = r * r;
+    // sin r = r - r^3/3! + ... + r^17/17!, cos r = 1 - r^2/2! + ... + r^16/16!
+    double ps = 1.0 / 355687428096000.0;                  // 1/17!
+    ps = fma(ps, r2, -1.0 / 1307674368000.0);             // 1/15!
+    ps = fma(ps, r2, 1.0 / 6227020800.0);                 // 1/13!
+    ps = fma(ps, r2, -1.0 / 39916800.0);                  // 1/11!
+    ps = fma(ps, r2, 1.0 / 362880.0);                     // 1/9!
+    ps = fma(ps, r2, -1.0 / 5040.0);                      // 1/7!
+    ps = fma(ps, r2, 1.0 / 120.0);                        // 1/5!
+    ps = fma(ps, r2, -1.0 / 6.0);                         // 1/3!
+    const double sr = fma(ps * r2, r, r);
+    double pc = 1.0 / 20922789888000.0;                   // 1/16!
+    pc = fma(pc, r2, -1.0 / 87178291200.0);               // 1/14!
+    pc = fma(pc, r2, 1.0 / 479001600.0);                  // 1/12!
+    pc = fma(pc, r2, -1.0 / 3628800.0);                   // 1/10!
+    pc = fma(pc, r2, 1.0 / 40320.0);                      // 1/8!
+    pc = fma(pc, r2, -1.0 / 720.0);                       // 1/6!
+    pc = fma(pc, r2, 1.0 / 24.0);                         // 1/4!
+    pc = fma(pc, r2, -0.5);                               // 1/2!
+    const double cr = fma(pc, r2, 1.0);
+    const int q = (int)((long long)n & 3);
+    const double sv = q == 0 ? sr : q == 1 ? cr : q == 2 ? -sr : -cr;
+    const double cv = q == 0 ? cr : q == 1 ? -sr : q == 2 ? -cr : sr;
+    *c = (float)cv;
+    *s = (float)sv;
 }
 
 // ---------------------------------------------------------------- launchers
 
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
-                           double theta, int n_spans, const kvlink_span* spans,
+                           const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
                            int max_span_len, const View& src, const View& dst,
                            hipStream_t stream);
 
@@ -166,7 +205,7 @@ struct AttendArgs {
     const int32_t* seq_cached;
     const int32_t* new_pos;
     const int32_t* new_visible;
-    double theta;
+    RopeFreqs freqs;
     float scale;
     void* out;
     float* lse;

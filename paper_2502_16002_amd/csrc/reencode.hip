@@ -11,8 +11,9 @@
 //     on them;
 //   * a workgroup owns up to kRows rows of one document for kLH (layer, head)
 //     pairs, so the document's cos/sin table is built once (double-precision
-//     angles, in LDS) and then held in registers: each thread always handles
-//     the same slice of the rotation pairs;
+//     angles reduced and evaluated in registers, stored to LDS) and then held
+//     in registers: each thread always handles the same slice of the rotation
+//     pairs;
 //   * each thread moves 16-byte vectors: the slice [j0, j0+E) and its partner
 //     slice [j0+d/2, j0+d/2+E), consecutive threads cover one row, then the
 //     next row, so a wavefront reads and writes whole contiguous rows;
@@ -32,7 +33,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                                                             const kvlink_span* __restrict__ spans,
                                                             int n_lh, int n_kv_heads,
-                                                            double theta) {
+                                                            RopeFreqs freqs) {
     constexpr int H = D / 2;                 // rotation pairs per vector
     constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte access
     constexpr int TPV = H / E;               // threads per vector
@@ -47,7 +48,7 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     const int nlh = min(kLH, n_lh - lh0);
 
     for (int j = threadIdx.x; j < H; j += kThreads)
-        rope_cos_sin(sp.delta, j, D, theta, &s_cos[j], &s_sin[j]);
+        rope_cos_sin(sp.delta, j, freqs, &s_cos[j], &s_sin[j]);
     __syncthreads();
 
     const int sub = threadIdx.x % TPV;
@@ -98,33 +99,33 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 }
 
 template <typename T, int D>
-hipError_t launch(int n_layers, int n_kv_heads, double theta, int n_spans,
+hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_spans,
                   const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
                   hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
     dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
     hipLaunchKernelGGL((reencode_kernel<T, D>), grid, dim3(kThreads), 0, stream, src, dst, spans,
-                       n_lh, n_kv_heads, theta);
+                       n_lh, n_kv_heads, freqs);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
-                           double theta, int n_spans, const kvlink_span* spans,
+                           const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
                            int max_span_len, const View& src, const View& dst,
                            hipStream_t stream) {
     if (dt == KVLINK_BF16) {
         if (head_dim == 128)
-            return launch<bf16_t, 128>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len,
+            return launch<bf16_t, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len,
                                        src, dst, stream);
-        return launch<bf16_t, 64>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src,
+        return launch<bf16_t, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
                                   dst, stream);
     }
     if (head_dim == 128)
-        return launch<float, 128>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src,
+        return launch<float, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
                                   dst, stream);
-    return launch<float, 64>(n_layers, n_kv_heads, theta, n_spans, spans, max_span_len, src, dst,
+    return launch<float, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src, dst,
                              stream);
 }
 
