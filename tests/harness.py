@@ -113,3 +113,102 @@ class ContiguousRun:
         q, kn, vn = workloads.request_new(w, ld, 0)
         f = lambda x: workloads.as_f64(w, x)
         return f(kc), f(vc), f(q), f(kn), f(vn)
+
+
+# ------------------------------------------------------------------- paged
+
+
+class PagedRun:
+    """The shared-pool workload: stored document caches live once in a paged
+    pool (pages placed by the workload's permutation); every request gets
+    re-encoded K copies in its own pages, and reads V straight from the pool
+    pages of its documents through its V block table (values are never
+    rewritten), with fresh pages after them for its new tokens."""
+
+    def __init__(self, w, split_keys=0, device="cuda", seed=11):
+        import torch
+        from paper_2502_16002_amd.runtime import Batch, dtype_code, paged_view
+        assert w.pool
+        self.w = w
+        L, H, d, P = w.n_layers, w.n_kv_heads, w.head_dim, w.page_size
+        rng = np.random.default_rng(seed)
+        self.lds = [workloads.layer_data(w, l) for l in range(L)]
+        doc_pages = [(n + P - 1) // P for n in w.doc_table_len]
+        assert all(n % P == 0 for n in w.doc_table_len)
+        n_pool_pages = sum(doc_pages)
+        perm = w.pool_page_perm
+        first = np.concatenate([[0], np.cumsum(doc_pages)[:-1]])
+        max_doc_pages = max(doc_pages)
+        pool_table = np.zeros((len(w.doc_table_len), max_doc_pages), np.int32)
+        for j, (f, npg) in enumerate(zip(first, doc_pages)):
+            pool_table[j, :npg] = perm[f:f + npg]
+        self.pool_table = torch.from_numpy(pool_table).to(device)
+
+        sdp = np.concatenate([[0], np.cumsum([len(x) for x in w.docs])]).astype(np.int32)
+        dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
+        lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
+        src_seq = [j for s in range(w.n_seqs) for j in w.docs[s]]
+        self.batch = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
+                           sdp, dl, lc, w.n_query, doc_src_seq=src_seq,
+                           doc_src_row=[0] * len(dl), split_keys=split_keys, device=device)
+        b = self.batch
+        td = b.torch_dtype
+        # pool tensors [L][page][H][P][d]; V gets extra fresh pages for new tokens
+        max_new_pages = (b.max_new + P - 1) // P
+        n_fresh = w.n_seqs * max_new_pages
+        self.k_pool = torch.zeros((L, n_pool_pages, H, P, d), dtype=td, device=device)
+        self.v_all = torch.zeros((L, n_pool_pages + n_fresh, H, P, d), dtype=td, device=device)
+        row0 = workloads.doc_row0(w)
+        for l, ld in enumerate(self.lds):
+            for j, n in enumerate(w.doc_table_len):
+                k = to_torch(w, ld.k_store[:, row0[j]:row0[j] + n], device)   # [H][n][d]
+                v = to_torch(w, ld.v_store[:, row0[j]:row0[j] + n], device)
+                for pg in range(doc_pages[j]):
+                    phys = int(pool_table[j, pg])
+                    self.k_pool[l, phys] = k[:, pg * P:(pg + 1) * P]
+                    self.v_all[l, phys] = v[:, pg * P:(pg + 1) * P]
+        # per-request K pages (shuffled) and V tables (pool pages, then fresh)
+        seq_cached = b.layout["seq_cached"]
+        self.max_pages = max(int((seq_cached[s] + w.n_new(s) + P - 1) // P) for s in range(w.n_seqs))
+        k_table = rng.permutation(w.n_seqs * self.max_pages).astype(np.int32).reshape(w.n_seqs, -1)
+        v_table = np.zeros((w.n_seqs, self.max_pages), np.int32)
+        for s in range(w.n_seqs):
+            pages = [int(pool_table[j, pg]) for j in w.docs[s] for pg in range(doc_pages[j])]
+            assert len(pages) * P == seq_cached[s]
+            fresh = n_pool_pages + s * max_new_pages + np.arange(self.max_pages - len(pages))
+            v_table[s] = np.concatenate([pages, fresh]).astype(np.int32)
+        self.k_table_np, self.v_table_np = k_table, v_table
+        self.k_table = torch.from_numpy(k_table).to(device)
+        self.v_table = torch.from_numpy(v_table).to(device)
+        self.k_dst = torch.zeros((L, w.n_seqs * self.max_pages, H, P, d), dtype=td, device=device)
+        self.src_view = paged_view(self.k_pool, n_pool_pages, H, P, d, self.pool_table, max_doc_pages)
+        self.k_view = paged_view(self.k_dst, w.n_seqs * self.max_pages, H, P, d, self.k_table,
+                                 self.max_pages)
+        self.v_view = paged_view(self.v_all, n_pool_pages + n_fresh, H, P, d, self.v_table,
+                                 self.max_pages)
+        self.q = [to_torch(w, ld.q_new, device) for ld in self.lds]
+        self.kn = [to_torch(w, ld.k_new, device) for ld in self.lds]
+        self.vn = [to_torch(w, ld.v_new, device) for ld in self.lds]
+        self.out = [b.new_out() for _ in range(L)]
+        self.lse = [b.new_lse() for _ in range(L)]
+
+    def run(self):
+        import torch
+        self.batch.reencode(self.src_view, self.k_view)
+        for l in range(self.w.n_layers):
+            self.batch.attend(l, self.q[l], self.kn[l], self.vn[l], self.k_view, self.v_view,
+                              self.out[l], self.lse[l])
+        torch.cuda.synchronize()
+
+    def request_rows(self, table, s, rows):
+        """(page, slot) of logical rows of request s under a block table."""
+        P = self.w.page_size
+        rows = np.asarray(rows)
+        return table[s, rows // P], rows % P
+
+    def oracle_inputs(self, l, s):
+        w, ld = self.w, self.lds[l]
+        kc, vc = workloads.request_cache(w, ld, s)
+        q, kn, vn = workloads.request_new(w, ld, s)
+        f = lambda x: workloads.as_f64(w, x)
+        return f(kc), f(vc), f(q), f(kn), f(vn)

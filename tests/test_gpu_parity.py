@@ -212,3 +212,41 @@ def test_run_twice_is_bitwise_identical():
     first = run.out[0].clone()
     run.run()
     assert torch.equal(first.view(torch.int16), run.out[0].view(torch.int16))
+
+
+# ---------------------------------------------------------------- paged pool
+
+
+def test_paged_pool_reencode_and_attention():
+    """Shared 64-document pool in 16-token pages, 16 requests: per-request
+    re-encoded K copies in shuffled pages, V read from the pool pages."""
+    from harness import PagedRun
+    w = workloads.llama8b_paged()
+    run = PagedRun(w)
+    run.run()
+    b = run.batch
+    k_dst = to_f64(run.k_dst[0])                       # [pages][H][P][d]
+    rng = np.random.default_rng(9)
+    for s in [0, 5, 15]:
+        kc, vc, q, kn, vn = run.oracle_inputs(0, s)
+        d0, d1 = int(np.sum([len(x) for x in w.docs[:s]])), None
+        spans = b.layout["spans"][d0:d0 + len(w.docs[s])]
+        for sp in spans[[0, 7, 19]]:
+            rows = np.arange(sp[3], sp[3] + sp[4])
+            pg, slot = run.request_rows(run.k_table_np, s, rows)
+            got = k_dst[pg, :, slot, :].transpose(1, 0, 2)      # [H][n][d]
+            ref = oracle.reencode(kc[:, rows], int(sp[5]), w.rope_theta)
+            check_close(w, got, ref, f"paged re-encode request {s}")
+            check_bf16_rounding(got, ref, f"paged re-encode request {s}")
+        n0, n1 = int(b.layout["seq_new_ptr"][s]), int(b.layout["seq_new_ptr"][s + 1])
+        rows = np.sort(rng.choice(n1 - n0, 12, replace=False))
+        ref, ref_lse = oracle.attend(w.doc_len(s), w.link_count[s], w.n_query[s], q, kn, vn, kc,
+                                     vc, w.rope_theta, w.scale, rows=rows)
+        got = to_f64(run.out[0])[n0 + rows]
+        check_close(w, got, ref, f"paged attention request {s}")
+        lse = to_f64(run.lse[0])[n0 + rows]
+        assert float(np.max(np.abs(lse - ref_lse))) <= 2e-2
+    # values in the pool pages are untouched
+    ld = run.lds[0]
+    assert np.array_equal(to_f64(run.v_all[0, int(run.pool_table[3, 2])]),
+                          workloads.as_f64(w, ld.v_store[:, 3 * 256 + 32:3 * 256 + 48]).reshape(8, 16, 128))
