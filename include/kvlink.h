@@ -242,6 +242,21 @@ kvlink_status kvlink_attend_new_tokens(
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
     void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * kvlink_attend_split_keys — host-side choice of split_keys for
+ * kvlink_attend_new_tokens from the batch's layout (outputs of
+ * kvlink_build_layout: seq_new_ptr[n_seqs+1], new_visible[n_new]) and the
+ * device's compute-unit count.  It estimates, for every candidate split
+ * size, the makespan of the split workgroups over the compute units (each
+ * workgroup costs a fixed overhead plus a per-64-key tile cost) plus the
+ * traffic of the split partials, and returns the cheapest candidate (a
+ * positive multiple of 128).  Returns 0 (meaning "use the library default")
+ * for invalid input; never fails otherwise.  Pure host computation.
+ */
+int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int32_t n_seqs, const int32_t* seq_new_ptr,
+                                 const int32_t* new_visible, int32_t n_compute_units);
+
 /* Message of the last non-OK status on the calling thread ("" if none). */
 const char* kvlink_last_error(void);
 

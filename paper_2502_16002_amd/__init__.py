@@ -65,6 +65,8 @@ def _load():
         vp, vp, vp, vp, vp, vp, vp, kvlink_kv_view, kvlink_kv_view, i32, vp, vp, i32,
         vp, sz, vp]
     lib.kvlink_attend_new_tokens.restype = ctypes.c_int
+    lib.kvlink_attend_split_keys.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, i32]
+    lib.kvlink_attend_split_keys.restype = i32
     lib.kvlink_last_error.restype = ctypes.c_char_p
     lib.kvlink_version.restype = ctypes.c_char_p
     return lib
@@ -169,6 +171,16 @@ def kvlink_attend_workspace_bytes(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs
     return int(_lib.kvlink_attend_workspace_bytes(int(dtype), int(n_q_heads), int(n_kv_heads),
                                                   int(head_dim), int(n_seqs), int(n_new_total),
                                                   int(max_new), int(max_cached), int(split_keys)))
+
+
+def kvlink_attend_split_keys(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, new_visible,
+                             n_compute_units):
+    """Host-side split size for the batch (0: invalid input)."""
+    snp = np.ascontiguousarray(np.asarray(seq_new_ptr, dtype=np.int32))
+    vis = np.ascontiguousarray(np.asarray(new_visible, dtype=np.int32))
+    return int(_lib.kvlink_attend_split_keys(int(dtype), int(n_q_heads), int(n_kv_heads),
+                                             int(head_dim), len(snp) - 1, _ptr(snp), _ptr(vis),
+                                             int(n_compute_units)))
 
 
 def kvlink_attend_new_tokens(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,

@@ -5,7 +5,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <string>
+#include <vector>
 
 #include "kvlink_internal.h"
 
@@ -302,6 +304,82 @@ kvlink_status kvlink_attend_new_tokens(
         return ok();
     } catch (...) {
         return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_attend_new_tokens");
+    }
+}
+
+int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int32_t n_seqs, const int32_t* seq_new_ptr,
+                                 const int32_t* new_visible, int32_t n_compute_units) {
+    try {
+        if (!dtype_ok(dtype) || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
+            (head_dim != 64 && head_dim != 128) || n_seqs < 1 || !seq_new_ptr || !new_visible ||
+            n_compute_units < 1)
+            return 0;
+        const int group = n_q_heads / n_kv_heads;
+        int max_new = 0;
+        for (int s = 0; s < n_seqs; ++s) max_new = std::max(max_new, seq_new_ptr[s + 1] - seq_new_ptr[s]);
+        if (max_new < 1) return 0;
+        kvlink::AttendPlan pl;
+        if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs,
+                                      seq_new_ptr[n_seqs], max_new, 0, 128, &pl))
+            return 0;
+        // virtual key count of every row block (the same for every KV head)
+        std::vector<int64_t> nvirt;
+        int64_t max_keys = 0, rows_total = 0;
+        for (int s = 0; s < n_seqs; ++s) {
+            const int n0 = seq_new_ptr[s], rows_s = (seq_new_ptr[s + 1] - n0) * group;
+            rows_total += rows_s;
+            for (int rho0 = 0; rho0 < rows_s; rho0 += pl.row_block) {
+                const int r_last = (std::min(rho0 + pl.row_block, rows_s) - 1) / group;
+                const int64_t nv = (int64_t)new_visible[n0 + r_last] + r_last + 1;
+                nvirt.push_back(nv);
+                max_keys = std::max(max_keys, nv);
+            }
+        }
+        // cost model (microseconds), fitted to MI355X timings of the 10- and
+        // 40-document Llama-8B-shaped workloads over split sizes 128..4096:
+        // a workgroup costs a fixed 5 us plus 2.2 us per 64-key tile, with an
+        // effective two workgroups in flight per compute unit; partial
+        // traffic at an effective 4 TB/s
+        const double fixed = 5.0, per_tile = pl.use_mfma ? (head_dim == 128 ? 2.2 : 1.4) : 1.0;
+        const int slots = 2 * n_compute_units;
+        double best = 1e300;
+        int32_t best_sk = 128;
+        std::vector<double> load(slots);
+        std::vector<double> jobs;
+        for (int64_t sk = 128; sk < max_keys + 128; sk += 128) {
+            jobs.clear();
+            int64_t max_splits = 1;
+            for (int64_t nv : nvirt) {
+                const int64_t n = (nv + sk - 1) / sk;
+                max_splits = std::max(max_splits, n);
+                for (int64_t c = 0; c < n; ++c) {
+                    const int64_t keys = std::min(sk, nv - c * sk);
+                    for (int h = 0; h < n_kv_heads; ++h) jobs.push_back(fixed + per_tile * ((keys + 63) / 64));
+                }
+            }
+            // longest job first onto the least loaded slot
+            std::sort(jobs.begin(), jobs.end(), std::greater<double>());
+            std::fill(load.begin(), load.end(), 0.0);
+            std::make_heap(load.begin(), load.end(), std::greater<double>());
+            for (double j : jobs) {
+                std::pop_heap(load.begin(), load.end(), std::greater<double>());
+                load.back() += j;
+                std::push_heap(load.begin(), load.end(), std::greater<double>());
+            }
+            double t = *std::max_element(load.begin(), load.end());
+            if (max_splits > 1)
+                t += 3.0 + 2.0 * (double)rows_total * n_kv_heads * max_splits * (head_dim + 2) * 4.0 /
+                               4.0e6;
+            if (t < best * 0.98) {   // prefer fewer splits on near ties
+                best = t;
+                best_sk = (int32_t)sk;
+            }
+            if (max_splits == 1) break;
+        }
+        return best_sk;
+    } catch (...) {
+        return 0;
     }
 }
 

@@ -21,7 +21,8 @@ import numpy as np
 import torch
 
 from . import (KVLINK_BF16, KVLINK_F32, SPAN_FIELDS, kv_view, kvlink_attend_new_tokens,
-               kvlink_attend_workspace_bytes, kvlink_build_layout, kvlink_reencode_keys)
+               kvlink_attend_split_keys, kvlink_attend_workspace_bytes, kvlink_build_layout,
+               kvlink_reencode_keys)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
@@ -70,6 +71,12 @@ class Batch:
         self.set_split_keys(split_keys)
 
     def set_split_keys(self, split_keys):
+        """split_keys 0 plans the split size from the layout and the device."""
+        if split_keys == 0 and self.n_new > 0:
+            cus = torch.cuda.get_device_properties(torch.device(self.device)).multi_processor_count
+            split_keys = kvlink_attend_split_keys(self.dtype, self.n_q_heads, self.n_kv_heads,
+                                                  self.head_dim, self.layout["seq_new_ptr"],
+                                                  self.layout["new_visible"], cus)
         self.split_keys = split_keys
         self.ws_bytes = kvlink_attend_workspace_bytes(self.dtype, self.n_q_heads, self.n_kv_heads,
                                                       self.head_dim, self.n_seqs, self.n_new,

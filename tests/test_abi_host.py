@@ -227,3 +227,22 @@ def test_workspace_bytes(kv):
     assert f(kv.KVLINK_BF16, 32, 8, 128, 1, 114, 114, 2000, 100) == 0
     # more splits need more partial storage
     assert f(kv.KVLINK_F32, 4, 2, 64, 1, 22, 22, 96, 128) >= f(kv.KVLINK_F32, 4, 2, 64, 1, 22, 22, 96, 1024)
+
+
+def test_split_planner(kv):
+    """The host split planner returns a positive multiple of 128 for valid
+    layouts, no more than the longest row block needs, and 0 on bad input."""
+    for name in ["tiny-f32-3x32", "llama8b-32layer-10doc", "llama8b-32layer-40x512",
+                 "llama8b-paged-16req"]:
+        w = workloads.get(name)
+        sdp = np.concatenate([[0], np.cumsum([len(d) for d in w.docs])])
+        dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
+        lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
+        L = kv.kvlink_build_layout(sdp, dl, lc, w.n_query)
+        dt = kv.KVLINK_F32 if w.dtype == "f32" else kv.KVLINK_BF16
+        sk = kv.kvlink_attend_split_keys(dt, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                         L["seq_new_ptr"], L["new_visible"], 256)
+        assert sk > 0 and sk % 128 == 0
+        assert sk < int(L["totals"][5]) + 128
+    assert kv.kvlink_attend_split_keys(kv.KVLINK_BF16, 32, 8, 96, [0, 4], [1, 2, 3, 4], 256) == 0
+    assert kv.kvlink_attend_split_keys(kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 0) == 0
