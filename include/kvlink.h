@@ -257,6 +257,32 @@ int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t 
                                  int32_t head_dim, int32_t n_seqs, const int32_t* seq_new_ptr,
                                  const int32_t* new_visible, int32_t n_compute_units);
 
+/*
+ * kvlink_attend_stages — kvlink_attend_new_tokens run stage by stage, with
+ * identical arguments plus a bit mask of the stages to launch:
+ *   KVLINK_STAGE_ROPE     steps 1 and 2 (RoPE of the new tokens, append of
+ *                         their keys and values, rotated q to the workspace)
+ *   KVLINK_STAGE_SPLIT    step 3 over every key split (writes the output
+ *                         directly when one split covers every row block,
+ *                         split partials to the workspace otherwise)
+ *   KVLINK_STAGE_COMBINE  log-sum-exp merge of the split partials into out
+ *                         and lse (no launch when there is one split)
+ * Stages must run in this order, on the same stream, with the same workspace
+ * and arguments; kvlink_attend_new_tokens is all three.  For callers that
+ * time or overlap the stages separately.  Errors as kvlink_attend_new_tokens,
+ * plus KVLINK_ERR_INVALID_ARG for an empty or unknown mask.
+ */
+enum { KVLINK_STAGE_ROPE = 1, KVLINK_STAGE_SPLIT = 2, KVLINK_STAGE_COMBINE = 4 };
+
+kvlink_status kvlink_attend_stages(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages);
+
 /* Message of the last non-OK status on the calling thread ("" if none). */
 const char* kvlink_last_error(void);
 

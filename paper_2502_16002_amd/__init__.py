@@ -15,6 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkvlink.so")
 
 KVLINK_F32, KVLINK_BF16 = 0, 1
+KVLINK_STAGE_ROPE, KVLINK_STAGE_SPLIT, KVLINK_STAGE_COMBINE = 1, 2, 4
+KVLINK_STAGE_ALL = 7
 STATUS = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_LAYOUT",
           4: "ERR_WORKSPACE", 5: "ERR_HIP"}
 
@@ -65,6 +67,8 @@ def _load():
         vp, vp, vp, vp, vp, vp, vp, kvlink_kv_view, kvlink_kv_view, i32, vp, vp, i32,
         vp, sz, vp]
     lib.kvlink_attend_new_tokens.restype = ctypes.c_int
+    lib.kvlink_attend_stages.argtypes = lib.kvlink_attend_new_tokens.argtypes + [ctypes.c_uint32]
+    lib.kvlink_attend_stages.restype = ctypes.c_int
     lib.kvlink_attend_split_keys.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, i32]
     lib.kvlink_attend_split_keys.restype = i32
     lib.kvlink_last_error.restype = ctypes.c_char_p
@@ -194,3 +198,17 @@ def kvlink_attend_new_tokens(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta,
         _ptr(d_seq_new_ptr), _ptr(d_seq_cached), _ptr(d_new_pos), _ptr(d_new_visible),
         _ptr(q_new), _ptr(k_new), _ptr(v_new), k_cache, v_cache, int(layer), _ptr(out),
         _ptr(lse), int(split_keys), _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def kvlink_attend_stages(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
+                         n_seqs, n_new_total, max_new, max_cached, d_seq_new_ptr, d_seq_cached,
+                         d_new_pos, d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer,
+                         out, lse, split_keys, workspace, workspace_bytes, stream=None,
+                         stages=KVLINK_STAGE_ALL):
+    _check(_lib.kvlink_attend_stages(
+        int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), float(rope_theta),
+        float(softmax_scale), int(n_seqs), int(n_new_total), int(max_new), int(max_cached),
+        _ptr(d_seq_new_ptr), _ptr(d_seq_cached), _ptr(d_new_pos), _ptr(d_new_visible),
+        _ptr(q_new), _ptr(k_new), _ptr(v_new), k_cache, v_cache, int(layer), _ptr(out),
+        _ptr(lse), int(split_keys), _ptr(workspace), int(workspace_bytes), _stream(stream),
+        int(stages)))

@@ -32,10 +32,12 @@ using namespace attn;
 
 // --------------------------------------------------------------- prologue
 
-// One workgroup per new token: the token's cos/sin table (double-precision
-// angles) goes to LDS, then every q head and every k head is rotated with
-// 16-byte accesses (q to the workspace, k to the cache row T_c + r) and the v
-// heads are copied to the same cache row.
+// One workgroup per new token.  The token's q, k and v vectors are requested
+// first (they do not depend on the layout), then the token's cos/sin table is
+// built (double-precision angles, in registers, stored to LDS) while they are
+// in flight; every q head and k head is rotated with 16-byte accesses (q to
+// the workspace, k to the cache row T_c + r) and the v heads are copied to
+// the same cache row.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_new_kernel(
     const T* __restrict__ q_new, const T* __restrict__ k_new, const T* __restrict__ v_new,
@@ -45,13 +47,38 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
     constexpr int H = D / 2;
     constexpr int E = 16 / (int)sizeof(T);
     constexpr int TPV = H / E;               // threads per head vector
+    constexpr int HPP = 256 / TPV;           // head vectors per pass
+    constexpr int kPre = 2;                  // passes whose loads are issued up front
+    constexpr int VPH = D / E;               // 16-byte vectors per v head
     __shared__ float s_cos[H], s_sin[H];
     const int n = blockIdx.x;
+    const int nh = n_q_heads + n_kv_heads;
+    const int sub = threadIdx.x % TPV;
+    auto src_of = [&](int hv) {
+        return hv < n_q_heads ? q_new + ((int64_t)n * n_q_heads + hv) * D
+                              : k_new + ((int64_t)n * n_kv_heads + (hv - n_q_heads)) * D;
+    };
+    uint4 lo[kPre], hi[kPre], vv = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+        const int hv = threadIdx.x / TPV + u * HPP;
+        if (hv < nh) {
+            const T* src = src_of(hv);
+            lo[u] = *reinterpret_cast<const uint4*>(src + sub * E);
+            hi[u] = *reinterpret_cast<const uint4*>(src + H + sub * E);
+        }
+    }
+    const bool has_v = threadIdx.x < n_kv_heads * VPH;
+    if (has_v) {
+        const int hk = threadIdx.x / VPH, cch = threadIdx.x % VPH;
+        vv = *reinterpret_cast<const uint4*>(v_new + ((int64_t)n * n_kv_heads + hk) * D + cch * E);
+    }
+
     const int s = seq_of(seq_new_ptr, n_seqs, n);
     const int row = seq_cached[s] + (n - seq_new_ptr[s]);
-    for (int j = threadIdx.x; j < H; j += 256) rope_cos_sin(new_pos[n], j, freqs, &s_cos[j], &s_sin[j]);
+    const int pos = new_pos[n];
+    for (int j = threadIdx.x; j < H; j += 256) rope_cos_sin(pos, j, freqs, &s_cos[j], &s_sin[j]);
     __syncthreads();
-    const int sub = threadIdx.x % TPV;
     float c[E], sn[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -60,20 +87,12 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
     }
     T* kb = reinterpret_cast<T*>(k.base);
     T* vb = reinterpret_cast<T*>(v.base);
-    for (int hv = threadIdx.x / TPV; hv < n_q_heads + n_kv_heads; hv += 256 / TPV) {
-        const T* src;
-        T* dst;
-        if (hv < n_q_heads) {
-            src = q_new + ((int64_t)n * n_q_heads + hv) * D;
-            dst = q_rot + ((int64_t)n * n_q_heads + hv) * D;
-        } else {
-            const int hk = hv - n_q_heads;
-            src = k_new + ((int64_t)n * n_kv_heads + hk) * D;
-            dst = kb + view_offset(k, layer, hk, s, row);
-        }
+    auto rotate_store = [&](int hv, const uint4& l4, const uint4& h4) {
+        T* dst = hv < n_q_heads ? q_rot + ((int64_t)n * n_q_heads + hv) * D
+                                : kb + view_offset(k, layer, hv - n_q_heads, s, row);
         float a[E], b[E], x[E], y[E];
-        unpack16<T>(*reinterpret_cast<const uint4*>(src + sub * E), a);
-        unpack16<T>(*reinterpret_cast<const uint4*>(src + H + sub * E), b);
+        unpack16<T>(l4, a);
+        unpack16<T>(h4, b);
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             x[e] = a[e] * c[e] - b[e] * sn[e];
@@ -81,9 +100,22 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
         }
         *reinterpret_cast<uint4*>(dst + sub * E) = pack16<T>(x);
         *reinterpret_cast<uint4*>(dst + H + sub * E) = pack16<T>(y);
+    };
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+        const int hv = threadIdx.x / TPV + u * HPP;
+        if (hv < nh) rotate_store(hv, lo[u], hi[u]);
     }
-    constexpr int VPH = D / E;               // 16-byte vectors per v head
-    for (int i = threadIdx.x; i < n_kv_heads * VPH; i += 256) {
+    for (int hv = threadIdx.x / TPV + kPre * HPP; hv < nh; hv += HPP) {
+        const T* src = src_of(hv);
+        rotate_store(hv, *reinterpret_cast<const uint4*>(src + sub * E),
+                     *reinterpret_cast<const uint4*>(src + H + sub * E));
+    }
+    if (has_v) {
+        const int hk = threadIdx.x / VPH, cch = threadIdx.x % VPH;
+        *reinterpret_cast<uint4*>(vb + view_offset(v, layer, hk, s, row) + cch * E) = vv;
+    }
+    for (int i = threadIdx.x + 256; i < n_kv_heads * VPH; i += 256) {
         const int hk = i / VPH, cch = i % VPH;
         *reinterpret_cast<uint4*>(vb + view_offset(v, layer, hk, s, row) + cch * E) =
             *reinterpret_cast<const uint4*>(v_new + ((int64_t)n * n_kv_heads + hk) * D + cch * E);
@@ -275,7 +307,8 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 template <typename T, int D>
-hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t stream) {
+hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t stream,
+                        unsigned stages) {
     char* ws = reinterpret_cast<char*>(a.workspace);
     T* q_rot = reinterpret_cast<T*>(ws);
     KParams p;
@@ -299,23 +332,29 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.out = a.out;
     p.lse = a.lse;
 
-    hipLaunchKernelGGL((rope_new_kernel<T, D>), dim3(pl.n_new_total), dim3(256), 0, stream,
-                       reinterpret_cast<const T*>(a.q_new), reinterpret_cast<const T*>(a.k_new),
-                       reinterpret_cast<const T*>(a.v_new), q_rot, a.k, a.v, a.layer, pl.n_seqs,
-                       pl.n_q_heads, pl.n_kv_heads, a.seq_new_ptr, a.seq_cached, a.new_pos,
-                       a.freqs);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-
-    const int n_rb = (pl.max_new * pl.group + pl.row_block - 1) / pl.row_block;
-    dim3 grid(pl.n_splits, n_rb, pl.n_seqs * pl.n_kv_heads);
-    if (pl.use_mfma) {
-        e = launch_attend_mfma(D, p, grid, stream);
-    } else {
-        hipLaunchKernelGGL((attend_valu_kernel<T, D>), grid, dim3(256), 0, stream, p);
+    hipError_t e = hipSuccess;
+    if (stages & KVLINK_STAGE_ROPE) {
+        hipLaunchKernelGGL((rope_new_kernel<T, D>), dim3(pl.n_new_total), dim3(256), 0, stream,
+                           reinterpret_cast<const T*>(a.q_new), reinterpret_cast<const T*>(a.k_new),
+                           reinterpret_cast<const T*>(a.v_new), q_rot, a.k, a.v, a.layer,
+                           pl.n_seqs, pl.n_q_heads, pl.n_kv_heads, a.seq_new_ptr, a.seq_cached,
+                           a.new_pos, a.freqs);
         e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    if (e != hipSuccess || pl.n_splits == 1) return e;
+
+    if (stages & KVLINK_STAGE_SPLIT) {
+        const int n_rb = (pl.max_new * pl.group + pl.row_block - 1) / pl.row_block;
+        dim3 grid(pl.n_splits, n_rb, pl.n_seqs * pl.n_kv_heads);
+        if (pl.use_mfma) {
+            e = launch_attend_mfma(D, p, grid, stream);
+        } else {
+            hipLaunchKernelGGL((attend_valu_kernel<T, D>), grid, dim3(256), 0, stream, p);
+            e = hipGetLastError();
+        }
+        if (e != hipSuccess) return e;
+    }
+    if (!(stages & KVLINK_STAGE_COMBINE) || pl.n_splits == 1) return hipSuccess;
 
     const int64_t n_rows = (int64_t)pl.n_new_total * pl.n_q_heads;
     hipLaunchKernelGGL((combine_kernel<T, D>), dim3((unsigned)((n_rows + 3) / 4)), dim3(256), 0,
@@ -371,12 +410,12 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
 }
 
 hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,
-                         hipStream_t stream) {
+                         hipStream_t stream, unsigned stages) {
     if (dt == KVLINK_BF16)
-        return p.head_dim == 128 ? launch_typed<bf16_t, 128>(p, a, stream)
-                                 : launch_typed<bf16_t, 64>(p, a, stream);
-    return p.head_dim == 128 ? launch_typed<float, 128>(p, a, stream)
-                             : launch_typed<float, 64>(p, a, stream);
+        return p.head_dim == 128 ? launch_typed<bf16_t, 128>(p, a, stream, stages)
+                                 : launch_typed<bf16_t, 64>(p, a, stream, stages);
+    return p.head_dim == 128 ? launch_typed<float, 128>(p, a, stream, stages)
+                             : launch_typed<float, 64>(p, a, stream, stages);
 }
 
 }  // namespace kvlink

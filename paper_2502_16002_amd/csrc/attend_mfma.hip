@@ -182,52 +182,67 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     const int split = blockIdx.x;
     const int s = blockIdx.z / p.n_kv_heads, h = blockIdx.z % p.n_kv_heads;
     const int G = p.group;
+    // request descriptors (independent loads)
     const int n0 = p.seq_new_ptr[s];
     const int rows_s = (p.seq_new_ptr[s + 1] - n0) * G;
+    const int Tc = p.seq_cached[s];
     const int rho0 = blockIdx.y * kRB;
     if (rho0 >= rows_s) return;
-    const BlockKeys bk = block_keys(p.new_visible, n0, rows_s, rho0, kRB, G);
-    const int kbeg = split * p.split_keys;
-    if (kbeg >= bk.nvirt) return;
-    const int kend = min(kbeg + p.split_keys, bk.nvirt);
-    const int Tc = p.seq_cached[s];
-    const float c2 = p.scale_log2;   // > 0
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int rho_w = rho0 + wave * kRT * 16;      // first row of this wave
 
-    // Rows of this lane (one per row tile).  Row r may see virtual key v iff
-    // v < lo (cached rows up to its document, within the split) or
-    // cmax <= v <= hi (new rows up to its own, within the split).
-    int tok[kRT], lo[kRT], hi[kRT];
+    // Everything below depends on n0 only and is requested together before
+    // the split's key range is known: the block's key bound, the visible
+    // prefix of this wave's first token and of every row, and the Q operand.
+    const int r_last = (min(rho0 + kRB, rows_s) - 1) / G;
+    const int cmax = p.new_visible[n0 + r_last];
+    const int wave_vis_min = p.new_visible[n0 + min(rho_w, rows_s - 1) / G];
+    int tok[kRT], vis[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         const int rho = rho_w + 16 * rt + lr;
         tok[rt] = rho < rows_s ? rho / G : -1;
-        const int vis = tok[rt] >= 0 ? p.new_visible[n0 + tok[rt]] : 0;
-        lo[rt] = min(vis, kend);
-        hi[rt] = tok[rt] >= 0 ? min(bk.cmax + tok[rt], kend - 1) : -1;
+        vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
     }
-    // keys below this bound are visible to every row of the wave (its
-    // first token sees the fewest cached rows)
-    const int wave_vis_min = p.new_visible[n0 + min(rho_w, rows_s - 1) / G];
-
-    // Q^T operand, loaded once
     const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
-    bf16x8 qB[kRT][DS];
+    uint4 qraw[kRT][DS];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         const int rho = rho_w + 16 * rt + lr;
-        const int tq = max(tok[rt], 0);
-        const int64_t qrow = ((int64_t)(n0 + tq) * p.n_q_heads + h * G + rho % G) * D;
+        const int64_t qrow = ((int64_t)(n0 + max(tok[rt], 0)) * p.n_q_heads + h * G + rho % G) * D;
 #pragma unroll
-        for (int ds = 0; ds < DS; ++ds) {
-            uint4 v = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
-            if (tok[rt] < 0) v = uint4{0u, 0u, 0u, 0u};
-            qB[rt][ds] = as_bf16x8(v);
-        }
+        for (int ds = 0; ds < DS; ++ds)
+            qraw[rt][ds] = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
     }
+
+    // the block's virtual key range: cached rows its last token sees, then
+    // the new rows up to its last token; this workgroup's split of it
+    BlockKeys bk;
+    bk.r_last = r_last;
+    bk.cmax = cmax;
+    bk.nvirt = cmax + r_last + 1;
+    const int kbeg = split * p.split_keys;
+    if (kbeg >= bk.nvirt) return;
+    const int kend = min(kbeg + p.split_keys, bk.nvirt);
+    const float c2 = p.scale_log2;   // > 0
+
+    // Row r may see virtual key v iff v < lo (cached rows up to its document,
+    // within the split) or cmax <= v <= hi (new rows up to its own, within
+    // the split).
+    int lo[kRT], hi[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) {
+        lo[rt] = tok[rt] >= 0 ? min(vis[rt], kend) : 0;
+        hi[rt] = tok[rt] >= 0 ? min(bk.cmax + tok[rt], kend - 1) : -1;
+    }
+    bf16x8 qB[kRT][DS];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+            qB[rt][ds] = as_bf16x8(tok[rt] >= 0 ? qraw[rt][ds] : uint4{0u, 0u, 0u, 0u});
 
     floatx4 o[DT][kRT];
 #pragma unroll

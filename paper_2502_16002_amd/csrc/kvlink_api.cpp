@@ -234,15 +234,18 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
     return p.total_bytes;
 }
 
-kvlink_status kvlink_attend_new_tokens(
+kvlink_status kvlink_attend_stages(
     kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
     double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
-    void* workspace, size_t workspace_bytes, void* stream) {
+    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages) {
     try {
+        const uint32_t all = KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE;
+        if (stages == 0 || (stages & ~all))
+            return fail(KVLINK_ERR_INVALID_ARG, "stage mask %u", (unsigned)stages);
         if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
         if (head_dim != 64 && head_dim != 128)
             return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
@@ -299,12 +302,29 @@ kvlink_status kvlink_attend_new_tokens(
         a.out = out;
         a.lse = lse;
         a.workspace = workspace;
-        hipError_t e = kvlink::launch_attend(dtype, plan, a, reinterpret_cast<hipStream_t>(stream));
+        hipError_t e =
+            kvlink::launch_attend(dtype, plan, a, reinterpret_cast<hipStream_t>(stream), stages);
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
         return ok();
     } catch (...) {
-        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_attend_new_tokens");
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_attend_stages");
     }
+}
+
+kvlink_status kvlink_attend_new_tokens(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    void* workspace, size_t workspace_bytes, void* stream) {
+    return kvlink_attend_stages(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
+                                n_seqs, n_new_total, max_new, max_cached, d_seq_new_ptr,
+                                d_seq_cached, d_new_pos, d_new_visible, q_new, k_new, v_new,
+                                k_cache, v_cache, layer, out, lse, split_keys, workspace,
+                                workspace_bytes, stream,
+                                KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE);
 }
 
 int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,

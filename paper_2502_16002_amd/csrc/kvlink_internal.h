@@ -213,6 +213,6 @@ struct AttendArgs {
 };
 
 hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,
-                         hipStream_t stream);
+                         hipStream_t stream, unsigned stages);
 
 }  // namespace kvlink

@@ -20,9 +20,9 @@ innermost):
 import numpy as np
 import torch
 
-from . import (KVLINK_BF16, KVLINK_F32, SPAN_FIELDS, kv_view, kvlink_attend_new_tokens,
-               kvlink_attend_split_keys, kvlink_attend_workspace_bytes, kvlink_build_layout,
-               kvlink_reencode_keys)
+from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
+               kvlink_attend_new_tokens, kvlink_attend_split_keys, kvlink_attend_stages,
+               kvlink_attend_workspace_bytes, kvlink_build_layout, kvlink_reencode_keys)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
@@ -91,14 +91,19 @@ class Batch:
                              self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
                              src_view, dst_view, stream)
 
-    def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None):
-        """RoPE + append of the new tokens and their attention, one layer."""
-        kvlink_attend_new_tokens(self.dtype, self.n_q_heads, self.n_kv_heads, self.head_dim,
-                                 self.rope_theta, self.softmax_scale, self.n_seqs, self.n_new,
-                                 self.max_new, self.max_cached, self.d_seq_new_ptr,
-                                 self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
-                                 k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys,
-                                 self.workspace, self.ws_bytes, stream)
+    def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None,
+               stages=KVLINK_STAGE_ALL):
+        """RoPE + append of the new tokens and their attention, one layer
+        (all stages, or the ones named by the stage mask)."""
+        args = (self.dtype, self.n_q_heads, self.n_kv_heads, self.head_dim, self.rope_theta,
+                self.softmax_scale, self.n_seqs, self.n_new, self.max_new, self.max_cached,
+                self.d_seq_new_ptr, self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
+                k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys, self.workspace,
+                self.ws_bytes, stream)
+        if stages == KVLINK_STAGE_ALL:
+            kvlink_attend_new_tokens(*args)
+        else:
+            kvlink_attend_stages(*args, stages=stages)
 
     def new_out(self):
         return torch.empty((self.n_new, self.n_q_heads, self.head_dim), dtype=self.torch_dtype,

@@ -216,6 +216,18 @@ def test_attend_validation(kv, change, status):
     assert kv.kvlink_last_error()
 
 
+@pytest.mark.parametrize("stages", [0, 8, 15])
+def test_attend_stages_rejects_bad_masks(kv, stages):
+    a = _attend_args(kv)
+    with pytest.raises(kv.KVLinkError) as e:
+        kv.kvlink_attend_stages(a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"],
+                                a["n_seqs"], a["n_new"], a["max_new"], a["max_cached"], a["snp"],
+                                a["sc"], a["pos"], a["vis"], a["q"], a["k"], a["v"], a["kview"],
+                                a["vview"], a["layer"], a["out"], a["lse"], a["split"], a["ws"],
+                                a["ws_bytes"], stream=0, stages=stages)
+    assert e.value.status == 1
+
+
 def test_attend_no_new_tokens_is_a_no_op(kv):
     _call_attend(kv, _attend_args(kv, n_new=0, max_new=0))
 

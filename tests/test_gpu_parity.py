@@ -214,6 +214,27 @@ def test_run_twice_is_bitwise_identical():
     assert torch.equal(first.view(torch.int16), run.out[0].view(torch.int16))
 
 
+@pytest.mark.parametrize("split", [0, 256])
+def test_stage_by_stage_matches_all_stages(split):
+    """The three stages launched one call at a time give the same bits as the
+    single call."""
+    import torch
+    from paper_2502_16002_amd import (KVLINK_STAGE_COMBINE, KVLINK_STAGE_ROPE,
+                                      KVLINK_STAGE_SPLIT)
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[0], split_keys=split)
+    run.run()
+    first, first_lse = run.out[0].clone(), run.lse[0].clone()
+    run.out[0].zero_()
+    run.lse[0].zero_()
+    for st in [KVLINK_STAGE_ROPE, KVLINK_STAGE_SPLIT, KVLINK_STAGE_COMBINE]:
+        run.batch.attend(0, run.q[0], run.kn[0], run.vn[0], run.k_view, run.v_view, run.out[0],
+                         run.lse[0], stages=st)
+    torch.cuda.synchronize()
+    assert torch.equal(first.view(torch.int16), run.out[0].view(torch.int16))
+    assert torch.equal(first_lse, run.lse[0])
+
+
 # ---------------------------------------------------------------- paged pool
 
 
