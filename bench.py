@@ -13,6 +13,7 @@ the algorithmic HBM GB/s, TFLOP/s and the roofline fraction of the dominant
 kernel, and the CPU oracle timed on a bounded sample as a reported baseline.
 """
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -29,6 +30,15 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16
 VALU_F32_PEAK_TFLOPS = 157.3
 
 METRIC = "µs/layer and HBM GB/s for re-encode+new-token attention at 8B shape; % roofline"
+
+CSRC = os.path.join(ROOT, "paper_2502_16002_amd", "csrc")
+# sources that decide each kernel's memory traffic (hashed to tell whether
+# the committed counter figures still describe the kernel that runs)
+KERNEL_SOURCES = {
+    "attend_mfma_kernel": ["attend_mfma.hip", "attend_common.h", "kvlink_internal.h"],
+    "reencode_kernel": ["reencode.hip", "kvlink_internal.h"],
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b-32layer-10doc.md")
 
 
 def parse():
@@ -94,14 +104,74 @@ class Setup:
     def reencode(self, i=0):
         self.batch.reencode(self.src_views[i], self.dst_views[i])
 
-    def attend(self, l, i=0):
+    def attend(self, l, i=0, stages=7, workspace=None):
         self.batch.attend(l, self.q[l], self.kn[l], self.vn[l], self.dst_views[i], self.v_view,
-                          self.out, self.lse)
+                          self.out, self.lse, stages=stages, workspace=workspace)
 
     def step(self):
         self.reencode(0)
         for l in range(self.w.n_layers):
             self.attend(l, 0)
+
+    def time_stages(self, iters):
+        """Average duration of one launch of each attention stage, measured
+        with events on the stream the library launches on (torch's current
+        stream).  Every layer gets its own workspace, so a pass can run the
+        RoPE stage of all layers, then the split attention of all layers,
+        then the combine of all layers, each group back to back between two
+        events; a spin kernel ahead of each pass covers the host's enqueueing
+        so that the events bracket device time, not host launch gaps."""
+        import torch
+        L = self.w.n_layers
+        if not hasattr(self, "ws_layers"):
+            self.ws_layers = [torch.empty_like(self.batch.workspace) for _ in range(L)]
+        tot = {"rope": 0.0, "split": 0.0, "combine": 0.0}
+
+        def one_pass(record):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            ev[0].record()
+            for l in range(L):
+                self.attend(l, stages=1, workspace=self.ws_layers[l])
+            ev[1].record()
+            for l in range(L):
+                self.attend(l, stages=2, workspace=self.ws_layers[l])
+            ev[2].record()
+            for l in range(L):
+                self.attend(l, stages=4, workspace=self.ws_layers[l])
+            ev[3].record()
+            return ev
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        one_pass(False)
+        host_s = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        for _ in range(iters):
+            backlog(2.0 * host_s + 2e-3)
+            ev = one_pass(True)
+            torch.cuda.synchronize()
+            tot["rope"] += ev[0].elapsed_time(ev[1])
+            tot["split"] += ev[1].elapsed_time(ev[2])
+            tot["combine"] += ev[2].elapsed_time(ev[3])
+        return {k: v / (iters * L) for k, v in tot.items()}
+
+
+_SLEEP_CYCLES_PER_S = None
+
+
+def backlog(seconds):
+    """Occupy the current stream for about `seconds` with torch's spin kernel,
+    so that work enqueued after it starts back to back."""
+    import torch
+    global _SLEEP_CYCLES_PER_S
+    if _SLEEP_CYCLES_PER_S is None:
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        torch.cuda._sleep(10_000_000)
+        e.record()
+        torch.cuda.synchronize()
+        _SLEEP_CYCLES_PER_S = 10_000_000 / (s.elapsed_time(e) * 1e-3)
+    torch.cuda._sleep(int(seconds * _SLEEP_CYCLES_PER_S))
 
 
 def algorithmic(w, batch):
@@ -118,9 +188,40 @@ def algorithmic(w, batch):
                 pairs_per_qhead=pairs, cached_tokens=Tc, new_tokens=n_new)
 
 
-def time_region(fn, iters):
+def source_hash(kernel):
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary: rows
+    `| kernel | workload | source hash | fetch bytes | write bytes |`.  None when
+    there is no row for this kernel and workload, or the kernel's sources
+    changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    want = source_hash(kernel)
+    for line in open(TRAFFIC_FILE):
+        cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
+        if len(cells) == 5 and cells[0] == kernel and cells[1] == workload and cells[2] == want:
+            return int(cells[3]) + int(cells[4])
+    return None
+
+
+def time_region(fn, iters, host_ahead=False):
+    """Average device time of fn over iters calls.  With host_ahead, a spin
+    kernel first covers the host's enqueueing so that the region measures
+    back-to-back device execution (used for the isolated kernel timings)."""
     import torch
     torch.cuda.synchronize()
+    if host_ahead:
+        t0 = time.perf_counter()
+        fn(0)
+        torch.cuda.synchronize()
+        backlog(2.0 * (time.perf_counter() - t0) * iters + 2e-3)
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
     for i in range(iters):
@@ -189,36 +290,53 @@ def main():
     it = args.kernel_iters
     for i in range(2):
         st.reencode(i)
-    re_ms = time_region(lambda i: st.reencode(i % 2), it)
-    at_ms = time_region(lambda i: [st.attend(l) for l in range(w.n_layers)], it) / w.n_layers
+    re_ms = time_region(lambda i: st.reencode(i % 2), it, host_ahead=True)
+    at_ms = time_region(lambda i: [st.attend(l) for l in range(w.n_layers)], it,
+                        host_ahead=True) / w.n_layers
+    stage_ms = st.time_stages(max(1, it // 4))
 
     L = w.n_layers
     us_layer = ms_step * 1000.0 / L
     step_bytes = alg["reencode_bytes"] + L * alg["attend_bytes"]
     step_flops = L * alg["attend_flops"]
     re_gbps = alg["reencode_bytes"] / (re_ms * 1e-3) / 1e9
-    at_gbps = alg["attend_bytes"] / (at_ms * 1e-3) / 1e9
-    at_tflops = alg["attend_flops"] / (at_ms * 1e-3) / 1e12
-    ai = alg["attend_flops"] / alg["attend_bytes"]
     peak_flops = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
+    ai = alg["attend_flops"] / alg["attend_bytes"]
     at_bound = "mfma" if ai > peak_flops * 1e12 / (HBM_PEAK_GBPS * 1e9) else "hbm"
+
+    def traffic(kernel):
+        return measured_traffic(kernel, w.name)
+
     re_roof = {"kernel": "reencode_kernel", "bound": "hbm", "achieved": round(re_gbps, 1),
                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(re_gbps / HBM_PEAK_GBPS, 4),
-               "traffic": None, "us_per_launch": round(re_ms * 1000, 2),
+               "traffic": traffic("reencode_kernel"), "us_per_launch": round(re_ms * 1000, 2),
                "bytes_per_launch": alg["reencode_bytes"]}
-    if at_bound == "hbm":
-        at_roof = {"kernel": "attend (rope_new + attention + combine)", "bound": "hbm",
-                   "achieved": round(at_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                   "frac": round(at_gbps / HBM_PEAK_GBPS, 4), "traffic": None}
-    else:
-        at_roof = {"kernel": "attend (rope_new + attention + combine)", "bound": "mfma",
-                   "achieved": round(at_tflops, 2), "peak": peak_flops, "unit": "TFLOP/s",
-                   "frac": round(at_tflops / peak_flops, 4), "traffic": None}
-    at_roof.update({"us_per_launch": round(at_ms * 1000, 2),
-                    "bytes_per_launch": alg["attend_bytes"],
-                    "flops_per_launch": alg["attend_flops"],
-                    "hbm_gbps": round(at_gbps, 1), "tflops": round(at_tflops, 2)})
-    dominant_attend = L * at_ms > re_ms
+
+    def attn_roof(kernel, ms):
+        gbps = alg["attend_bytes"] / (ms * 1e-3) / 1e9
+        tflops = alg["attend_flops"] / (ms * 1e-3) / 1e12
+        if at_bound == "hbm":
+            r = {"kernel": kernel, "bound": "hbm", "achieved": round(gbps, 1),
+                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        else:
+            r = {"kernel": kernel, "bound": "mfma", "achieved": round(tflops, 2),
+                 "peak": peak_flops, "unit": "TFLOP/s", "frac": round(tflops / peak_flops, 4)}
+        r.update({"us_per_launch": round(ms * 1000, 2), "bytes_per_launch": alg["attend_bytes"],
+                  "flops_per_launch": alg["attend_flops"], "hbm_gbps": round(gbps, 1),
+                  "tflops": round(tflops, 2)})
+        return r
+
+    group = w.n_q_heads // w.n_kv_heads
+    mfma = w.dtype == "bf16" and st.batch.max_new * group >= 32   # the library's own choice
+    split_kernel = "attend_mfma_kernel" if mfma else "attend_valu_kernel"
+    at_roof = attn_roof(split_kernel, stage_ms["split"])
+    at_roof["traffic"] = traffic(split_kernel) if split_kernel in KERNEL_SOURCES else None
+    stages = {"rope_new_us": round(stage_ms["rope"] * 1000, 2),
+              "split_attention_us": round(stage_ms["split"] * 1000, 2),
+              "combine_us": round(stage_ms["combine"] * 1000, 2),
+              "all_stages_one_call_us": round(at_ms * 1000, 2),
+              "reencode_us_per_layer": round(re_ms * 1000 / L, 2)}
+    dominant_attend = L * stage_ms["split"] > re_ms
     res = {
         "metric": METRIC,
         "value": round(us_layer, 3),
@@ -242,6 +360,7 @@ def main():
         "tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 3),
         "roofline": at_roof if dominant_attend else re_roof,
         "roofline_other": re_roof if dominant_attend else at_roof,
+        "per_layer_kernels": stages,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, alg)

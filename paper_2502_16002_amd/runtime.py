@@ -92,13 +92,17 @@ class Batch:
                              src_view, dst_view, stream)
 
     def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None,
-               stages=KVLINK_STAGE_ALL):
+               stages=KVLINK_STAGE_ALL, workspace=None):
         """RoPE + append of the new tokens and their attention, one layer
-        (all stages, or the ones named by the stage mask)."""
+        (all stages, or the ones named by the stage mask).  `workspace`
+        replaces the batch's own (at least ws_bytes, 256-byte aligned)."""
+        ws = self.workspace if workspace is None else workspace
+        if ws.numel() * ws.element_size() < self.ws_bytes:
+            raise ValueError("workspace smaller than ws_bytes")
         args = (self.dtype, self.n_q_heads, self.n_kv_heads, self.head_dim, self.rope_theta,
                 self.softmax_scale, self.n_seqs, self.n_new, self.max_new, self.max_cached,
                 self.d_seq_new_ptr, self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
-                k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys, self.workspace,
+                k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys, ws,
                 self.ws_bytes, stream)
         if stages == KVLINK_STAGE_ALL:
             kvlink_attend_new_tokens(*args)
