@@ -34,6 +34,7 @@
 // more than 2^kTau), so the rescale of O and l and the cross-lane reduction
 // are off the common path.
 #include <algorithm>
+#include <type_traits>
 
 #include "attend_common.h"
 
@@ -42,6 +43,8 @@ namespace attn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 
@@ -74,74 +77,71 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8, v);
 }
 
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-    return (uint32_t)from_f32<bf16_t>(a).bits | ((uint32_t)from_f32<bf16_t>(b).bits << 16);
-}
 
 // Transposed reads of the V^T operands of one 32-key sub-tile: r[dt][h] for
-// dt < DT (16-dim tiles) and h in {0, 1} (keys 4g.. and 16+4g..), from the
-// LDS byte addresses a[dt][h].  Issued as one block followed by a single
-// wait on the LDS counter; the results are early-clobber outputs, since a
-// read's data may return while later reads of the block still need their
-// address registers.  The V tile was written by direct-to-LDS loads
+// dt < DT (16-dim tiles) and h in {0, 1} (keys 4g.. and 16+4g..).  a[dt] is
+// the LDS byte address of tile dt's first read; the second half of the keys
+// sits OFF bytes further (an immediate offset).  Issued as one block followed
+// by a single wait on the LDS counter; the results are early-clobber outputs,
+// since a read's data may return while later reads of the block still need
+// their address registers.  The V tile was written by direct-to-LDS loads
 // whose completion the caller has already waited for (vector-memory counter
 // and a workgroup barrier), so no further wait on those loads is needed.
-template <int DT>
-__device__ __forceinline__ void read_vt(const uint32_t (&a)[DT][2], uint2 (&r)[DT][2]);
+template <int DT, int OFF0, int OFF1>
+__device__ __forceinline__ void read_vt(const uint32_t (&a)[DT], uint2 (&r)[DT][2]);
 
 // (The host compilation pass sees only the declarations: the register
 // constraints exist for the GPU target alone.)
-template <>
-__device__ __forceinline__ void read_vt<8>(const uint32_t (&a)[8][2], uint2 (&r)[8][2]) {
+#define KVLINK_TR_READ(o, i, off) "ds_read_b64_tr_b16 %" #o ", %" #i " offset:%" #off "\n\t"
+template <int OFF0, int OFF1>
+__device__ __forceinline__ void read_vt8(const uint32_t (&a)[8], uint2 (&r)[8][2]) {
 #if defined(__HIP_DEVICE_COMPILE__)
     asm volatile(
-        "ds_read_b64_tr_b16 %0, %16\n\t"
-        "ds_read_b64_tr_b16 %1, %17\n\t"
-        "ds_read_b64_tr_b16 %2, %18\n\t"
-        "ds_read_b64_tr_b16 %3, %19\n\t"
-        "ds_read_b64_tr_b16 %4, %20\n\t"
-        "ds_read_b64_tr_b16 %5, %21\n\t"
-        "ds_read_b64_tr_b16 %6, %22\n\t"
-        "ds_read_b64_tr_b16 %7, %23\n\t"
-        "ds_read_b64_tr_b16 %8, %24\n\t"
-        "ds_read_b64_tr_b16 %9, %25\n\t"
-        "ds_read_b64_tr_b16 %10, %26\n\t"
-        "ds_read_b64_tr_b16 %11, %27\n\t"
-        "ds_read_b64_tr_b16 %12, %28\n\t"
-        "ds_read_b64_tr_b16 %13, %29\n\t"
-        "ds_read_b64_tr_b16 %14, %30\n\t"
-        "ds_read_b64_tr_b16 %15, %31\n\t"
+        KVLINK_TR_READ(0, 16, 24) KVLINK_TR_READ(1, 16, 25)
+        KVLINK_TR_READ(2, 17, 24) KVLINK_TR_READ(3, 17, 25)
+        KVLINK_TR_READ(4, 18, 24) KVLINK_TR_READ(5, 18, 25)
+        KVLINK_TR_READ(6, 19, 24) KVLINK_TR_READ(7, 19, 25)
+        KVLINK_TR_READ(8, 20, 24) KVLINK_TR_READ(9, 20, 25)
+        KVLINK_TR_READ(10, 21, 24) KVLINK_TR_READ(11, 21, 25)
+        KVLINK_TR_READ(12, 22, 24) KVLINK_TR_READ(13, 22, 25)
+        KVLINK_TR_READ(14, 23, 24) KVLINK_TR_READ(15, 23, 25)
         "s_waitcnt lgkmcnt(0)"
         : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
           "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1]), "=&v"(r[4][0]), "=&v"(r[4][1]),
           "=&v"(r[5][0]), "=&v"(r[5][1]), "=&v"(r[6][0]), "=&v"(r[6][1]), "=&v"(r[7][0]),
           "=&v"(r[7][1])
-        : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]),
-          "v"(a[3][0]), "v"(a[3][1]), "v"(a[4][0]), "v"(a[4][1]), "v"(a[5][0]), "v"(a[5][1]),
-          "v"(a[6][0]), "v"(a[6][1]), "v"(a[7][0]), "v"(a[7][1])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]),
+          "v"(a[7]), "i"(OFF0), "i"(OFF1)
         : "memory");
 #endif
 }
 
-template <>
-__device__ __forceinline__ void read_vt<4>(const uint32_t (&a)[4][2], uint2 (&r)[4][2]) {
+template <int OFF0, int OFF1>
+__device__ __forceinline__ void read_vt4(const uint32_t (&a)[4], uint2 (&r)[4][2]) {
 #if defined(__HIP_DEVICE_COMPILE__)
     asm volatile(
-        "ds_read_b64_tr_b16 %0, %8\n\t"
-        "ds_read_b64_tr_b16 %1, %9\n\t"
-        "ds_read_b64_tr_b16 %2, %10\n\t"
-        "ds_read_b64_tr_b16 %3, %11\n\t"
-        "ds_read_b64_tr_b16 %4, %12\n\t"
-        "ds_read_b64_tr_b16 %5, %13\n\t"
-        "ds_read_b64_tr_b16 %6, %14\n\t"
-        "ds_read_b64_tr_b16 %7, %15\n\t"
+        KVLINK_TR_READ(0, 8, 12) KVLINK_TR_READ(1, 8, 13)
+        KVLINK_TR_READ(2, 9, 12) KVLINK_TR_READ(3, 9, 13)
+        KVLINK_TR_READ(4, 10, 12) KVLINK_TR_READ(5, 10, 13)
+        KVLINK_TR_READ(6, 11, 12) KVLINK_TR_READ(7, 11, 13)
         "s_waitcnt lgkmcnt(0)"
         : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
           "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1])
-        : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]),
-          "v"(a[3][0]), "v"(a[3][1])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "i"(OFF0), "i"(OFF1)
         : "memory");
 #endif
+}
+#undef KVLINK_TR_READ
+
+template <int DT, int OFF0, int OFF1>
+__device__ __forceinline__ void read_vt(const uint32_t (&a)[DT], uint2 (&r)[DT][2]) {
+    if constexpr (DT == 8) read_vt8<OFF0, OFF1>(a, r);
+    else read_vt4<OFF0, OFF1>(a, r);
+}
+
+// bf16 pair (RNE) of two floats, low half first: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2));
 }
 
 // LDS byte address of a pointer into a __shared__ array (the low 32 bits of
@@ -249,12 +249,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) o[dt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m[kRT], lsum[kRT], thr[kRT];
+    float m[kRT], lsum[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         m[rt] = kNoMax;
         lsum[rt] = 0.f;
-        thr[rt] = -3.0e38f;   // the first finite score takes the slow path
     }
 
     const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
@@ -285,6 +284,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         const int key = pos / CH, pc = pos % CH;
         v_key[i] = key;
         v_off[i] = 16 * (pc ^ (key & (CH - 1)));          // logical chunk stored at slot pc
+    }
+    // per-lane part of the V^T operand reads (see the product below): lane
+    // (lg, lr) reads key 4lg + lr/4 (plus multiples of 16, which leave the
+    // swizzle unchanged), logical chunk 2dt + (lr/2)%2, half lr%2
+    uint32_t v_rel[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int key = 4 * lg + (lr >> 2);
+        const int c = 2 * dt + ((lr >> 1) & 1);
+        v_rel[dt] = key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
     }
     const bool contiguous = kp.table == nullptr && vp.table == nullptr;
     const int fast_end = min(kend, bk.cmax);              // rows here are the keys themselves
@@ -330,11 +339,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         if (t + kStages - 1 < n_tiles) issue_tile(t + kStages - 1);
 
         const unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
-        const unsigned char* vt = st + Smem<D>::k_bytes;
+        // V^T operand addresses of this stage (the sub-tile and key-half
+        // parts are immediate offsets of the reads)
+        uint32_t va[DT];
+        const uint32_t vt = lds_addr(st + Smem<D>::k_bytes);
 #pragma unroll
-        for (int sc = 0; sc < 2; ++sc) {
+        for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
+
+        auto sub_tile = [&](auto sc_const) {
+            constexpr int sc = decltype(sc_const)::value;
             const int v0 = kbeg + t * kTile + 32 * sc;
-            if (v0 >= kend) break;
 
             // S^T = K Q^T
             floatx4 sacc[2][kRT];
@@ -396,68 +410,65 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
                 }
             }
 
-            // online softmax in base 2 with a lazily raised maximum: the
-            // slow path runs only if some raw score exceeds thr = (m + kTau)
-            // / scale_log2
-            float mx[kRT];
+            // online softmax in base 2 with a lazily raised maximum, on
+            // x = s * scale_log2 - m: the slow path (cross-lane maximum,
+            // rescale of O and l) runs only if some x exceeds kTau.  The
+            // maximum is taken over x, the result of a fused multiply-add,
+            // so no NaN-quieting is needed in front of it.
+            float x[kRT][8];
             bool over = false;
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt) {
-                mx[rt] = fmaxf(fmaxf(fmaxf(sacc[0][rt][0], sacc[0][rt][1]),
-                                     fmaxf(sacc[0][rt][2], sacc[0][rt][3])),
-                               fmaxf(fmaxf(sacc[1][rt][0], sacc[1][rt][1]),
-                                     fmaxf(sacc[1][rt][2], sacc[1][rt][3])));
-                over |= mx[rt] > thr[rt];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    x[rt][j] = __builtin_fmaf(sacc[j >> 2][rt][j & 3], c2, -m[rt]);
+                const float mx = fmaxf(fmaxf(fmaxf(x[rt][0], x[rt][1]), fmaxf(x[rt][2], x[rt][3])),
+                                       fmaxf(fmaxf(x[rt][4], x[rt][5]), fmaxf(x[rt][6], x[rt][7])));
+                over |= mx > kTau;
             }
             if (__builtin_amdgcn_ballot_w64(over)) {
+                // from the raw scores: x loses them while m is still kNoMax
 #pragma unroll
                 for (int rt = 0; rt < kRT; ++rt) {
-                    float r = mx[rt];
+                    float r = fmaxf(fmaxf(fmaxf(sacc[0][rt][0], sacc[0][rt][1]),
+                                          fmaxf(sacc[0][rt][2], sacc[0][rt][3])),
+                                    fmaxf(fmaxf(sacc[1][rt][0], sacc[1][rt][1]),
+                                          fmaxf(sacc[1][rt][2], sacc[1][rt][3])));
                     r = fmaxf(r, __shfl_xor(r, 16));
                     r = fmaxf(r, __shfl_xor(r, 32));
                     const float m_new = fmaxf(m[rt], r * c2);
                     const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
                     m[rt] = m_new;
-                    thr[rt] = (m_new + kTau) / c2;
                     lsum[rt] *= alpha;
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        x[rt][j] = __builtin_fmaf(sacc[j >> 2][rt][j & 3], c2, -m_new);
                 }
             }
+            // p = 2^x, packed to bf16 pairs; the row sum adds the rounded
+            // pairs (the weights the product below uses) with dot products
+            // against (1, 1)
             uint32_t pk[kRT][4];
+            const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) {
-                float pr[2][4];
+            for (int rt = 0; rt < kRT; ++rt)
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        pr[kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][rt][i], c2, -m[rt]));
-                lsum[rt] += ((pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3])) +
-                            ((pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]));
-                pk[rt][0] = pack_bf16(pr[0][0], pr[0][1]);
-                pk[rt][1] = pack_bf16(pr[0][2], pr[0][3]);
-                pk[rt][2] = pack_bf16(pr[1][0], pr[1][1]);
-                pk[rt][3] = pack_bf16(pr[1][2], pr[1][3]);
-            }
+                for (int j = 0; j < 4; ++j) {
+                    pk[rt][j] = pack2(__builtin_amdgcn_exp2f(x[rt][2 * j]),
+                                      __builtin_amdgcn_exp2f(x[rt][2 * j + 1]));
+                    lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(
+                        __builtin_bit_cast(bf16x2, pk[rt][j]), ones, lsum[rt], false);
+                }
 
             // O^T += V^T P^T.  For a 16-lane block, the transpose read gives
             // lane i element i%4 of the 4-element rows supplied by lanes
             // 4k + i/4 (k = 0..3); lane j therefore supplies key
             // 32sc + 16h + 4lg + j/4, dims 16dt + 4(j%4).., so that lane i
             // receives keys 4lg+k (k = 0..3) of dim 16dt + i.
-            uint32_t va[DT][2];
             uint2 vr[DT][2];
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int hh = 0; hh < 2; ++hh) {
-                    const int key = 32 * sc + 16 * hh + 4 * lg + (lr >> 2);
-                    const int c = 2 * dt + ((lr >> 1) & 1);
-                    va[dt][hh] = lds_addr(vt + key * (2 * D) + 16 * (c ^ (key & (CH - 1))) +
-                                          8 * (lr & 1));
-                }
-            read_vt<DT>(va, vr);
+            read_vt<DT, 32 * sc * 2 * D, (32 * sc + 16) * 2 * D>(va, vr);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
                 const uint2* half = vr[dt];
@@ -468,7 +479,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
                         a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
                         0, 0, 0);
             }
-        }
+        };
+        sub_tile(std::integral_constant<int, 0>{});
+        if (kbeg + t * kTile + 32 < kend) sub_tile(std::integral_constant<int, 1>{});
     }
 
     // row sums: add the four lane groups that hold each row
@@ -491,7 +504,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
             for (int dt = 0; dt < DT; ++dt) {
                 const floatx4 v = o[dt][rt];
                 *reinterpret_cast<uint2*>(out + 16 * dt + 4 * lg) =
-                    uint2{pack_bf16(v[0] * inv, v[1] * inv), pack_bf16(v[2] * inv, v[3] * inv)};
+                    uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
             }
             if (p.lse && lg == 0) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
         } else {
