@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b-32layer-10doc")
-    ap.add_argument("--split-keys", type=int, default=0)
+    ap.add_argument("--workgroups", type=int, default=0,
+                    help="workgroups of the split attention (0: the library's schedule)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-iters", type=int, default=20)
     return ap.parse_args()
@@ -64,7 +65,7 @@ class Setup:
     """Device buffers of a single-request workload (documents stored back to
     back, concatenated cache with room for the new tokens)."""
 
-    def __init__(self, w, split_keys, device="cuda"):
+    def __init__(self, w, n_workgroups, device="cuda"):
         import torch
         import workloads
         from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
@@ -74,7 +75,7 @@ class Setup:
         docs = w.docs[0]
         self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                                [0, len(docs)], w.doc_len(0), w.link_count[0], w.n_query,
-                               doc_src_row=[int(row0[j]) for j in docs], split_keys=split_keys,
+                               doc_src_row=[int(row0[j]) for j in docs], n_workgroups=n_workgroups,
                                device=device)
         R = int(sum(w.doc_table_len))
         self.cap = cap = b.max_total
@@ -276,10 +277,10 @@ def main():
     w = workloads.get(args.workload)
     if w.pool:
         raise SystemExit("paged workloads are parity cases, not bench lines")
-    st = Setup(w, args.split_keys)
+    st = Setup(w, args.workgroups)
     alg = algorithmic(w, st.batch)
     print(f"# setup done: {w.name} cached={alg['cached_tokens']} new={alg['new_tokens']} "
-          f"splits={st.batch.split_keys}", file=sys.stderr, flush=True)
+          f"workgroups={st.batch.n_workgroups} segments={st.batch.plan.n_segments}", file=sys.stderr, flush=True)
 
     for _ in range(args.warmup):
         st.step()
@@ -355,7 +356,8 @@ def main():
                    "rope_theta": w.rope_theta, "documents": len(w.docs[0]),
                    "link_tokens_per_doc": w.link_count[0][0], "query_tokens": w.n_query[0],
                    "cached_tokens": alg["cached_tokens"], "new_tokens": alg["new_tokens"],
-                   "split_keys": st.batch.split_keys},
+                   "attention_workgroups": st.batch.n_workgroups,
+                   "attention_segments": st.batch.plan.n_segments},
         "hbm_gbps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 3),
         "roofline": at_roof if dominant_attend else re_roof,

@@ -10,6 +10,7 @@
  *
  *   kvlink_build_layout       index maps of the concatenated sequence (host)
  *   kvlink_reencode_keys      K' = R(delta_i) K for every cached key (GPU)
+ *   kvlink_attend_make_plan   balanced split-K schedule of a batch (host)
  *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
  *                             append of their keys/values to the cache and
  *                             split-K GQA attention over the cache (GPU)
@@ -181,13 +182,71 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
                                    kvlink_kv_view src, kvlink_kv_view dst, void* stream);
 
 /*
- * Workspace bytes kvlink_attend_new_tokens needs for these sizes (same
- * meaning as its arguments, including split_keys).  Returns 0 for invalid
- * sizes.
+ * Schedule of the split-K attention of a request batch (host-built once per
+ * batch, reused for every layer).  The new-token rows of each request are
+ * packed per KV head as row = token * group + head-in-group (group =
+ * n_q_heads / n_kv_heads) and cut into row blocks of row_block rows; a
+ * (request, KV head, row block) unit walks the keys its last token sees in
+ * 64-key tiles.  The tiles of all units, in unit order, are dealt out to
+ * n_workgroups workgroups as equal contiguous ranges (the split-K of
+ * flash-decoding with the splits balanced across units); each piece of a
+ * unit that one workgroup covers is a segment, and a unit with several
+ * segments has its partial results merged by a log-sum-exp combine.
+ *
+ * The table (int32, built on the host by kvlink_attend_make_plan, then
+ * copied to the device by the caller) holds, in order:
+ *   n_workgroups x {first unit, first tile in it, tile count, first segment}
+ *   n_units x {request, KV head, first row of the block, tile count}
+ *   n_units + 1 first-segment offsets of the units
+ *   n_seqs + 1 first-unit offsets of the requests
+ */
+typedef struct {
+    const int32_t* table; /* device copy of the table (NULL in make_plan's output) */
+    int32_t table_len;    /* int32 entries of the table */
+    int32_t n_workgroups;
+    int32_t n_units;
+    int32_t n_segments;
+    int32_t row_block;    /* rows per unit: 256 on the matrix-core path, 16 otherwise */
+    int32_t n_seqs;
+} kvlink_attend_plan;
+
+/*
+ * kvlink_attend_make_plan — build the schedule (pure host computation).
+ *
+ *   seq_new_ptr[n_seqs+1], new_visible[n_new]  host outputs of
+ *                    kvlink_build_layout for the batch
+ *   n_compute_units  compute units of the device (sizes the schedule)
+ *   n_workgroups     0: chosen by a cost model (every workgroup costs a fixed
+ *                    set-up per segment plus a per-tile cost, the launch is
+ *                    as long as its longest workgroup, and split partials
+ *                    add a combine launch and their traffic); > 0: that many
+ *                    workgroups (capped at the tile count)
+ *   table, table_capacity  host array for the table; with table == NULL
+ *                    only *plan is filled (to size the array)
+ *   plan             out: counts and row_block; plan->table is set to NULL
+ *                    (the caller stores the device copy's address there)
+ *
+ * The result of the attention does not depend on the schedule beyond float
+ * rounding order.  Errors: KVLINK_ERR_INVALID_ARG (null required pointer,
+ * n_seqs < 1, n_compute_units < 1, n_workgroups < 0, table too small),
+ * KVLINK_ERR_UNSUPPORTED (head_dim, dtype, group), KVLINK_ERR_LAYOUT
+ * (seq_new_ptr not non-decreasing from 0, new_visible negative).
+ */
+kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                      int32_t head_dim, int32_t n_seqs,
+                                      const int32_t* seq_new_ptr, const int32_t* new_visible,
+                                      int32_t n_compute_units, int32_t n_workgroups,
+                                      int32_t* table, int64_t table_capacity,
+                                      kvlink_attend_plan* plan);
+
+/*
+ * Workspace bytes kvlink_attend_new_tokens needs (rotated queries, plus the
+ * split partials when some unit has several segments).  Returns 0 for
+ * invalid sizes or a null plan.
  */
 size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
-                                     int32_t head_dim, int32_t n_seqs, int32_t n_new_total,
-                                     int32_t max_new, int32_t max_cached, int32_t split_keys);
+                                     int32_t head_dim, int32_t n_new_total,
+                                     const kvlink_attend_plan* plan);
 
 /*
  * kvlink_attend_new_tokens — one layer of the forward pass over the new
@@ -218,10 +277,14 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *                              and its values, with room for the new rows
  *   out   [n_new_total][n_q_heads][head_dim]    device, dtype
  *   lse   [n_new_total][n_q_heads] float, or NULL
- *   split_keys                 keys per split of the split-K schedule: 0 lets
- *                              the library choose from the sizes; otherwise a
- *                              positive multiple of 128 (the result does not
- *                              depend on it beyond float rounding order)
+ *   plan                       schedule from kvlink_attend_make_plan for the
+ *                              same batch, with plan.table pointing at the
+ *                              device copy of its table.  Its row_block must
+ *                              match this call's path (KVLINK_ERR_INVALID_ARG
+ *                              otherwise).  The kernels clamp every index
+ *                              they read from the table to the batch's
+ *                              bounds, so a stale table gives wrong results
+ *                              but no out-of-bounds access.
  *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
  *                              device bytes, 256-byte aligned
  *
@@ -239,34 +302,19 @@ kvlink_status kvlink_attend_new_tokens(
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
-    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
     void* workspace, size_t workspace_bytes, void* stream);
-
-/*
- * kvlink_attend_split_keys — host-side choice of split_keys for
- * kvlink_attend_new_tokens from the batch's layout (outputs of
- * kvlink_build_layout: seq_new_ptr[n_seqs+1], new_visible[n_new]) and the
- * device's compute-unit count.  It estimates, for every candidate split
- * size, the makespan of the split workgroups over the compute units (each
- * workgroup costs a fixed overhead plus a per-64-key tile cost) plus the
- * traffic of the split partials, and returns the cheapest candidate (a
- * positive multiple of 128).  Returns 0 (meaning "use the library default")
- * for invalid input; never fails otherwise.  Pure host computation.
- */
-int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
-                                 int32_t head_dim, int32_t n_seqs, const int32_t* seq_new_ptr,
-                                 const int32_t* new_visible, int32_t n_compute_units);
 
 /*
  * kvlink_attend_stages — kvlink_attend_new_tokens run stage by stage, with
  * identical arguments plus a bit mask of the stages to launch:
  *   KVLINK_STAGE_ROPE     steps 1 and 2 (RoPE of the new tokens, append of
  *                         their keys and values, rotated q to the workspace)
- *   KVLINK_STAGE_SPLIT    step 3 over every key split (writes the output
- *                         directly when one split covers every row block,
- *                         split partials to the workspace otherwise)
+ *   KVLINK_STAGE_SPLIT    step 3 over every segment of the plan (a unit
+ *                         with one segment writes out and lse directly, the
+ *                         others write split partials to the workspace)
  *   KVLINK_STAGE_COMBINE  log-sum-exp merge of the split partials into out
- *                         and lse (no launch when there is one split)
+ *                         and lse (no launch when every unit has one segment)
  * Stages must run in this order, on the same stream, with the same workspace
  * and arguments; kvlink_attend_new_tokens is all three.  For callers that
  * time or overlap the stages separately.  Errors as kvlink_attend_new_tokens,
@@ -280,7 +328,7 @@ kvlink_status kvlink_attend_stages(
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
-    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
     void* workspace, size_t workspace_bytes, void* stream, uint32_t stages);
 
 /* Message of the last non-OK status on the calling thread ("" if none). */

@@ -48,6 +48,16 @@ class kvlink_span(ctypes.Structure):
 SPAN_FIELDS = 6   # int32 fields of kvlink_span, in declaration order
 
 
+class kvlink_attend_plan(ctypes.Structure):
+    _fields_ = [("table", ctypes.c_void_p),
+                ("table_len", ctypes.c_int32),
+                ("n_workgroups", ctypes.c_int32),
+                ("n_units", ctypes.c_int32),
+                ("n_segments", ctypes.c_int32),
+                ("row_block", ctypes.c_int32),
+                ("n_seqs", ctypes.c_int32)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -60,17 +70,19 @@ def _load():
     lib.kvlink_reencode_keys.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32,
                                          kvlink_kv_view, kvlink_kv_view, vp]
     lib.kvlink_reencode_keys.restype = ctypes.c_int
-    lib.kvlink_attend_workspace_bytes.argtypes = [ctypes.c_int] + [i32] * 8
+    lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, i32, i32,
+                                            vp, i64, ctypes.POINTER(kvlink_attend_plan)]
+    lib.kvlink_attend_make_plan.restype = ctypes.c_int
+    lib.kvlink_attend_workspace_bytes.argtypes = [ctypes.c_int, i32, i32, i32, i32,
+                                                  ctypes.POINTER(kvlink_attend_plan)]
     lib.kvlink_attend_workspace_bytes.restype = sz
     lib.kvlink_attend_new_tokens.argtypes = [
         ctypes.c_int, i32, i32, i32, f64, f32, i32, i32, i32, i32,
-        vp, vp, vp, vp, vp, vp, vp, kvlink_kv_view, kvlink_kv_view, i32, vp, vp, i32,
-        vp, sz, vp]
+        vp, vp, vp, vp, vp, vp, vp, kvlink_kv_view, kvlink_kv_view, i32, vp, vp,
+        kvlink_attend_plan, vp, sz, vp]
     lib.kvlink_attend_new_tokens.restype = ctypes.c_int
     lib.kvlink_attend_stages.argtypes = lib.kvlink_attend_new_tokens.argtypes + [ctypes.c_uint32]
     lib.kvlink_attend_stages.restype = ctypes.c_int
-    lib.kvlink_attend_split_keys.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, i32]
-    lib.kvlink_attend_split_keys.restype = i32
     lib.kvlink_last_error.restype = ctypes.c_char_p
     lib.kvlink_version.restype = ctypes.c_char_p
     return lib
@@ -170,45 +182,50 @@ def kvlink_reencode_keys(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_sp
                                      int(max_span_len), src, dst, _stream(stream)))
 
 
-def kvlink_attend_workspace_bytes(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs, n_new_total,
-                                  max_new, max_cached, split_keys=0):
-    return int(_lib.kvlink_attend_workspace_bytes(int(dtype), int(n_q_heads), int(n_kv_heads),
-                                                  int(head_dim), int(n_seqs), int(n_new_total),
-                                                  int(max_new), int(max_cached), int(split_keys)))
-
-
-def kvlink_attend_split_keys(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, new_visible,
-                             n_compute_units):
-    """Host-side split size for the batch (0: invalid input)."""
+def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, new_visible,
+                            n_compute_units, n_workgroups=0):
+    """Host-built split-K schedule: returns (plan, table) with table an int32
+    numpy array; plan.table is None until the caller sets it to the address
+    of a device copy of the table."""
     snp = np.ascontiguousarray(np.asarray(seq_new_ptr, dtype=np.int32))
     vis = np.ascontiguousarray(np.asarray(new_visible, dtype=np.int32))
-    return int(_lib.kvlink_attend_split_keys(int(dtype), int(n_q_heads), int(n_kv_heads),
-                                             int(head_dim), len(snp) - 1, _ptr(snp), _ptr(vis),
-                                             int(n_compute_units)))
+    plan = kvlink_attend_plan()
+    args = (int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), len(snp) - 1, _ptr(snp),
+            _ptr(vis), int(n_compute_units), int(n_workgroups))
+    _check(_lib.kvlink_attend_make_plan(*args, None, 0, ctypes.byref(plan)))
+    table = np.zeros(max(plan.table_len, 1), np.int32)
+    _check(_lib.kvlink_attend_make_plan(*args, _ptr(table), len(table), ctypes.byref(plan)))
+    return plan, table[:plan.table_len]
+
+
+def kvlink_attend_workspace_bytes(dtype, n_q_heads, n_kv_heads, head_dim, n_new_total, plan):
+    return int(_lib.kvlink_attend_workspace_bytes(int(dtype), int(n_q_heads), int(n_kv_heads),
+                                                  int(head_dim), int(n_new_total),
+                                                  ctypes.byref(plan)))
 
 
 def kvlink_attend_new_tokens(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                              n_seqs, n_new_total, max_new, max_cached, d_seq_new_ptr,
                              d_seq_cached, d_new_pos, d_new_visible, q_new, k_new, v_new,
-                             k_cache, v_cache, layer, out, lse, split_keys, workspace,
+                             k_cache, v_cache, layer, out, lse, plan, workspace,
                              workspace_bytes, stream=None):
     _check(_lib.kvlink_attend_new_tokens(
         int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), float(rope_theta),
         float(softmax_scale), int(n_seqs), int(n_new_total), int(max_new), int(max_cached),
         _ptr(d_seq_new_ptr), _ptr(d_seq_cached), _ptr(d_new_pos), _ptr(d_new_visible),
         _ptr(q_new), _ptr(k_new), _ptr(v_new), k_cache, v_cache, int(layer), _ptr(out),
-        _ptr(lse), int(split_keys), _ptr(workspace), int(workspace_bytes), _stream(stream)))
+        _ptr(lse), plan, _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
 def kvlink_attend_stages(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                          n_seqs, n_new_total, max_new, max_cached, d_seq_new_ptr, d_seq_cached,
                          d_new_pos, d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer,
-                         out, lse, split_keys, workspace, workspace_bytes, stream=None,
+                         out, lse, plan, workspace, workspace_bytes, stream=None,
                          stages=KVLINK_STAGE_ALL):
     _check(_lib.kvlink_attend_stages(
         int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), float(rope_theta),
         float(softmax_scale), int(n_seqs), int(n_new_total), int(max_new), int(max_cached),
         _ptr(d_seq_new_ptr), _ptr(d_seq_cached), _ptr(d_new_pos), _ptr(d_new_visible),
         _ptr(q_new), _ptr(k_new), _ptr(v_new), k_cache, v_cache, int(layer), _ptr(out),
-        _ptr(lse), int(split_keys), _ptr(workspace), int(workspace_bytes), _stream(stream),
+        _ptr(lse), plan, _ptr(workspace), int(workspace_bytes), _stream(stream),
         int(stages)))

@@ -128,23 +128,33 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
 // workgroup (4 per wavefront), 64-key tiles staged to LDS as float, one key
 // per lane for the scores, one or two head-dim columns per lane for P.V.
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
-    constexpr int RB = 16, KT = 64, RPW = 4, DPL = D / 64;
-    __shared__ float s_q[RB][D];
-    __shared__ float s_k[KT][D + 1];
-    __shared__ float s_v[KT][D];
+constexpr int kValuRB = 16, kValuKT = 64;
 
-    const int split = blockIdx.x;
-    const int s = blockIdx.z / p.n_kv_heads, h = blockIdx.z % p.n_kv_heads;
+template <int D>
+struct ValuSmem {
+    float q[kValuRB][D];
+    float k[kValuKT][D + 1];
+    float v[kValuKT][D];
+};
+
+// One segment: tiles [tile_a, tile_b) of KV head h's rows [rho0, rho0 + 16)
+// of request s.  Early returns are uniform over the workgroup.
+template <typename T, int D>
+__device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, int s, int h,
+                                             int rho0, int tile_a, int tile_b, int seg,
+                                             bool direct) {
+    constexpr int RB = kValuRB, KT = kValuKT, RPW = 4, DPL = D / 64;
+    auto& s_q = sm.q;
+    auto& s_k = sm.k;
+    auto& s_v = sm.v;
+
     const int n0 = p.seq_new_ptr[s];
     const int rows_s = (p.seq_new_ptr[s + 1] - n0) * p.group;
-    const int rho0 = blockIdx.y * RB;
-    if (rho0 >= rows_s) return;
+    if (rho0 < 0 || rho0 >= rows_s) return;
     const BlockKeys bk = block_keys(p.new_visible, n0, rows_s, rho0, RB, p.group);
-    const int kbeg = split * p.split_keys;
+    const int kbeg = tile_a * KT;
     if (kbeg >= bk.nvirt) return;
-    const int kend = min(kbeg + p.split_keys, bk.nvirt);
+    const int kend = min(tile_b * KT, bk.nvirt);
     const int Tc = p.seq_cached[s];
 
     const T* q_rot = reinterpret_cast<const T*>(p.q_rot);
@@ -225,14 +235,14 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
         const int rho = rho0 + wave * RPW + i;
         const int hq = h * p.group + rho % p.group;
         const int64_t orow = (int64_t)(n0 + tok[i]) * p.n_q_heads + hq;
-        if (p.n_splits == 1) {
+        if (direct) {
             T* out = reinterpret_cast<T*>(p.out);
             const float inv = 1.f / l[i];
 #pragma unroll
             for (int dd = 0; dd < DPL; ++dd) out[orow * D + lane + 64 * dd] = from_f32<T>(o[i][dd] * inv);
             if (p.lse && lane == 0) p.lse[orow] = (m[i] + log2f(l[i])) * kLn2;
         } else {
-            const int64_t pi = orow * p.n_splits + split;
+            const int64_t pi = (int64_t)seg * RB + (rho - rho0);
 #pragma unroll
             for (int dd = 0; dd < DPL; ++dd) p.part_o[pi * D + lane + 64 * dd] = o[i][dd];
             if (lane == 0) {
@@ -243,12 +253,36 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
     }
 }
 
+// Persistent workgroups over the schedule, as the matrix-core kernel.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
+    __shared__ ValuSmem<D> sm;
+    const int4 w = p.plan_wg[blockIdx.x];
+    int u = w.x, a = w.y, left = w.z, seg = w.w;
+    for (bool first = true; left > 0 && u >= 0 && u < p.n_units; first = false) {
+        const int4 un = p.plan_unit[u];
+        const int b = min(un.w, a + left);
+        if (a < 0 || a >= b || un.x < 0 || un.x >= p.n_seqs || un.y < 0 || un.y >= p.n_kv_heads)
+            break;
+        const bool direct = unit_is_direct(p, u);
+        if (!direct && (seg < 0 || seg >= p.n_segments)) break;
+        if (!first) __syncthreads();
+        valu_segment<T, D>(p, sm, un.x, un.y, un.z, a, b, seg, direct);
+        left -= b - a;
+        ++u;
+        ++seg;
+        a = 0;
+    }
+}
+
 // ------------------------------------------------------------- combine
 
-// One wavefront per (new token, query head) row.  The maximum over the
-// splits is taken first (lane-strided), then the splits are accumulated four
-// at a time with all their loads issued together, so the row costs a few
-// memory round trips instead of two per split.
+// One wavefront per (new token, query head) row of a unit with several
+// segments (rows of single-segment units were written by the split kernel).
+// The maximum over the segments is taken first (lane-strided), then the
+// segments are accumulated four at a time with all their loads issued
+// together, so the row costs a few memory round trips instead of two per
+// segment.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total) {
     constexpr int DPL = D / 64;   // consecutive dims per lane
@@ -260,14 +294,19 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     const int n0 = p.seq_new_ptr[s];
     const int rows_s = (p.seq_new_ptr[s + 1] - n0) * p.group;
     const int rho = (n - n0) * p.group + hq % p.group;
-    const int rho0 = rho / p.row_block * p.row_block;
-    const BlockKeys bk = block_keys(p.new_visible, n0, rows_s, rho0, p.row_block, p.group);
-    const int nsp = (bk.nvirt + p.split_keys - 1) / p.split_keys;
-    const float* ml = p.part_ml + orow * p.n_splits * 2;
-    const float* po = p.part_o + orow * p.n_splits * D + lane * DPL;
+    const int nrb = (rows_s + p.row_block - 1) / p.row_block;
+    const int u = p.seq_unit[s] + (hq / p.group) * nrb + rho / p.row_block;
+    if (u < 0 || u >= p.n_units) return;
+    const int c0 = max(p.unit_seg[u], 0), c1 = min(p.unit_seg[u + 1], p.n_segments);
+    const int nsp = c1 - c0;
+    if (nsp <= 1) return;
+    const int64_t r0 = (int64_t)c0 * p.row_block + rho % p.row_block;   // first partial row
+    const int64_t stride = p.row_block;                                  // rows per segment
+    const float* ml = p.part_ml + r0 * 2;
+    const float* po = p.part_o + r0 * D + lane * DPL;
 
     float M = -INFINITY;
-    for (int c = lane; c < nsp; c += 64) M = fmaxf(M, ml[2 * c]);
+    for (int c = lane; c < nsp; c += 64) M = fmaxf(M, ml[2 * stride * c]);
     M = wave_max(M);
 
     float L = 0.f, acc[DPL];
@@ -277,25 +316,25 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     for (; c + 4 <= nsp; c += 4) {
         float mc[4], lc[4], oc[4][DPL];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            mc[u] = ml[2 * (c + u)];
-            lc[u] = ml[2 * (c + u) + 1];
+        for (int i = 0; i < 4; ++i) {
+            mc[i] = ml[2 * stride * (c + i)];
+            lc[i] = ml[2 * stride * (c + i) + 1];
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) oc[u][e] = po[(c + u) * D + e];
+            for (int e = 0; e < DPL; ++e) oc[i][e] = po[stride * D * (c + i) + e];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const float w = __builtin_amdgcn_exp2f(mc[u] - M);   // 0 for an empty split
-            L += w * lc[u];
+        for (int i = 0; i < 4; ++i) {
+            const float w = __builtin_amdgcn_exp2f(mc[i] - M);   // 0 for an empty segment
+            L += w * lc[i];
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) acc[e] += w * oc[u][e];
+            for (int e = 0; e < DPL; ++e) acc[e] += w * oc[i][e];
         }
     }
     for (; c < nsp; ++c) {
-        const float w = __builtin_amdgcn_exp2f(ml[2 * c] - M);
-        L += w * ml[2 * c + 1];
+        const float w = __builtin_amdgcn_exp2f(ml[2 * stride * c] - M);
+        L += w * ml[2 * stride * c + 1];
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) acc[e] += w * po[c * D + e];
+        for (int e = 0; e < DPL; ++e) acc[e] += w * po[stride * D * c + e];
     }
     T* out = reinterpret_cast<T*>(p.out) + orow * D + lane * DPL;
     const float inv = 1.f / L;
@@ -324,9 +363,13 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.seq_cached = a.seq_cached;
     p.new_visible = a.new_visible;
     p.scale_log2 = a.scale * kLog2e;
-    p.split_keys = pl.split_keys;
-    p.n_splits = pl.n_splits;
     p.row_block = pl.row_block;
+    p.n_units = pl.n_units;
+    p.n_segments = pl.n_segments;
+    p.plan_wg = reinterpret_cast<const int4*>(pl.table);
+    p.plan_unit = reinterpret_cast<const int4*>(pl.table + 4 * (size_t)pl.n_wg);
+    p.unit_seg = pl.table + 4 * (size_t)pl.n_wg + 4 * (size_t)pl.n_units;
+    p.seq_unit = p.unit_seg + pl.n_units + 1;
     p.part_o = reinterpret_cast<float*>(ws + pl.q_rot_bytes);
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
     p.out = a.out;
@@ -343,18 +386,16 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
         if (e != hipSuccess) return e;
     }
 
-    if (stages & KVLINK_STAGE_SPLIT) {
-        const int n_rb = (pl.max_new * pl.group + pl.row_block - 1) / pl.row_block;
-        dim3 grid(pl.n_splits, n_rb, pl.n_seqs * pl.n_kv_heads);
+    if ((stages & KVLINK_STAGE_SPLIT) && pl.n_wg > 0) {
         if (pl.use_mfma) {
-            e = launch_attend_mfma(D, p, grid, stream);
+            e = launch_attend_mfma(D, p, pl.n_wg, stream);
         } else {
-            hipLaunchKernelGGL((attend_valu_kernel<T, D>), grid, dim3(256), 0, stream, p);
+            hipLaunchKernelGGL((attend_valu_kernel<T, D>), dim3(pl.n_wg), dim3(256), 0, stream, p);
             e = hipGetLastError();
         }
         if (e != hipSuccess) return e;
     }
-    if (!(stages & KVLINK_STAGE_COMBINE) || pl.n_splits == 1) return hipSuccess;
+    if (!(stages & KVLINK_STAGE_COMBINE) || !pl.partials) return hipSuccess;
 
     const int64_t n_rows = (int64_t)pl.n_new_total * pl.n_q_heads;
     hipLaunchKernelGGL((combine_kernel<T, D>), dim3((unsigned)((n_rows + 3) / 4)), dim3(256), 0,
@@ -364,44 +405,40 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
 
 }  // namespace
 
-bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim, int n_seqs,
-                      int n_new_total, int max_new, int max_cached, int split_keys,
-                      AttendPlan* p) {
+int attend_row_block(bool use_mfma) { return use_mfma ? attend_mfma_row_block() : kValuRB; }
+
+bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
+                      int n_new_total, const kvlink_attend_plan& sched, AttendPlan* p) {
     if (n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads) return false;
     if (head_dim != 64 && head_dim != 128) return false;
-    if (n_seqs < 1 || n_new_total < 0 || max_new < 0 || max_cached < 0) return false;
-    if (split_keys < 0 || split_keys % 128) return false;
+    if (n_new_total < 0 || sched.n_seqs < 1) return false;
+    if (sched.row_block != attend_mfma_row_block() && sched.row_block != kValuRB) return false;
+    if (sched.n_workgroups < 0 || sched.n_units < 0 || sched.n_segments < sched.n_units)
+        return false;
+    if (sched.n_workgroups > 0 && (sched.n_units < 1 || sched.n_segments < 1)) return false;
+    const int64_t want = 4 * (int64_t)sched.n_workgroups + 5 * (int64_t)sched.n_units + 1 +
+                         sched.n_seqs + 1;
+    if (sched.table_len != want) return false;
     const size_t elem = dt == KVLINK_BF16 ? 2 : 4;
     p->n_q_heads = n_q_heads;
     p->n_kv_heads = n_kv_heads;
     p->group = n_q_heads / n_kv_heads;
     p->head_dim = head_dim;
-    p->n_seqs = n_seqs;
+    p->n_seqs = sched.n_seqs;
     p->n_new_total = n_new_total;
-    p->max_new = max_new;
-    p->max_cached = max_cached;
-    // matrix cores where the GQA-packed rows of a KV head form a real dense
-    // contraction; the VALU schedule for fp32 and for thin row counts
-    p->use_mfma = dt == KVLINK_BF16 && (int64_t)max_new * p->group >= 32;
-    p->row_block = p->use_mfma ? attn::attend_mfma_row_block() : 16;
-    const int64_t max_keys = (int64_t)max_cached + max_new;
-    if (split_keys == 0) {
-        // aim at a few workgroups per compute unit, splits of at least 256 keys
-        const int64_t target = p->use_mfma ? 512 : 1024;
-        const int64_t n_rb = (int64_t)n_seqs * n_kv_heads *
-                             (((int64_t)max_new * p->group + p->row_block - 1) / p->row_block);
-        const int64_t want_splits = n_rb > 0 ? (target + n_rb - 1) / n_rb : 1;
-        int64_t sk = (max_keys + want_splits - 1) / std::max<int64_t>(want_splits, 1);
-        sk = (sk + 127) / 128 * 128;
-        split_keys = (int)std::max<int64_t>(256, sk);
-    }
-    p->split_keys = split_keys;
-    p->n_splits = (int)std::max<int64_t>(1, (max_keys + split_keys - 1) / split_keys);
+    p->row_block = sched.row_block;
+    p->use_mfma = sched.row_block == attend_mfma_row_block();
+    p->n_wg = sched.n_workgroups;
+    p->n_units = sched.n_units;
+    p->n_segments = sched.n_segments;
+    p->table = sched.table;
+    p->partials = sched.n_segments > sched.n_units;
     const int64_t rows = (int64_t)n_new_total * n_q_heads;
     p->q_rot_bytes = align256((size_t)rows * head_dim * elem);
-    if (p->n_splits > 1) {
-        p->part_o_bytes = align256((size_t)rows * p->n_splits * head_dim * sizeof(float));
-        p->part_ml_bytes = align256((size_t)rows * p->n_splits * 2 * sizeof(float));
+    if (p->partials) {
+        const size_t prow = (size_t)sched.n_segments * sched.row_block;
+        p->part_o_bytes = align256(prow * head_dim * sizeof(float));
+        p->part_ml_bytes = align256(prow * 2 * sizeof(float));
     } else {
         p->part_o_bytes = p->part_ml_bytes = 0;
     }

@@ -45,7 +45,11 @@ __device__ __forceinline__ BlockKeys block_keys(const int32_t* new_visible, int 
     return b;
 }
 
-// Arguments of the split kernels and the combine.
+// Arguments of the split kernels and the combine.  The schedule table (see
+// the schedule's description in the public header) is read through plan_wg
+// (n_wg x int4 {unit, first tile, tile count, first segment}), plan_unit
+// (n_units x int4 {request, KV head, first row, tile count}), unit_seg
+// (n_units + 1) and seq_unit (n_seqs + 1).
 struct KParams {
     const void* q_rot;
     View k, v;
@@ -54,15 +58,23 @@ struct KParams {
     const int32_t* seq_cached;
     const int32_t* new_visible;
     float scale_log2;
-    int split_keys, n_splits, row_block;
-    float* part_o;
-    float* part_ml;
+    int row_block, n_units, n_segments;
+    const int4* plan_wg;
+    const int4* plan_unit;
+    const int32_t* unit_seg;
+    const int32_t* seq_unit;
+    float* part_o;    // [segment][row in block][head_dim]
+    float* part_ml;   // [segment][row in block][2]: running max (log2 units), sum
     void* out;
     float* lse;
 };
 
+// A unit has one segment: its workgroup writes out and lse directly.
+__device__ __forceinline__ bool unit_is_direct(const KParams& p, int u) {
+    return p.unit_seg[u + 1] - p.unit_seg[u] == 1;
+}
 
-hipError_t launch_attend_mfma(int head_dim, const KParams& p, dim3 grid, hipStream_t stream);
+hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
 // GQA rows per workgroup of the MFMA kernel
 int attend_mfma_row_block();
 

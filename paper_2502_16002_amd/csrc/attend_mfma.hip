@@ -1,12 +1,15 @@
 // attend_mfma.hip — bf16 split-K attention of the new tokens on gfx950 matrix
 // cores (v_mfma_f32_16x16x32_bf16, float accumulation).
 //
-// A workgroup owns one KV head, kRB = 256 GQA-packed rows (64 tokens x 4
-// heads for a group of 4) and one split of the block's virtual key range.
-// Each of its eight wavefronts owns 32 of the rows and walks every key of
-// the split (two wavefronts per SIMD, so one's softmax overlaps the other's
-// matrix products); K and V tiles of 64 keys are brought into LDS once per
-// workgroup and shared by the eight waves:
+// A unit is one KV head's kRB = 256 GQA-packed rows (64 tokens x 4 heads for
+// a group of 4) of one request; its keys are walked in 64-key tiles.  The
+// workgroups are persistent: each owns an equal contiguous range of the
+// schedule's tiles, which may cover the end of one unit and the start of the
+// next (one segment per unit touched).  Each of the eight wavefronts owns 32
+// of the unit's rows and walks every key of the segment (two wavefronts per
+// SIMD, so one's softmax can overlap the other's matrix products); K and V
+// tiles are brought into LDS once per workgroup and shared by the eight
+// waves:
 //
 //   * the tiles are loaded straight from global memory into a four-stage
 //     LDS ring with 16-byte direct-to-LDS loads (each wave issues an eighth
@@ -168,8 +171,13 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// One segment of a unit: tiles [tile_a, tile_b) of the key range of KV head
+// h's rows [rho0, rho0 + kRB) of request s.  Every early return is uniform
+// over the workgroup.
 template <int D>
-__global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
+__device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem, int s, int h,
+                                               int rho0, int tile_a, int tile_b, int seg,
+                                               bool direct) {
     constexpr int DT = D / 16;         // 16-dim tiles of O^T
     constexpr int DS = D / 32;         // 32-dim steps of S^T = K Q^T
     constexpr int KB = 4 * DS;         // 1 KB operand blocks of a K tile
@@ -177,17 +185,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     constexpr int CH = D / 8;          // 16-byte chunks per V row
     constexpr int LPW = (KB + VI) / kWaves;    // direct loads per wave per tile
     static_assert((KB % kWaves) == 0 && (VI % kWaves) == 0, "tile split");
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
 
-    const int split = blockIdx.x;
-    const int s = blockIdx.z / p.n_kv_heads, h = blockIdx.z % p.n_kv_heads;
     const int G = p.group;
     // request descriptors (independent loads)
     const int n0 = p.seq_new_ptr[s];
     const int rows_s = (p.seq_new_ptr[s + 1] - n0) * G;
     const int Tc = p.seq_cached[s];
-    const int rho0 = blockIdx.y * kRB;
-    if (rho0 >= rows_s) return;
+    if (rho0 < 0 || rho0 >= rows_s) return;
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
@@ -223,9 +227,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     bk.r_last = r_last;
     bk.cmax = cmax;
     bk.nvirt = cmax + r_last + 1;
-    const int kbeg = split * p.split_keys;
+    const int kbeg = tile_a * kTile;
     if (kbeg >= bk.nvirt) return;
-    const int kend = min(kbeg + p.split_keys, bk.nvirt);
+    const int kend = min(tile_b * kTile, bk.nvirt);
     const float c2 = p.scale_log2;   // > 0
 
     // Row r may see virtual key v iff v < lo (cached rows up to its document,
@@ -324,164 +328,235 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         }
     };
 
-#pragma unroll
-    for (int t = 0; t < kStages - 1; ++t)
-        if (t < n_tiles) issue_tile(t);
+    // ---- pieces of a 32-key sub-tile (stage st, half h of its tile)
 
-    for (int t = 0; t < n_tiles; ++t) {
-        // this wave's loads of tile t are done when at most those of the
-        // next kStages-2 tiles are still outstanding; the barrier makes every
-        // wave's part visible and frees the stage of tile t-1 for tile
-        // t+kStages-1
-        const int ahead = min(kStages - 2, n_tiles - 1 - t);
-        if (ahead >= 2) wait_vm<2 * LPW>(); else if (ahead == 1) wait_vm<LPW>(); else wait_vm<0>();
-        __syncthreads();
-        if (t + kStages - 1 < n_tiles) issue_tile(t + kStages - 1);
-
-        const unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
-        // V^T operand addresses of this stage (the sub-tile and key-half
-        // parts are immediate offsets of the reads)
-        uint32_t va[DT];
-        const uint32_t vt = lds_addr(st + Smem<D>::k_bytes);
+    // one 16-key half kt of S^T = K Q^T
+    auto qk_half = [&](const unsigned char* st, auto h_const, auto kt_const,
+                       floatx4 (&sacc)[2][kRT]) {
+        constexpr int h = decltype(h_const)::value, kt = decltype(kt_const)::value;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
-
-        auto sub_tile = [&](auto sc_const) {
-            constexpr int sc = decltype(sc_const)::value;
-            const int v0 = kbeg + t * kTile + 32 * sc;
-
-            // S^T = K Q^T
-            floatx4 sacc[2][kRT];
+        for (int rt = 0; rt < kRT; ++rt) sacc[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-                for (int rt = 0; rt < kRT; ++rt) sacc[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ds = 0; ds < DS; ++ds) {
-                    const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(
-                        st + ((sc * 2 + kt) * DS + ds) * 1024 + lane * 16));
-#pragma unroll
-                    for (int rt = 0; rt < kRT; ++rt)
-                        sacc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qB[rt][ds],
-                                                                               sacc[kt][rt], 0, 0, 0);
-                }
-            }
-
-            // mask, by the kind of sub-tile (wave-uniform): keys below every
-            // row's visible prefix need none; keys in the cached region need
-            // v < lo; keys in the new-token region need v <= hi; a sub-tile
-            // across cmax needs both tests.  Lane group g holds key offsets
-            // 16kt + 4g + i of the sub-tile.
-            const int vb = v0 + 4 * lg;
-            if (v0 + 32 > wave_vis_min) {
-                if (v0 + 32 <= bk.cmax) {
-#pragma unroll
-                    for (int rt = 0; rt < kRT; ++rt) {
-                        const int t_lo = lo[rt] - vb;
-#pragma unroll
-                        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                sacc[kt][rt][i] = 16 * kt + i < t_lo ? sacc[kt][rt][i] : -INFINITY;
-                    }
-                } else if (v0 >= bk.cmax) {
-#pragma unroll
-                    for (int rt = 0; rt < kRT; ++rt) {
-                        const int t_hi = hi[rt] - vb;
-#pragma unroll
-                        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                sacc[kt][rt][i] = 16 * kt + i <= t_hi ? sacc[kt][rt][i] : -INFINITY;
-                    }
-                } else {
-#pragma unroll
-                    for (int rt = 0; rt < kRT; ++rt) {
-                        const int t_lo = lo[rt] - vb, t_c = bk.cmax - vb, t_hi = hi[rt] - vb;
-#pragma unroll
-                        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const int o = 16 * kt + i;
-                                const bool ok = o < t_lo || (o >= t_c && o <= t_hi);
-                                sacc[kt][rt][i] = ok ? sacc[kt][rt][i] : -INFINITY;
-                            }
-                    }
-                }
-            }
-
-            // online softmax in base 2 with a lazily raised maximum, on
-            // x = s * scale_log2 - m: the slow path (cross-lane maximum,
-            // rescale of O and l) runs only if some x exceeds kTau.  The
-            // maximum is taken over x, the result of a fused multiply-add,
-            // so no NaN-quieting is needed in front of it.
-            float x[kRT][8];
-            bool over = false;
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    x[rt][j] = __builtin_fmaf(sacc[j >> 2][rt][j & 3], c2, -m[rt]);
-                const float mx = fmaxf(fmaxf(fmaxf(x[rt][0], x[rt][1]), fmaxf(x[rt][2], x[rt][3])),
-                                       fmaxf(fmaxf(x[rt][4], x[rt][5]), fmaxf(x[rt][6], x[rt][7])));
-                over |= mx > kTau;
-            }
-            if (__builtin_amdgcn_ballot_w64(over)) {
-                // from the raw scores: x loses them while m is still kNoMax
-#pragma unroll
-                for (int rt = 0; rt < kRT; ++rt) {
-                    float r = fmaxf(fmaxf(fmaxf(sacc[0][rt][0], sacc[0][rt][1]),
-                                          fmaxf(sacc[0][rt][2], sacc[0][rt][3])),
-                                    fmaxf(fmaxf(sacc[1][rt][0], sacc[1][rt][1]),
-                                          fmaxf(sacc[1][rt][2], sacc[1][rt][3])));
-                    r = fmaxf(r, __shfl_xor(r, 16));
-                    r = fmaxf(r, __shfl_xor(r, 32));
-                    const float m_new = fmaxf(m[rt], r * c2);
-                    const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
-                    m[rt] = m_new;
-                    lsum[rt] *= alpha;
-#pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        x[rt][j] = __builtin_fmaf(sacc[j >> 2][rt][j & 3], c2, -m_new);
-                }
-            }
-            // p = 2^x, packed to bf16 pairs; the row sum adds the rounded
-            // pairs (the weights the product below uses) with dot products
-            // against (1, 1)
-            uint32_t pk[kRT][4];
-            const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+        for (int ds = 0; ds < DS; ++ds) {
+            const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(
+                st + ((h * 2 + kt) * DS + ds) * 1024 + lane * 16));
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    pk[rt][j] = pack2(__builtin_amdgcn_exp2f(x[rt][2 * j]),
-                                      __builtin_amdgcn_exp2f(x[rt][2 * j + 1]));
-                    lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(
-                        __builtin_bit_cast(bf16x2, pk[rt][j]), ones, lsum[rt], false);
-                }
+                sacc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qB[rt][ds],
+                                                                       sacc[kt][rt], 0, 0, 0);
+        }
+    };
 
-            // O^T += V^T P^T.  For a 16-lane block, the transpose read gives
-            // lane i element i%4 of the 4-element rows supplied by lanes
-            // 4k + i/4 (k = 0..3); lane j therefore supplies key
-            // 32sc + 16h + 4lg + j/4, dims 16dt + 4(j%4).., so that lane i
-            // receives keys 4lg+k (k = 0..3) of dim 16dt + i.
-            uint2 vr[DT][2];
-            read_vt<DT, 32 * sc * 2 * D, (32 * sc + 16) * 2 * D>(va, vr);
+    // keys below every row's visible prefix need no mask; keys in the cached
+    // region need v < lo; keys in the new-token region need v <= hi; a
+    // sub-tile across cmax needs both tests (the kind is wave-uniform).
+    // Lane group g holds key offsets 16kt + 4g + i of the sub-tile.
+    auto mask = [&](floatx4 (&sacc)[2][kRT], int v0) {
+        const int vb = v0 + 4 * lg;
+        if (v0 + 32 <= wave_vis_min) return;
+        if (v0 + 32 <= bk.cmax) {
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const uint2* half = vr[dt];
-                const bf16x8 a = as_bf16x8(uint4{half[0].x, half[0].y, half[1].x, half[1].y});
+            for (int rt = 0; rt < kRT; ++rt) {
+                const int t_lo = lo[rt] - vb;
 #pragma unroll
-                for (int rt = 0; rt < kRT; ++rt)
-                    o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
-                        0, 0, 0);
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        sacc[kt][rt][i] = 16 * kt + i < t_lo ? sacc[kt][rt][i] : -INFINITY;
             }
-        };
-        sub_tile(std::integral_constant<int, 0>{});
-        if (kbeg + t * kTile + 32 < kend) sub_tile(std::integral_constant<int, 1>{});
+        } else if (v0 >= bk.cmax) {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const int t_hi = hi[rt] - vb;
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        sacc[kt][rt][i] = 16 * kt + i <= t_hi ? sacc[kt][rt][i] : -INFINITY;
+            }
+        } else {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const int t_lo = lo[rt] - vb, t_c = bk.cmax - vb, t_hi = hi[rt] - vb;
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int o = 16 * kt + i;
+                        const bool ok = o < t_lo || (o >= t_c && o <= t_hi);
+                        sacc[kt][rt][i] = ok ? sacc[kt][rt][i] : -INFINITY;
+                    }
+            }
+        }
+    };
+
+    // O^T += V^T P^T.  For a 16-lane block, the transpose read gives lane i
+    // element i%4 of the 4-element rows supplied by lanes 4k + i/4 (k =
+    // 0..3); lane j therefore supplies key 32h + 16e + 4lg + j/4 (e: key
+    // half), dims 16dt + 4(j%4).., so that lane i receives keys 4lg+k (k =
+    // 0..3) of dim 16dt + i.  The sub-tile and key-half parts of the
+    // addresses are immediate offsets.
+    auto pv = [&](const unsigned char* st, auto h_const, const uint32_t (&pk)[kRT][4]) {
+        constexpr int h = decltype(h_const)::value;
+        const uint32_t vt = lds_addr(st + Smem<D>::k_bytes);
+        uint32_t va[DT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
+        uint2 vr[DT][2];
+        read_vt<DT, 32 * h * 2 * D, (32 * h + 16) * 2 * D>(va, vr);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const uint2* half = vr[dt];
+            const bf16x8 a = as_bf16x8(uint4{half[0].x, half[0].y, half[1].x, half[1].y});
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt)
+                o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
+                    0, 0, 0);
+        }
+    };
+
+    // One step of the pipeline: sub-tile `cur` (S in s_cur, keys from v0,
+    // values in half hc of stage stc) becomes P and is added to O, while the
+    // matrix cores compute S of the next sub-tile (half hn of stage stn) into
+    // s_nxt.  The online softmax works in base 2 on x = s * scale_log2 - m
+    // with a lazily raised maximum: the slow path (cross-lane maximum,
+    // rescale of O and l) runs only if some x exceeds kTau; the maximum is
+    // taken over x, the result of a fused multiply-add, so no NaN-quieting is
+    // needed in front of it.  P is packed to bf16 pairs; the row sum adds the
+    // rounded pairs (the weights the product uses) with dot products against
+    // (1, 1).
+    //
+    // The vector work is written out in chunks, one per product of the next
+    // S (d-step ds, row tile rt), each chunk fenced by a scheduling barrier:
+    // a product occupies the matrix core for 16 cycles, during which the
+    // wave issues the chunk's independent vector instructions.
+    auto step = [&](floatx4 (&s_cur)[2][kRT], floatx4 (&s_nxt)[2][kRT], int v0,
+                    const unsigned char* stc, auto hc, const unsigned char* stn, auto hn) {
+        constexpr int h_n = decltype(hn)::value;
+        static_assert(kRT == 2, "chunking assumes two row tiles");
+        mask(s_cur, v0);
+
+        // K operands of the next sub-tile (both key halves)
+        bf16x8 ka[2][DS];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int ds = 0; ds < DS; ++ds)
+                ka[kt][ds] = as_bf16x8(*reinterpret_cast<const uint4*>(
+                    stn + ((h_n * 2 + kt) * DS + ds) * 1024 + lane * 16));
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) s_nxt[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+        // first half: products of key half 0, with x = s * c2 - m and the
+        // maxima (16 fused multiply-adds over the 2 * DS products)
+        float x[kRT][8];
+        constexpr int NP = 2 * DS;                 // products per key half
+        constexpr int FPC = 16 / NP;               // multiply-adds per chunk
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            const int ds = i / 2, rt = i % 2;
+            s_nxt[0][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[0][ds], qB[rt][ds],
+                                                                   s_nxt[0][rt], 0, 0, 0);
+#pragma unroll
+            for (int f = 0; f < FPC; ++f) {
+                const int idx = i * FPC + f, r = idx / 8, j = idx % 8;
+                x[r][j] = __builtin_fmaf(s_cur[j >> 2][r][j & 3], c2, -m[r]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        bool over = false;
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            const float mx = fmaxf(fmaxf(fmaxf(x[rt][0], x[rt][1]), fmaxf(x[rt][2], x[rt][3])),
+                                   fmaxf(fmaxf(x[rt][4], x[rt][5]), fmaxf(x[rt][6], x[rt][7])));
+            over |= mx > kTau;
+        }
+
+        if (__builtin_amdgcn_ballot_w64(over)) {
+            // from the raw scores: x loses them while m is still kNoMax
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                float r = fmaxf(fmaxf(fmaxf(s_cur[0][rt][0], s_cur[0][rt][1]),
+                                      fmaxf(s_cur[0][rt][2], s_cur[0][rt][3])),
+                                fmaxf(fmaxf(s_cur[1][rt][0], s_cur[1][rt][1]),
+                                      fmaxf(s_cur[1][rt][2], s_cur[1][rt][3])));
+                r = fmaxf(r, __shfl_xor(r, 16));
+                r = fmaxf(r, __shfl_xor(r, 32));
+                const float m_new = fmaxf(m[rt], r * c2);
+                const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
+                m[rt] = m_new;
+                lsum[rt] *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    x[rt][j] = __builtin_fmaf(s_cur[j >> 2][rt][j & 3], c2, -m_new);
+            }
+        }
+
+        // second half: products of key half 1, with p = 2^x packed to bf16
+        // and the row sums (8 pairs over the 2 * DS products)
+        uint32_t pk[kRT][4];
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+        constexpr int PPC = 8 / NP;                // pairs per chunk
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            const int ds = i / 2, rt = i % 2;
+            s_nxt[1][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[1][ds], qB[rt][ds],
+                                                                   s_nxt[1][rt], 0, 0, 0);
+#pragma unroll
+            for (int f = 0; f < PPC; ++f) {
+                const int idx = i * PPC + f, r = idx / 4, j = idx % 4;
+                pk[r][j] = pack2(__builtin_amdgcn_exp2f(x[r][2 * j]),
+                                 __builtin_amdgcn_exp2f(x[r][2 * j + 1]));
+                lsum[r] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[r][j]),
+                                                          ones, lsum[r], false);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+        pv(stc, hc, pk);
+    };
+
+    // ---- software pipeline over 32-key sub-tiles j = 0, 1, ... (tile j/2,
+    // half j%2).  Step j turns S of sub-tile j into P V while the matrix
+    // cores compute S of sub-tile j+1 (for the last sub-tile, a discarded
+    // product over the current stage).  The barrier that makes tile t visible
+    // sits in step 2t-1, after which the stage of tile t-2 (no longer read by
+    // any wave) receives tile t+2; tile t-1's values stay until that step's
+    // P V.  The prologue issues tiles 0..2.
+    const int n_sub = (kend - kbeg + 31) / 32;
+    auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
+    constexpr std::integral_constant<int, 0> H0{};
+    constexpr std::integral_constant<int, 1> H1{};
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+        if (t < n_tiles) issue_tile(t);
+    if (n_tiles >= 3) wait_vm<2 * LPW>(); else if (n_tiles == 2) wait_vm<LPW>(); else wait_vm<0>();
+    __syncthreads();
+
+    floatx4 s_a[2][kRT], s_b[2][kRT];
+    qk_half(stage_of(0), H0, H0, s_a);
+    qk_half(stage_of(0), H0, H1, s_a);
+    for (int t = 0; t < n_tiles; ++t) {
+        const unsigned char* st = stage_of(t);
+        const int j0 = 2 * t;
+        // even step: sub-tile (t, 0) -> next (t, 1), same stage
+        step(s_a, s_b, kbeg + 32 * j0, st, H0, st, H1);
+        if (j0 + 1 >= n_sub) break;
+        // odd step: sub-tile (t, 1) -> next (t+1, 0), behind tile t+1's barrier
+        const bool more = t + 1 < n_tiles;
+        if (more) {
+            // this wave's loads of tile t+1 are done when at most those of
+            // tile t+2 are outstanding
+            if (t + 2 < n_tiles) wait_vm<LPW>(); else wait_vm<0>();
+            __syncthreads();
+            if (t + 3 < n_tiles) issue_tile(t + 3);
+        }
+        step(s_b, s_a, kbeg + 32 * (j0 + 1), st, H1, more ? stage_of(t + 1) : st, H0);
     }
 
     // row sums: add the four lane groups that hold each row
@@ -497,7 +572,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         if (tok[rt] < 0) continue;
         const int rho = rho_w + 16 * rt + lr;
         const int64_t orow = (int64_t)(n0 + tok[rt]) * p.n_q_heads + h * G + rho % G;
-        if (p.n_splits == 1) {
+        if (direct) {
             bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + orow * D;
             const float inv = 1.f / lsum[rt];
 #pragma unroll
@@ -508,7 +583,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
             }
             if (p.lse && lg == 0) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
         } else {
-            const int64_t pi = orow * p.n_splits + split;
+            const int64_t pi = (int64_t)seg * kRB + (rho - rho0);
             float* po = p.part_o + pi * D;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -521,11 +596,37 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
     }
 }
 
+// A persistent workgroup walks its range of the schedule: one segment per
+// unit the range touches.  Indices read from the table are checked against
+// the table's own counts before use.
+template <int D>
+__global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
+    const int4 w = p.plan_wg[blockIdx.x];
+    int u = w.x, a = w.y, left = w.z, seg = w.w;
+    for (bool first = true; left > 0 && u >= 0 && u < p.n_units; first = false) {
+        const int4 un = p.plan_unit[u];
+        const int b = min(un.w, a + left);
+        if (a < 0 || a >= b || un.x < 0 || un.x >= p.n_seqs || un.y < 0 || un.y >= p.n_kv_heads)
+            break;
+        const bool direct = unit_is_direct(p, u);
+        if (!direct && (seg < 0 || seg >= p.n_segments)) break;
+        // the previous segment's waves are done with every LDS stage
+        if (!first) __syncthreads();
+        attend_segment<D>(p, smem, un.x, un.y, un.z, a, b, seg, direct);
+        left -= b - a;
+        ++u;
+        ++seg;
+        a = 0;
+    }
+}
+
 }  // namespace
 
 int attend_mfma_row_block() { return kRB; }
 
-hipError_t launch_attend_mfma(int head_dim, const KParams& p, dim3 grid, hipStream_t stream) {
+hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream) {
+    const dim3 grid(n_wg);
     if (head_dim == 128)
         hipLaunchKernelGGL(attend_mfma_kernel<128>, grid, dim3(64 * kWaves), 0, stream, p);
     else

@@ -223,13 +223,59 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
     }
 }
 
+kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
+                                      int32_t head_dim, int32_t n_seqs,
+                                      const int32_t* seq_new_ptr, const int32_t* new_visible,
+                                      int32_t n_compute_units, int32_t n_workgroups,
+                                      int32_t* table, int64_t table_capacity,
+                                      kvlink_attend_plan* plan) {
+    try {
+        if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_q_heads must be a positive multiple of n_kv_heads");
+        const int group = n_q_heads / n_kv_heads;
+        if (group != 1 && group != 2 && group != 4 && group != 8)
+            return fail(KVLINK_ERR_UNSUPPORTED, "GQA group %d (built: 1, 2, 4, 8)", group);
+        if (n_seqs < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_seqs must be >= 1");
+        if (!seq_new_ptr || !new_visible || !plan)
+            return fail(KVLINK_ERR_INVALID_ARG, "seq_new_ptr, new_visible and plan are required");
+        if (n_compute_units < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_compute_units must be >= 1");
+        if (n_workgroups < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_workgroups must be >= 0");
+        std::vector<int32_t> tab;
+        kvlink::PlanCounts c;
+        const char* why = "";
+        const int st = kvlink::build_attend_schedule(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs,
+                                                     seq_new_ptr, new_visible, n_compute_units,
+                                                     n_workgroups, table ? &tab : nullptr, &c, &why);
+        if (st != KVLINK_OK) return fail((kvlink_status)st, "%s", why);
+        if (c.table_len > INT32_MAX) return fail(KVLINK_ERR_LAYOUT, "schedule table too large");
+        if (table) {
+            if (table_capacity < c.table_len)
+                return fail(KVLINK_ERR_INVALID_ARG, "table holds %lld entries, needs %lld",
+                            (long long)table_capacity, (long long)c.table_len);
+            std::copy(tab.begin(), tab.end(), table);
+        }
+        plan->table = nullptr;
+        plan->table_len = (int32_t)c.table_len;
+        plan->n_workgroups = c.n_wg;
+        plan->n_units = c.n_units;
+        plan->n_segments = c.n_segments;
+        plan->row_block = c.row_block;
+        plan->n_seqs = n_seqs;
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_INVALID_ARG, "unexpected exception in kvlink_attend_make_plan");
+    }
+}
+
 size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
-                                     int32_t head_dim, int32_t n_seqs, int32_t n_new_total,
-                                     int32_t max_new, int32_t max_cached, int32_t split_keys) {
-    if (!dtype_ok(dtype)) return 0;
+                                     int32_t head_dim, int32_t n_new_total,
+                                     const kvlink_attend_plan* plan) {
+    if (!dtype_ok(dtype) || !plan) return 0;
     kvlink::AttendPlan p;
-    if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs, n_new_total,
-                                  max_new, max_cached, split_keys, &p))
+    if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_new_total, *plan, &p))
         return 0;
     return p.total_bytes;
 }
@@ -240,7 +286,7 @@ kvlink_status kvlink_attend_stages(
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
-    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan sched,
     void* workspace, size_t workspace_bytes, void* stream, uint32_t stages) {
     try {
         const uint32_t all = KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE;
@@ -264,11 +310,17 @@ kvlink_status kvlink_attend_stages(
             return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
         if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
             return fail(KVLINK_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
-        if (split_keys < 0 || split_keys % 128)
-            return fail(KVLINK_ERR_INVALID_ARG, "split_keys must be 0 or a positive multiple of 128");
-        if (n_seqs > 65535 / n_kv_heads)
-            return fail(KVLINK_ERR_UNSUPPORTED, "n_seqs * n_kv_heads above 65535");
         if (n_new_total == 0) return ok();
+        if (!sched.table) return fail(KVLINK_ERR_INVALID_ARG, "plan.table is NULL");
+        if (reinterpret_cast<uintptr_t>(sched.table) % 16)
+            return fail(KVLINK_ERR_INVALID_ARG, "plan.table is not 16-byte aligned");
+        if (sched.n_seqs != n_seqs)
+            return fail(KVLINK_ERR_INVALID_ARG, "plan is for %d requests, call has %d", sched.n_seqs,
+                        n_seqs);
+        const bool mfma = kvlink::attend_uses_mfma(dtype, group, max_new);
+        if (sched.row_block != kvlink::attend_row_block(mfma))
+            return fail(KVLINK_ERR_INVALID_ARG, "plan row_block %d does not match this call's path (%d)",
+                        sched.row_block, kvlink::attend_row_block(mfma));
         if (!d_seq_new_ptr || !d_seq_cached || !d_new_pos || !d_new_visible)
             return fail(KVLINK_ERR_INVALID_ARG, "a layout descriptor pointer is NULL");
         if (!q_new || !k_new || !v_new || !out)
@@ -277,9 +329,9 @@ kvlink_status kvlink_attend_stages(
         if (st != KVLINK_OK) return st;
         if ((st = check_view(v_cache, dtype, "v_cache")) != KVLINK_OK) return st;
         kvlink::AttendPlan plan;
-        if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs, n_new_total,
-                                      max_new, max_cached, split_keys, &plan))
-            return fail(KVLINK_ERR_INVALID_ARG, "invalid attention sizes");
+        if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_new_total, sched,
+                                      &plan))
+            return fail(KVLINK_ERR_INVALID_ARG, "invalid attention sizes or plan counts");
         if (!workspace) return fail(KVLINK_ERR_WORKSPACE, "workspace is NULL");
         if (reinterpret_cast<uintptr_t>(workspace) % 256)
             return fail(KVLINK_ERR_WORKSPACE, "workspace is not 256-byte aligned");
@@ -317,90 +369,14 @@ kvlink_status kvlink_attend_new_tokens(
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
-    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, int32_t split_keys,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
     void* workspace, size_t workspace_bytes, void* stream) {
     return kvlink_attend_stages(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                                 n_seqs, n_new_total, max_new, max_cached, d_seq_new_ptr,
                                 d_seq_cached, d_new_pos, d_new_visible, q_new, k_new, v_new,
-                                k_cache, v_cache, layer, out, lse, split_keys, workspace,
+                                k_cache, v_cache, layer, out, lse, plan, workspace,
                                 workspace_bytes, stream,
                                 KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE);
-}
-
-int32_t kvlink_attend_split_keys(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
-                                 int32_t head_dim, int32_t n_seqs, const int32_t* seq_new_ptr,
-                                 const int32_t* new_visible, int32_t n_compute_units) {
-    try {
-        if (!dtype_ok(dtype) || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
-            (head_dim != 64 && head_dim != 128) || n_seqs < 1 || !seq_new_ptr || !new_visible ||
-            n_compute_units < 1)
-            return 0;
-        const int group = n_q_heads / n_kv_heads;
-        int max_new = 0;
-        for (int s = 0; s < n_seqs; ++s) max_new = std::max(max_new, seq_new_ptr[s + 1] - seq_new_ptr[s]);
-        if (max_new < 1) return 0;
-        kvlink::AttendPlan pl;
-        if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs,
-                                      seq_new_ptr[n_seqs], max_new, 0, 128, &pl))
-            return 0;
-        // virtual key count of every row block (the same for every KV head)
-        std::vector<int64_t> nvirt;
-        int64_t max_keys = 0, rows_total = 0;
-        for (int s = 0; s < n_seqs; ++s) {
-            const int n0 = seq_new_ptr[s], rows_s = (seq_new_ptr[s + 1] - n0) * group;
-            rows_total += rows_s;
-            for (int rho0 = 0; rho0 < rows_s; rho0 += pl.row_block) {
-                const int r_last = (std::min(rho0 + pl.row_block, rows_s) - 1) / group;
-                const int64_t nv = (int64_t)new_visible[n0 + r_last] + r_last + 1;
-                nvirt.push_back(nv);
-                max_keys = std::max(max_keys, nv);
-            }
-        }
-        // cost model (microseconds), fitted to MI355X timings of the 10- and
-        // 40-document Llama-8B-shaped workloads over split sizes 128..4096:
-        // a workgroup costs a fixed 5 us plus 2.2 us per 64-key tile, with an
-        // effective two workgroups in flight per compute unit; partial
-        // traffic at an effective 4 TB/s
-        const double fixed = 5.0, per_tile = pl.use_mfma ? (head_dim == 128 ? 2.2 : 1.4) : 1.0;
-        const int slots = 2 * n_compute_units;
-        double best = 1e300;
-        int32_t best_sk = 128;
-        std::vector<double> load(slots);
-        std::vector<double> jobs;
-        for (int64_t sk = 128; sk < max_keys + 128; sk += 128) {
-            jobs.clear();
-            int64_t max_splits = 1;
-            for (int64_t nv : nvirt) {
-                const int64_t n = (nv + sk - 1) / sk;
-                max_splits = std::max(max_splits, n);
-                for (int64_t c = 0; c < n; ++c) {
-                    const int64_t keys = std::min(sk, nv - c * sk);
-                    for (int h = 0; h < n_kv_heads; ++h) jobs.push_back(fixed + per_tile * ((keys + 63) / 64));
-                }
-            }
-            // longest job first onto the least loaded slot
-            std::sort(jobs.begin(), jobs.end(), std::greater<double>());
-            std::fill(load.begin(), load.end(), 0.0);
-            std::make_heap(load.begin(), load.end(), std::greater<double>());
-            for (double j : jobs) {
-                std::pop_heap(load.begin(), load.end(), std::greater<double>());
-                load.back() += j;
-                std::push_heap(load.begin(), load.end(), std::greater<double>());
-            }
-            double t = *std::max_element(load.begin(), load.end());
-            if (max_splits > 1)
-                t += 3.0 + 2.0 * (double)rows_total * n_kv_heads * max_splits * (head_dim + 2) * 4.0 /
-                               4.0e6;
-            if (t < best * 0.98) {   // prefer fewer splits on near ties
-                best = t;
-                best_sk = (int32_t)sk;
-            }
-            if (max_splits == 1) break;
-        }
-        return best_sk;
-    } catch (...) {
-        return 0;
-    }
 }
 
 const char* kvlink_last_error(void) { return g_error.c_str(); }

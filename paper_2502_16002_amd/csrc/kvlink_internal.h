@@ -7,6 +7,8 @@
 
 #include "kvlink.h"
 
+#include <vector>
+
 namespace kvlink {
 
 // ------------------------------------------------------------ element types
@@ -181,19 +183,39 @@ hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv
                            int max_span_len, const View& src, const View& dst,
                            hipStream_t stream);
 
+// Sizes of one attention call, from the arguments and the schedule.
 struct AttendPlan {
     int n_q_heads, n_kv_heads, group, head_dim;
-    int n_seqs, n_new_total, max_new, max_cached;
-    int split_keys, n_splits;
-    int row_block;          // GQA rows per workgroup
+    int n_seqs, n_new_total;
+    int row_block;          // GQA rows per unit
     bool use_mfma;
+    int n_wg, n_units, n_segments;
+    const int32_t* table;   // device copy of the schedule table
+    bool partials;          // some unit has several segments
     size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
 };
 
-// Fills every field from the sizes; returns false on invalid sizes.
+// Rows per unit of the path the sizes select: the matrix-core kernel where
+// the GQA-packed rows of a KV head form a real dense contraction (bf16 and at
+// least 32 rows), the VALU kernel otherwise.
+bool attend_uses_mfma(kvlink_dtype dt, int group, int max_new);
+int attend_row_block(bool use_mfma);
+
+// Fills every field from the sizes and the schedule's counts; returns false
+// on invalid sizes or counts.
 bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
-                      int n_seqs, int n_new_total, int max_new, int max_cached, int split_keys,
-                      AttendPlan* p);
+                      int n_new_total, const kvlink_attend_plan& sched, AttendPlan* p);
+
+// The schedule of kvlink_attend_make_plan (host).  Returns a kvlink_status
+// and, on failure, a message in *why.
+struct PlanCounts {
+    int n_wg, n_units, n_segments, row_block;
+    int64_t table_len;
+};
+int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
+                          int n_seqs, const int32_t* seq_new_ptr, const int32_t* new_visible,
+                          int n_compute_units, int n_workgroups, std::vector<int32_t>* table,
+                          PlanCounts* counts, const char** why);
 
 struct AttendArgs {
     const void* q_new;

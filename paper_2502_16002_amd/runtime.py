@@ -21,7 +21,7 @@ import numpy as np
 import torch
 
 from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
-               kvlink_attend_new_tokens, kvlink_attend_split_keys, kvlink_attend_stages,
+               kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_stages,
                kvlink_attend_workspace_bytes, kvlink_build_layout, kvlink_reencode_keys)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
@@ -47,7 +47,7 @@ class Batch:
 
     def __init__(self, dtype, n_layers, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                  seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq=None, doc_src_row=None,
-                 doc_src_pos0=None, split_keys=0, device="cuda"):
+                 doc_src_pos0=None, n_workgroups=0, device="cuda"):
         self.dtype = dtype
         self.torch_dtype = TORCH_DTYPE[dtype]
         self.n_layers, self.n_q_heads, self.n_kv_heads = n_layers, n_q_heads, n_kv_heads
@@ -68,19 +68,20 @@ class Batch:
         self.d_seq_cached = up(self.layout["seq_cached"])
         self.d_new_pos = up(self.layout["new_pos"])
         self.d_new_visible = up(self.layout["new_visible"])
-        self.set_split_keys(split_keys)
+        self.set_schedule(n_workgroups)
 
-    def set_split_keys(self, split_keys):
-        """split_keys 0 plans the split size from the layout and the device."""
-        if split_keys == 0 and self.n_new > 0:
-            cus = torch.cuda.get_device_properties(torch.device(self.device)).multi_processor_count
-            split_keys = kvlink_attend_split_keys(self.dtype, self.n_q_heads, self.n_kv_heads,
-                                                  self.head_dim, self.layout["seq_new_ptr"],
-                                                  self.layout["new_visible"], cus)
-        self.split_keys = split_keys
+    def set_schedule(self, n_workgroups=0):
+        """Build the split-K schedule (n_workgroups 0: the library's cost
+        model for this device), upload its table and size the workspace."""
+        cus = torch.cuda.get_device_properties(torch.device(self.device)).multi_processor_count
+        self.plan, table = kvlink_attend_make_plan(self.dtype, self.n_q_heads, self.n_kv_heads,
+                                                   self.head_dim, self.layout["seq_new_ptr"],
+                                                   self.layout["new_visible"], cus, n_workgroups)
+        self.plan_table = torch.from_numpy(np.ascontiguousarray(table)).to(self.device)
+        self.plan.table = self.plan_table.data_ptr()
+        self.n_workgroups = self.plan.n_workgroups
         self.ws_bytes = kvlink_attend_workspace_bytes(self.dtype, self.n_q_heads, self.n_kv_heads,
-                                                      self.head_dim, self.n_seqs, self.n_new,
-                                                      self.max_new, self.max_cached, split_keys)
+                                                      self.head_dim, self.n_new, self.plan)
         if self.ws_bytes == 0:
             raise ValueError("invalid attention sizes")
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
@@ -102,7 +103,7 @@ class Batch:
         args = (self.dtype, self.n_q_heads, self.n_kv_heads, self.head_dim, self.rope_theta,
                 self.softmax_scale, self.n_seqs, self.n_new, self.max_new, self.max_cached,
                 self.d_seq_new_ptr, self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
-                k_new, v_new, k_view, v_view, layer, out, lse, self.split_keys, ws,
+                k_new, v_new, k_view, v_view, layer, out, lse, self.plan, ws,
                 self.ws_bytes, stream)
         if stages == KVLINK_STAGE_ALL:
             kvlink_attend_new_tokens(*args)

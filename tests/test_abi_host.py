@@ -172,21 +172,40 @@ def test_reencode_empty_is_a_no_op(kv):
                             stream=0)
 
 
+def _plan(kv, dtype=None, hq=8, hkv=2, d=128, snp=(0, 10), vis=(100,) * 10, n_wg=0):
+    dtype = kv.KVLINK_BF16 if dtype is None else dtype
+    plan, _ = kv.kvlink_attend_make_plan(dtype, hq, hkv, d, list(snp), list(vis), 256, n_wg)
+    plan.table = 4096          # a fake, aligned device address: nothing is launched
+    return plan
+
+
 def _attend_args(kv, **change):
     a = dict(dtype=kv.KVLINK_BF16, hq=8, hkv=2, d=128, theta=5e5, scale=0.088, n_seqs=1,
              n_new=10, max_new=10, max_cached=100, snp=16, sc=16, pos=16, vis=16, q=4096,
              k=4096, v=4096, kview=_view(kv), vview=_view(kv), layer=0, out=4096, lse=None,
-             split=0, ws=1 << 20, ws_bytes=1 << 30)
+             plan=None, ws=1 << 20, ws_bytes=1 << 30)
     a.update(change)
+    if a["plan"] is None:
+        a["plan"] = _plan(kv)
     return a
 
 
-def _call_attend(kv, a):
-    kv.kvlink_attend_new_tokens(a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"],
-                                a["n_seqs"], a["n_new"], a["max_new"], a["max_cached"], a["snp"],
-                                a["sc"], a["pos"], a["vis"], a["q"], a["k"], a["v"], a["kview"],
-                                a["vview"], a["layer"], a["out"], a["lse"], a["split"], a["ws"],
-                                a["ws_bytes"], stream=0)
+def _call_attend(kv, a, stages=None):
+    args = (a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"], a["n_seqs"],
+            a["n_new"], a["max_new"], a["max_cached"], a["snp"], a["sc"], a["pos"], a["vis"],
+            a["q"], a["k"], a["v"], a["kview"], a["vview"], a["layer"], a["out"], a["lse"],
+            a["plan"], a["ws"], a["ws_bytes"])
+    if stages is None:
+        kv.kvlink_attend_new_tokens(*args, stream=0)
+    else:
+        kv.kvlink_attend_stages(*args, stream=0, stages=stages)
+
+
+def _bad_plan(kv, **fields):
+    p = _plan(kv)
+    for k, v in fields.items():
+        setattr(p, k, v)
+    return p
 
 
 @pytest.mark.parametrize("change,status", [
@@ -200,7 +219,6 @@ def _call_attend(kv, a):
     (dict(scale=float("inf")), 1),
     (dict(scale=0.0), 1),
     (dict(scale=-0.1), 1),
-    (dict(split=100), 1),
     (dict(snp=None), 1),
     (dict(q=None), 1),
     (dict(out=None), 1),
@@ -208,8 +226,22 @@ def _call_attend(kv, a):
     (dict(ws=1000), 4),                    # misaligned
     (dict(ws_bytes=16), 4),
     (dict(layer=-1), 1),
+    ("table", 1),                          # plan without a device table
+    ("table_misaligned", 1),
+    ("row_block", 1),                      # plan of the other path
+    ("n_seqs", 1),
+    ("table_len", 1),
+    ("thin", 1),                           # VALU-path plan for an MFMA-path call
 ])
 def test_attend_validation(kv, change, status):
+    if isinstance(change, str):
+        plan = {"table": lambda: _bad_plan(kv, table=None),
+                "table_misaligned": lambda: _bad_plan(kv, table=4100),
+                "row_block": lambda: _bad_plan(kv, row_block=16),
+                "n_seqs": lambda: _bad_plan(kv, n_seqs=2),
+                "table_len": lambda: _bad_plan(kv, table_len=3),
+                "thin": lambda: _plan(kv, snp=(0, 4), vis=(100,) * 4)}[change]()
+        change = dict(plan=plan)
     with pytest.raises(kv.KVLinkError) as e:
         _call_attend(kv, _attend_args(kv, **change))
     assert e.value.status == status
@@ -218,13 +250,8 @@ def test_attend_validation(kv, change, status):
 
 @pytest.mark.parametrize("stages", [0, 8, 15])
 def test_attend_stages_rejects_bad_masks(kv, stages):
-    a = _attend_args(kv)
     with pytest.raises(kv.KVLinkError) as e:
-        kv.kvlink_attend_stages(a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"],
-                                a["n_seqs"], a["n_new"], a["max_new"], a["max_cached"], a["snp"],
-                                a["sc"], a["pos"], a["vis"], a["q"], a["k"], a["v"], a["kview"],
-                                a["vview"], a["layer"], a["out"], a["lse"], a["split"], a["ws"],
-                                a["ws_bytes"], stream=0, stages=stages)
+        _call_attend(kv, _attend_args(kv), stages=stages)
     assert e.value.status == 1
 
 
@@ -234,27 +261,127 @@ def test_attend_no_new_tokens_is_a_no_op(kv):
 
 def test_workspace_bytes(kv):
     f = kv.kvlink_attend_workspace_bytes
-    assert f(kv.KVLINK_BF16, 32, 8, 128, 1, 114, 114, 2000, 0) > 114 * 32 * 128 * 2
-    assert f(kv.KVLINK_BF16, 32, 8, 96, 1, 114, 114, 2000, 0) == 0
-    assert f(kv.KVLINK_BF16, 32, 8, 128, 1, 114, 114, 2000, 100) == 0
-    # more splits need more partial storage
-    assert f(kv.KVLINK_F32, 4, 2, 64, 1, 22, 22, 96, 128) >= f(kv.KVLINK_F32, 4, 2, 64, 1, 22, 22, 96, 1024)
+    bf, f32 = kv.KVLINK_BF16, kv.KVLINK_F32
+    one = _plan(kv, n_wg=1)                   # one segment per unit: no partials
+    assert one.n_segments == one.n_units
+    assert f(bf, 8, 2, 128, 10, one) == _align(10 * 8 * 128 * 2)
+    assert f(bf, 8, 2, 96, 10, one) == 0
+    many = _plan(kv, n_wg=1 << 20)            # one tile per segment
+    assert many.n_segments > many.n_units
+    assert f(bf, 8, 2, 128, 10, many) == (_align(10 * 8 * 128 * 2) +
+                                           _align(many.n_segments * 256 * 128 * 4) +
+                                           _align(many.n_segments * 256 * 2 * 4))
+    thin = _plan(kv, f32, 4, 2, 64, (0, 22), [200] * 22, n_wg=5)
+    assert thin.row_block == 16 and thin.n_segments > thin.n_units
+    assert f(f32, 4, 2, 64, 22, thin) > f(f32, 4, 2, 64, 22, _plan(kv, f32, 4, 2, 64, (0, 22),
+                                                                     [200] * 22, n_wg=1))
 
 
-def test_split_planner(kv):
-    """The host split planner returns a positive multiple of 128 for valid
-    layouts, no more than the longest row block needs, and 0 on bad input."""
-    for name in ["tiny-f32-3x32", "llama8b-32layer-10doc", "llama8b-32layer-40x512",
-                 "llama8b-paged-16req"]:
-        w = workloads.get(name)
-        sdp = np.concatenate([[0], np.cumsum([len(d) for d in w.docs])])
-        dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
-        lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
-        L = kv.kvlink_build_layout(sdp, dl, lc, w.n_query)
-        dt = kv.KVLINK_F32 if w.dtype == "f32" else kv.KVLINK_BF16
-        sk = kv.kvlink_attend_split_keys(dt, w.n_q_heads, w.n_kv_heads, w.head_dim,
-                                         L["seq_new_ptr"], L["new_visible"], 256)
-        assert sk > 0 and sk % 128 == 0
-        assert sk < int(L["totals"][5]) + 128
-    assert kv.kvlink_attend_split_keys(kv.KVLINK_BF16, 32, 8, 96, [0, 4], [1, 2, 3, 4], 256) == 0
-    assert kv.kvlink_attend_split_keys(kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 0) == 0
+def _align(x):
+    return (x + 255) // 256 * 256
+
+
+def _decode(plan, table, n_seqs):
+    """Split a schedule table into its sections (layout in include/kvlink.h)."""
+    t = np.asarray(table)
+    n_wg, n_u = plan.n_workgroups, plan.n_units
+    wg = t[:4 * n_wg].reshape(n_wg, 4)
+    units = t[4 * n_wg:4 * n_wg + 4 * n_u].reshape(n_u, 4)
+    o = 4 * n_wg + 4 * n_u
+    unit_seg = t[o:o + n_u + 1]
+    seq_unit = t[o + n_u + 1:o + n_u + 1 + n_seqs + 1]
+    assert len(t) == o + n_u + 1 + n_seqs + 1 == plan.table_len
+    return wg, units, unit_seg, seq_unit
+
+
+def _expected_units(L, G, hkv, rb):
+    """(s, h, rho0, tiles) of every unit, from the layout and the attention
+    map of Sec. 2.3: the block's last token sees new_visible cached rows and
+    the new rows up to its own."""
+    snp, vis = L["seq_new_ptr"], L["new_visible"]
+    out, seq_unit = [], []
+    for s in range(len(snp) - 1):
+        seq_unit.append(len(out))
+        rows_s = int(snp[s + 1] - snp[s]) * G
+        for h in range(hkv):
+            for rho0 in range(0, rows_s, rb):
+                r_last = (min(rho0 + rb, rows_s) - 1) // G
+                nvirt = int(vis[snp[s] + r_last]) + r_last + 1
+                out.append((s, h, rho0, -(-nvirt // 64)))
+    seq_unit.append(len(out))
+    return np.array(out, np.int64).reshape(-1, 4), np.array(seq_unit)
+
+
+def _check_schedule(kv, w, n_wg_req):
+    sdp = np.concatenate([[0], np.cumsum([len(d) for d in w.docs])])
+    dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
+    lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
+    L = kv.kvlink_build_layout(sdp, dl, lc, w.n_query)
+    dt = kv.KVLINK_F32 if w.dtype == "f32" else kv.KVLINK_BF16
+    plan, table = kv.kvlink_attend_make_plan(dt, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                             L["seq_new_ptr"], L["new_visible"], 256, n_wg_req)
+    G = w.n_q_heads // w.n_kv_heads
+    max_new = int(np.max(np.diff(L["seq_new_ptr"])))
+    assert plan.row_block == (256 if w.dtype == "bf16" and max_new * G >= 32 else 16)
+    wg, units, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
+    exp_units, exp_seq_unit = _expected_units(L, G, w.n_kv_heads, plan.row_block)
+    assert np.array_equal(units, exp_units)
+    assert np.array_equal(seq_unit, exp_seq_unit)
+    T = int(units[:, 3].sum())
+    n = plan.n_workgroups
+    assert 1 <= n <= T
+    if n_wg_req:
+        assert n == min(n_wg_req, T)
+    # equal contiguous ranges that cover every tile of every unit once, in order
+    counts = wg[:, 2]
+    assert counts.min() >= T // n and counts.max() <= -(-T // n) and counts.sum() == T
+    off = np.concatenate([[0], np.cumsum(units[:, 3])])
+    start = np.concatenate([[0], np.cumsum(counts)])
+    seg = 0
+    first_seg = {}
+    for w_i in range(n):
+        u, t0, cnt, s0 = (int(x) for x in wg[w_i])
+        assert off[u] + t0 == start[w_i] and 0 <= t0 < units[u, 3]
+        assert s0 == seg
+        left = cnt
+        while left > 0:
+            take = min(int(units[u, 3]) - t0, left)
+            first_seg.setdefault(u, seg)
+            seg += 1
+            left -= take
+            u, t0 = u + 1, 0
+    assert seg == plan.n_segments
+    assert [first_seg[u] for u in range(plan.n_units)] + [seg] == list(unit_seg)
+    return plan
+
+
+@pytest.mark.parametrize("name", ["tiny-f32-3x32", "llama1b-1layer-10doc",
+                                  "llama8b-32layer-10doc", "llama8b-32layer-40x512",
+                                  "llama8b-paged-16req"])
+def test_attend_schedule(kv, name):
+    """Every schedule, chosen by the cost model or forced, deals every tile of
+    every unit out exactly once, in equal contiguous ranges, with consistent
+    segment numbering."""
+    w = workloads.get(name)
+    chosen = _check_schedule(kv, w, 0)
+    for n in [1, 3, 64, 1 << 20]:
+        _check_schedule(kv, w, n)
+    # the long-context workload's tile count keeps the whole chip busy
+    if name == "llama8b-32layer-40x512":
+        assert chosen.n_workgroups >= 240
+
+
+def test_attend_schedule_errors(kv):
+    mk = kv.kvlink_attend_make_plan
+    with pytest.raises(kv.KVLinkError) as e:
+        mk(kv.KVLINK_BF16, 32, 8, 96, [0, 4], [1, 2, 3, 4], 256)
+    assert e.value.status == 2
+    for args, status in [((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 0), 1),
+                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 256, -1), 1),
+                         ((kv.KVLINK_BF16, 32, 8, 128, [1, 4], [1, 2, 3, 4], 256), 3),
+                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4, 3], [1, 2, 3, 4], 256), 3),
+                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, -2, 3, 4], 256), 3),
+                         ((kv.KVLINK_BF16, 32, 6, 128, [0, 4], [1, 2, 3, 4], 256), 1)]:
+        with pytest.raises(kv.KVLinkError) as e:
+            mk(*args)
+        assert e.value.status == status, args
