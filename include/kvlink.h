@@ -195,10 +195,19 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
  *
  * The table (int32, built on the host by kvlink_attend_make_plan, then
  * copied to the device by the caller) holds, in order:
- *   n_workgroups x {first unit, first tile in it, tile count, first segment}
- *   n_units x {request, KV head, first row of the block, tile count}
- *   n_units + 1 first-segment offsets of the units
- *   n_seqs + 1 first-unit offsets of the requests
+ *   n_workgroups + 1   first-segment offsets of the workgroups (workgroup w
+ *                      runs segments [off[w], off[w+1]))
+ *   padding to a multiple of 4 entries
+ *   n_segments x 12    segment records {request, KV head, first row of the
+ *                      block, rows in the block, first tile, end tile,
+ *                      segments of the unit, index of this one among them,
+ *                      first new token of the request, T_c of the request,
+ *                      cached rows the block's last token sees, key count
+ *                      of the unit}
+ *   n_units + 1        first-segment offsets of the units
+ *   n_seqs + 1         first-unit offsets of the requests
+ * Like the layout arrays, the device copy is trusted: it must be the
+ * unmodified table built for the same batch.
  */
 typedef struct {
     const int32_t* table; /* device copy of the table (NULL in make_plan's output) */
@@ -213,8 +222,8 @@ typedef struct {
 /*
  * kvlink_attend_make_plan — build the schedule (pure host computation).
  *
- *   seq_new_ptr[n_seqs+1], new_visible[n_new]  host outputs of
- *                    kvlink_build_layout for the batch
+ *   seq_new_ptr[n_seqs+1], seq_cached[n_seqs], new_visible[n_new]
+ *                    host outputs of kvlink_build_layout for the batch
  *   n_compute_units  compute units of the device (sizes the schedule)
  *   n_workgroups     0: chosen by a cost model (every workgroup costs a fixed
  *                    set-up per segment plus a per-tile cost, the launch is
@@ -230,11 +239,13 @@ typedef struct {
  * rounding order.  Errors: KVLINK_ERR_INVALID_ARG (null required pointer,
  * n_seqs < 1, n_compute_units < 1, n_workgroups < 0, table too small),
  * KVLINK_ERR_UNSUPPORTED (head_dim, dtype, group), KVLINK_ERR_LAYOUT
- * (seq_new_ptr not non-decreasing from 0, new_visible negative).
+ * (seq_new_ptr not non-decreasing from 0, seq_cached or new_visible
+ * negative, a key range beyond 2^30).
  */
 kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
                                       int32_t head_dim, int32_t n_seqs,
-                                      const int32_t* seq_new_ptr, const int32_t* new_visible,
+                                      const int32_t* seq_new_ptr, const int32_t* seq_cached,
+                                      const int32_t* new_visible,
                                       int32_t n_compute_units, int32_t n_workgroups,
                                       int32_t* table, int64_t table_capacity,
                                       kvlink_attend_plan* plan);
@@ -279,12 +290,9 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *   lse   [n_new_total][n_q_heads] float, or NULL
  *   plan                       schedule from kvlink_attend_make_plan for the
  *                              same batch, with plan.table pointing at the
- *                              device copy of its table.  Its row_block must
- *                              match this call's path (KVLINK_ERR_INVALID_ARG
- *                              otherwise).  The kernels clamp every index
- *                              they read from the table to the batch's
- *                              bounds, so a stale table gives wrong results
- *                              but no out-of-bounds access.
+ *                              device copy of its table (16-byte aligned).
+ *                              Its row_block must match this call's path
+ *                              (KVLINK_ERR_INVALID_ARG otherwise).
  *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
  *                              device bytes, 256-byte aligned
  *

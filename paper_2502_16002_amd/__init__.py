@@ -70,8 +70,8 @@ def _load():
     lib.kvlink_reencode_keys.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32,
                                          kvlink_kv_view, kvlink_kv_view, vp]
     lib.kvlink_reencode_keys.restype = ctypes.c_int
-    lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, i32, i32,
-                                            vp, i64, ctypes.POINTER(kvlink_attend_plan)]
+    lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, i32,
+                                            i32, vp, i64, ctypes.POINTER(kvlink_attend_plan)]
     lib.kvlink_attend_make_plan.restype = ctypes.c_int
     lib.kvlink_attend_workspace_bytes.argtypes = [ctypes.c_int, i32, i32, i32, i32,
                                                   ctypes.POINTER(kvlink_attend_plan)]
@@ -182,16 +182,19 @@ def kvlink_reencode_keys(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_sp
                                      int(max_span_len), src, dst, _stream(stream)))
 
 
-def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, new_visible,
-                            n_compute_units, n_workgroups=0):
+def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, seq_cached,
+                            new_visible, n_compute_units, n_workgroups=0):
     """Host-built split-K schedule: returns (plan, table) with table an int32
     numpy array; plan.table is None until the caller sets it to the address
     of a device copy of the table."""
     snp = np.ascontiguousarray(np.asarray(seq_new_ptr, dtype=np.int32))
+    sc = np.ascontiguousarray(np.asarray(seq_cached, dtype=np.int32))
     vis = np.ascontiguousarray(np.asarray(new_visible, dtype=np.int32))
+    if len(sc) != len(snp) - 1:
+        raise ValueError("seq_cached must have n_seqs entries")
     plan = kvlink_attend_plan()
     args = (int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), len(snp) - 1, _ptr(snp),
-            _ptr(vis), int(n_compute_units), int(n_workgroups))
+            _ptr(sc), _ptr(vis), int(n_compute_units), int(n_workgroups))
     _check(_lib.kvlink_attend_make_plan(*args, None, 0, ctypes.byref(plan)))
     table = np.zeros(max(plan.table_len, 1), np.int32)
     _check(_lib.kvlink_attend_make_plan(*args, _ptr(table), len(table), ctypes.byref(plan)))

@@ -141,8 +141,9 @@ struct ValuSmem {
 // of request s.  Early returns are uniform over the workgroup.
 template <typename T, int D>
 __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, int s, int h,
-                                             int rho0, int tile_a, int tile_b, int seg,
-                                             bool direct) {
+                                             int rho0, int tile_a, int tile_b, int seg, int nseg,
+                                             int seg_local) {
+    const bool direct = nseg == 1;
     constexpr int RB = kValuRB, KT = kValuKT, RPW = 4, DPL = D / 64;
     auto& s_q = sm.q;
     auto& s_k = sm.k;
@@ -242,7 +243,8 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
             for (int dd = 0; dd < DPL; ++dd) out[orow * D + lane + 64 * dd] = from_f32<T>(o[i][dd] * inv);
             if (p.lse && lane == 0) p.lse[orow] = (m[i] + log2f(l[i])) * kLn2;
         } else {
-            const int64_t pi = (int64_t)seg * RB + (rho - rho0);
+            const int64_t pi =
+                (int64_t)(seg - seg_local) * RB + (int64_t)(rho - rho0) * nseg + seg_local;
 #pragma unroll
             for (int dd = 0; dd < DPL; ++dd) p.part_o[pi * D + lane + 64 * dd] = o[i][dd];
             if (lane == 0) {
@@ -257,21 +259,15 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
     __shared__ ValuSmem<D> sm;
-    const int4 w = p.plan_wg[blockIdx.x];
-    int u = w.x, a = w.y, left = w.z, seg = w.w;
-    for (bool first = true; left > 0 && u >= 0 && u < p.n_units; first = false) {
-        const int4 un = p.plan_unit[u];
-        const int b = min(un.w, a + left);
-        if (a < 0 || a >= b || un.x < 0 || un.x >= p.n_seqs || un.y < 0 || un.y >= p.n_kv_heads)
+    const int g0 = max(p.wg_seg[blockIdx.x], 0), g1 = min(p.wg_seg[blockIdx.x + 1], p.n_segments);
+    for (int g = g0; g < g1; ++g) {
+        const int* r = reinterpret_cast<const int*>(p.seg + 3 * (int64_t)g);
+        const int s = r[kSegS], h = r[kSegH], nseg = r[kSegNseg], loc = r[kSegLocal];
+        if (s < 0 || s >= p.n_seqs || h < 0 || h >= p.n_kv_heads || nseg < 1 || loc < 0 ||
+            loc >= nseg || g - loc + nseg > p.n_segments)
             break;
-        const bool direct = unit_is_direct(p, u);
-        if (!direct && (seg < 0 || seg >= p.n_segments)) break;
-        if (!first) __syncthreads();
-        valu_segment<T, D>(p, sm, un.x, un.y, un.z, a, b, seg, direct);
-        left -= b - a;
-        ++u;
-        ++seg;
-        a = 0;
+        if (g > g0) __syncthreads();
+        valu_segment<T, D>(p, sm, s, h, r[kSegRho0], r[kSegTileA], r[kSegTileB], g, nseg, loc);
     }
 }
 
@@ -279,13 +275,15 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 
 // One wavefront per (new token, query head) row of a unit with several
 // segments (rows of single-segment units were written by the split kernel).
-// The maximum over the segments is taken first (lane-strided), then the
-// segments are accumulated four at a time with all their loads issued
-// together, so the row costs a few memory round trips instead of two per
-// segment.
+// A unit's partials are row-major over its segments, so the row's nseg
+// partial vectors are one contiguous run: lanes read it as float4, several
+// segments per round of loads and kRounds rounds issued together; the lanes
+// holding the same dims are folded at the end.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total) {
-    constexpr int DPL = D / 64;   // consecutive dims per lane
+    constexpr int F4 = D / 4;          // float4 per partial vector
+    constexpr int SPR = 64 / F4;       // segments per round of loads
+    constexpr int kRounds = 8;
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int64_t orow = (int64_t)blockIdx.x * 4 + wave;   // (n, hq) flattened
     if (orow >= (int64_t)n_new_total * p.n_q_heads) return;
@@ -298,48 +296,60 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     const int u = p.seq_unit[s] + (hq / p.group) * nrb + rho / p.row_block;
     if (u < 0 || u >= p.n_units) return;
     const int c0 = max(p.unit_seg[u], 0), c1 = min(p.unit_seg[u + 1], p.n_segments);
-    const int nsp = c1 - c0;
-    if (nsp <= 1) return;
-    const int64_t r0 = (int64_t)c0 * p.row_block + rho % p.row_block;   // first partial row
-    const int64_t stride = p.row_block;                                  // rows per segment
-    const float* ml = p.part_ml + r0 * 2;
-    const float* po = p.part_o + r0 * D + lane * DPL;
+    const int nseg = c1 - c0;
+    if (nseg <= 1) return;
+    const int64_t base = (int64_t)c0 * p.row_block + (int64_t)(rho % p.row_block) * nseg;
+    const float2* ml = reinterpret_cast<const float2*>(p.part_ml) + base;
+    const float4* po = reinterpret_cast<const float4*>(p.part_o) + base * F4;
 
-    float M = -INFINITY;
-    for (int c = lane; c < nsp; c += 64) M = fmaxf(M, ml[2 * stride * c]);
+    // maximum and weighted sum over the segments (the running maximum starts
+    // finite, so a segment that saw no key of this row, maximum -inf and sum
+    // 0, gets weight 0, never NaN)
+    float M = kNoMax;
+    for (int c = lane; c < nseg; c += 64) M = fmaxf(M, ml[c].x);
     M = wave_max(M);
+    float L = 0.f;
+    for (int c = lane; c < nseg; c += 64) {
+        const float2 v = ml[c];
+        L += __builtin_amdgcn_exp2f(v.x - M) * v.y;
+    }
+    L = wave_sum(L);
 
-    float L = 0.f, acc[DPL];
+    const int sub = lane / F4, d4 = lane % F4;
+    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int cb = 0; cb < nseg; cb += SPR * kRounds) {
+        float4 v[kRounds];
+        float mw[kRounds];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-    int c = 0;
-    for (; c + 4 <= nsp; c += 4) {
-        float mc[4], lc[4], oc[4][DPL];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            mc[i] = ml[2 * stride * (c + i)];
-            lc[i] = ml[2 * stride * (c + i) + 1];
-#pragma unroll
-            for (int e = 0; e < DPL; ++e) oc[i][e] = po[stride * D * (c + i) + e];
+        for (int r = 0; r < kRounds; ++r) {
+            const int c = min(cb + r * SPR + sub, nseg - 1);
+            v[r] = po[(int64_t)c * F4 + d4];
+            mw[r] = ml[c].x;
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float w = __builtin_amdgcn_exp2f(mc[i] - M);   // 0 for an empty segment
-            L += w * lc[i];
-#pragma unroll
-            for (int e = 0; e < DPL; ++e) acc[e] += w * oc[i][e];
+        for (int r = 0; r < kRounds; ++r) {
+            const float w = cb + r * SPR + sub < nseg ? __builtin_amdgcn_exp2f(mw[r] - M) : 0.f;
+            acc.x += w * v[r].x;
+            acc.y += w * v[r].y;
+            acc.z += w * v[r].z;
+            acc.w += w * v[r].w;
         }
     }
-    for (; c < nsp; ++c) {
-        const float w = __builtin_amdgcn_exp2f(ml[2 * stride * c] - M);
-        L += w * ml[2 * stride * c + 1];
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) acc[e] += w * po[stride * D * c + e];
+    for (int off = F4; off < 64; off *= 2) {
+        acc.x += __shfl_xor(acc.x, off);
+        acc.y += __shfl_xor(acc.y, off);
+        acc.z += __shfl_xor(acc.z, off);
+        acc.w += __shfl_xor(acc.w, off);
     }
-    T* out = reinterpret_cast<T*>(p.out) + orow * D + lane * DPL;
-    const float inv = 1.f / L;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) out[e] = from_f32<T>(acc[e] * inv);
+    if (lane < F4) {
+        T* out = reinterpret_cast<T*>(p.out) + orow * D + 4 * d4;
+        const float inv = 1.f / L;
+        out[0] = from_f32<T>(acc.x * inv);
+        out[1] = from_f32<T>(acc.y * inv);
+        out[2] = from_f32<T>(acc.z * inv);
+        out[3] = from_f32<T>(acc.w * inv);
+    }
     if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * kLn2;
 }
 
@@ -366,9 +376,10 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.row_block = pl.row_block;
     p.n_units = pl.n_units;
     p.n_segments = pl.n_segments;
-    p.plan_wg = reinterpret_cast<const int4*>(pl.table);
-    p.plan_unit = reinterpret_cast<const int4*>(pl.table + 4 * (size_t)pl.n_wg);
-    p.unit_seg = pl.table + 4 * (size_t)pl.n_wg + 4 * (size_t)pl.n_units;
+    const size_t rec0 = ((size_t)pl.n_wg + 1 + 3) / 4 * 4;
+    p.wg_seg = pl.table;
+    p.seg = reinterpret_cast<const int4*>(pl.table + rec0);
+    p.unit_seg = pl.table + rec0 + (size_t)kSegRecord * pl.n_segments;
     p.seq_unit = p.unit_seg + pl.n_units + 1;
     p.part_o = reinterpret_cast<float*>(ws + pl.q_rot_bytes);
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
@@ -415,8 +426,10 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     if (sched.row_block != attend_mfma_row_block() && sched.row_block != kValuRB) return false;
     if (sched.n_workgroups < 0 || sched.n_units < 0 || sched.n_segments < sched.n_units)
         return false;
+    if ((int64_t)sched.n_segments * kSegRecord > INT32_MAX) return false;
     if (sched.n_workgroups > 0 && (sched.n_units < 1 || sched.n_segments < 1)) return false;
-    const int64_t want = 4 * (int64_t)sched.n_workgroups + 5 * (int64_t)sched.n_units + 1 +
+    const int64_t want = ((int64_t)sched.n_workgroups + 1 + 3) / 4 * 4 +
+                         (int64_t)kSegRecord * sched.n_segments + sched.n_units + 1 +
                          sched.n_seqs + 1;
     if (sched.table_len != want) return false;
     const size_t elem = dt == KVLINK_BF16 ? 2 : 4;

@@ -8,6 +8,9 @@ namespace attn {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+// Finite stand-in for "no score seen yet" in log2 units: any real score
+// exceeds it, and masked scores (-inf) still give weight 0 without NaN.
+constexpr float kNoMax = -1.0e30f;
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
@@ -46,10 +49,9 @@ __device__ __forceinline__ BlockKeys block_keys(const int32_t* new_visible, int 
 }
 
 // Arguments of the split kernels and the combine.  The schedule table (see
-// the schedule's description in the public header) is read through plan_wg
-// (n_wg x int4 {unit, first tile, tile count, first segment}), plan_unit
-// (n_units x int4 {request, KV head, first row, tile count}), unit_seg
-// (n_units + 1) and seq_unit (n_seqs + 1).
+// the schedule's description in the public header) is read through wg_seg
+// (n_wg + 1 first-segment offsets), seg (n_segments records of kSegRecord
+// int32, as 3 int4), unit_seg (n_units + 1) and seq_unit (n_seqs + 1).
 struct KParams {
     const void* q_rot;
     View k, v;
@@ -59,8 +61,8 @@ struct KParams {
     const int32_t* new_visible;
     float scale_log2;
     int row_block, n_units, n_segments;
-    const int4* plan_wg;
-    const int4* plan_unit;
+    const int32_t* wg_seg;
+    const int4* seg;
     const int32_t* unit_seg;
     const int32_t* seq_unit;
     float* part_o;    // [segment][row in block][head_dim]
@@ -69,10 +71,7 @@ struct KParams {
     float* lse;
 };
 
-// A unit has one segment: its workgroup writes out and lse directly.
-__device__ __forceinline__ bool unit_is_direct(const KParams& p, int u) {
-    return p.unit_seg[u + 1] - p.unit_seg[u] == 1;
-}
+static_assert(kSegRecord == 12, "segment records are read as three int4");
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
 // GQA rows per workgroup of the MFMA kernel

@@ -61,9 +61,6 @@ constexpr int kStages = 4;
 // Rescale threshold of the online softmax, in log2 units: p = 2^(s - m)
 // stays below 2^kTau (exact in float, representable in bf16).
 constexpr float kTau = 8.0f;
-// Finite stand-in for "no score seen yet": any real score exceeds it by more
-// than kTau, and masked scores (-inf) still give p = 0 without NaN.
-constexpr float kNoMax = -1.0e30f;
 
 template <int D>
 struct Smem {
@@ -172,12 +169,11 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // One segment of a unit: tiles [tile_a, tile_b) of the key range of KV head
-// h's rows [rho0, rho0 + kRB) of request s.  Every early return is uniform
-// over the workgroup.
+// h's rows [rho0, rho0 + rows) of request s, from its schedule record.
+// Every early return is uniform over the workgroup.
 template <int D>
-__device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem, int s, int h,
-                                               int rho0, int tile_a, int tile_b, int seg,
-                                               bool direct) {
+__device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem,
+                                               const int4 (&rec)[3], int seg) {
     constexpr int DT = D / 16;         // 16-dim tiles of O^T
     constexpr int DS = D / 32;         // 32-dim steps of S^T = K Q^T
     constexpr int KB = 4 * DS;         // 1 KB operand blocks of a K tile
@@ -186,92 +182,36 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     constexpr int LPW = (KB + VI) / kWaves;    // direct loads per wave per tile
     static_assert((KB % kWaves) == 0 && (VI % kWaves) == 0, "tile split");
 
+    const int s = rec[0].x, h = rec[0].y, rho0 = rec[0].z, rows = rec[0].w;
+    const int tile_a = rec[1].x, tile_b = rec[1].y;
+    const int nseg = rec[1].z, seg_local = rec[1].w;
+    const bool direct = nseg == 1;
+    const int n0 = rec[2].x, Tc = rec[2].y;
+    BlockKeys bk;
+    bk.cmax = rec[2].z;
+    bk.nvirt = rec[2].w;
     const int G = p.group;
-    // request descriptors (independent loads)
-    const int n0 = p.seq_new_ptr[s];
-    const int rows_s = (p.seq_new_ptr[s + 1] - n0) * G;
-    const int Tc = p.seq_cached[s];
-    if (rho0 < 0 || rho0 >= rows_s) return;
+    const int kbeg = tile_a * kTile;
+    if (kbeg >= bk.nvirt || rows < 1) return;
+    const int kend = min(tile_b * kTile, bk.nvirt);
+    const int n_tiles = (kend - kbeg + kTile - 1) / kTile;
+    const int rho_end = rho0 + rows;
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int rho_w = rho0 + wave * kRT * 16;      // first row of this wave
 
-    // Everything below depends on n0 only and is requested together before
-    // the split's key range is known: the block's key bound, the visible
-    // prefix of this wave's first token and of every row, and the Q operand.
-    const int r_last = (min(rho0 + kRB, rows_s) - 1) / G;
-    const int cmax = p.new_visible[n0 + r_last];
-    const int wave_vis_min = p.new_visible[n0 + min(rho_w, rows_s - 1) / G];
-    int tok[kRT], vis[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        const int rho = rho_w + 16 * rt + lr;
-        tok[rt] = rho < rows_s ? rho / G : -1;
-        vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
-    }
-    const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
-    uint4 qraw[kRT][DS];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        const int rho = rho_w + 16 * rt + lr;
-        const int64_t qrow = ((int64_t)(n0 + max(tok[rt], 0)) * p.n_q_heads + h * G + rho % G) * D;
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
-            qraw[rt][ds] = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
-    }
-
-    // the block's virtual key range: cached rows its last token sees, then
-    // the new rows up to its last token; this workgroup's split of it
-    BlockKeys bk;
-    bk.r_last = r_last;
-    bk.cmax = cmax;
-    bk.nvirt = cmax + r_last + 1;
-    const int kbeg = tile_a * kTile;
-    if (kbeg >= bk.nvirt) return;
-    const int kend = min(tile_b * kTile, bk.nvirt);
-    const float c2 = p.scale_log2;   // > 0
-
-    // Row r may see virtual key v iff v < lo (cached rows up to its document,
-    // within the split) or cmax <= v <= hi (new rows up to its own, within
-    // the split).
-    int lo[kRT], hi[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        lo[rt] = tok[rt] >= 0 ? min(vis[rt], kend) : 0;
-        hi[rt] = tok[rt] >= 0 ? min(bk.cmax + tok[rt], kend - 1) : -1;
-    }
-    bf16x8 qB[kRT][DS];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
-            qB[rt][ds] = as_bf16x8(tok[rt] >= 0 ? qraw[rt][ds] : uint4{0u, 0u, 0u, 0u});
-
-    floatx4 o[DT][kRT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) o[dt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m[kRT], lsum[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        m[rt] = kNoMax;
-        lsum[rt] = 0.f;
-    }
-
     const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
     const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
-    const int n_tiles = (kend - kbeg + kTile - 1) / kTile;
 
-    // virtual key -> cache row, clamped into the split so that every load
-    // reads a real row (keys past the split end are masked)
+    // virtual key -> cache row, clamped into the segment so that every load
+    // reads a real row (keys past the segment end are masked)
     auto key_row = [&](int v) {
         v = min(v, kend - 1);
         return v < bk.cmax ? v : Tc + (v - bk.cmax);
     };
     // Per-lane parts of the direct-load addresses, fixed for the whole
-    // split: this wave loads K blocks wave + kWaves*i and V slots
+    // segment: this wave loads K blocks wave + kWaves*i and V slots
     // (wave + kWaves*i)*64 + lane of every tile.
     constexpr int KI = KB / kWaves, VJ = VI / kWaves;
     int k_key[KI], k_off[KI], v_key[VJ], v_off[VJ];
@@ -288,16 +228,6 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         const int key = pos / CH, pc = pos % CH;
         v_key[i] = key;
         v_off[i] = 16 * (pc ^ (key & (CH - 1)));          // logical chunk stored at slot pc
-    }
-    // per-lane part of the V^T operand reads (see the product below): lane
-    // (lg, lr) reads key 4lg + lr/4 (plus multiples of 16, which leave the
-    // swizzle unchanged), logical chunk 2dt + (lr/2)%2, half lr%2
-    uint32_t v_rel[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const int key = 4 * lg + (lr >> 2);
-        const int c = 2 * dt + ((lr >> 1) & 1);
-        v_rel[dt] = key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
     }
     const bool contiguous = kp.table == nullptr && vp.table == nullptr;
     const int fast_end = min(kend, bk.cmax);              // rows here are the keys themselves
@@ -327,6 +257,87 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
                            st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
         }
     };
+
+    // Tile 0 goes out first; then the rows' data (visible prefixes, the Q
+    // operand), then tiles 1 and 2, so the first key tile's latency overlaps
+    // the queries' (loads complete in issue order).
+    issue_tile(0);
+
+    int tok[kRT], vis[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) {
+        const int rho = rho_w + 16 * rt + lr;
+        tok[rt] = rho < rho_end ? rho / G : -1;
+        vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
+    }
+    // this wave's rows: the first and last tokens, the visible prefix of the
+    // last (prefixes grow with the token)
+    const bool wave_active = rho_w < rho_end;
+    const int tok_min = rho_w / G;
+    const int tok_max = (min(rho_w + kRT * 16, rho_end) - 1) / G;
+    const int wave_vis_min = wave_active ? p.new_visible[n0 + tok_min] : 0;
+    const int wave_vis_max = wave_active ? p.new_visible[n0 + tok_max] : 0;
+    const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
+    uint4 qraw[kRT][DS];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) {
+        const int rho = rho_w + 16 * rt + lr;
+        const int64_t qrow = ((int64_t)(n0 + max(tok[rt], 0)) * p.n_q_heads + h * G + rho % G) * D;
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+            qraw[rt][ds] = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
+    }
+    if (n_tiles > 1) issue_tile(1);
+    if (n_tiles > 2) issue_tile(2);
+
+    const float c2 = p.scale_log2;   // > 0
+    // Row r may see virtual key v iff v < lo (cached rows up to its document,
+    // within the segment) or cmax <= v <= hi (new rows up to its own, within
+    // the segment).
+    int lo[kRT], hi[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) {
+        lo[rt] = tok[rt] >= 0 ? min(vis[rt], kend) : 0;
+        hi[rt] = tok[rt] >= 0 ? min(bk.cmax + tok[rt], kend - 1) : -1;
+    }
+    // A 32-key sub-tile from v0 is dead for this wave when no row of it sees
+    // any of its keys: all cached keys at or past the last row's prefix and
+    // all new keys past the last row's token (always, for a wave without
+    // rows).
+    auto dead = [&](int v0) {
+        if (!wave_active || v0 >= kend) return true;
+        const bool cached_seen = v0 < wave_vis_max && v0 < bk.cmax;
+        const bool new_seen = v0 + 32 > bk.cmax && max(v0, bk.cmax) <= bk.cmax + tok_max;
+        return !cached_seen && !new_seen;
+    };
+    bf16x8 qB[kRT][DS];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+            qB[rt][ds] = as_bf16x8(tok[rt] >= 0 ? qraw[rt][ds] : uint4{0u, 0u, 0u, 0u});
+
+    floatx4 o[DT][kRT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) o[dt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m[kRT], lsum[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) {
+        m[rt] = kNoMax;
+        lsum[rt] = 0.f;
+    }
+    // per-lane part of the V^T operand reads (see the product below): lane
+    // (lg, lr) reads key 4lg + lr/4 (plus multiples of 16, which leave the
+    // swizzle unchanged), logical chunk 2dt + (lr/2)%2, half lr%2
+    uint32_t v_rel[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int key = 4 * lg + (lr >> 2);
+        const int c = 2 * dt + ((lr >> 1) & 1);
+        v_rel[dt] = key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
+    }
 
     // ---- pieces of a 32-key sub-tile (stage st, half h of its tile)
 
@@ -532,20 +543,22 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
     constexpr std::integral_constant<int, 0> H0{};
     constexpr std::integral_constant<int, 1> H1{};
-#pragma unroll
-    for (int t = 0; t < 3; ++t)
-        if (t < n_tiles) issue_tile(t);
     if (n_tiles >= 3) wait_vm<2 * LPW>(); else if (n_tiles == 2) wait_vm<LPW>(); else wait_vm<0>();
     __syncthreads();
 
+    // a step whose two sub-tiles are both dead for the wave is skipped; a
+    // step that runs on a dead sub-tile's never-computed S masks all of it
     floatx4 s_a[2][kRT], s_b[2][kRT];
-    qk_half(stage_of(0), H0, H0, s_a);
-    qk_half(stage_of(0), H0, H1, s_a);
+    if (!dead(kbeg)) {
+        qk_half(stage_of(0), H0, H0, s_a);
+        qk_half(stage_of(0), H0, H1, s_a);
+    }
     for (int t = 0; t < n_tiles; ++t) {
         const unsigned char* st = stage_of(t);
         const int j0 = 2 * t;
+        const int v0 = kbeg + 32 * j0;
         // even step: sub-tile (t, 0) -> next (t, 1), same stage
-        step(s_a, s_b, kbeg + 32 * j0, st, H0, st, H1);
+        if (!(dead(v0) && dead(v0 + 32))) step(s_a, s_b, v0, st, H0, st, H1);
         if (j0 + 1 >= n_sub) break;
         // odd step: sub-tile (t, 1) -> next (t+1, 0), behind tile t+1's barrier
         const bool more = t + 1 < n_tiles;
@@ -556,7 +569,8 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             __syncthreads();
             if (t + 3 < n_tiles) issue_tile(t + 3);
         }
-        step(s_b, s_a, kbeg + 32 * (j0 + 1), st, H1, more ? stage_of(t + 1) : st, H0);
+        if (!(dead(v0 + 32) && dead(v0 + 64)))
+            step(s_b, s_a, v0 + 32, st, H1, more ? stage_of(t + 1) : st, H0);
     }
 
     // row sums: add the four lane groups that hold each row
@@ -583,7 +597,10 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             }
             if (p.lse && lg == 0) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
         } else {
-            const int64_t pi = (int64_t)seg * kRB + (rho - rho0);
+            // the unit's partials are row-major over its segments, so the
+            // combine reads one contiguous run per row
+            const int64_t pi =
+                (int64_t)(seg - seg_local) * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
             float* po = p.part_o + pi * D;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -596,28 +613,22 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     }
 }
 
-// A persistent workgroup walks its range of the schedule: one segment per
-// unit the range touches.  Indices read from the table are checked against
-// the table's own counts before use.
+// A persistent workgroup runs its run of segments of the schedule.
 template <int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
-    const int4 w = p.plan_wg[blockIdx.x];
-    int u = w.x, a = w.y, left = w.z, seg = w.w;
-    for (bool first = true; left > 0 && u >= 0 && u < p.n_units; first = false) {
-        const int4 un = p.plan_unit[u];
-        const int b = min(un.w, a + left);
-        if (a < 0 || a >= b || un.x < 0 || un.x >= p.n_seqs || un.y < 0 || un.y >= p.n_kv_heads)
+    const int g0 = max(p.wg_seg[blockIdx.x], 0), g1 = min(p.wg_seg[blockIdx.x + 1], p.n_segments);
+    for (int g = g0; g < g1; ++g) {
+        int4 rec[3];
+#pragma unroll
+        for (int i = 0; i < 3; ++i) rec[i] = p.seg[3 * (int64_t)g + i];
+        if (rec[0].x < 0 || rec[0].x >= p.n_seqs || rec[0].y < 0 || rec[0].y >= p.n_kv_heads ||
+            rec[0].w > kRB || rec[1].z < 1 || rec[1].w < 0 || rec[1].w >= rec[1].z ||
+            g - rec[1].w + rec[1].z > p.n_segments)
             break;
-        const bool direct = unit_is_direct(p, u);
-        if (!direct && (seg < 0 || seg >= p.n_segments)) break;
         // the previous segment's waves are done with every LDS stage
-        if (!first) __syncthreads();
-        attend_segment<D>(p, smem, un.x, un.y, un.z, a, b, seg, direct);
-        left -= b - a;
-        ++u;
-        ++seg;
-        a = 0;
+        if (g > g0) __syncthreads();
+        attend_segment<D>(p, smem, rec, g);
     }
 }
 

@@ -225,7 +225,8 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
 
 kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
                                       int32_t head_dim, int32_t n_seqs,
-                                      const int32_t* seq_new_ptr, const int32_t* new_visible,
+                                      const int32_t* seq_new_ptr, const int32_t* seq_cached,
+                                      const int32_t* new_visible,
                                       int32_t n_compute_units, int32_t n_workgroups,
                                       int32_t* table, int64_t table_capacity,
                                       kvlink_attend_plan* plan) {
@@ -239,16 +240,18 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
         if (group != 1 && group != 2 && group != 4 && group != 8)
             return fail(KVLINK_ERR_UNSUPPORTED, "GQA group %d (built: 1, 2, 4, 8)", group);
         if (n_seqs < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_seqs must be >= 1");
-        if (!seq_new_ptr || !new_visible || !plan)
-            return fail(KVLINK_ERR_INVALID_ARG, "seq_new_ptr, new_visible and plan are required");
+        if (!seq_new_ptr || !seq_cached || !new_visible || !plan)
+            return fail(KVLINK_ERR_INVALID_ARG,
+                        "seq_new_ptr, seq_cached, new_visible and plan are required");
         if (n_compute_units < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_compute_units must be >= 1");
         if (n_workgroups < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_workgroups must be >= 0");
         std::vector<int32_t> tab;
         kvlink::PlanCounts c;
         const char* why = "";
         const int st = kvlink::build_attend_schedule(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs,
-                                                     seq_new_ptr, new_visible, n_compute_units,
-                                                     n_workgroups, table ? &tab : nullptr, &c, &why);
+                                                     seq_new_ptr, seq_cached, new_visible,
+                                                     n_compute_units, n_workgroups,
+                                                     table ? &tab : nullptr, &c, &why);
         if (st != KVLINK_OK) return fail((kvlink_status)st, "%s", why);
         if (c.table_len > INT32_MAX) return fail(KVLINK_ERR_LAYOUT, "schedule table too large");
         if (table) {

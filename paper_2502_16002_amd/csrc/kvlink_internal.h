@@ -206,6 +206,12 @@ int attend_row_block(bool use_mfma);
 bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                       int n_new_total, const kvlink_attend_plan& sched, AttendPlan* p);
 
+// Segment record of the schedule table: kSegRecord int32 fields.
+enum {
+    kSegS = 0, kSegH, kSegRho0, kSegRows, kSegTileA, kSegTileB, kSegNseg, kSegLocal,
+    kSegN0, kSegTc, kSegCmax, kSegNvirt, kSegRecord
+};
+
 // The schedule of kvlink_attend_make_plan (host).  Returns a kvlink_status
 // and, on failure, a message in *why.
 struct PlanCounts {
@@ -213,9 +219,9 @@ struct PlanCounts {
     int64_t table_len;
 };
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
-                          int n_seqs, const int32_t* seq_new_ptr, const int32_t* new_visible,
-                          int n_compute_units, int n_workgroups, std::vector<int32_t>* table,
-                          PlanCounts* counts, const char** why);
+                          int n_seqs, const int32_t* seq_new_ptr, const int32_t* seq_cached,
+                          const int32_t* new_visible, int n_compute_units, int n_workgroups,
+                          std::vector<int32_t>* table, PlanCounts* counts, const char** why);
 
 struct AttendArgs {
     const void* q_new;

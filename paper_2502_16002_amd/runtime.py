@@ -76,6 +76,7 @@ class Batch:
         cus = torch.cuda.get_device_properties(torch.device(self.device)).multi_processor_count
         self.plan, table = kvlink_attend_make_plan(self.dtype, self.n_q_heads, self.n_kv_heads,
                                                    self.head_dim, self.layout["seq_new_ptr"],
+                                                   self.layout["seq_cached"],
                                                    self.layout["new_visible"], cus, n_workgroups)
         self.plan_table = torch.from_numpy(np.ascontiguousarray(table)).to(self.device)
         self.plan.table = self.plan_table.data_ptr()

@@ -174,7 +174,8 @@ def test_reencode_empty_is_a_no_op(kv):
 
 def _plan(kv, dtype=None, hq=8, hkv=2, d=128, snp=(0, 10), vis=(100,) * 10, n_wg=0):
     dtype = kv.KVLINK_BF16 if dtype is None else dtype
-    plan, _ = kv.kvlink_attend_make_plan(dtype, hq, hkv, d, list(snp), list(vis), 256, n_wg)
+    tc = [max(vis)] * (len(snp) - 1)
+    plan, _ = kv.kvlink_attend_make_plan(dtype, hq, hkv, d, list(snp), tc, list(vis), 256, n_wg)
     plan.table = 4096          # a fake, aligned device address: nothing is launched
     return plan
 
@@ -281,35 +282,42 @@ def _align(x):
     return (x + 255) // 256 * 256
 
 
+REC = 12   # int32 fields of a segment record
+
+
 def _decode(plan, table, n_seqs):
     """Split a schedule table into its sections (layout in include/kvlink.h)."""
     t = np.asarray(table)
-    n_wg, n_u = plan.n_workgroups, plan.n_units
-    wg = t[:4 * n_wg].reshape(n_wg, 4)
-    units = t[4 * n_wg:4 * n_wg + 4 * n_u].reshape(n_u, 4)
-    o = 4 * n_wg + 4 * n_u
+    n_wg, n_seg, n_u = plan.n_workgroups, plan.n_segments, plan.n_units
+    wg_seg = t[:n_wg + 1]
+    r0 = (n_wg + 1 + 3) // 4 * 4
+    recs = t[r0:r0 + REC * n_seg].reshape(n_seg, REC)
+    o = r0 + REC * n_seg
     unit_seg = t[o:o + n_u + 1]
     seq_unit = t[o + n_u + 1:o + n_u + 1 + n_seqs + 1]
     assert len(t) == o + n_u + 1 + n_seqs + 1 == plan.table_len
-    return wg, units, unit_seg, seq_unit
+    return wg_seg, recs, unit_seg, seq_unit
 
 
 def _expected_units(L, G, hkv, rb):
-    """(s, h, rho0, tiles) of every unit, from the layout and the attention
-    map of Sec. 2.3: the block's last token sees new_visible cached rows and
-    the new rows up to its own."""
-    snp, vis = L["seq_new_ptr"], L["new_visible"]
+    """(s, h, rho0, rows, n0, T_c, cmax, nvirt, tiles) of every unit, from
+    the layout and the attention map of Sec. 2.3: the block's last token sees
+    new_visible cached rows and the new rows up to its own."""
+    snp, vis, sc = L["seq_new_ptr"], L["new_visible"], L["seq_cached"]
     out, seq_unit = [], []
     for s in range(len(snp) - 1):
         seq_unit.append(len(out))
+        n0 = int(snp[s])
         rows_s = int(snp[s + 1] - snp[s]) * G
         for h in range(hkv):
             for rho0 in range(0, rows_s, rb):
-                r_last = (min(rho0 + rb, rows_s) - 1) // G
-                nvirt = int(vis[snp[s] + r_last]) + r_last + 1
-                out.append((s, h, rho0, -(-nvirt // 64)))
+                rows = min(rb, rows_s - rho0)
+                r_last = (rho0 + rows - 1) // G
+                cmax = int(vis[n0 + r_last])
+                nvirt = cmax + r_last + 1
+                out.append((s, h, rho0, rows, n0, int(sc[s]), cmax, nvirt, -(-nvirt // 64)))
     seq_unit.append(len(out))
-    return np.array(out, np.int64).reshape(-1, 4), np.array(seq_unit)
+    return np.array(out, np.int64).reshape(-1, 9), np.array(seq_unit)
 
 
 def _check_schedule(kv, w, n_wg_req):
@@ -319,39 +327,54 @@ def _check_schedule(kv, w, n_wg_req):
     L = kv.kvlink_build_layout(sdp, dl, lc, w.n_query)
     dt = kv.KVLINK_F32 if w.dtype == "f32" else kv.KVLINK_BF16
     plan, table = kv.kvlink_attend_make_plan(dt, w.n_q_heads, w.n_kv_heads, w.head_dim,
-                                             L["seq_new_ptr"], L["new_visible"], 256, n_wg_req)
+                                             L["seq_new_ptr"], L["seq_cached"], L["new_visible"],
+                                             256, n_wg_req)
     G = w.n_q_heads // w.n_kv_heads
     max_new = int(np.max(np.diff(L["seq_new_ptr"])))
-    assert plan.row_block == (256 if w.dtype == "bf16" and max_new * G >= 32 else 16)
-    wg, units, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
-    exp_units, exp_seq_unit = _expected_units(L, G, w.n_kv_heads, plan.row_block)
-    assert np.array_equal(units, exp_units)
+    mfma = w.dtype == "bf16" and max_new * G >= 32
+    assert plan.row_block == (256 if mfma else 16)
+    wg_seg, recs, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
+    units, exp_seq_unit = _expected_units(L, G, w.n_kv_heads, plan.row_block)
+    assert plan.n_units == len(units)
     assert np.array_equal(seq_unit, exp_seq_unit)
-    T = int(units[:, 3].sum())
+    T = int(units[:, 8].sum())
     n = plan.n_workgroups
     assert 1 <= n <= T
     if n_wg_req:
         assert n == min(n_wg_req, T)
-    # equal contiguous ranges that cover every tile of every unit once, in order
-    counts = wg[:, 2]
-    assert counts.min() >= T // n and counts.max() <= -(-T // n) and counts.sum() == T
-    off = np.concatenate([[0], np.cumsum(units[:, 3])])
-    start = np.concatenate([[0], np.cumsum(counts)])
-    seg = 0
-    first_seg = {}
+    # segments: in unit order, each unit's tiles covered once by contiguous
+    # ranges, the record's fields those of its unit, with the unit's segment
+    # count and the segment's index among them
+    assert wg_seg[0] == 0 and wg_seg[-1] == plan.n_segments and np.all(np.diff(wg_seg) >= 0)
+    u_prev, t_next = 0, 0
+    count = np.zeros(len(units), np.int64)
+    unit_of = np.searchsorted(unit_seg, np.arange(len(recs)), side="right") - 1
+    for i, r in enumerate(recs):
+        u = int(unit_of[i])
+        assert r[7] == i - unit_seg[u]
+        if u != u_prev:
+            assert u == u_prev + 1 and t_next == units[u_prev, 8]
+            u_prev, t_next = u, 0
+        assert (r[4], r[5]) == (t_next, r[5]) and r[5] > r[4]
+        t_next = int(r[5])
+        exp = units[u]
+        assert tuple(r[[0, 1, 2, 3, 8, 9, 10, 11]]) == tuple(exp[:8])
+        count[u] += 1
+        if count[u] == 1:
+            assert unit_seg[u] == i
+    assert u_prev == len(units) - 1 and t_next == units[-1, 8]
+    assert np.all(count >= 1) and unit_seg[-1] == len(recs)
+    for i, r in enumerate(recs):
+        assert r[6] == count[int(unit_of[i])]
+    # contiguous runs of equal cost (a tile of a unit whose rows fill at
+    # most four of the eight wavefronts costs half): every run starts and
+    # ends within one tile of its share
+    weight = np.where(mfma & (-(-units[:, 3] // 32) <= 4), 0.5, 1.0) if mfma else np.ones(len(units))
+    cost = np.zeros(n)
     for w_i in range(n):
-        u, t0, cnt, s0 = (int(x) for x in wg[w_i])
-        assert off[u] + t0 == start[w_i] and 0 <= t0 < units[u, 3]
-        assert s0 == seg
-        left = cnt
-        while left > 0:
-            take = min(int(units[u, 3]) - t0, left)
-            first_seg.setdefault(u, seg)
-            seg += 1
-            left -= take
-            u, t0 = u + 1, 0
-    assert seg == plan.n_segments
-    assert [first_seg[u] for u in range(plan.n_units)] + [seg] == list(unit_seg)
+        for i in range(wg_seg[w_i], wg_seg[w_i + 1]):
+            cost[w_i] += (recs[i, 5] - recs[i, 4]) * weight[int(unit_of[i])]
+    assert cost.max() - cost.min() <= 2.0 + 1e-9
     return plan
 
 
@@ -368,20 +391,22 @@ def test_attend_schedule(kv, name):
         _check_schedule(kv, w, n)
     # the long-context workload's tile count keeps the whole chip busy
     if name == "llama8b-32layer-40x512":
-        assert chosen.n_workgroups >= 240
+        assert chosen.n_workgroups >= 200
 
 
 def test_attend_schedule_errors(kv):
     mk = kv.kvlink_attend_make_plan
+    bf = kv.KVLINK_BF16
     with pytest.raises(kv.KVLinkError) as e:
-        mk(kv.KVLINK_BF16, 32, 8, 96, [0, 4], [1, 2, 3, 4], 256)
+        mk(bf, 32, 8, 96, [0, 4], [10], [1, 2, 3, 4], 256)
     assert e.value.status == 2
-    for args, status in [((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 0), 1),
-                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, 2, 3, 4], 256, -1), 1),
-                         ((kv.KVLINK_BF16, 32, 8, 128, [1, 4], [1, 2, 3, 4], 256), 3),
-                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4, 3], [1, 2, 3, 4], 256), 3),
-                         ((kv.KVLINK_BF16, 32, 8, 128, [0, 4], [1, -2, 3, 4], 256), 3),
-                         ((kv.KVLINK_BF16, 32, 6, 128, [0, 4], [1, 2, 3, 4], 256), 1)]:
+    for args, status in [((bf, 32, 8, 128, [0, 4], [10], [1, 2, 3, 4], 0), 1),
+                         ((bf, 32, 8, 128, [0, 4], [10], [1, 2, 3, 4], 256, -1), 1),
+                         ((bf, 32, 8, 128, [1, 4], [10], [1, 2, 3, 4], 256), 3),
+                         ((bf, 32, 8, 128, [0, 4, 3], [10, 10], [1, 2, 3, 4], 256), 3),
+                         ((bf, 32, 8, 128, [0, 4], [10], [1, -2, 3, 4], 256), 3),
+                         ((bf, 32, 8, 128, [0, 4], [-1], [1, 2, 3, 4], 256), 3),
+                         ((bf, 32, 6, 128, [0, 4], [10], [1, 2, 3, 4], 256), 1)]:
         with pytest.raises(kv.KVLinkError) as e:
             mk(*args)
         assert e.value.status == status, args
