@@ -195,16 +195,16 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
  *
  * The table (int32, built on the host by kvlink_attend_make_plan, then
  * copied to the device by the caller) holds, in order:
- *   n_workgroups + 1   first-segment offsets of the workgroups (workgroup w
- *                      runs segments [off[w], off[w+1]))
- *   padding to a multiple of 4 entries
- *   n_segments x 12    segment records {request, KV head, first row of the
+ *   n_segments x 16    segment records {request, KV head, first row of the
  *                      block, rows in the block, first tile, end tile,
  *                      segments of the unit, index of this one among them,
  *                      first new token of the request, T_c of the request,
  *                      cached rows the block's last token sees, key count
- *                      of the unit}
- *   n_units + 1        first-segment offsets of the units
+ *                      of the unit, first segment of the unit in unit
+ *                      order, next record of the same workgroup (-1: none),
+ *                      unit, 0}; record w (w < n_workgroups) is workgroup
+ *                      w's first segment
+ *   n_units + 1        first-segment offsets of the units, in unit order
  *   n_seqs + 1         first-unit offsets of the requests
  * Like the layout arrays, the device copy is trusted: it must be the
  * unmodified table built for the same batch.

@@ -141,7 +141,7 @@ struct ValuSmem {
 // of request s.  Early returns are uniform over the workgroup.
 template <typename T, int D>
 __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, int s, int h,
-                                             int rho0, int tile_a, int tile_b, int seg, int nseg,
+                                             int rho0, int tile_a, int tile_b, int part, int nseg,
                                              int seg_local) {
     const bool direct = nseg == 1;
     constexpr int RB = kValuRB, KT = kValuKT, RPW = 4, DPL = D / 64;
@@ -243,8 +243,7 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
             for (int dd = 0; dd < DPL; ++dd) out[orow * D + lane + 64 * dd] = from_f32<T>(o[i][dd] * inv);
             if (p.lse && lane == 0) p.lse[orow] = (m[i] + log2f(l[i])) * kLn2;
         } else {
-            const int64_t pi =
-                (int64_t)(seg - seg_local) * RB + (int64_t)(rho - rho0) * nseg + seg_local;
+            const int64_t pi = (int64_t)part * RB + (int64_t)(rho - rho0) * nseg + seg_local;
 #pragma unroll
             for (int dd = 0; dd < DPL; ++dd) p.part_o[pi * D + lane + 64 * dd] = o[i][dd];
             if (lane == 0) {
@@ -259,15 +258,14 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
     __shared__ ValuSmem<D> sm;
-    const int g0 = max(p.wg_seg[blockIdx.x], 0), g1 = min(p.wg_seg[blockIdx.x + 1], p.n_segments);
-    for (int g = g0; g < g1; ++g) {
-        const int* r = reinterpret_cast<const int*>(p.seg + 3 * (int64_t)g);
-        const int s = r[kSegS], h = r[kSegH], nseg = r[kSegNseg], loc = r[kSegLocal];
-        if (s < 0 || s >= p.n_seqs || h < 0 || h >= p.n_kv_heads || nseg < 1 || loc < 0 ||
-            loc >= nseg || g - loc + nseg > p.n_segments)
-            break;
-        if (g > g0) __syncthreads();
-        valu_segment<T, D>(p, sm, s, h, r[kSegRho0], r[kSegTileA], r[kSegTileB], g, nseg, loc);
+    for (int g = blockIdx.x, first = 1; g >= 0 && g < p.n_segments; first = 0) {
+        int4 rec[4];
+        load_record(p, g, rec);
+        if (!record_ok(p, rec, g)) break;
+        if (!first) __syncthreads();
+        valu_segment<T, D>(p, sm, rec[0].x, rec[0].y, rec[0].z, rec[1].x, rec[1].y, rec[3].x,
+                           rec[1].z, rec[1].w);
+        g = rec[3].y;
     }
 }
 
@@ -376,10 +374,8 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.row_block = pl.row_block;
     p.n_units = pl.n_units;
     p.n_segments = pl.n_segments;
-    const size_t rec0 = ((size_t)pl.n_wg + 1 + 3) / 4 * 4;
-    p.wg_seg = pl.table;
-    p.seg = reinterpret_cast<const int4*>(pl.table + rec0);
-    p.unit_seg = pl.table + rec0 + (size_t)kSegRecord * pl.n_segments;
+    p.seg = reinterpret_cast<const int4*>(pl.table);
+    p.unit_seg = pl.table + (size_t)kSegRecord * pl.n_segments;
     p.seq_unit = p.unit_seg + pl.n_units + 1;
     p.part_o = reinterpret_cast<float*>(ws + pl.q_rot_bytes);
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
@@ -428,9 +424,9 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
         return false;
     if ((int64_t)sched.n_segments * kSegRecord > INT32_MAX) return false;
     if (sched.n_workgroups > 0 && (sched.n_units < 1 || sched.n_segments < 1)) return false;
-    const int64_t want = ((int64_t)sched.n_workgroups + 1 + 3) / 4 * 4 +
-                         (int64_t)kSegRecord * sched.n_segments + sched.n_units + 1 +
-                         sched.n_seqs + 1;
+    const int64_t want =
+        (int64_t)kSegRecord * sched.n_segments + sched.n_units + 1 + sched.n_seqs + 1;
+    if (sched.n_segments < sched.n_workgroups) return false;
     if (sched.table_len != want) return false;
     const size_t elem = dt == KVLINK_BF16 ? 2 : 4;
     p->n_q_heads = n_q_heads;

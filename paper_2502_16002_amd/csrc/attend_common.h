@@ -49,9 +49,9 @@ __device__ __forceinline__ BlockKeys block_keys(const int32_t* new_visible, int 
 }
 
 // Arguments of the split kernels and the combine.  The schedule table (see
-// the schedule's description in the public header) is read through wg_seg
-// (n_wg + 1 first-segment offsets), seg (n_segments records of kSegRecord
-// int32, as 3 int4), unit_seg (n_units + 1) and seq_unit (n_seqs + 1).
+// the schedule's description in the public header) is read through seg
+// (n_segments records of kSegRecord int32, as 4 int4; record w is workgroup
+// w's first segment), unit_seg (n_units + 1) and seq_unit (n_seqs + 1).
 struct KParams {
     const void* q_rot;
     View k, v;
@@ -61,7 +61,6 @@ struct KParams {
     const int32_t* new_visible;
     float scale_log2;
     int row_block, n_units, n_segments;
-    const int32_t* wg_seg;
     const int4* seg;
     const int32_t* unit_seg;
     const int32_t* seq_unit;
@@ -71,7 +70,23 @@ struct KParams {
     float* lse;
 };
 
-static_assert(kSegRecord == 12, "segment records are read as three int4");
+static_assert(kSegRecord == 16, "segment records are read as four int4");
+
+// Record g of the schedule (uniform loads).
+__device__ __forceinline__ void load_record(const KParams& p, int g, int4 (&rec)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rec[i] = p.seg[4 * (int64_t)g + i];
+}
+
+// The record's indices fit the launch: request, head, rows of one block,
+// segment numbering within the unit's partials, and a chain that only moves
+// forward (so a workgroup's walk ends).
+__device__ __forceinline__ bool record_ok(const KParams& p, const int4 (&rec)[4], int g) {
+    const int nseg = rec[1].z, loc = rec[1].w, part = rec[3].x, next = rec[3].y;
+    return rec[0].x >= 0 && rec[0].x < p.n_seqs && rec[0].y >= 0 && rec[0].y < p.n_kv_heads &&
+           rec[0].w >= 0 && rec[0].w <= p.row_block && nseg >= 1 && loc >= 0 && loc < nseg &&
+           part >= 0 && part + nseg <= p.n_segments && (next < 0 || next > g);
+}
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
 // GQA rows per workgroup of the MFMA kernel

@@ -173,7 +173,7 @@ __device__ __forceinline__ void wait_vm() {
 // Every early return is uniform over the workgroup.
 template <int D>
 __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem,
-                                               const int4 (&rec)[3], int seg) {
+                                               const int4 (&rec)[4]) {
     constexpr int DT = D / 16;         // 16-dim tiles of O^T
     constexpr int DS = D / 32;         // 32-dim steps of S^T = K Q^T
     constexpr int KB = 4 * DS;         // 1 KB operand blocks of a K tile
@@ -184,7 +184,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
     const int s = rec[0].x, h = rec[0].y, rho0 = rec[0].z, rows = rec[0].w;
     const int tile_a = rec[1].x, tile_b = rec[1].y;
-    const int nseg = rec[1].z, seg_local = rec[1].w;
+    const int nseg = rec[1].z, seg_local = rec[1].w, part = rec[3].x;
     const bool direct = nseg == 1;
     const int n0 = rec[2].x, Tc = rec[2].y;
     BlockKeys bk;
@@ -599,8 +599,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         } else {
             // the unit's partials are row-major over its segments, so the
             // combine reads one contiguous run per row
-            const int64_t pi =
-                (int64_t)(seg - seg_local) * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
+            const int64_t pi = (int64_t)part * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
             float* po = p.part_o + pi * D;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -613,22 +612,19 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     }
 }
 
-// A persistent workgroup runs its run of segments of the schedule.
+// A persistent workgroup runs its chain of segments of the schedule: record
+// blockIdx.x first, then the records its `next` fields name.
 template <int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
-    const int g0 = max(p.wg_seg[blockIdx.x], 0), g1 = min(p.wg_seg[blockIdx.x + 1], p.n_segments);
-    for (int g = g0; g < g1; ++g) {
-        int4 rec[3];
-#pragma unroll
-        for (int i = 0; i < 3; ++i) rec[i] = p.seg[3 * (int64_t)g + i];
-        if (rec[0].x < 0 || rec[0].x >= p.n_seqs || rec[0].y < 0 || rec[0].y >= p.n_kv_heads ||
-            rec[0].w > kRB || rec[1].z < 1 || rec[1].w < 0 || rec[1].w >= rec[1].z ||
-            g - rec[1].w + rec[1].z > p.n_segments)
-            break;
+    for (int g = blockIdx.x, first = 1; g >= 0 && g < p.n_segments; first = 0) {
+        int4 rec[4];
+        load_record(p, g, rec);
+        if (!record_ok(p, rec, g)) break;
         // the previous segment's waves are done with every LDS stage
-        if (g > g0) __syncthreads();
-        attend_segment<D>(p, smem, rec, g);
+        if (!first) __syncthreads();
+        attend_segment<D>(p, smem, rec);
+        g = rec[3].y;
     }
 }
 

@@ -7,28 +7,37 @@
 // Sec. 2.3: every position at or before the token's own) followed by the new
 // rows up to that token; it walks them in 64-key tiles.
 //
-// All tiles, units in (s, h, b) order, are dealt out to the workgroups as
-// contiguous ranges of equal cost, so every workgroup gets the same work
-// whatever the mix of long and short units (the row blocks of link tokens
-// early in the context see few keys, those of the queries see all of them).
-// A tile of a unit whose rows fill at most half the workgroup's wavefronts
-// costs half (its other wavefronts sit idle and their SIMDs run one
-// wavefront instead of two).  A workgroup's range crosses unit boundaries;
-// each piece is a segment with its own partial result, merged by the combine
-// when a unit has several.  Each segment gets a record with everything its
-// workgroup needs to issue its first key-tile loads after a single table
-// read.
+// A schedule gives every workgroup one or more segments (a contiguous tile
+// range of one unit); a unit cut into several segments has its partial
+// results merged by the combine.  Two ways of cutting are considered for
+// each workgroup count n:
 //
-// The number of workgroups comes from a cost model: a workgroup costs a fixed
-// set-up per segment (loads of its rows' queries and the first key tiles)
-// plus a per-tile cost; the launch lasts as long as its longest workgroup;
-// units with several segments add the combine launch and the traffic of
-// their partials.  Constants are fitted to MI355X timings of the Llama-8B
-// shaped 10- and 40-document workloads.
+//   * unit-aligned: with n >= units, every workgroup gets one segment and
+//     each unit k_u near-equal pieces, the k_u chosen greedily to minimise
+//     the longest piece; with n < units, whole units are packed onto the
+//     workgroups longest first;
+//   * equal ranges: the tiles of all units, in order, cut into n contiguous
+//     ranges of equal cost, crossing unit boundaries (perfect balance, but a
+//     workgroup whose range crosses a boundary pays a second segment).
+//
+// The cheaper of the two, and the cheapest n, come from a cost model fitted
+// to MI355X timings of the Llama-8B-shaped workloads: a segment costs a
+// fixed set-up (its record, the first key tiles and queries, the partial
+// write), a tile costs a per-tile time, and a tile of a unit whose rows
+// fill at most half the wavefronts costs half (its other wavefronts sit
+// idle, and their SIMDs run one wavefront instead of two); the launch lasts
+// as long as its longest workgroup; split units add the combine launch and
+// the traffic of their partials.
+//
+// Segment records are numbered so that record w is workgroup w's first
+// segment; further segments of a workgroup follow the first n and are
+// chained by the record's `next` field.  A workgroup therefore issues its
+// first key-tile loads after one table read.
 #include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <queue>
 #include <vector>
 
 #include "kvlink_internal.h"
@@ -43,24 +52,33 @@ struct Unit {
     double weight;   // cost of one tile relative to a full row block
 };
 
+struct Seg {
+    int w, u;
+    int64_t t0, len;
+};
+
 struct CostModel {
-    double per_segment_us, per_tile_us;
+    double per_segment_us, per_tile_us, combine_us, combine_bytes_per_us;
     int slots_per_cu;
 };
 
+// Fitted to sweeps of the workgroup count on the 10- and 40-document
+// workloads: the split launch costs about 15 us plus 1.6-2.2 us per tile of
+// its longest workgroup (8 us of that fixed part recurs for every further
+// segment of a workgroup); the combine about 6 us plus its partial traffic,
+// written and read back at an effective ~6 TB/s.
 CostModel cost_model(bool mfma, int head_dim) {
-    if (mfma) return {4.0, head_dim == 128 ? 2.1 : 1.3, 1};
-    return {3.0, head_dim == 128 ? 1.0 : 0.6, head_dim == 128 ? 2 : 4};
+    if (mfma) return {8.0, head_dim == 128 ? 1.9 : 1.2, 6.0, 6.0e6, 1};
+    return {4.0, head_dim == 128 ? 1.0 : 0.6, 4.0, 6.0e6, head_dim == 128 ? 2 : 4};
 }
 
-// Pieces of n contiguous ranges of equal cost over the units' tiles (a
-// tile of unit u costs units[u].weight).  Calls f(w, u, first tile, count)
-// for every non-empty piece, in order.
-template <typename F>
-void for_each_piece(const std::vector<Unit>& units, const std::vector<double>& woff, int n, F&& f) {
-    const double W = woff.back();
+// n contiguous ranges of equal cost over the units' tiles in order
+void cut_equal_ranges(const std::vector<Unit>& units, int n, std::vector<Seg>* segs) {
+    double W = 0.0;
+    for (const Unit& x : units) W += x.tiles * x.weight;
     size_t u = 0;
     int64_t t_in_u = 0;   // next tile of unit u to hand out
+    double done = 0.0;    // cost handed out before tile t_in_u of unit u
     for (int w = 0; w < n; ++w) {
         const double end = w + 1 == n ? W : W * (w + 1) / n;
         while (u < units.size()) {
@@ -69,32 +87,99 @@ void for_each_piece(const std::vector<Unit>& units, const std::vector<double>& w
                 t_in_u = 0;
                 continue;
             }
-            // tiles of unit u whose start lies before `end`
-            const double start_w = woff[u] + t_in_u * units[u].weight;
-            if (start_w >= end - 1e-9 && w + 1 < n) break;
+            if (done >= end - 1e-9 && w + 1 < n) break;
+            // the tiles of unit u that start before `end`
             int64_t take = w + 1 == n ? units[u].tiles - t_in_u
-                                      : (int64_t)std::ceil((end - start_w) / units[u].weight - 1e-9);
+                                      : (int64_t)std::ceil((end - done) / units[u].weight - 1e-9);
             take = std::max<int64_t>(1, std::min<int64_t>(take, units[u].tiles - t_in_u));
-            f(w, (int)u, t_in_u, take);
+            segs->push_back({w, (int)u, t_in_u, take});
             t_in_u += take;
+            done += take * units[u].weight;
         }
     }
 }
 
-double estimate_us(const std::vector<Unit>& units, const std::vector<double>& woff, int n,
-                   const CostModel& cm, int head_dim) {
-    std::vector<double> wg(n, 0.0);
-    std::vector<int> pieces(units.size(), 0);
-    for_each_piece(units, woff, n, [&](int w, int u, int64_t, int64_t len) {
-        wg[w] += cm.per_segment_us + cm.per_tile_us * units[u].weight * (double)len;
-        ++pieces[u];
+// unit-aligned cut (see the file comment)
+void cut_unit_aligned(const std::vector<Unit>& units, int n, std::vector<Seg>* segs) {
+    const int nu = (int)units.size();
+    if (n >= nu) {
+        std::vector<int> k(nu, 1);
+        auto longest = [&](int u) {
+            return std::ceil((double)units[u].tiles / k[u]) * units[u].weight;
+        };
+        std::priority_queue<std::pair<double, int>> pq;   // (longest piece, -unit)
+        for (int u = 0; u < nu; ++u) pq.push({longest(u), -u});
+        for (int extra = n - nu; extra > 0 && !pq.empty();) {
+            const int u = -pq.top().second;
+            pq.pop();
+            if (k[u] >= units[u].tiles) continue;   // one tile per piece already
+            ++k[u];
+            --extra;
+            pq.push({longest(u), -u});
+        }
+        int w = 0;
+        for (int u = 0; u < nu; ++u)
+            for (int i = 0; i < k[u]; ++i) {
+                const int64_t t0 = (int64_t)units[u].tiles * i / k[u];
+                const int64_t t1 = (int64_t)units[u].tiles * (i + 1) / k[u];
+                segs->push_back({w++, u, t0, t1 - t0});
+            }
+        return;
+    }
+    // fewer workgroups than units: whole units, longest first onto the least
+    // loaded workgroup
+    std::vector<int> order(nu);
+    for (int u = 0; u < nu; ++u) order[u] = u;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+        return units[a].tiles * units[a].weight > units[b].tiles * units[b].weight;
     });
+    std::priority_queue<std::pair<double, int>> load;   // (-load, -workgroup)
+    for (int w = 0; w < n; ++w) load.push({0.0, -w});
+    std::vector<int> owner(nu);
+    for (int u : order) {
+        auto top = load.top();
+        load.pop();
+        owner[u] = -top.second;
+        load.push({top.first - units[u].tiles * units[u].weight, top.second});
+    }
+    for (int u = 0; u < nu; ++u) segs->push_back({owner[u], u, 0, units[u].tiles});
+}
+
+// Renumbers the workgroups of a cut densely (a cut may leave some of the n
+// workgroups without work: equal ranges narrower than a tile, or a unit that
+// cannot be cut finer than one tile per piece) and returns their count.
+int compact_workgroups(std::vector<Seg>* segs) {
+    std::vector<int> id;
+    for (Seg& g : *segs) {
+        if (g.w >= (int)id.size()) id.resize(g.w + 1, -1);
+    }
+    int n = 0;
+    for (const Seg& g : *segs)
+        if (id[g.w] < 0) id[g.w] = n++;
+    for (Seg& g : *segs) g.w = id[g.w];
+    return n;
+}
+
+int used_workgroups(const std::vector<Seg>& segs) {
+    int n = 0;
+    for (const Seg& g : segs) n = std::max(n, g.w + 1);
+    return n;
+}
+
+double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
+                   const CostModel& cm, int head_dim) {
+    std::vector<double> wg(used_workgroups(segs), 0.0);
+    std::vector<int> pieces(units.size(), 0);
+    for (const Seg& g : segs) {
+        wg[g.w] += cm.per_segment_us + cm.per_tile_us * units[g.u].weight * (double)g.len;
+        ++pieces[g.u];
+    }
     double t = *std::max_element(wg.begin(), wg.end());
     double bytes = 0.0;
     for (size_t u = 0; u < units.size(); ++u)
         if (pieces[u] > 1)
             bytes += 2.0 * pieces[u] * units[u].rows * (head_dim + 2) * 4.0;   // write + read
-    if (bytes > 0.0) t += 3.0 + bytes / 4.0e6;   // combine launch, ~4 TB/s effective
+    if (bytes > 0.0) t += cm.combine_us + bytes / cm.combine_bytes_per_us;
     return t;
 }
 
@@ -135,9 +220,8 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     const bool mfma = attend_uses_mfma(dt, group, max_new);
     const int rb = attend_row_block(mfma);
 
-    // rows per wavefront of the kernel the path selects (8 x 32 rows on the
-    // matrix cores, 4 x 4 on the VALU path)
-    const int rows_per_wave = rb / 8 > 0 && mfma ? rb / 8 : rb / 4;
+    // rows per wavefront of the matrix-core kernel (eight wavefronts)
+    const int rows_per_wave = rb / 8;
     std::vector<Unit> units;
     std::vector<int32_t> seq_unit(n_seqs + 1);
     for (int s = 0; s < n_seqs; ++s) {
@@ -161,82 +245,101 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             }
     }
     seq_unit[n_seqs] = (int32_t)units.size();
-    std::vector<double> woff(units.size() + 1, 0.0);
     int64_t T = 0;
-    for (size_t u = 0; u < units.size(); ++u) {
-        woff[u + 1] = woff[u] + units[u].tiles * units[u].weight;
-        T += units[u].tiles;
-    }
+    for (const Unit& x : units) T += x.tiles;
 
-    int n = 0;
+    std::vector<Seg> segs, cand;
     if (T > 0) {
         const CostModel cm = cost_model(mfma, head_dim);
         const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
-        if (n_workgroups > 0) {
-            n = (int)std::min<int64_t>(n_workgroups, T);
-        } else {
-            double best = 1e300;
-            for (int c = 1; c <= max_n; ++c) {
-                const double t = estimate_us(units, woff, c, cm, head_dim);
-                if (t < best * 0.99) {   // fewer workgroups on near ties
+        double best = 1e300;
+        auto consider = [&](int c, bool any_cost) {
+            for (int way = 0; way < 2; ++way) {
+                cand.clear();
+                if (way == 0) cut_unit_aligned(units, c, &cand);
+                else cut_equal_ranges(units, c, &cand);
+                // a forced count takes only cuts that use every workgroup
+                if (compact_workgroups(&cand) < c && any_cost) continue;
+                const double t = estimate_us(units, cand, cm, head_dim);
+                if (t < best * 0.99) {   // fewer workgroups, unit-aligned cuts on near ties
                     best = t;
-                    n = c;
+                    segs = cand;
                 }
             }
+        };
+        if (n_workgroups > 0) {
+            consider((int)std::min<int64_t>(n_workgroups, T), true);
+        } else {
+            for (int c = 1; c <= max_n; ++c) consider(c, false);
         }
     }
+    const int n = used_workgroups(segs);
 
-    // segments in order; a workgroup owns a contiguous run of them
-    struct Seg {
-        int w, u;
-        int64_t t0, len;
-    };
-    std::vector<Seg> segs;
-    for_each_piece(units, woff, n, [&](int w, int u, int64_t t0, int64_t len) {
-        segs.push_back({w, u, t0, len});
-    });
-    std::vector<int32_t> wg_seg(n + 1, 0);
-    std::vector<int32_t> unit_seg(units.size() + 1, -1);
-    std::vector<int> pieces(units.size(), 0);
-    for (size_t i = 0; i < segs.size(); ++i) {
-        ++wg_seg[segs[i].w + 1];
-        if (unit_seg[segs[i].u] < 0) unit_seg[segs[i].u] = (int32_t)i;
-        ++pieces[segs[i].u];
-    }
-    for (int w = 0; w < n; ++w) wg_seg[w + 1] += wg_seg[w];
+    // segments per unit, in tile order, and the unit-order numbering used
+    // for the partials and the combine
     const int n_seg = (int)segs.size();
-    unit_seg[units.size()] = n_seg;
-    for (size_t u = units.size(); u-- > 0;)      // (only for T == 0: no pieces at all)
-        if (unit_seg[u] < 0) unit_seg[u] = unit_seg[u + 1];
+    std::vector<std::vector<int>> of_unit(units.size());
+    for (int i = 0; i < n_seg; ++i) of_unit[segs[i].u].push_back(i);
+    std::vector<int32_t> unit_seg(units.size() + 1, 0);
+    std::vector<int> local(n_seg);
+    for (size_t u = 0; u < units.size(); ++u) {
+        std::sort(of_unit[u].begin(), of_unit[u].end(),
+                  [&](int a, int b) { return segs[a].t0 < segs[b].t0; });
+        for (size_t j = 0; j < of_unit[u].size(); ++j) local[of_unit[u][j]] = (int)j;
+        unit_seg[u + 1] = unit_seg[u] + (int32_t)of_unit[u].size();
+    }
+    // record ids: workgroup w's first segment is record w, the others follow
+    // in order, chained by `next`
+    std::vector<int> order(n_seg);
+    for (int i = 0; i < n_seg; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return segs[a].w < segs[b].w; });
+    std::vector<int> rec_id(n_seg), next(n_seg, -1), last(n, -1);
+    int extra = n;
+    for (int i : order) {
+        const int w = segs[i].w;
+        if (last[w] < 0) {
+            rec_id[i] = w;
+        } else {
+            rec_id[i] = extra++;
+            next[last[w]] = rec_id[i];
+        }
+        last[w] = i;
+    }
+
+    if (extra != n_seg) {   // every workgroup of a compacted cut has a segment
+        *why = "internal error: schedule record numbering";
+        return KVLINK_ERR_LAYOUT;
+    }
 
     counts->n_wg = n;
     counts->n_units = (int)units.size();
     counts->n_segments = n_seg;
     counts->row_block = rb;
-    const int64_t rec0 = ((int64_t)n + 1 + 3) / 4 * 4;   // records start 16-byte aligned
-    counts->table_len = rec0 + (int64_t)kSegRecord * n_seg + (int64_t)units.size() + 1 + n_seqs + 1;
+    counts->table_len = (int64_t)kSegRecord * n_seg + (int64_t)units.size() + 1 + n_seqs + 1;
     if (table) {
         table->assign((size_t)counts->table_len, 0);
         int32_t* t = table->data();
-        std::copy(wg_seg.begin(), wg_seg.end(), t);
         for (int i = 0; i < n_seg; ++i) {
             const Seg& g = segs[i];
             const Unit& x = units[g.u];
-            int32_t* r = t + rec0 + (int64_t)kSegRecord * i;
+            int32_t* r = t + (int64_t)kSegRecord * rec_id[i];
             r[kSegS] = x.s;
             r[kSegH] = x.h;
             r[kSegRho0] = x.rho0;
             r[kSegRows] = x.rows;
             r[kSegTileA] = (int32_t)g.t0;
             r[kSegTileB] = (int32_t)(g.t0 + g.len);
-            r[kSegNseg] = pieces[g.u];
-            r[kSegLocal] = i - unit_seg[g.u];
+            r[kSegNseg] = unit_seg[g.u + 1] - unit_seg[g.u];
+            r[kSegLocal] = local[i];
             r[kSegN0] = x.n0;
             r[kSegTc] = x.Tc;
             r[kSegCmax] = x.cmax;
             r[kSegNvirt] = x.nvirt;
+            r[kSegPart] = unit_seg[g.u];
+            r[kSegNext] = next[i];
+            r[kSegUnit] = g.u;
         }
-        int32_t* us = t + rec0 + (int64_t)kSegRecord * n_seg;
+        int32_t* us = t + (int64_t)kSegRecord * n_seg;
         std::copy(unit_seg.begin(), unit_seg.end(), us);
         std::copy(seq_unit.begin(), seq_unit.end(), us + units.size() + 1);
     }

@@ -209,7 +209,7 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
 // Segment record of the schedule table: kSegRecord int32 fields.
 enum {
     kSegS = 0, kSegH, kSegRho0, kSegRows, kSegTileA, kSegTileB, kSegNseg, kSegLocal,
-    kSegN0, kSegTc, kSegCmax, kSegNvirt, kSegRecord
+    kSegN0, kSegTc, kSegCmax, kSegNvirt, kSegPart, kSegNext, kSegUnit, kSegSpare, kSegRecord
 };
 
 // The schedule of kvlink_attend_make_plan (host).  Returns a kvlink_status

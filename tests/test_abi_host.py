@@ -272,7 +272,7 @@ def test_workspace_bytes(kv):
     assert f(bf, 8, 2, 128, 10, many) == (_align(10 * 8 * 128 * 2) +
                                            _align(many.n_segments * 256 * 128 * 4) +
                                            _align(many.n_segments * 256 * 2 * 4))
-    thin = _plan(kv, f32, 4, 2, 64, (0, 22), [200] * 22, n_wg=5)
+    thin = _plan(kv, f32, 4, 2, 64, (0, 22), [200] * 22, n_wg=12)
     assert thin.row_block == 16 and thin.n_segments > thin.n_units
     assert f(f32, 4, 2, 64, 22, thin) > f(f32, 4, 2, 64, 22, _plan(kv, f32, 4, 2, 64, (0, 22),
                                                                      [200] * 22, n_wg=1))
@@ -282,21 +282,19 @@ def _align(x):
     return (x + 255) // 256 * 256
 
 
-REC = 12   # int32 fields of a segment record
+REC = 16   # int32 fields of a segment record
 
 
 def _decode(plan, table, n_seqs):
     """Split a schedule table into its sections (layout in include/kvlink.h)."""
     t = np.asarray(table)
-    n_wg, n_seg, n_u = plan.n_workgroups, plan.n_segments, plan.n_units
-    wg_seg = t[:n_wg + 1]
-    r0 = (n_wg + 1 + 3) // 4 * 4
-    recs = t[r0:r0 + REC * n_seg].reshape(n_seg, REC)
-    o = r0 + REC * n_seg
+    n_seg, n_u = plan.n_segments, plan.n_units
+    recs = t[:REC * n_seg].reshape(n_seg, REC)
+    o = REC * n_seg
     unit_seg = t[o:o + n_u + 1]
     seq_unit = t[o + n_u + 1:o + n_u + 1 + n_seqs + 1]
     assert len(t) == o + n_u + 1 + n_seqs + 1 == plan.table_len
-    return wg_seg, recs, unit_seg, seq_unit
+    return recs, unit_seg, seq_unit
 
 
 def _expected_units(L, G, hkv, rb):
@@ -333,48 +331,43 @@ def _check_schedule(kv, w, n_wg_req):
     max_new = int(np.max(np.diff(L["seq_new_ptr"])))
     mfma = w.dtype == "bf16" and max_new * G >= 32
     assert plan.row_block == (256 if mfma else 16)
-    wg_seg, recs, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
+    recs, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
     units, exp_seq_unit = _expected_units(L, G, w.n_kv_heads, plan.row_block)
     assert plan.n_units == len(units)
     assert np.array_equal(seq_unit, exp_seq_unit)
     T = int(units[:, 8].sum())
     n = plan.n_workgroups
-    assert 1 <= n <= T
+    assert 1 <= n <= T <= 10 ** 7 and plan.n_segments >= n
     if n_wg_req:
         assert n == min(n_wg_req, T)
-    # segments: in unit order, each unit's tiles covered once by contiguous
-    # ranges, the record's fields those of its unit, with the unit's segment
-    # count and the segment's index among them
-    assert wg_seg[0] == 0 and wg_seg[-1] == plan.n_segments and np.all(np.diff(wg_seg) >= 0)
-    u_prev, t_next = 0, 0
-    count = np.zeros(len(units), np.int64)
-    unit_of = np.searchsorted(unit_seg, np.arange(len(recs)), side="right") - 1
-    for i, r in enumerate(recs):
-        u = int(unit_of[i])
-        assert r[7] == i - unit_seg[u]
-        if u != u_prev:
-            assert u == u_prev + 1 and t_next == units[u_prev, 8]
-            u_prev, t_next = u, 0
-        assert (r[4], r[5]) == (t_next, r[5]) and r[5] > r[4]
-        t_next = int(r[5])
-        exp = units[u]
-        assert tuple(r[[0, 1, 2, 3, 8, 9, 10, 11]]) == tuple(exp[:8])
-        count[u] += 1
-        if count[u] == 1:
-            assert unit_seg[u] == i
-    assert u_prev == len(units) - 1 and t_next == units[-1, 8]
-    assert np.all(count >= 1) and unit_seg[-1] == len(recs)
-    for i, r in enumerate(recs):
-        assert r[6] == count[int(unit_of[i])]
-    # contiguous runs of equal cost (a tile of a unit whose rows fill at
-    # most four of the eight wavefronts costs half): every run starts and
-    # ends within one tile of its share
-    weight = np.where(mfma & (-(-units[:, 3] // 32) <= 4), 0.5, 1.0) if mfma else np.ones(len(units))
-    cost = np.zeros(n)
+    # every workgroup's chain starts at its own record, only moves forward,
+    # and together the chains visit every record once
+    seen = np.zeros(len(recs), bool)
+    chain_of = np.full(len(recs), -1)
     for w_i in range(n):
-        for i in range(wg_seg[w_i], wg_seg[w_i + 1]):
-            cost[w_i] += (recs[i, 5] - recs[i, 4]) * weight[int(unit_of[i])]
-    assert cost.max() - cost.min() <= 2.0 + 1e-9
+        g = w_i
+        while g >= 0:
+            assert not seen[g]
+            seen[g] = True
+            chain_of[g] = w_i
+            nxt = int(recs[g, 13])
+            assert nxt < 0 or nxt > g
+            g = nxt
+    assert seen.all()
+    # per unit: its segments cover its tiles once, in order of their index,
+    # and every record carries its unit's fields, segment count and first
+    # segment in unit order
+    assert unit_seg[0] == 0 and np.all(np.diff(unit_seg) >= 1) and unit_seg[-1] == len(recs)
+    for u in range(len(units)):
+        mine = recs[recs[:, 14] == u]
+        assert len(mine) == unit_seg[u + 1] - unit_seg[u]
+        mine = mine[np.argsort(mine[:, 7])]
+        assert list(mine[:, 7]) == list(range(len(mine)))
+        assert mine[0, 4] == 0 and mine[-1, 5] == units[u, 8]
+        assert np.array_equal(mine[1:, 4], mine[:-1, 5]) and np.all(mine[:, 5] > mine[:, 4])
+        for r in mine:
+            assert tuple(r[[0, 1, 2, 3, 8, 9, 10, 11]]) == tuple(units[u, :8])
+            assert r[6] == len(mine) and r[12] == unit_seg[u] and r[15] == 0
     return plan
 
 
@@ -383,8 +376,8 @@ def _check_schedule(kv, w, n_wg_req):
                                   "llama8b-paged-16req"])
 def test_attend_schedule(kv, name):
     """Every schedule, chosen by the cost model or forced, deals every tile of
-    every unit out exactly once, in equal contiguous ranges, with consistent
-    segment numbering."""
+    every unit out exactly once, in contiguous segments with consistent
+    numbering and forward chains per workgroup."""
     w = workloads.get(name)
     chosen = _check_schedule(kv, w, 0)
     for n in [1, 3, 64, 1 << 20]:
