@@ -18,16 +18,30 @@
 //     slice [j0+d/2, j0+d/2+E), consecutive threads cover one row, then the
 //     next row, so a wavefront reads and writes whole contiguous rows;
 //   * kUnroll vectors are loaded before any is stored, to keep enough bytes in
-//     flight per wavefront.
+//     flight per wavefront;
+//   * loads and stores are non-temporal (every byte is touched once), and a
+//     workgroup covers 16 rows, so the many short documents of a request
+//     spread evenly over the compute units.
 #include "kvlink_internal.h"
 
 namespace kvlink {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRows = 64;
+constexpr int kRows = 16;
 constexpr int kLH = 8;
 constexpr int kUnroll = 4;
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_stream(const void* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return uint4{v.x, v.y, v.z, v.w};
+}
+
+__device__ __forceinline__ void store_stream(const uint4& v, void* p) {
+    __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
+}
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
@@ -73,8 +87,8 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                 const int64_t so =
                     view_offset(src, layer, head, sp.src_seq, sp.src_row + r0 + row) + sub * E;
                 const T* p = reinterpret_cast<const T*>(src.base) + so;
-                lo[u] = *reinterpret_cast<const uint4*>(p);
-                hi[u] = *reinterpret_cast<const uint4*>(p + H);
+                lo[u] = load_stream(p);
+                hi[u] = load_stream(p + H);
                 doff[u] = view_offset(dst, layer, head, sp.dst_seq, sp.dst_row + r0 + row) + sub * E;
             }
         }
@@ -91,8 +105,8 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                     y[e] = a[e] * s[e] + b[e] * c[e];
                 }
                 T* q = reinterpret_cast<T*>(dst.base) + doff[u];
-                *reinterpret_cast<uint4*>(q) = pack16<T>(x);
-                *reinterpret_cast<uint4*>(q + H) = pack16<T>(y);
+                store_stream(pack16<T>(x), q);
+                store_stream(pack16<T>(y), q + H);
             }
         }
     }
