@@ -243,9 +243,12 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
             for (int dd = 0; dd < DPL; ++dd) out[orow * D + lane + 64 * dd] = from_f32<T>(o[i][dd] * inv);
             if (p.lse && lane == 0) p.lse[orow] = (m[i] + log2f(l[i])) * kLn2;
         } else {
+            // O / l in the workload dtype (0 for a row that saw no key here)
             const int64_t pi = (int64_t)part * RB + (int64_t)(rho - rho0) * nseg + seg_local;
+            const float inv = l[i] > 0.f ? 1.f / l[i] : 0.f;
+            T* po = reinterpret_cast<T*>(p.part_o) + pi * D;
 #pragma unroll
-            for (int dd = 0; dd < DPL; ++dd) p.part_o[pi * D + lane + 64 * dd] = o[i][dd];
+            for (int dd = 0; dd < DPL; ++dd) po[lane + 64 * dd] = from_f32<T>(o[i][dd] * inv);
             if (lane == 0) {
                 p.part_ml[pi * 2] = m[i];
                 p.part_ml[pi * 2 + 1] = l[i];
@@ -273,15 +276,18 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 
 // One wavefront per (new token, query head) row of a unit with several
 // segments (rows of single-segment units were written by the split kernel).
-// A unit's partials are row-major over its segments, so the row's nseg
-// partial vectors are one contiguous run: lanes read it as float4, several
-// segments per round of loads and kRounds rounds issued together; the lanes
-// holding the same dims are folded at the end.
+// A unit's partials (O / l in the workload dtype, with float (m, l)) are
+// row-major over its segments, so the row's nseg partial vectors are one
+// contiguous run: lanes read it 16 bytes at a time, several segments per
+// round of loads and kRounds rounds issued together; the lanes holding the
+// same dims are folded at the end.  out = sum_s w_s (O/l)_s / sum_s w_s with
+// w_s = 2^(m_s - M) l_s.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total) {
-    constexpr int F4 = D / 4;          // float4 per partial vector
-    constexpr int SPR = 64 / F4;       // segments per round of loads
-    constexpr int kRounds = 8;
+    constexpr int EPL = 16 / (int)sizeof(T);   // elements per 16-byte load
+    constexpr int LPS = D / EPL;               // lanes per partial vector
+    constexpr int SPR = 64 / LPS;              // segments per round of loads
+    constexpr int kRounds = 4;
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int64_t orow = (int64_t)blockIdx.x * 4 + wave;   // (n, hq) flattened
     if (orow >= (int64_t)n_new_total * p.n_q_heads) return;
@@ -298,11 +304,10 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     if (nseg <= 1) return;
     const int64_t base = (int64_t)c0 * p.row_block + (int64_t)(rho % p.row_block) * nseg;
     const float2* ml = reinterpret_cast<const float2*>(p.part_ml) + base;
-    const float4* po = reinterpret_cast<const float4*>(p.part_o) + base * F4;
+    const uint4* po = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(p.part_o) + base * D);
 
-    // maximum and weighted sum over the segments (the running maximum starts
-    // finite, so a segment that saw no key of this row, maximum -inf and sum
-    // 0, gets weight 0, never NaN)
+    // the running maximum starts finite, so a segment that saw no key of this
+    // row (maximum -inf or the finite floor, sum 0) weighs 0, never NaN
     float M = kNoMax;
     for (int c = lane; c < nseg; c += 64) M = fmaxf(M, ml[c].x);
     M = wave_max(M);
@@ -313,40 +318,39 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total
     }
     L = wave_sum(L);
 
-    const int sub = lane / F4, d4 = lane % F4;
-    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int sub = lane / LPS, dl = lane % LPS;
+    float acc[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
     for (int cb = 0; cb < nseg; cb += SPR * kRounds) {
-        float4 v[kRounds];
-        float mw[kRounds];
+        uint4 v[kRounds];
+        float2 mw[kRounds];
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
             const int c = min(cb + r * SPR + sub, nseg - 1);
-            v[r] = po[(int64_t)c * F4 + d4];
-            mw[r] = ml[c].x;
+            v[r] = po[(int64_t)c * LPS + dl];
+            mw[r] = ml[c];
         }
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
-            const float w = cb + r * SPR + sub < nseg ? __builtin_amdgcn_exp2f(mw[r] - M) : 0.f;
-            acc.x += w * v[r].x;
-            acc.y += w * v[r].y;
-            acc.z += w * v[r].z;
-            acc.w += w * v[r].w;
+            const float w =
+                cb + r * SPR + sub < nseg ? __builtin_amdgcn_exp2f(mw[r].x - M) * mw[r].y : 0.f;
+            float x[EPL];
+            unpack16<T>(v[r], x);
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[e] += w * x[e];
         }
     }
 #pragma unroll
-    for (int off = F4; off < 64; off *= 2) {
-        acc.x += __shfl_xor(acc.x, off);
-        acc.y += __shfl_xor(acc.y, off);
-        acc.z += __shfl_xor(acc.z, off);
-        acc.w += __shfl_xor(acc.w, off);
-    }
-    if (lane < F4) {
-        T* out = reinterpret_cast<T*>(p.out) + orow * D + 4 * d4;
+    for (int off = LPS; off < 64; off *= 2)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] += __shfl_xor(acc[e], off);
+    if (lane < LPS) {
         const float inv = 1.f / L;
-        out[0] = from_f32<T>(acc.x * inv);
-        out[1] = from_f32<T>(acc.y * inv);
-        out[2] = from_f32<T>(acc.z * inv);
-        out[3] = from_f32<T>(acc.w * inv);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] *= inv;
+        *reinterpret_cast<uint4*>(reinterpret_cast<T*>(p.out) + orow * D + EPL * dl) =
+            pack16<T>(acc);
     }
     if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * kLn2;
 }
@@ -377,7 +381,7 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.seg = reinterpret_cast<const int4*>(pl.table);
     p.unit_seg = pl.table + (size_t)kSegRecord * pl.n_segments;
     p.seq_unit = p.unit_seg + pl.n_units + 1;
-    p.part_o = reinterpret_cast<float*>(ws + pl.q_rot_bytes);
+    p.part_o = ws + pl.q_rot_bytes;
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
     p.out = a.out;
     p.lse = a.lse;
@@ -446,7 +450,7 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->q_rot_bytes = align256((size_t)rows * head_dim * elem);
     if (p->partials) {
         const size_t prow = (size_t)sched.n_segments * sched.row_block;
-        p->part_o_bytes = align256(prow * head_dim * sizeof(float));
+        p->part_o_bytes = align256(prow * head_dim * elem);
         p->part_ml_bytes = align256(prow * 2 * sizeof(float));
     } else {
         p->part_o_bytes = p->part_ml_bytes = 0;

@@ -64,8 +64,8 @@ struct KParams {
     const int4* seg;
     const int32_t* unit_seg;
     const int32_t* seq_unit;
-    float* part_o;    // [segment][row in block][head_dim]
-    float* part_ml;   // [segment][row in block][2]: running max (log2 units), sum
+    void* part_o;     // split partials O / l, in the workload dtype
+    float* part_ml;   // their (running max in log2 units, sum) pairs
     void* out;
     float* lse;
 };

@@ -586,25 +586,24 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         if (tok[rt] < 0) continue;
         const int rho = rho_w + 16 * rt + lr;
         const int64_t orow = (int64_t)(n0 + tok[rt]) * p.n_q_heads + h * G + rho % G;
-        if (direct) {
-            bf16_t* out = reinterpret_cast<bf16_t*>(p.out) + orow * D;
-            const float inv = 1.f / lsum[rt];
+        // the output, or this segment's partial: O / l in bf16 (0 for a row
+        // that saw no key of the segment) with (m, l) in float.  A unit's
+        // partials are row-major over its segments, so the combine reads one
+        // contiguous run per row.
+        const float inv = lsum[rt] > 0.f ? 1.f / lsum[rt] : 0.f;
+        const int64_t pi = (int64_t)part * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
+        bf16_t* dst = direct ? reinterpret_cast<bf16_t*>(p.out) + orow * D
+                             : reinterpret_cast<bf16_t*>(p.part_o) + pi * D;
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const floatx4 v = o[dt][rt];
-                *reinterpret_cast<uint2*>(out + 16 * dt + 4 * lg) =
-                    uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
-            }
-            if (p.lse && lg == 0) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
-        } else {
-            // the unit's partials are row-major over its segments, so the
-            // combine reads one contiguous run per row
-            const int64_t pi = (int64_t)part * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
-            float* po = p.part_o + pi * D;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = o[dt][rt];
-            if (lg == 0) {
+        for (int dt = 0; dt < DT; ++dt) {
+            const floatx4 v = o[dt][rt];
+            *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
+                uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
+        }
+        if (lg == 0) {
+            if (direct) {
+                if (p.lse) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
+            } else {
                 p.part_ml[pi * 2] = m[rt];
                 p.part_ml[pi * 2 + 1] = lsum[rt];
             }

@@ -167,7 +167,7 @@ int used_workgroups(const std::vector<Seg>& segs) {
 }
 
 double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
-                   const CostModel& cm, int head_dim) {
+                   const CostModel& cm, int head_dim, int elem) {
     std::vector<double> wg(used_workgroups(segs), 0.0);
     std::vector<int> pieces(units.size(), 0);
     for (const Seg& g : segs) {
@@ -178,7 +178,7 @@ double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
     double bytes = 0.0;
     for (size_t u = 0; u < units.size(); ++u)
         if (pieces[u] > 1)
-            bytes += 2.0 * pieces[u] * units[u].rows * (head_dim + 2) * 4.0;   // write + read
+            bytes += 2.0 * pieces[u] * units[u].rows * (head_dim * elem + 8.0);   // write + read
     if (bytes > 0.0) t += cm.combine_us + bytes / cm.combine_bytes_per_us;
     return t;
 }
@@ -260,7 +260,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
                 else cut_equal_ranges(units, c, &cand);
                 // a forced count takes only cuts that use every workgroup
                 if (compact_workgroups(&cand) < c && any_cost) continue;
-                const double t = estimate_us(units, cand, cm, head_dim);
+                const double t = estimate_us(units, cand, cm, head_dim, dt == KVLINK_BF16 ? 2 : 4);
                 if (t < best * 0.99) {   // fewer workgroups, unit-aligned cuts on near ties
                     best = t;
                     segs = cand;

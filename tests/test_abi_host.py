@@ -270,7 +270,7 @@ def test_workspace_bytes(kv):
     many = _plan(kv, n_wg=1 << 20)            # one tile per segment
     assert many.n_segments > many.n_units
     assert f(bf, 8, 2, 128, 10, many) == (_align(10 * 8 * 128 * 2) +
-                                           _align(many.n_segments * 256 * 128 * 4) +
+                                           _align(many.n_segments * 256 * 128 * 2) +
                                            _align(many.n_segments * 256 * 2 * 4))
     thin = _plan(kv, f32, 4, 2, 64, (0, 22), [200] * 22, n_wg=12)
     assert thin.row_block == 16 and thin.n_segments > thin.n_units
