@@ -51,6 +51,8 @@ def parse():
                     help="workgroups of the split attention (0: the library's schedule)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-iters", type=int, default=20)
+    ap.add_argument("--eager", action="store_true",
+                    help="time steps launched from Python instead of a captured HIP graph")
     return ap.parse_args()
 
 
@@ -285,7 +287,23 @@ def main():
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
-    ms_step = time_region(lambda i: st.step(), args.steps)
+    ms_step_eager = time_region(lambda i: st.step(), args.steps)
+    # the same step captured once in a HIP graph (torch's capture records the
+    # library's launches on the capture stream) and replayed: the device work
+    # is identical, without the host's per-launch cost
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        st.step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        st.step()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms_step_graph = time_region(lambda i: graph.replay(), args.steps)
+    ms_step = ms_step_eager if args.eager else ms_step_graph
 
     # isolated kernels, on the stream they are launched on (torch's current)
     it = args.kernel_iters
@@ -351,7 +369,8 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded, Llama-shaped caches; no weights or datasets)",
-        "config": {"workload": w.name, "n_layers": L, "n_q_heads": w.n_q_heads,
+        "config": {"workload": w.name, "launch": "eager" if args.eager else "hip_graph",
+                   "n_layers": L, "n_q_heads": w.n_q_heads,
                    "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "rope_theta": w.rope_theta, "documents": len(w.docs[0]),
                    "link_tokens_per_doc": w.link_count[0][0], "query_tokens": w.n_query[0],
@@ -363,6 +382,8 @@ def main():
         "roofline": at_roof if dominant_attend else re_roof,
         "roofline_other": re_roof if dominant_attend else at_roof,
         "per_layer_kernels": stages,
+        "us_per_layer_eager_launch": round(ms_step_eager * 1000.0 / L, 3),
+        "us_per_layer_graph_launch": round(ms_step_graph * 1000.0 / L, 3),
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, alg)

@@ -238,6 +238,43 @@ def test_stage_by_stage_matches_all_stages(n_wg):
     assert torch.equal(first_lse, run.lse[0])
 
 
+def test_graph_replay_matches_eager():
+    """The path captured in a HIP graph (torch's graph capture records the
+    library's launches on the capture stream) gives the eager result on
+    every replay, with eager work and synchronisations between replays."""
+    import torch
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[0])
+    run.run()
+    ref_out, ref_lse = run.out[0].clone(), run.lse[0].clone()
+    ref_k = run.k_dst.clone()
+
+    def step():
+        run.batch.reencode(run.src_view, run.k_view)
+        run.batch.attend(0, run.q[0], run.kn[0], run.vn[0], run.k_view, run.v_view, run.out[0],
+                         run.lse[0])
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(3):
+        run.out[0].zero_()
+        run.lse[0].zero_()
+        run.k_dst.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(run.out[0].view(torch.int16), ref_out.view(torch.int16)), i
+        assert torch.equal(run.lse[0], ref_lse), i
+        assert torch.equal(run.k_dst.view(torch.int16), ref_k.view(torch.int16)), i
+        run.run()                                  # eager work between replays
+        assert torch.equal(run.out[0].view(torch.int16), ref_out.view(torch.int16)), i
+
+
 # ---------------------------------------------------------------- paged pool
 
 
