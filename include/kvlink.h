@@ -204,8 +204,10 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
  *                      order, next record of the same workgroup (-1: none),
  *                      unit, 0}; record w (w < n_workgroups) is workgroup
  *                      w's first segment
- *   n_units + 1        first-segment offsets of the units, in unit order
- *   n_seqs + 1         first-unit offsets of the requests
+ *   n_units x 8        unit records {request, KV head, first row of the
+ *                      block, rows in the block, first new token of the
+ *                      request, first segment in unit order, segments, 0}
+ *   n_split_units      the units with more than one segment (combined)
  * Like the layout arrays, the device copy is trusted: it must be the
  * unmodified table built for the same batch.
  */
@@ -217,6 +219,7 @@ typedef struct {
     int32_t n_segments;
     int32_t row_block;    /* rows per unit: 256 on the matrix-core path, 16 otherwise */
     int32_t n_seqs;
+    int32_t n_split_units; /* units with more than one segment */
 } kvlink_attend_plan;
 
 /*

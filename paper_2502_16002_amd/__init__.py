@@ -55,7 +55,8 @@ class kvlink_attend_plan(ctypes.Structure):
                 ("n_units", ctypes.c_int32),
                 ("n_segments", ctypes.c_int32),
                 ("row_block", ctypes.c_int32),
-                ("n_seqs", ctypes.c_int32)]
+                ("n_seqs", ctypes.c_int32),
+                ("n_split_units", ctypes.c_int32)]
 
 
 def _load():

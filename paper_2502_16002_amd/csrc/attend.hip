@@ -274,85 +274,91 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 
 // ------------------------------------------------------------- combine
 
-// One wavefront per (new token, query head) row of a unit with several
-// segments (rows of single-segment units were written by the split kernel).
-// A unit's partials (O / l in the workload dtype, with float (m, l)) are
-// row-major over its segments, so the row's nseg partial vectors are one
-// contiguous run: lanes read it 16 bytes at a time, several segments per
-// round of loads and kRounds rounds issued together; the lanes holding the
-// same dims are folded at the end.  out = sum_s w_s (O/l)_s / sum_s w_s with
-// w_s = 2^(m_s - M) l_s.
+// The rows of units with several segments (rows of single-segment units
+// were written by the split kernel).  Workgroup (x, y) takes rows
+// [x * RPB, (x+1) * RPB) of the y-th such unit, from its unit record; a row is
+// handled by LPS lanes, each holding 16 bytes of every partial vector.  A
+// unit's partials (O / l in the workload dtype, float (m, l)) are row-major
+// over its segments, so a row's are one contiguous run; up to LPS segments
+// are requested in one round, lane j of the row's group holding segment j's
+// (m, l).  out = sum_s w_s (O/l)_s / sum_s w_s with w_s = 2^(m_s - M) l_s.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void combine_kernel(KParams p, int n_new_total) {
+__global__ __launch_bounds__(256) void combine_kernel(KParams p) {
     constexpr int EPL = 16 / (int)sizeof(T);   // elements per 16-byte load
-    constexpr int LPS = D / EPL;               // lanes per partial vector
-    constexpr int SPR = 64 / LPS;              // segments per round of loads
-    constexpr int kRounds = 4;
+    constexpr int LPS = D / EPL;               // lanes per row
+    constexpr int RPW = 64 / LPS;              // rows per wavefront
+    constexpr int RPB = 4 * RPW;               // rows per workgroup
+    constexpr int CAP = LPS;                   // segments per round of loads
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-    const int64_t orow = (int64_t)blockIdx.x * 4 + wave;   // (n, hq) flattened
-    if (orow >= (int64_t)n_new_total * p.n_q_heads) return;
-    const int n = (int)(orow / p.n_q_heads), hq = (int)(orow % p.n_q_heads);
-    const int s = seq_of(p.seq_new_ptr, p.n_seqs, n);
-    const int n0 = p.seq_new_ptr[s];
-    const int rows_s = (p.seq_new_ptr[s + 1] - n0) * p.group;
-    const int rho = (n - n0) * p.group + hq % p.group;
-    const int nrb = (rows_s + p.row_block - 1) / p.row_block;
-    const int u = p.seq_unit[s] + (hq / p.group) * nrb + rho / p.row_block;
-    if (u < 0 || u >= p.n_units) return;
-    const int c0 = max(p.unit_seg[u], 0), c1 = min(p.unit_seg[u + 1], p.n_segments);
-    const int nseg = c1 - c0;
-    if (nseg <= 1) return;
-    const int64_t base = (int64_t)c0 * p.row_block + (int64_t)(rho % p.row_block) * nseg;
-    const float2* ml = reinterpret_cast<const float2*>(p.part_ml) + base;
-    const uint4* po = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(p.part_o) + base * D);
+    const int grp = lane / LPS, gl = lane % LPS;
+    for (int su = blockIdx.y; su < p.n_split; su += gridDim.y) {
+        const int u = p.split_units[su];
+        if (u < 0 || u >= p.n_units) continue;
+        const int4 u0 = p.unit[2 * (int64_t)u], u1 = p.unit[2 * (int64_t)u + 1];
+        const int s = u0.x, h = u0.y, rho0 = u0.z, rows = u0.w;
+        const int n0 = u1.x, seg0 = u1.y, nseg = u1.z;
+        if (s < 0 || s >= p.n_seqs || h < 0 || h >= p.n_kv_heads || rows < 1 ||
+            rows > p.row_block || seg0 < 0 || nseg < 2 || seg0 + nseg > p.n_segments)
+            continue;
+        const int r = blockIdx.x * RPB + wave * RPW + grp;
+        if (blockIdx.x * RPB >= rows) continue;
+        const bool valid = r < rows;
+        const int rr = valid ? r : rows - 1;   // in-bounds addresses for spare lanes
+        const int64_t base = (int64_t)seg0 * p.row_block + (int64_t)rr * nseg;
+        const float2* ml = reinterpret_cast<const float2*>(p.part_ml) + base;
+        const uint4* po =
+            reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(p.part_o) + base * D);
 
-    // the running maximum starts finite, so a segment that saw no key of this
-    // row (maximum -inf or the finite floor, sum 0) weighs 0, never NaN
-    float M = kNoMax;
-    for (int c = lane; c < nseg; c += 64) M = fmaxf(M, ml[c].x);
-    M = wave_max(M);
-    float L = 0.f;
-    for (int c = lane; c < nseg; c += 64) {
-        const float2 v = ml[c];
-        L += __builtin_amdgcn_exp2f(v.x - M) * v.y;
+        // the running maximum starts finite, so a segment that saw no key of
+        // this row (maximum -inf or the finite floor, sum 0) weighs 0
+        float M = kNoMax, L = 0.f, acc[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+        for (int cb = 0; cb < nseg; cb += CAP) {
+            const int nb = min(CAP, nseg - cb);
+            const float2 mine = ml[cb + min(gl, nb - 1)];
+            uint4 v[CAP];
+#pragma unroll
+            for (int i = 0; i < CAP; ++i) v[i] = po[(int64_t)(cb + min(i, nb - 1)) * LPS + gl];
+            float mb = gl < nb ? mine.x : kNoMax;
+#pragma unroll
+            for (int off = 1; off < LPS; off *= 2) mb = fmaxf(mb, __shfl_xor(mb, off));
+            const float Mn = fmaxf(M, mb);
+            const float a = __builtin_amdgcn_exp2f(M - Mn);
+            const float w_mine = gl < nb ? __builtin_amdgcn_exp2f(mine.x - Mn) * mine.y : 0.f;
+            float ws = w_mine;
+#pragma unroll
+            for (int off = 1; off < LPS; off *= 2) ws += __shfl_xor(ws, off);
+            L = L * a + ws;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[e] *= a;
+#pragma unroll
+            for (int i = 0; i < CAP; ++i) {
+                const float w = __shfl(w_mine, grp * LPS + i);   // 0 past the last segment
+                float x[EPL];
+                unpack16<T>(v[i], x);
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) acc[e] += w * x[e];
+            }
+            M = Mn;
+        }
+        if (valid) {
+            const int rho = rho0 + r;
+            const int64_t orow =
+                (int64_t)(n0 + rho / p.group) * p.n_q_heads + h * p.group + rho % p.group;
+            const float inv = 1.f / L;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[e] *= inv;
+            *reinterpret_cast<uint4*>(reinterpret_cast<T*>(p.out) + orow * D + EPL * gl) =
+                pack16<T>(acc);
+            if (p.lse && gl == 0) p.lse[orow] = (M + log2f(L)) * kLn2;
+        }
     }
-    L = wave_sum(L);
+}
 
-    const int sub = lane / LPS, dl = lane % LPS;
-    float acc[EPL];
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-    for (int cb = 0; cb < nseg; cb += SPR * kRounds) {
-        uint4 v[kRounds];
-        float2 mw[kRounds];
-#pragma unroll
-        for (int r = 0; r < kRounds; ++r) {
-            const int c = min(cb + r * SPR + sub, nseg - 1);
-            v[r] = po[(int64_t)c * LPS + dl];
-            mw[r] = ml[c];
-        }
-#pragma unroll
-        for (int r = 0; r < kRounds; ++r) {
-            const float w =
-                cb + r * SPR + sub < nseg ? __builtin_amdgcn_exp2f(mw[r].x - M) * mw[r].y : 0.f;
-            float x[EPL];
-            unpack16<T>(v[r], x);
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) acc[e] += w * x[e];
-        }
-    }
-#pragma unroll
-    for (int off = LPS; off < 64; off *= 2)
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] += __shfl_xor(acc[e], off);
-    if (lane < LPS) {
-        const float inv = 1.f / L;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] *= inv;
-        *reinterpret_cast<uint4*>(reinterpret_cast<T*>(p.out) + orow * D + EPL * dl) =
-            pack16<T>(acc);
-    }
-    if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * kLn2;
+template <typename T, int D>
+constexpr int combine_rows_per_block() {
+    return 4 * (64 / (D / (16 / (int)sizeof(T))));
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -379,8 +385,9 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.n_units = pl.n_units;
     p.n_segments = pl.n_segments;
     p.seg = reinterpret_cast<const int4*>(pl.table);
-    p.unit_seg = pl.table + (size_t)kSegRecord * pl.n_segments;
-    p.seq_unit = p.unit_seg + pl.n_units + 1;
+    p.unit = reinterpret_cast<const int4*>(pl.table + (size_t)kSegRecord * pl.n_segments);
+    p.split_units = pl.table + (size_t)kSegRecord * pl.n_segments + (size_t)kUnitRecord * pl.n_units;
+    p.n_split = pl.n_split;
     p.part_o = ws + pl.q_rot_bytes;
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
     p.out = a.out;
@@ -408,9 +415,9 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     }
     if (!(stages & KVLINK_STAGE_COMBINE) || !pl.partials) return hipSuccess;
 
-    const int64_t n_rows = (int64_t)pl.n_new_total * pl.n_q_heads;
-    hipLaunchKernelGGL((combine_kernel<T, D>), dim3((unsigned)((n_rows + 3) / 4)), dim3(256), 0,
-                       stream, p, pl.n_new_total);
+    constexpr int rpb = combine_rows_per_block<T, D>();
+    const dim3 grid((pl.row_block + rpb - 1) / rpb, std::min(pl.n_split, 65535));
+    hipLaunchKernelGGL((combine_kernel<T, D>), grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -428,9 +435,11 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
         return false;
     if ((int64_t)sched.n_segments * kSegRecord > INT32_MAX) return false;
     if (sched.n_workgroups > 0 && (sched.n_units < 1 || sched.n_segments < 1)) return false;
-    const int64_t want =
-        (int64_t)kSegRecord * sched.n_segments + sched.n_units + 1 + sched.n_seqs + 1;
+    const int64_t want = (int64_t)kSegRecord * sched.n_segments +
+                         (int64_t)kUnitRecord * sched.n_units + sched.n_split_units;
     if (sched.n_segments < sched.n_workgroups) return false;
+    if (sched.n_split_units < 0 || sched.n_split_units > sched.n_units) return false;
+    if ((sched.n_split_units > 0) != (sched.n_segments > sched.n_units)) return false;
     if (sched.table_len != want) return false;
     const size_t elem = dt == KVLINK_BF16 ? 2 : 4;
     p->n_q_heads = n_q_heads;
@@ -445,7 +454,8 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->n_units = sched.n_units;
     p->n_segments = sched.n_segments;
     p->table = sched.table;
-    p->partials = sched.n_segments > sched.n_units;
+    p->partials = sched.n_split_units > 0;
+    p->n_split = sched.n_split_units;
     const int64_t rows = (int64_t)n_new_total * n_q_heads;
     p->q_rot_bytes = align256((size_t)rows * head_dim * elem);
     if (p->partials) {

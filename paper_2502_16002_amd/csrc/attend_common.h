@@ -51,7 +51,8 @@ __device__ __forceinline__ BlockKeys block_keys(const int32_t* new_visible, int 
 // Arguments of the split kernels and the combine.  The schedule table (see
 // the schedule's description in the public header) is read through seg
 // (n_segments records of kSegRecord int32, as 4 int4; record w is workgroup
-// w's first segment), unit_seg (n_units + 1) and seq_unit (n_seqs + 1).
+// w's first segment), unit (n_units records of kUnitRecord int32, as 2 int4)
+// and split_units (the n_split units with several segments).
 struct KParams {
     const void* q_rot;
     View k, v;
@@ -62,8 +63,9 @@ struct KParams {
     float scale_log2;
     int row_block, n_units, n_segments;
     const int4* seg;
-    const int32_t* unit_seg;
-    const int32_t* seq_unit;
+    const int4* unit;
+    const int32_t* split_units;
+    int n_split;
     void* part_o;     // split partials O / l, in the workload dtype
     float* part_ml;   // their (running max in log2 units, sum) pairs
     void* out;
@@ -71,6 +73,7 @@ struct KParams {
 };
 
 static_assert(kSegRecord == 16, "segment records are read as four int4");
+static_assert(kUnitRecord == 8, "unit records are read as two int4");
 
 // Record g of the schedule (uniform loads).
 __device__ __forceinline__ void load_record(const KParams& p, int g, int4 (&rec)[4]) {

@@ -32,7 +32,8 @@
 // Segment records are numbered so that record w is workgroup w's first
 // segment; further segments of a workgroup follow the first n and are
 // chained by the record's `next` field.  A workgroup therefore issues its
-// first key-tile loads after one table read.
+// first key-tile loads after one table read.  Unit records and the list of
+// units with several segments drive the combine the same way.
 #include <algorithm>
 #include <climits>
 #include <cmath>
@@ -223,9 +224,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     // rows per wavefront of the matrix-core kernel (eight wavefronts)
     const int rows_per_wave = rb / 8;
     std::vector<Unit> units;
-    std::vector<int32_t> seq_unit(n_seqs + 1);
     for (int s = 0; s < n_seqs; ++s) {
-        seq_unit[s] = (int32_t)units.size();
         const int n0 = seq_new_ptr[s];
         const int rows_s = (seq_new_ptr[s + 1] - n0) * group;
         for (int h = 0; h < n_kv_heads; ++h)
@@ -244,7 +243,6 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
                                  seq_cached[s], vis, (int)nvirt, weight});
             }
     }
-    seq_unit[n_seqs] = (int32_t)units.size();
     int64_t T = 0;
     for (const Unit& x : units) T += x.tiles;
 
@@ -315,7 +313,12 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     counts->n_units = (int)units.size();
     counts->n_segments = n_seg;
     counts->row_block = rb;
-    counts->table_len = (int64_t)kSegRecord * n_seg + (int64_t)units.size() + 1 + n_seqs + 1;
+    std::vector<int32_t> split;
+    for (size_t u = 0; u < units.size(); ++u)
+        if (unit_seg[u + 1] - unit_seg[u] > 1) split.push_back((int32_t)u);
+    counts->n_split = (int)split.size();
+    counts->table_len = (int64_t)kSegRecord * n_seg + (int64_t)kUnitRecord * units.size() +
+                        (int64_t)split.size();
     if (table) {
         table->assign((size_t)counts->table_len, 0);
         int32_t* t = table->data();
@@ -339,9 +342,18 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             r[kSegNext] = next[i];
             r[kSegUnit] = g.u;
         }
-        int32_t* us = t + (int64_t)kSegRecord * n_seg;
-        std::copy(unit_seg.begin(), unit_seg.end(), us);
-        std::copy(seq_unit.begin(), seq_unit.end(), us + units.size() + 1);
+        int32_t* ut = t + (int64_t)kSegRecord * n_seg;
+        for (size_t u = 0; u < units.size(); ++u) {
+            int32_t* r = ut + (int64_t)kUnitRecord * u;
+            r[kUnitS] = units[u].s;
+            r[kUnitH] = units[u].h;
+            r[kUnitRho0] = units[u].rho0;
+            r[kUnitRows] = units[u].rows;
+            r[kUnitN0] = units[u].n0;
+            r[kUnitSeg0] = unit_seg[u];
+            r[kUnitNseg] = unit_seg[u + 1] - unit_seg[u];
+        }
+        std::copy(split.begin(), split.end(), ut + (int64_t)kUnitRecord * units.size());
     }
     return KVLINK_OK;
 }

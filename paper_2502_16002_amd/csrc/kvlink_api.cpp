@@ -267,6 +267,7 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
         plan->n_segments = c.n_segments;
         plan->row_block = c.row_block;
         plan->n_seqs = n_seqs;
+        plan->n_split_units = c.n_split;
         return ok();
     } catch (...) {
         return fail(KVLINK_ERR_INVALID_ARG, "unexpected exception in kvlink_attend_make_plan");

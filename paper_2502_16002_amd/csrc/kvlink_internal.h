@@ -189,7 +189,7 @@ struct AttendPlan {
     int n_seqs, n_new_total;
     int row_block;          // GQA rows per unit
     bool use_mfma;
-    int n_wg, n_units, n_segments;
+    int n_wg, n_units, n_segments, n_split;
     const int32_t* table;   // device copy of the schedule table
     bool partials;          // some unit has several segments
     size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
@@ -212,10 +212,16 @@ enum {
     kSegN0, kSegTc, kSegCmax, kSegNvirt, kSegPart, kSegNext, kSegUnit, kSegSpare, kSegRecord
 };
 
+// Unit record of the schedule table: kUnitRecord int32 fields.
+enum {
+    kUnitS = 0, kUnitH, kUnitRho0, kUnitRows, kUnitN0, kUnitSeg0, kUnitNseg, kUnitSpare,
+    kUnitRecord
+};
+
 // The schedule of kvlink_attend_make_plan (host).  Returns a kvlink_status
 // and, on failure, a message in *why.
 struct PlanCounts {
-    int n_wg, n_units, n_segments, row_block;
+    int n_wg, n_units, n_segments, row_block, n_split;
     int64_t table_len;
 };
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,

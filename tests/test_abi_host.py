@@ -288,13 +288,13 @@ REC = 16   # int32 fields of a segment record
 def _decode(plan, table, n_seqs):
     """Split a schedule table into its sections (layout in include/kvlink.h)."""
     t = np.asarray(table)
-    n_seg, n_u = plan.n_segments, plan.n_units
+    n_seg, n_u, n_sp = plan.n_segments, plan.n_units, plan.n_split_units
     recs = t[:REC * n_seg].reshape(n_seg, REC)
     o = REC * n_seg
-    unit_seg = t[o:o + n_u + 1]
-    seq_unit = t[o + n_u + 1:o + n_u + 1 + n_seqs + 1]
-    assert len(t) == o + n_u + 1 + n_seqs + 1 == plan.table_len
-    return recs, unit_seg, seq_unit
+    unit_recs = t[o:o + 8 * n_u].reshape(n_u, 8)
+    split = t[o + 8 * n_u:o + 8 * n_u + n_sp]
+    assert len(t) == o + 8 * n_u + n_sp == plan.table_len
+    return recs, unit_recs, split
 
 
 def _expected_units(L, G, hkv, rb):
@@ -331,10 +331,9 @@ def _check_schedule(kv, w, n_wg_req):
     max_new = int(np.max(np.diff(L["seq_new_ptr"])))
     mfma = w.dtype == "bf16" and max_new * G >= 32
     assert plan.row_block == (256 if mfma else 16)
-    recs, unit_seg, seq_unit = _decode(plan, table, w.n_seqs)
-    units, exp_seq_unit = _expected_units(L, G, w.n_kv_heads, plan.row_block)
+    recs, unit_recs, split = _decode(plan, table, w.n_seqs)
+    units, _ = _expected_units(L, G, w.n_kv_heads, plan.row_block)
     assert plan.n_units == len(units)
-    assert np.array_equal(seq_unit, exp_seq_unit)
     T = int(units[:, 8].sum())
     n = plan.n_workgroups
     assert 1 <= n <= T <= 10 ** 7 and plan.n_segments >= n
@@ -356,11 +355,16 @@ def _check_schedule(kv, w, n_wg_req):
     assert seen.all()
     # per unit: its segments cover its tiles once, in order of their index,
     # and every record carries its unit's fields, segment count and first
-    # segment in unit order
-    assert unit_seg[0] == 0 and np.all(np.diff(unit_seg) >= 1) and unit_seg[-1] == len(recs)
+    # segment in unit order; the unit records and the split list agree
+    nseg = np.array([np.sum(recs[:, 14] == u) for u in range(len(units))])
+    unit_seg = np.concatenate([[0], np.cumsum(nseg)])
+    assert np.all(nseg >= 1) and unit_seg[-1] == len(recs)
+    assert np.array_equal(unit_recs[:, :5], units[:, [0, 1, 2, 3, 4]])
+    assert np.array_equal(unit_recs[:, 5], unit_seg[:-1]) and np.array_equal(unit_recs[:, 6], nseg)
+    assert np.all(unit_recs[:, 7] == 0)
+    assert list(split) == [u for u in range(len(units)) if nseg[u] > 1]
     for u in range(len(units)):
         mine = recs[recs[:, 14] == u]
-        assert len(mine) == unit_seg[u + 1] - unit_seg[u]
         mine = mine[np.argsort(mine[:, 7])]
         assert list(mine[:, 7]) == list(range(len(mine)))
         assert mine[0, 4] == 0 and mine[-1, 5] == units[u, 8]
