@@ -139,6 +139,77 @@ __device__ __forceinline__ void read_vt(const uint32_t (&a)[DT], uint2 (&r)[DT][
     else read_vt4<OFF0, OFF1>(a, r);
 }
 
+// The same reads issued without the wait: the caller waits with wait_vt,
+// whose in-out operands keep every use of r after the wait.  Only valid
+// where the compiler issues no LDS access of its own in between (its own
+// waits would then also cover these reads, which is correct but slower).
+#define KVLINK_TR_ISSUE(o, i, off) "ds_read_b64_tr_b16 %" #o ", %" #i " offset:%" #off "\n\t"
+template <int OFF0, int OFF1>
+__device__ __forceinline__ void issue_vt8(const uint32_t (&a)[8], uint2 (&r)[8][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile(
+        KVLINK_TR_ISSUE(0, 16, 24) KVLINK_TR_ISSUE(1, 16, 25)
+        KVLINK_TR_ISSUE(2, 17, 24) KVLINK_TR_ISSUE(3, 17, 25)
+        KVLINK_TR_ISSUE(4, 18, 24) KVLINK_TR_ISSUE(5, 18, 25)
+        KVLINK_TR_ISSUE(6, 19, 24) KVLINK_TR_ISSUE(7, 19, 25)
+        KVLINK_TR_ISSUE(8, 20, 24) KVLINK_TR_ISSUE(9, 20, 25)
+        KVLINK_TR_ISSUE(10, 21, 24) KVLINK_TR_ISSUE(11, 21, 25)
+        KVLINK_TR_ISSUE(12, 22, 24) KVLINK_TR_ISSUE(13, 22, 25)
+        KVLINK_TR_ISSUE(14, 23, 24) KVLINK_TR_ISSUE(15, 23, 25)
+        : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
+          "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1]), "=&v"(r[4][0]), "=&v"(r[4][1]),
+          "=&v"(r[5][0]), "=&v"(r[5][1]), "=&v"(r[6][0]), "=&v"(r[6][1]), "=&v"(r[7][0]),
+          "=&v"(r[7][1])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]),
+          "v"(a[7]), "i"(OFF0), "i"(OFF1)
+        : "memory");
+#endif
+}
+
+template <int OFF0, int OFF1>
+__device__ __forceinline__ void issue_vt4(const uint32_t (&a)[4], uint2 (&r)[4][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile(
+        KVLINK_TR_ISSUE(0, 8, 12) KVLINK_TR_ISSUE(1, 8, 13)
+        KVLINK_TR_ISSUE(2, 9, 12) KVLINK_TR_ISSUE(3, 9, 13)
+        KVLINK_TR_ISSUE(4, 10, 12) KVLINK_TR_ISSUE(5, 10, 13)
+        KVLINK_TR_ISSUE(6, 11, 12) KVLINK_TR_ISSUE(7, 11, 13)
+        : "=&v"(r[0][0]), "=&v"(r[0][1]), "=&v"(r[1][0]), "=&v"(r[1][1]), "=&v"(r[2][0]),
+          "=&v"(r[2][1]), "=&v"(r[3][0]), "=&v"(r[3][1])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "i"(OFF0), "i"(OFF1)
+        : "memory");
+#endif
+}
+#undef KVLINK_TR_ISSUE
+
+__device__ __forceinline__ void wait_vt(uint2 (&r)[8][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]), "+v"(r[2][0]),
+                   "+v"(r[2][1]), "+v"(r[3][0]), "+v"(r[3][1]), "+v"(r[4][0]), "+v"(r[4][1]),
+                   "+v"(r[5][0]), "+v"(r[5][1]), "+v"(r[6][0]), "+v"(r[6][1]), "+v"(r[7][0]),
+                   "+v"(r[7][1])
+                 :
+                 : "memory");
+#endif
+}
+
+__device__ __forceinline__ void wait_vt(uint2 (&r)[4][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]), "+v"(r[2][0]),
+                   "+v"(r[2][1]), "+v"(r[3][0]), "+v"(r[3][1])
+                 :
+                 : "memory");
+#endif
+}
+
+template <int DT, int OFF0, int OFF1>
+__device__ __forceinline__ void issue_vt(const uint32_t (&a)[DT], uint2 (&r)[DT][2]) {
+    if constexpr (DT == 8) issue_vt8<OFF0, OFF1>(a, r);
+    else issue_vt4<OFF0, OFF1>(a, r);
+}
+
 // bf16 pair (RNE) of two floats, low half first: one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{a, b}, bf16x2));
@@ -407,14 +478,16 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // half), dims 16dt + 4(j%4).., so that lane i receives keys 4lg+k (k =
     // 0..3) of dim 16dt + i.  The sub-tile and key-half parts of the
     // addresses are immediate offsets.
-    auto pv = [&](const unsigned char* st, auto h_const, const uint32_t (&pk)[kRT][4]) {
+    auto v_issue = [&](const unsigned char* st, auto h_const, uint2 (&vr)[DT][2]) {
         constexpr int h = decltype(h_const)::value;
         const uint32_t vt = lds_addr(st + Smem<D>::k_bytes);
         uint32_t va[DT];
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
-        uint2 vr[DT][2];
-        read_vt<DT, 32 * h * 2 * D, (32 * h + 16) * 2 * D>(va, vr);
+        issue_vt<DT, 32 * h * 2 * D, (32 * h + 16) * 2 * D>(va, vr);
+    };
+    auto pv = [&](uint2 (&vr)[DT][2], const uint32_t (&pk)[kRT][4]) {
+        wait_vt(vr);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             const uint2* half = vr[dt];
@@ -508,6 +581,17 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             }
         }
 
+        // the V^T operands of this sub-tile go out now and are waited for just
+        // before the P V products; the K operands still to be used must have
+        // arrived first, or the compiler's own waits for them (which know
+        // nothing of these reads) would also wait for the V reads
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) asm volatile("" ::"v"(ka[1][ds]));
+#endif
+        uint2 vr[DT][2];
+        v_issue(stc, hc, vr);
+
         // second half: products of key half 1, with p = 2^x packed to bf16
         // and the row sums (8 pairs over the 2 * DS products)
         uint32_t pk[kRT][4];
@@ -529,7 +613,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             __builtin_amdgcn_sched_barrier(0);
         }
 
-        pv(stc, hc, pk);
+        pv(vr, pk);
     };
 
     // ---- software pipeline over 32-key sub-tiles j = 0, 1, ... (tile j/2,
