@@ -177,10 +177,81 @@ def backlog(seconds):
     torch.cuda._sleep(int(seconds * _SLEEP_CYCLES_PER_S))
 
 
+class PagedSetup(Setup):
+    """Device buffers of the shared-pool workload: the stored document caches
+    live once in a paged pool (16-token pages, placed by the workload's page
+    permutation); every request gets re-encoded K copies in pages of its own
+    (shuffled), and reads V straight from the pool pages of its documents
+    through its V block table, with fresh pages after them for its new
+    tokens."""
+
+    def __init__(self, w, n_workgroups, device="cuda", seed=11):
+        import torch
+        import workloads
+        from paper_2502_16002_amd.runtime import Batch, dtype_code, paged_view
+        self.w = w
+        L, H, d, P = w.n_layers, w.n_kv_heads, w.head_dim, w.page_size
+        rng = np.random.default_rng(seed)
+        doc_pages = [(n + P - 1) // P for n in w.doc_table_len]
+        n_pool = sum(doc_pages)
+        first = np.concatenate([[0], np.cumsum(doc_pages)[:-1]])
+        pool_table = np.zeros((len(doc_pages), max(doc_pages)), np.int32)
+        for j, (f, npg) in enumerate(zip(first, doc_pages)):
+            pool_table[j, :npg] = w.pool_page_perm[f:f + npg]
+        sdp = np.concatenate([[0], np.cumsum([len(x) for x in w.docs])]).astype(np.int32)
+        dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
+        lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
+        src_seq = [j for s in range(w.n_seqs) for j in w.docs[s]]
+        self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
+                               sdp, dl, lc, w.n_query, doc_src_seq=src_seq,
+                               doc_src_row=[0] * len(dl), n_workgroups=n_workgroups,
+                               device=device)
+        td = b.torch_dtype
+        max_new_pages = (b.max_new + P - 1) // P
+        n_fresh = w.n_seqs * max_new_pages
+        self.pool_table = torch.from_numpy(pool_table).to(device)
+        k_pool = torch.zeros((L, n_pool, H, P, d), dtype=td, device=device)
+        self.v_all = torch.zeros((L, n_pool + n_fresh, H, P, d), dtype=td, device=device)
+        row0 = workloads.doc_row0(w)
+        self.q, self.kn, self.vn = [], [], []
+        for l in range(L):
+            ld = workloads.layer_data(w, l)
+            for j, n in enumerate(w.doc_table_len):
+                k = to_torch(w, ld.k_store[:, row0[j]:row0[j] + n], device)
+                v = to_torch(w, ld.v_store[:, row0[j]:row0[j] + n], device)
+                for pg in range(doc_pages[j]):
+                    phys = int(pool_table[j, pg])
+                    k_pool[l, phys] = k[:, pg * P:(pg + 1) * P]
+                    self.v_all[l, phys] = v[:, pg * P:(pg + 1) * P]
+            self.q.append(to_torch(w, ld.q_new, device))
+            self.kn.append(to_torch(w, ld.k_new, device))
+            self.vn.append(to_torch(w, ld.v_new, device))
+        seq_cached = b.layout["seq_cached"]
+        max_pages = max(int((seq_cached[s] + w.n_new(s) + P - 1) // P) for s in range(w.n_seqs))
+        k_table = rng.permutation(w.n_seqs * max_pages).astype(np.int32).reshape(w.n_seqs, -1)
+        v_table = np.zeros((w.n_seqs, max_pages), np.int32)
+        for s in range(w.n_seqs):
+            pages = [int(pool_table[j, pg]) for j in w.docs[s] for pg in range(doc_pages[j])]
+            fresh = n_pool + s * max_new_pages + np.arange(max_pages - len(pages))
+            v_table[s] = np.concatenate([pages, fresh]).astype(np.int32)
+        self.k_table = torch.from_numpy(k_table).to(device)
+        self.v_table = torch.from_numpy(v_table).to(device)
+        self.k_src = [k_pool, k_pool.clone()]
+        self.k_dst = [torch.zeros((L, w.n_seqs * max_pages, H, P, d), dtype=td, device=device)
+                      for _ in range(2)]
+        self.src_views = [paged_view(t, n_pool, H, P, d, self.pool_table, max(doc_pages))
+                          for t in self.k_src]
+        self.dst_views = [paged_view(t, w.n_seqs * max_pages, H, P, d, self.k_table, max_pages)
+                          for t in self.k_dst]
+        self.v_view = paged_view(self.v_all, n_pool + n_fresh, H, P, d, self.v_table, max_pages)
+        self.out = b.new_out()
+        self.lse = b.new_lse()
+
+
 def algorithmic(w, batch):
     """Bytes and flops the method itself moves (per the closed forms)."""
     es = 2 if w.dtype == "bf16" else 4
-    Tc = int(batch.layout["seq_cached"][0])
+    Tc = int(batch.layout["seq_cached"].astype(np.int64).sum())
     n_new = batch.n_new
     H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
     re_bytes = 2 * w.n_layers * H * Tc * d * es
@@ -277,9 +348,7 @@ def main():
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workloads.get(args.workload)
-    if w.pool:
-        raise SystemExit("paged workloads are parity cases, not bench lines")
-    st = Setup(w, args.workgroups)
+    st = (PagedSetup if w.pool else Setup)(w, args.workgroups)
     alg = algorithmic(w, st.batch)
     print(f"# setup done: {w.name} cached={alg['cached_tokens']} new={alg['new_tokens']} "
           f"workgroups={st.batch.n_workgroups} segments={st.batch.plan.n_segments}", file=sys.stderr, flush=True)
@@ -370,10 +439,10 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic (seeded, Llama-shaped caches; no weights or datasets)",
         "config": {"workload": w.name, "launch": "eager" if args.eager else "hip_graph",
-                   "n_layers": L, "n_q_heads": w.n_q_heads,
+                   "requests": w.n_seqs, "n_layers": L, "n_q_heads": w.n_q_heads,
                    "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
-                   "rope_theta": w.rope_theta, "documents": len(w.docs[0]),
-                   "link_tokens_per_doc": w.link_count[0][0], "query_tokens": w.n_query[0],
+                   "rope_theta": w.rope_theta, "documents": sum(len(x) for x in w.docs),
+                   "link_tokens_per_doc": w.link_count[0][0], "query_tokens": int(sum(w.n_query)),
                    "cached_tokens": alg["cached_tokens"], "new_tokens": alg["new_tokens"],
                    "attention_workgroups": st.batch.n_workgroups,
                    "attention_segments": st.batch.plan.n_segments},
@@ -385,7 +454,7 @@ def main():
         "us_per_layer_eager_launch": round(ms_step_eager * 1000.0 / L, 3),
         "us_per_layer_graph_launch": round(ms_step_graph * 1000.0 / L, 3),
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and w.n_seqs == 1:
         res["cpu_baseline"] = cpu_baseline(w, alg)
     print(json.dumps(res), flush=True)
 
