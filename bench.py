@@ -38,6 +38,8 @@ KERNEL_SOURCES = {
     "attend_mfma_kernel": ["attend_mfma.hip", "attend_common.h", "kvlink_internal.h"],
     "reencode_kernel": ["reencode.hip", "kvlink_internal.h"],
 }
+# split-attention kernel by the schedule's row block
+SPLIT_KERNEL = {256: "attend_mfma_kernel", 16: "attend_valu_kernel"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b-32layer-10doc.md")
 
 
@@ -112,7 +114,9 @@ class Setup:
                           self.out, self.lse, stages=stages, workspace=workspace)
 
     def step(self):
-        self.reencode(0)
+        # a decoding step attends over a cache re-encoded at prefill
+        if not self.w.decode:
+            self.reencode(0)
         for l in range(self.w.n_layers):
             self.attend(l, 0)
 
@@ -320,7 +324,7 @@ def cpu_baseline(w, alg, budget_s=15.0):
         kc, vc, q, kn, vn = f(kc), f(vc), f(q), f(kn), f(vn)
         t0 = time.perf_counter()
         r0, g = 0, 0
-        for j, L in enumerate(w.doc_len(0)):
+        for j, L in enumerate([] if w.decode else w.doc_len(0)):
             oracle.reencode(kc[:, r0:r0 + L], g, w.rope_theta)
             r0 += L
             g += L + w.link_count[0][j]
@@ -332,9 +336,10 @@ def cpu_baseline(w, alg, budget_s=15.0):
             break
     return {"value": round(total / layers * 1e6, 1), "unit": "us/layer",
             "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{layers} of {w.n_layers} layers in full (re-encode of all "
-                      f"{len(w.doc_len(0))} documents + attention of all {alg['new_tokens']} "
-                      f"new tokens x {w.n_q_heads} heads), {total:.1f} s",
+            "sample": f"{layers} of {w.n_layers} layers in full ("
+                      + ("" if w.decode else f"re-encode of all {len(w.doc_len(0))} documents + ")
+                      + f"attention of all {alg['new_tokens']} new tokens x {w.n_q_heads} heads), "
+                      f"{total:.1f} s",
             "cpu": platform.processor() or platform.machine()}
 
 
@@ -385,7 +390,7 @@ def main():
 
     L = w.n_layers
     us_layer = ms_step * 1000.0 / L
-    step_bytes = alg["reencode_bytes"] + L * alg["attend_bytes"]
+    step_bytes = (0 if w.decode else alg["reencode_bytes"]) + L * alg["attend_bytes"]
     step_flops = L * alg["attend_flops"]
     re_gbps = alg["reencode_bytes"] / (re_ms * 1e-3) / 1e9
     peak_flops = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else VALU_F32_PEAK_TFLOPS
@@ -414,9 +419,7 @@ def main():
                   "tflops": round(tflops, 2)})
         return r
 
-    group = w.n_q_heads // w.n_kv_heads
-    mfma = w.dtype == "bf16" and st.batch.max_new * group >= 32   # the library's own choice
-    split_kernel = "attend_mfma_kernel" if mfma else "attend_valu_kernel"
+    split_kernel = SPLIT_KERNEL[st.batch.plan.row_block]      # the library's own choice
     at_roof = attn_roof(split_kernel, stage_ms["split"])
     at_roof["traffic"] = traffic(split_kernel) if split_kernel in KERNEL_SOURCES else None
     stages = {"rope_new_us": round(stage_ms["rope"] * 1000, 2),
@@ -424,7 +427,7 @@ def main():
               "combine_us": round(stage_ms["combine"] * 1000, 2),
               "all_stages_one_call_us": round(at_ms * 1000, 2),
               "reencode_us_per_layer": round(re_ms * 1000 / L, 2)}
-    dominant_attend = L * stage_ms["split"] > re_ms
+    dominant_attend = w.decode or L * stage_ms["split"] > re_ms
     res = {
         "metric": METRIC,
         "value": round(us_layer, 3),
@@ -445,7 +448,8 @@ def main():
                    "link_tokens_per_doc": w.link_count[0][0], "query_tokens": int(sum(w.n_query)),
                    "cached_tokens": alg["cached_tokens"], "new_tokens": alg["new_tokens"],
                    "attention_workgroups": st.batch.n_workgroups,
-                   "attention_segments": st.batch.plan.n_segments},
+                   "attention_segments": st.batch.plan.n_segments,
+                   "step": "decode: attention only" if w.decode else "re-encode + attention"},
         "hbm_gbps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 3),
         "roofline": at_roof if dominant_attend else re_roof,

@@ -217,7 +217,7 @@ typedef struct {
     int32_t n_workgroups;
     int32_t n_units;
     int32_t n_segments;
-    int32_t row_block;    /* rows per unit: 256 on the matrix-core path, 16 otherwise */
+    int32_t row_block;    /* rows per unit: 256 for bf16 (matrix-core kernel), 16 for fp32 */
     int32_t n_seqs;
     int32_t n_split_units; /* units with more than one segment */
 } kvlink_attend_plan;

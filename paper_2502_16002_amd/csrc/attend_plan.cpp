@@ -186,9 +186,7 @@ double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
 
 }  // namespace
 
-bool attend_uses_mfma(kvlink_dtype dt, int group, int max_new) {
-    return dt == KVLINK_BF16 && (int64_t)max_new * group >= 32;
-}
+bool attend_uses_mfma(kvlink_dtype dt) { return dt == KVLINK_BF16; }
 
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                           int n_seqs, const int32_t* seq_new_ptr, const int32_t* seq_cached,
@@ -199,15 +197,11 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
         *why = "seq_new_ptr[0] must be 0";
         return KVLINK_ERR_LAYOUT;
     }
-    int max_new = 0;
-    for (int s = 0; s < n_seqs; ++s) {
-        const int n = seq_new_ptr[s + 1] - seq_new_ptr[s];
-        if (n < 0) {
+    for (int s = 0; s < n_seqs; ++s)
+        if (seq_new_ptr[s + 1] < seq_new_ptr[s]) {
             *why = "seq_new_ptr is not non-decreasing";
             return KVLINK_ERR_LAYOUT;
         }
-        max_new = std::max(max_new, n);
-    }
     for (int n = 0; n < seq_new_ptr[n_seqs]; ++n)
         if (new_visible[n] < 0) {
             *why = "new_visible is negative";
@@ -218,7 +212,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             *why = "seq_cached is negative";
             return KVLINK_ERR_LAYOUT;
         }
-    const bool mfma = attend_uses_mfma(dt, group, max_new);
+    const bool mfma = attend_uses_mfma(dt);
     const int rb = attend_row_block(mfma);
 
     // rows per wavefront of the matrix-core kernel (eight wavefronts)

@@ -321,7 +321,7 @@ kvlink_status kvlink_attend_stages(
         if (sched.n_seqs != n_seqs)
             return fail(KVLINK_ERR_INVALID_ARG, "plan is for %d requests, call has %d", sched.n_seqs,
                         n_seqs);
-        const bool mfma = kvlink::attend_uses_mfma(dtype, group, max_new);
+        const bool mfma = kvlink::attend_uses_mfma(dtype);
         if (sched.row_block != kvlink::attend_row_block(mfma))
             return fail(KVLINK_ERR_INVALID_ARG, "plan row_block %d does not match this call's path (%d)",
                         sched.row_block, kvlink::attend_row_block(mfma));

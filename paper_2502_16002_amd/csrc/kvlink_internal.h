@@ -195,10 +195,12 @@ struct AttendPlan {
     size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
 };
 
-// Rows per unit of the path the sizes select: the matrix-core kernel where
-// the GQA-packed rows of a KV head form a real dense contraction (bf16 and at
-// least 32 rows), the VALU kernel otherwise.
-bool attend_uses_mfma(kvlink_dtype dt, int group, int max_new);
+// The split kernel a dtype runs on: bf16 on the matrix cores at every row
+// count (with only a few GQA rows per KV head, as in a decoding step, the
+// padded 16x16x32 products still take far fewer issue cycles than VALU dot
+// products, and the pass stays bound by the K/V stream), fp32 on the VALU
+// kernel.
+bool attend_uses_mfma(kvlink_dtype dt);
 int attend_row_block(bool use_mfma);
 
 // Fills every field from the sizes and the schedule's counts; returns false

@@ -232,7 +232,7 @@ def _bad_plan(kv, **fields):
     ("row_block", 1),                      # plan of the other path
     ("n_seqs", 1),
     ("table_len", 1),
-    ("thin", 1),                           # VALU-path plan for an MFMA-path call
+    ("other_dtype", 1),                    # bf16 (matrix-core) plan for an fp32 call
 ])
 def test_attend_validation(kv, change, status):
     if isinstance(change, str):
@@ -241,8 +241,8 @@ def test_attend_validation(kv, change, status):
                 "row_block": lambda: _bad_plan(kv, row_block=16),
                 "n_seqs": lambda: _bad_plan(kv, n_seqs=2),
                 "table_len": lambda: _bad_plan(kv, table_len=3),
-                "thin": lambda: _plan(kv, snp=(0, 4), vis=(100,) * 4)}[change]()
-        change = dict(plan=plan)
+                "other_dtype": lambda: _plan(kv)}[change]()
+        change = dict(plan=plan, dtype=kv.KVLINK_F32) if change == "other_dtype" else dict(plan=plan)
     with pytest.raises(kv.KVLinkError) as e:
         _call_attend(kv, _attend_args(kv, **change))
     assert e.value.status == status

@@ -275,6 +275,39 @@ def test_graph_replay_matches_eager():
         assert torch.equal(run.out[0].view(torch.int16), ref_out.view(torch.int16)), i
 
 
+# ---------------------------------------------------------------- decode step
+
+
+def test_decode_step_long_cache():
+    """One new query token (4 GQA rows per KV head) over the 20,480-token
+    re-encoded cache of the long workload: every output row and the append."""
+    w = workloads.llama8b_long_decode(n_layers=2)
+    run = ContiguousRun(w, layers=[0, 1])
+    run.run()
+    assert run.batch.plan.row_block == 256          # few rows still take the matrix cores
+    for l in [0, 1]:
+        _print("decode layer", l, _check_attend(run, l, tag="decode"))
+    _check_append(run, 1)
+
+
+def test_decode_step_paged_pool():
+    """One new token for each of the 16 shared-pool requests, keys and values
+    read through the block tables."""
+    from harness import PagedRun
+    w = workloads.llama8b_paged_decode()
+    run = PagedRun(w)
+    run.run()
+    b = run.batch
+    got_all, lse_all = to_f64(run.out[0]), to_f64(run.lse[0])
+    for s in range(w.n_seqs):
+        kc, vc, q, kn, vn = run.oracle_inputs(0, s)
+        ref, ref_lse = oracle.attend(w.doc_len(s), w.link_count[s], w.n_query[s], q, kn, vn, kc,
+                                     vc, w.rope_theta, w.scale)
+        n0 = int(b.layout["seq_new_ptr"][s])
+        check_close(w, got_all[n0:n0 + 1], ref, f"paged decode request {s}")
+        assert float(np.max(np.abs(lse_all[n0:n0 + 1] - ref_lse))) <= 2e-2
+
+
 # ---------------------------------------------------------------- paged pool
 
 

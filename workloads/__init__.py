@@ -71,6 +71,7 @@ class Workload:
     page_size: int = 0
     pool_page_perm: Optional[np.ndarray] = None
     description: str = ""
+    decode: bool = False            # a decoding step: the cache is already re-encoded
     extra: dict = field(default_factory=dict)
 
     @property
@@ -94,11 +95,12 @@ class Workload:
         return 1.0 / float(np.sqrt(self.head_dim))
 
 
-def _make(name, dtype, n_layers, hq, hkv, d, theta, seed, lens, links, nq, desc):
+def _make(name, dtype, n_layers, hq, hkv, d, theta, seed, lens, links, nq, desc, decode=False):
     return Workload(name=name, dtype=dtype, n_layers=n_layers, n_q_heads=hq, n_kv_heads=hkv,
                     head_dim=d, rope_theta=theta, seed=seed,
                     doc_table_len=list(lens), docs=[list(range(len(lens)))],
-                    link_count=[[links] * len(lens)], n_query=[nq], description=desc)
+                    link_count=[[links] * len(lens)], n_query=[nq], description=desc,
+                    decode=decode)
 
 
 def tiny_f32(seed=2502):
@@ -152,12 +154,35 @@ def llama8b_paged(seed=2506, n_layers=1):
                     description="Llama-3.1-8B shape, shared 64x256-token paged pool, 16 requests")
 
 
+def llama8b_long_decode(seed=2505, n_layers=32):
+    """One decoding step after the long-context prefill: the 40 x 512-token
+    cache of the long workload (already re-encoded) and a single new query
+    token per layer, 4 GQA rows per KV head."""
+    return _make("llama8b-decode-40x512", "bf16", n_layers, 32, 8, 128, 5e5, seed,
+                 [512] * 40, 0, 1, "Llama-3.1-8B shape, decode step over 40 docs of 512 tokens",
+                 decode=True)
+
+
+def llama8b_paged_decode(seed=2506, n_layers=1):
+    """One decoding step of the 16 shared-pool requests: each request's 20
+    documents read through its page tables and one new query token."""
+    w = llama8b_paged(seed, n_layers)
+    w.name = "llama8b-paged-decode-16req"
+    w.link_count = [[0] * len(d) for d in w.docs]
+    w.n_query = [1] * w.n_seqs
+    w.decode = True
+    w.description = "Llama-3.1-8B shape, decode step of 16 requests over the shared paged pool"
+    return w
+
+
 WORKLOADS = {
     "tiny-f32-3x32": tiny_f32,
     "llama1b-1layer-10doc": llama1b_layer,
     "llama8b-32layer-10doc": llama8b_10doc,
     "llama8b-32layer-40x512": llama8b_long,
     "llama8b-paged-16req": llama8b_paged,
+    "llama8b-decode-40x512": llama8b_long_decode,
+    "llama8b-paged-decode-16req": llama8b_paged_decode,
 }
 
 
