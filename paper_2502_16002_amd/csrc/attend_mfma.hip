@@ -268,7 +268,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     const int n_tiles = (kend - kbeg + kTile - 1) / kTile;
     const int rho_end = rho0 + rows;
 
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int rho_w = rho0 + wave * kRT * 16;      // first row of this wave
 
@@ -285,39 +285,57 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // segment: this wave loads K blocks wave + kWaves*i and V slots
     // (wave + kWaves*i)*64 + lane of every tile.
     constexpr int KI = KB / kWaves, VJ = VI / kWaves;
+    static_assert(64 / CH <= 16, "a V load spans one 16-key group");
     int k_key[KI], k_off[KI], v_key[VJ], v_off[VJ];
+    int k_key0[KI], v_key0[VJ];                           // first key of the load (uniform)
 #pragma unroll
     for (int i = 0; i < KI; ++i) {
         const int b = wave + kWaves * i;                  // K block (sc, kt, ds)
         const int ds = b % DS, kt = (b / DS) % 2, sc = b / (2 * DS);
-        k_key[i] = 32 * sc + 16 * kt + lr;
+        k_key0[i] = 32 * sc + 16 * kt;
+        k_key[i] = k_key0[i] + lr;
         k_off[i] = 64 * ds + 16 * lg;
     }
 #pragma unroll
     for (int i = 0; i < VJ; ++i) {
         const int pos = (wave + kWaves * i) * 64 + lane;  // 16-byte slot of the V tile
         const int key = pos / CH, pc = pos % CH;
+        v_key0[i] = (wave + kWaves * i) * 64 / CH;
         v_key[i] = key;
         v_off[i] = 16 * (pc ^ (key & (CH - 1)));          // logical chunk stored at slot pc
     }
-    const bool contiguous = kp.table == nullptr && vp.table == nullptr;
-    const int fast_end = min(kend, bk.cmax);              // rows here are the keys themselves
+    // rows below fast_end are the keys themselves; tiles there take their
+    // rows by 16-row groups (one page each, when paged)
+    const bool grouped = kp.groups_of_16() && vp.groups_of_16();
+    const int fast_end = grouped ? min(kend, bk.cmax) : 0;
 
     // this wave's share of tile t, straight into LDS stage t % kStages
     auto issue_tile = [&](int t) {
         unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
         const int tb = kbeg + t * kTile;
-        if (contiguous && tb + kTile <= fast_end) {
-            // the whole tile is cached rows tb.., one 64-bit add per load
-            const char* kt0 = kp.base + (int64_t)tb * kp.row_bytes;
-            const char* vt0 = vp.base + (int64_t)tb * vp.row_bytes;
+        if (tb + kTile <= fast_end) {
+            // a K block covers keys g..g+15 and a V load keys within one
+            // aligned 16-key group g, so one page per load; the page reads
+            // of the tile go out together, ahead of the address arithmetic
+            int kpg[KI] = {}, vpg[VJ] = {};
+            if (kp.table) {
+#pragma unroll
+                for (int i = 0; i < KI; ++i) kpg[i] = kp.page_of(tb + k_key0[i]);
+            }
+            if (vp.table) {
+#pragma unroll
+                for (int i = 0; i < VJ; ++i) vpg[i] = vp.page_of(tb + (v_key0[i] & ~15));
+            }
 #pragma unroll
             for (int i = 0; i < KI; ++i)
-                load_lds16(kt0 + k_key[i] * kp.row_bytes + k_off[i], st + (wave + kWaves * i) * 1024);
+                load_lds16(kp.in_page(kpg[i], tb + k_key0[i]) + lr * kp.row_bytes + k_off[i],
+                           st + (wave + kWaves * i) * 1024);
 #pragma unroll
-            for (int i = 0; i < VJ; ++i)
-                load_lds16(vt0 + v_key[i] * vp.row_bytes + v_off[i],
+            for (int i = 0; i < VJ; ++i) {
+                const int g = tb + (v_key0[i] & ~15);
+                load_lds16(vp.in_page(vpg[i], g) + (v_key[i] & 15) * vp.row_bytes + v_off[i],
                            st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
+            }
         } else {
 #pragma unroll
             for (int i = 0; i < KI; ++i)

@@ -100,10 +100,25 @@ struct RowPtr {
     const int32_t* table;      // paged: this sequence's block-table row, else NULL
     int64_t page_bytes;        // paged: page stride in bytes
     int32_t page_size;
+    int32_t page_shift;        // log2(page_size) for a power of two, else -1
     __device__ __forceinline__ const char* row(int r) const {
         if (!table) return base + (int64_t)r * row_bytes;
         const int pg = table[r / page_size];
         return base + (int64_t)pg * page_bytes + (int64_t)(r % page_size) * row_bytes;
+    }
+    // True when every aligned group of 16 rows lies in one page.
+    __device__ __forceinline__ bool groups_of_16() const { return !table || page_shift >= 4; }
+    // Paged slices whose 16-row groups lie in one page: the page of row r
+    // (the same in every lane), read through the scalar cache, so that the
+    // wavefront's vector loads in flight do not delay it.
+    __device__ __forceinline__ int page_of(int r) const {
+        return *(const __attribute__((address_space(4))) int32_t*)(table + (r >> page_shift));
+    }
+    // Row r of page pg (from page_of; ignored when contiguous); for r a
+    // multiple of 16, rows r..r+15 follow it at row_bytes.
+    __device__ __forceinline__ const char* in_page(int pg, int r) const {
+        if (!table) return base + (int64_t)r * row_bytes;
+        return base + (int64_t)pg * page_bytes + (int64_t)(r & (page_size - 1)) * row_bytes;
     }
 };
 
@@ -117,11 +132,13 @@ __device__ __forceinline__ RowPtr row_ptr(const View& v, int layer, int head, in
         r.table = v.block_table + (int64_t)seq * v.max_pages;
         r.page_bytes = v.page_stride * es;
         r.page_size = v.page_size;
+        r.page_shift = (v.page_size & (v.page_size - 1)) == 0 ? __builtin_ctz(v.page_size) : -1;
     } else {
         r.base += (int64_t)seq * v.seq_stride * es;
         r.table = nullptr;
         r.page_bytes = 0;
         r.page_size = 1;
+        r.page_shift = 0;
     }
     return r;
 }
