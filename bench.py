@@ -35,11 +35,14 @@ CSRC = os.path.join(ROOT, "paper_2502_16002_amd", "csrc")
 # sources that decide each kernel's memory traffic (hashed to tell whether
 # the committed counter figures still describe the kernel that runs)
 KERNEL_SOURCES = {
-    "attend_mfma_kernel": ["attend_mfma.hip", "attend_common.h", "kvlink_internal.h"],
+    "attend_mfma_kernel": ["attend_mfma.hip", "mfma_ops.h", "attend_common.h", "kvlink_internal.h"],
+    "attend_decode_kernel": ["attend_decode.hip", "mfma_ops.h", "attend_common.h",
+                             "kvlink_internal.h"],
     "reencode_kernel": ["reencode.hip", "kvlink_internal.h"],
 }
-# split-attention kernel by the schedule's row block
-SPLIT_KERNEL = {256: "attend_mfma_kernel", 16: "attend_valu_kernel"}
+# split-attention kernel by (dtype, the schedule's row block)
+SPLIT_KERNEL = {("bf16", 256): "attend_mfma_kernel", ("bf16", 16): "attend_decode_kernel",
+                ("f32", 16): "attend_valu_kernel"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b-32layer-10doc.md")
 
 
@@ -419,7 +422,7 @@ def main():
                   "tflops": round(tflops, 2)})
         return r
 
-    split_kernel = SPLIT_KERNEL[st.batch.plan.row_block]      # the library's own choice
+    split_kernel = SPLIT_KERNEL[(w.dtype, st.batch.plan.row_block)]   # the library's own choice
     at_roof = attn_roof(split_kernel, stage_ms["split"])
     at_roof["traffic"] = traffic(split_kernel) if split_kernel in KERNEL_SOURCES else None
     stages = {"rope_new_us": round(stage_ms["rope"] * 1000, 2),

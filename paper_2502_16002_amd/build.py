@@ -12,7 +12,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkvlink.so")
-SOURCES = ["kvlink_api.cpp", "attend_plan.cpp", "reencode.hip", "attend.hip", "attend_mfma.hip"]
+SOURCES = ["kvlink_api.cpp", "attend_plan.cpp", "reencode.hip", "attend.hip", "attend_mfma.hip",
+           "attend_decode.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -282,15 +282,25 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 // over its segments, so a row's are one contiguous run; up to LPS segments
 // are requested in one round, lane j of the row's group holding segment j's
 // (m, l).  out = sum_s w_s (O/l)_s / sum_s w_s with w_s = 2^(m_s - M) l_s.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void combine_kernel(KParams p) {
+// With kShare (16-row units: a decoding step's few rows over many segments),
+// when the block has fewer rows than lane groups and a row more than one run
+// of segments, S groups share a row, each taking every S-th run of LPS
+// segments, and merge their states through LDS.
+// (Four workgroups per compute unit, i.e. at most 128 registers per lane:
+// the partial loads in flight are what the kernel's speed depends on.)
+template <typename T, int D, bool kShare>
+__global__ __launch_bounds__(256, 4) void combine_kernel(KParams p) {
     constexpr int EPL = 16 / (int)sizeof(T);   // elements per 16-byte load
     constexpr int LPS = D / EPL;               // lanes per row
-    constexpr int RPW = 64 / LPS;              // rows per wavefront
-    constexpr int RPB = 4 * RPW;               // rows per workgroup
+    constexpr int RPW = 64 / LPS;              // lane groups (rows) per wavefront
+    constexpr int RPB = 4 * RPW;               // lane groups (rows) per workgroup
     constexpr int CAP = LPS;                   // segments per round of loads
+    constexpr int SH = kShare ? RPB : 1;
+    __shared__ float s_ml[SH][2];
+    __shared__ float s_acc[SH][LPS][EPL];
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int grp = lane / LPS, gl = lane % LPS;
+    const int q = wave * RPW + grp;            // lane group of the workgroup
     for (int su = blockIdx.y; su < p.n_split; su += gridDim.y) {
         const int u = p.split_units[su];
         if (u < 0 || u >= p.n_units) continue;
@@ -300,9 +310,13 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p) {
         if (s < 0 || s >= p.n_seqs || h < 0 || h >= p.n_kv_heads || rows < 1 ||
             rows > p.row_block || seg0 < 0 || nseg < 2 || seg0 + nseg > p.n_segments)
             continue;
-        const int r = blockIdx.x * RPB + wave * RPW + grp;
         if (blockIdx.x * RPB >= rows) continue;
-        const bool valid = r < rows;
+        const int here = min(RPB, rows - (int)blockIdx.x * RPB);
+        int S = 1;                                  // lane groups per row
+        if constexpr (kShare)
+            while (2 * S * here <= RPB && S * CAP < nseg) S *= 2;
+        const int r = blockIdx.x * RPB + q / S, phase = q % S;
+        const bool valid = q / S < here;
         const int rr = valid ? r : rows - 1;   // in-bounds addresses for spare lanes
         const int64_t base = (int64_t)seg0 * p.row_block + (int64_t)rr * nseg;
         const float2* ml = reinterpret_cast<const float2*>(p.part_ml) + base;
@@ -314,7 +328,8 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p) {
         float M = kNoMax, L = 0.f, acc[EPL];
 #pragma unroll
         for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-        for (int cb = 0; cb < nseg; cb += CAP) {
+        const int n_mine = valid ? nseg : 0;
+        for (int cb = phase * CAP; cb < n_mine; cb += S * CAP) {
             const int nb = min(CAP, nseg - cb);
             const float2 mine = ml[cb + min(gl, nb - 1)];
             uint4 v[CAP];
@@ -342,7 +357,31 @@ __global__ __launch_bounds__(256) void combine_kernel(KParams p) {
             }
             M = Mn;
         }
-        if (valid) {
+        if constexpr (kShare) {
+            if (S > 1) {   // uniform over the workgroup
+                if (gl == 0) {
+                    s_ml[q][0] = M;
+                    s_ml[q][1] = L;
+                }
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) s_acc[q][gl][e] = acc[e];
+                __syncthreads();
+                if (valid && phase == 0) {
+                    for (int k = 1; k < S; ++k) {
+                        const float Mk = s_ml[q + k][0];
+                        const float Mn = fmaxf(M, Mk);
+                        const float a = __builtin_amdgcn_exp2f(M - Mn);
+                        const float b = __builtin_amdgcn_exp2f(Mk - Mn);
+                        L = L * a + s_ml[q + k][1] * b;
+#pragma unroll
+                        for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * a + s_acc[q + k][gl][e] * b;
+                        M = Mn;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        if (valid && phase == 0) {
             const int rho = rho0 + r;
             const int64_t orow =
                 (int64_t)(n0 + rho / p.group) * p.n_q_heads + h * p.group + rho % p.group;
@@ -405,8 +444,10 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     }
 
     if ((stages & KVLINK_STAGE_SPLIT) && pl.n_wg > 0) {
-        if (pl.use_mfma) {
+        if (pl.path == kPathWide) {
             e = launch_attend_mfma(D, p, pl.n_wg, stream);
+        } else if (pl.path == kPathDecode) {
+            e = launch_attend_decode(D, p, pl.n_wg, stream);
         } else {
             hipLaunchKernelGGL((attend_valu_kernel<T, D>), dim3(pl.n_wg), dim3(256), 0, stream, p);
             e = hipGetLastError();
@@ -417,20 +458,31 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
 
     constexpr int rpb = combine_rows_per_block<T, D>();
     const dim3 grid((pl.row_block + rpb - 1) / rpb, std::min(pl.n_split, 65535));
-    hipLaunchKernelGGL((combine_kernel<T, D>), grid, dim3(256), 0, stream, p);
+    if (pl.row_block == kValuRB || pl.path == kPathDecode)
+        hipLaunchKernelGGL((combine_kernel<T, D, true>), grid, dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL((combine_kernel<T, D, false>), grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 
 }  // namespace
 
-int attend_row_block(bool use_mfma) { return use_mfma ? attend_mfma_row_block() : kValuRB; }
+int attend_row_block(AttendPath path) {
+    return path == kPathWide ? attn::attend_mfma_row_block()
+                             : path == kPathDecode ? attn::attend_decode_row_block() : kValuRB;
+}
 
 bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                       int n_new_total, const kvlink_attend_plan& sched, AttendPlan* p) {
     if (n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads) return false;
     if (head_dim != 64 && head_dim != 128) return false;
     if (n_new_total < 0 || sched.n_seqs < 1) return false;
-    if (sched.row_block != attend_mfma_row_block() && sched.row_block != kValuRB) return false;
+    // the kernel is fixed by the dtype and the schedule's row block
+    int path = -1;
+    if (dt == KVLINK_BF16 && sched.row_block == attend_row_block(kPathWide)) path = kPathWide;
+    if (dt == KVLINK_BF16 && sched.row_block == attend_row_block(kPathDecode)) path = kPathDecode;
+    if (dt == KVLINK_F32 && sched.row_block == attend_row_block(kPathValu)) path = kPathValu;
+    if (path < 0) return false;
     if (sched.n_workgroups < 0 || sched.n_units < 0 || sched.n_segments < sched.n_units)
         return false;
     if ((int64_t)sched.n_segments * kSegRecord > INT32_MAX) return false;
@@ -449,7 +501,7 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->n_seqs = sched.n_seqs;
     p->n_new_total = n_new_total;
     p->row_block = sched.row_block;
-    p->use_mfma = sched.row_block == attend_mfma_row_block();
+    p->path = path;
     p->n_wg = sched.n_workgroups;
     p->n_units = sched.n_units;
     p->n_segments = sched.n_segments;

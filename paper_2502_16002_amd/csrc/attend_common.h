@@ -92,8 +92,10 @@ __device__ __forceinline__ bool record_ok(const KParams& p, const int4 (&rec)[4]
 }
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
-// GQA rows per workgroup of the MFMA kernel
+hipError_t launch_attend_decode(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
+// GQA rows per unit of the wide-block and decode kernels
 int attend_mfma_row_block();
+int attend_decode_row_block();
 
 }  // namespace attn
 }  // namespace kvlink

@@ -63,13 +63,17 @@ struct CostModel {
     int slots_per_cu;
 };
 
-// Fitted to sweeps of the workgroup count on the 10- and 40-document
-// workloads: the split launch costs about 15 us plus 1.6-2.2 us per tile of
-// its longest workgroup (8 us of that fixed part recurs for every further
-// segment of a workgroup); the combine about 6 us plus its partial traffic,
-// written and read back at an effective ~6 TB/s.
-CostModel cost_model(bool mfma, int head_dim) {
-    if (mfma) return {8.0, head_dim == 128 ? 1.9 : 1.2, 6.0, 6.0e6, 1};
+// Wide-block kernel: fitted to sweeps of the workgroup count on the 10- and
+// 40-document workloads: the split launch costs about 15 us plus 1.6-2.2 us
+// per tile of its longest workgroup (8 us of that fixed part recurs for every
+// further segment of a workgroup); the combine about 6 us plus its partial
+// traffic, written and read back at an effective ~6 TB/s.  Decode kernel:
+// two workgroups per compute unit sharing the unit's HBM stream, so a tile
+// (64 keys of K and V) costs its bytes at an eighth of a compute unit's
+// share of ~6 TB/s, plus the start of a segment (its first loads' latency).
+CostModel cost_model(AttendPath path, int head_dim) {
+    if (path == kPathWide) return {8.0, head_dim == 128 ? 1.9 : 1.2, 6.0, 6.0e6, 1};
+    if (path == kPathDecode) return {3.0, head_dim == 128 ? 2.8 : 1.5, 6.0, 6.0e6, 2};
     return {4.0, head_dim == 128 ? 1.0 : 0.6, 4.0, 6.0e6, head_dim == 128 ? 2 : 4};
 }
 
@@ -186,7 +190,10 @@ double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
 
 }  // namespace
 
-bool attend_uses_mfma(kvlink_dtype dt) { return dt == KVLINK_BF16; }
+AttendPath attend_path(kvlink_dtype dt, int group, int max_new) {
+    if (dt != KVLINK_BF16) return kPathValu;
+    return (int64_t)group * max_new <= attend_row_block(kPathDecode) ? kPathDecode : kPathWide;
+}
 
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                           int n_seqs, const int32_t* seq_new_ptr, const int32_t* seq_cached,
@@ -197,11 +204,14 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
         *why = "seq_new_ptr[0] must be 0";
         return KVLINK_ERR_LAYOUT;
     }
-    for (int s = 0; s < n_seqs; ++s)
+    int max_new = 0;
+    for (int s = 0; s < n_seqs; ++s) {
         if (seq_new_ptr[s + 1] < seq_new_ptr[s]) {
             *why = "seq_new_ptr is not non-decreasing";
             return KVLINK_ERR_LAYOUT;
         }
+        max_new = std::max(max_new, seq_new_ptr[s + 1] - seq_new_ptr[s]);
+    }
     for (int n = 0; n < seq_new_ptr[n_seqs]; ++n)
         if (new_visible[n] < 0) {
             *why = "new_visible is negative";
@@ -212,10 +222,10 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             *why = "seq_cached is negative";
             return KVLINK_ERR_LAYOUT;
         }
-    const bool mfma = attend_uses_mfma(dt);
-    const int rb = attend_row_block(mfma);
+    const AttendPath path = attend_path(dt, group, max_new);
+    const int rb = attend_row_block(path);
 
-    // rows per wavefront of the matrix-core kernel (eight wavefronts)
+    // rows per wavefront of the wide-block kernel (eight wavefronts)
     const int rows_per_wave = rb / 8;
     std::vector<Unit> units;
     for (int s = 0; s < n_seqs; ++s) {
@@ -232,7 +242,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
                     return KVLINK_ERR_LAYOUT;
                 }
                 const int waves = (rows + rows_per_wave - 1) / rows_per_wave;
-                const double weight = mfma && waves <= 4 ? 0.5 : 1.0;
+                const double weight = path == kPathWide && waves <= 4 ? 0.5 : 1.0;
                 units.push_back({s, h, rho0, (int)((nvirt + kTileKeys - 1) / kTileKeys), rows, n0,
                                  seq_cached[s], vis, (int)nvirt, weight});
             }
@@ -242,7 +252,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
 
     std::vector<Seg> segs, cand;
     if (T > 0) {
-        const CostModel cm = cost_model(mfma, head_dim);
+        const CostModel cm = cost_model(path, head_dim);
         const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
         double best = 1e300;
         auto consider = [&](int c, bool any_cost) {

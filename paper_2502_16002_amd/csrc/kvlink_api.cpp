@@ -321,10 +321,10 @@ kvlink_status kvlink_attend_stages(
         if (sched.n_seqs != n_seqs)
             return fail(KVLINK_ERR_INVALID_ARG, "plan is for %d requests, call has %d", sched.n_seqs,
                         n_seqs);
-        const bool mfma = kvlink::attend_uses_mfma(dtype);
-        if (sched.row_block != kvlink::attend_row_block(mfma))
+        const int rb = kvlink::attend_row_block(kvlink::attend_path(dtype, group, max_new));
+        if (sched.row_block != rb)
             return fail(KVLINK_ERR_INVALID_ARG, "plan row_block %d does not match this call's path (%d)",
-                        sched.row_block, kvlink::attend_row_block(mfma));
+                        sched.row_block, rb);
         if (!d_seq_new_ptr || !d_seq_cached || !d_new_pos || !d_new_visible)
             return fail(KVLINK_ERR_INVALID_ARG, "a layout descriptor pointer is NULL");
         if (!q_new || !k_new || !v_new || !out)

@@ -205,20 +205,23 @@ struct AttendPlan {
     int n_q_heads, n_kv_heads, group, head_dim;
     int n_seqs, n_new_total;
     int row_block;          // GQA rows per unit
-    bool use_mfma;
+    int path;               // AttendPath
     int n_wg, n_units, n_segments, n_split;
     const int32_t* table;   // device copy of the schedule table
     bool partials;          // some unit has several segments
     size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
 };
 
-// The split kernel a dtype runs on: bf16 on the matrix cores at every row
-// count (with only a few GQA rows per KV head, as in a decoding step, the
-// padded 16x16x32 products still take far fewer issue cycles than VALU dot
-// products, and the pass stays bound by the K/V stream), fp32 on the VALU
-// kernel.
-bool attend_uses_mfma(kvlink_dtype dt);
-int attend_row_block(bool use_mfma);
+// The split kernel of a call.  bf16 runs on the matrix cores at every row
+// count: units of more than 16 GQA rows (group * new tokens of the longest
+// request) on the wide-block kernel (256-row units, K/V tiles shared by eight
+// wavefronts), smaller ones, as in a decoding step, on the decode kernel
+// (16-row units, each wavefront streaming its own keys), whose padded 16-row
+// products still take far fewer issue cycles than vector dot products.  fp32
+// runs on the VALU kernel (16-row units).
+enum AttendPath { kPathWide = 0, kPathDecode = 1, kPathValu = 2 };
+AttendPath attend_path(kvlink_dtype dt, int group, int max_new);
+int attend_row_block(AttendPath path);
 
 // Fills every field from the sizes and the schedule's counts; returns false
 // on invalid sizes or counts.

@@ -377,7 +377,8 @@ def _check_schedule(kv, w, n_wg_req):
 
 @pytest.mark.parametrize("name", ["tiny-f32-3x32", "llama1b-1layer-10doc",
                                   "llama8b-32layer-10doc", "llama8b-32layer-40x512",
-                                  "llama8b-paged-16req"])
+                                  "llama8b-paged-16req", "llama8b-decode-40x512",
+                                  "llama8b-paged-decode-16req"])
 def test_attend_schedule(kv, name):
     """Every schedule, chosen by the cost model or forced, deals every tile of
     every unit out exactly once, in contiguous segments with consistent
@@ -389,6 +390,13 @@ def test_attend_schedule(kv, name):
     # the long-context workload's tile count keeps the whole chip busy
     if name == "llama8b-32layer-40x512":
         assert chosen.n_workgroups >= 200
+    # the kernel: 16-row units for bf16 batches of at most 16 rows per KV
+    # head (decoding steps), 256-row units for the other bf16 batches
+    if w.dtype == "bf16":
+        rows = max(w.n_new(s) for s in range(w.n_seqs)) * (w.n_q_heads // w.n_kv_heads)
+        assert chosen.row_block == (16 if rows <= 16 else 256)
+    if w.decode:
+        assert chosen.n_workgroups >= 256     # two workgroups per compute unit fit
 
 
 def test_attend_schedule_errors(kv):

@@ -284,10 +284,30 @@ def test_decode_step_long_cache():
     w = workloads.llama8b_long_decode(n_layers=2)
     run = ContiguousRun(w, layers=[0, 1])
     run.run()
-    assert run.batch.plan.row_block == 256          # few rows still take the matrix cores
+    assert run.batch.plan.row_block == 16           # the decode kernel
     for l in [0, 1]:
         _print("decode layer", l, _check_attend(run, l, tag="decode"))
     _check_append(run, 1)
+
+
+@pytest.mark.parametrize("doc_len,link_count,n_query", [
+    ([37], [0], 1),                         # one token, one short document
+    ([130, 5, 260], [1, 0, 1], 2),          # 4 new tokens: 16 rows, tiles across documents
+    ([1, 1, 3, 1], [1, 0, 1, 1], 0),        # ragged, link tokens only (12 rows)
+    ([], [], 3),                            # no documents
+    ([700, 2000], [0, 0], 1),               # a long cache cut into many segments
+])
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_decode_kernel_layouts(doc_len, link_count, n_query, head_dim):
+    """Units of at most 16 rows (group 4, up to 4 new tokens) on the decode
+    kernel, for several workgroup counts."""
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2,
+                         head_dim=head_dim, dtype="bf16", rope_theta=5e5, seed=23)
+    for n_wg in [0, 1, 3, 1 << 20]:
+        run = ContiguousRun(w, layers=[0], n_workgroups=n_wg)
+        assert run.batch.plan.row_block == 16
+        run.run()
+        _check_attend(run, 0, tag=f"decode{doc_len}/{head_dim}/{n_wg}")
 
 
 def test_decode_step_paged_pool():
