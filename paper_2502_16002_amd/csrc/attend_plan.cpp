@@ -50,7 +50,9 @@ constexpr int kTileKeys = 64;
 
 struct Unit {
     int s, h, rho0, tiles, rows, n0, Tc, cmax, nvirt;
-    double weight;   // cost of one tile relative to a full row block
+    std::vector<double> prefix;   // prefix[t]: cost of tiles [0, t), in us
+    std::vector<float> live;      // live fraction of each tile
+    double cost(int64_t t0, int64_t len) const { return prefix[t0 + len] - prefix[t0]; }
 };
 
 struct Seg {
@@ -59,48 +61,118 @@ struct Seg {
 };
 
 struct CostModel {
-    double per_segment_us, per_tile_us, combine_us, combine_bytes_per_us;
+    // a segment costs per_segment_us + first_us * (live fraction of its first
+    // tile); a tile tile_us + live_us * (live fraction) + mask_us * (masked
+    // fraction)
+    double per_segment_us, first_us, tile_us, live_us, mask_us, combine_us, combine_bytes_per_us;
     int slots_per_cu;
 };
 
-// Wide-block kernel: fitted to sweeps of the workgroup count on the 10- and
-// 40-document workloads: the split launch costs about 15 us plus 1.6-2.2 us
-// per tile of its longest workgroup (8 us of that fixed part recurs for every
-// further segment of a workgroup); the combine about 6 us plus its partial
-// traffic, written and read back at an effective ~6 TB/s.  Decode kernel:
-// two workgroups per compute unit sharing the unit's HBM stream, so a tile
-// (64 keys of K and V) costs its bytes at an eighth of a compute unit's
-// share of ~6 TB/s, plus the start of a segment (its first loads' latency).
+// Wide-block kernel: fitted jointly to per-workgroup timelines of the 10-
+// and 40-document workloads.  A tile costs its stream of K and V (about
+// 1.6 us at the share of HBM a workgroup gets while all stream) plus its
+// products, which scale with the fraction of (wavefront, 32-key step) pairs
+// that are live: a wavefront skips a step none of its rows sees (link tokens
+// see only the documents before them), but the workgroup still streams the
+// tile.  A live step that some row of the wavefront sees only in part (it
+// runs the mask) costs about four times one seen whole.  A segment adds its
+// record and, for its first tile, the products that wait for the tile's
+// loads instead of overlapping them.  The combine costs about 6 us plus its partial
+// traffic, written and read back at an effective ~6 TB/s.  Decode kernel: two
+// workgroups per compute unit sharing the unit's HBM stream, so a tile (64
+// keys of K and V) costs its bytes at an eighth of a compute unit's share of
+// ~6 TB/s, plus the start of a segment (its first loads' latency).  VALU
+// kernel: fp32, a fixed cost per tile.
 CostModel cost_model(AttendPath path, int head_dim) {
-    if (path == kPathWide) return {8.0, head_dim == 128 ? 1.9 : 1.2, 6.0, 6.0e6, 1};
-    if (path == kPathDecode) return {3.0, head_dim == 128 ? 2.8 : 1.5, 6.0, 6.0e6, 2};
-    return {4.0, head_dim == 128 ? 1.0 : 0.6, 4.0, 6.0e6, head_dim == 128 ? 2 : 4};
+    const bool d128 = head_dim == 128;
+    const double f = d128 ? 1.0 : 0.63;   // head_dim 64: fewer bytes and products per key
+    if (path == kPathWide)
+        return {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 6.0, 6.0e6, 1};
+    if (path == kPathDecode) return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 6.0, 6.0e6, 2};
+    return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 4.0, 6.0e6, d128 ? 2 : 4};
+}
+
+// Live (wavefront, 32-key step) pairs of tile t of a wide-kernel unit, by the
+// rule the kernel skips a step with: step j of wavefront w is dead when none
+// of the wavefront's rows sees a key of sub-tiles j or j+1 (32 rows per
+// wavefront, eight wavefronts); *masked counts the live pairs whose
+// sub-tile is not wholly below the wavefront's smallest visible prefix.
+int live_pairs(const Unit& x, int t, int group, const int32_t* new_visible, int* masked) {
+    int cnt = 0;
+    *masked = 0;
+    for (int w = 0; w < 8; ++w) {
+        const int rw = x.rho0 + 32 * w;
+        if (rw >= x.rho0 + x.rows) continue;
+        const int tok_max = (std::min(rw + 32, x.rho0 + x.rows) - 1) / group;
+        const int vis_max = new_visible[x.n0 + tok_max];
+        const int vis_min = new_visible[x.n0 + rw / group];
+        auto dead = [&](int64_t v0) {
+            if (v0 >= x.nvirt) return true;
+            const bool cached_seen = v0 < vis_max && v0 < x.cmax;
+            const bool new_seen = v0 + 32 > x.cmax && std::max<int64_t>(v0, x.cmax) <= x.cmax + tok_max;
+            return !cached_seen && !new_seen;
+        };
+        for (int j = 0; j < 2; ++j) {
+            const int64_t v0 = (int64_t)kTileKeys * t + 32 * j;
+            if (!(dead(v0) && dead(v0 + 32))) {
+                ++cnt;
+                if (v0 + 32 > vis_min) ++*masked;
+            }
+        }
+    }
+    return cnt;
 }
 
 // n contiguous ranges of equal cost over the units' tiles in order
 void cut_equal_ranges(const std::vector<Unit>& units, int n, std::vector<Seg>* segs) {
     double W = 0.0;
-    for (const Unit& x : units) W += x.tiles * x.weight;
+    for (const Unit& x : units) W += x.prefix.back();
     size_t u = 0;
     int64_t t_in_u = 0;   // next tile of unit u to hand out
     double done = 0.0;    // cost handed out before tile t_in_u of unit u
     for (int w = 0; w < n; ++w) {
         const double end = w + 1 == n ? W : W * (w + 1) / n;
         while (u < units.size()) {
-            if (t_in_u >= units[u].tiles) {
+            const Unit& x = units[u];
+            if (t_in_u >= x.tiles) {
                 ++u;
                 t_in_u = 0;
                 continue;
             }
             if (done >= end - 1e-9 && w + 1 < n) break;
             // the tiles of unit u that start before `end`
-            int64_t take = w + 1 == n ? units[u].tiles - t_in_u
-                                      : (int64_t)std::ceil((end - done) / units[u].weight - 1e-9);
-            take = std::max<int64_t>(1, std::min<int64_t>(take, units[u].tiles - t_in_u));
+            int64_t take = x.tiles - t_in_u;
+            if (w + 1 < n) {
+                const double target = x.prefix[t_in_u] + (end - done);
+                const auto it = std::lower_bound(x.prefix.begin() + t_in_u + 1, x.prefix.end(),
+                                                 target - 1e-9);
+                take = std::min<int64_t>(take, (it - x.prefix.begin()) - t_in_u);
+            }
+            take = std::max<int64_t>(1, take);
             segs->push_back({w, (int)u, t_in_u, take});
+            done += x.cost(t_in_u, take);
             t_in_u += take;
-            done += take * units[u].weight;
         }
+    }
+}
+
+// [t0, t1) of unit x cut into k pieces of near-equal cost (piece i ends at the
+// first tile boundary past i+1 k-ths of the cost, at least one tile each)
+void cut_unit(const Unit& x, int k, std::vector<int64_t>* ends) {
+    ends->clear();
+    const double W = x.prefix.back();
+    int64_t t = 0;
+    for (int i = 0; i < k; ++i) {
+        int64_t e = x.tiles;
+        if (i + 1 < k) {
+            const double target = W * (i + 1) / k;
+            e = std::lower_bound(x.prefix.begin() + t + 1, x.prefix.end(), target - 1e-9) -
+                x.prefix.begin();
+            e = std::max<int64_t>(e, t + 1);
+            e = std::min<int64_t>(e, x.tiles - (k - 1 - i));   // room for the pieces left
+        }
+        ends->push_back(e);
+        t = e;
     }
 }
 
@@ -109,8 +181,13 @@ void cut_unit_aligned(const std::vector<Unit>& units, int n, std::vector<Seg>* s
     const int nu = (int)units.size();
     if (n >= nu) {
         std::vector<int> k(nu, 1);
+        std::vector<int64_t> ends;
         auto longest = [&](int u) {
-            return std::ceil((double)units[u].tiles / k[u]) * units[u].weight;
+            cut_unit(units[u], k[u], &ends);
+            double m = 0.0;
+            for (int i = 0, t = 0; i < k[u]; t = (int)ends[i], ++i)
+                m = std::max(m, units[u].cost(t, ends[i] - t));
+            return m;
         };
         std::priority_queue<std::pair<double, int>> pq;   // (longest piece, -unit)
         for (int u = 0; u < nu; ++u) pq.push({longest(u), -u});
@@ -123,12 +200,11 @@ void cut_unit_aligned(const std::vector<Unit>& units, int n, std::vector<Seg>* s
             pq.push({longest(u), -u});
         }
         int w = 0;
-        for (int u = 0; u < nu; ++u)
-            for (int i = 0; i < k[u]; ++i) {
-                const int64_t t0 = (int64_t)units[u].tiles * i / k[u];
-                const int64_t t1 = (int64_t)units[u].tiles * (i + 1) / k[u];
-                segs->push_back({w++, u, t0, t1 - t0});
-            }
+        for (int u = 0; u < nu; ++u) {
+            cut_unit(units[u], k[u], &ends);
+            for (int i = 0, t = 0; i < k[u]; t = (int)ends[i], ++i)
+                segs->push_back({w++, u, t, ends[i] - t});
+        }
         return;
     }
     // fewer workgroups than units: whole units, longest first onto the least
@@ -136,7 +212,7 @@ void cut_unit_aligned(const std::vector<Unit>& units, int n, std::vector<Seg>* s
     std::vector<int> order(nu);
     for (int u = 0; u < nu; ++u) order[u] = u;
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
-        return units[a].tiles * units[a].weight > units[b].tiles * units[b].weight;
+        return units[a].prefix.back() > units[b].prefix.back();
     });
     std::priority_queue<std::pair<double, int>> load;   // (-load, -workgroup)
     for (int w = 0; w < n; ++w) load.push({0.0, -w});
@@ -145,7 +221,7 @@ void cut_unit_aligned(const std::vector<Unit>& units, int n, std::vector<Seg>* s
         auto top = load.top();
         load.pop();
         owner[u] = -top.second;
-        load.push({top.first - units[u].tiles * units[u].weight, top.second});
+        load.push({top.first - units[u].prefix.back(), top.second});
     }
     for (int u = 0; u < nu; ++u) segs->push_back({owner[u], u, 0, units[u].tiles});
 }
@@ -176,7 +252,8 @@ double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
     std::vector<double> wg(used_workgroups(segs), 0.0);
     std::vector<int> pieces(units.size(), 0);
     for (const Seg& g : segs) {
-        wg[g.w] += cm.per_segment_us + cm.per_tile_us * units[g.u].weight * (double)g.len;
+        wg[g.w] += cm.per_segment_us + cm.first_us * units[g.u].live[g.t0] +
+                   units[g.u].cost(g.t0, g.len);
         ++pieces[g.u];
     }
     double t = *std::max_element(wg.begin(), wg.end());
@@ -225,8 +302,6 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     const AttendPath path = attend_path(dt, group, max_new);
     const int rb = attend_row_block(path);
 
-    // rows per wavefront of the wide-block kernel (eight wavefronts)
-    const int rows_per_wave = rb / 8;
     std::vector<Unit> units;
     for (int s = 0; s < n_seqs; ++s) {
         const int n0 = seq_new_ptr[s];
@@ -241,18 +316,27 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
                     *why = "key range too long";
                     return KVLINK_ERR_LAYOUT;
                 }
-                const int waves = (rows + rows_per_wave - 1) / rows_per_wave;
-                const double weight = path == kPathWide && waves <= 4 ? 0.5 : 1.0;
                 units.push_back({s, h, rho0, (int)((nvirt + kTileKeys - 1) / kTileKeys), rows, n0,
-                                 seq_cached[s], vis, (int)nvirt, weight});
+                                 seq_cached[s], vis, (int)nvirt, {}});
             }
     }
     int64_t T = 0;
     for (const Unit& x : units) T += x.tiles;
+    const CostModel cm = cost_model(path, head_dim);
+    for (Unit& x : units) {
+        x.prefix.assign((size_t)x.tiles + 1, 0.0);
+        x.live.assign((size_t)x.tiles, 1.0f);
+        for (int t = 0; t < x.tiles; ++t) {
+            int masked = 0;
+            const int live = path == kPathWide ? live_pairs(x, t, group, new_visible, &masked) : 16;
+            x.live[t] = (float)(live / 16.0);
+            x.prefix[t + 1] = x.prefix[t] + cm.tile_us + cm.live_us * live / 16.0 +
+                              cm.mask_us * masked / 16.0;
+        }
+    }
 
     std::vector<Seg> segs, cand;
     if (T > 0) {
-        const CostModel cm = cost_model(path, head_dim);
         const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
         double best = 1e300;
         auto consider = [&](int c, bool any_cost) {
