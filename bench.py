@@ -43,7 +43,8 @@ KERNEL_SOURCES = {
 # split-attention kernel by (dtype, the schedule's row block)
 SPLIT_KERNEL = {("bf16", 256): "attend_mfma_kernel", ("bf16", 16): "attend_decode_kernel",
                 ("f32", 16): "attend_valu_kernel"}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b-32layer-10doc.md")
+# committed counter summaries, one per workload
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_{workload}.md")
 
 
 def parse():
@@ -124,64 +125,52 @@ class Setup:
             self.attend(l, 0)
 
     def time_stages(self, iters):
-        """Average duration of one launch of each attention stage, measured
-        with events on the stream the library launches on (torch's current
-        stream).  Every layer gets its own workspace, so a pass can run the
-        RoPE stage of all layers, then the split attention of all layers,
-        then the combine of all layers, each group back to back between two
-        events; a spin kernel ahead of each pass covers the host's enqueueing
-        so that the events bracket device time, not host launch gaps."""
+        """Average duration of one launch of each attention stage.  Every
+        layer gets its own workspace, so the RoPE stages of all layers, the
+        split attentions of all layers and the combines of all layers can
+        each be captured as one HIP graph (torch's capture records the
+        library's launches); each graph is replayed `iters` times between two
+        events on the replay stream, so the events bracket back-to-back
+        device execution with no host gaps."""
         import torch
         L = self.w.n_layers
         if not hasattr(self, "ws_layers"):
             self.ws_layers = [torch.empty_like(self.batch.workspace) for _ in range(L)]
-        tot = {"rope": 0.0, "split": 0.0, "combine": 0.0}
 
-        def one_pass(record):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-            ev[0].record()
-            for l in range(L):
-                self.attend(l, stages=1, workspace=self.ws_layers[l])
-            ev[1].record()
-            for l in range(L):
-                self.attend(l, stages=2, workspace=self.ws_layers[l])
-            ev[2].record()
-            for l in range(L):
-                self.attend(l, stages=4, workspace=self.ws_layers[l])
-            ev[3].record()
-            return ev
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        one_pass(False)
-        host_s = time.perf_counter() - t0
-        torch.cuda.synchronize()
-        for _ in range(iters):
-            backlog(2.0 * host_s + 2e-3)
-            ev = one_pass(True)
+        def group(stage):
+            return lambda: [self.attend(l, stages=stage, workspace=self.ws_layers[l])
+                            for l in range(L)]
+        # every layer's partials and outputs exist before the stages run apart
+        for l in range(L):
+            self.attend(l, workspace=self.ws_layers[l])
+        out = {}
+        for name, stage in [("rope", 1), ("split", 2), ("combine", 4)]:
+            g = capture(group(stage))
+            g.replay()
             torch.cuda.synchronize()
-            tot["rope"] += ev[0].elapsed_time(ev[1])
-            tot["split"] += ev[1].elapsed_time(ev[2])
-            tot["combine"] += ev[2].elapsed_time(ev[3])
-        return {k: v / (iters * L) for k, v in tot.items()}
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            for _ in range(iters):
+                g.replay()
+            e.record()
+            torch.cuda.synchronize()
+            out[name] = s.elapsed_time(e) / (iters * L)
+        return out
 
 
-_SLEEP_CYCLES_PER_S = None
-
-
-def backlog(seconds):
-    """Occupy the current stream for about `seconds` with torch's spin kernel,
-    so that work enqueued after it starts back to back."""
+def capture(fn):
+    """fn's launches captured in a HIP graph (after one run on a side stream,
+    as torch's capture requires)."""
     import torch
-    global _SLEEP_CYCLES_PER_S
-    if _SLEEP_CYCLES_PER_S is None:
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        s.record()
-        torch.cuda._sleep(10_000_000)
-        e.record()
-        torch.cuda.synchronize()
-        _SLEEP_CYCLES_PER_S = 10_000_000 / (s.elapsed_time(e) * 1e-3)
-    torch.cuda._sleep(int(seconds * _SLEEP_CYCLES_PER_S))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
 
 
 class PagedSetup(Setup):
@@ -282,27 +271,22 @@ def measured_traffic(kernel, workload):
     `| kernel | workload | source hash | fetch bytes | write bytes |`.  None when
     there is no row for this kernel and workload, or the kernel's sources
     changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = TRAFFIC_FILE.format(workload=workload)
+    if not os.path.exists(path):
         return None
     want = source_hash(kernel)
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
         if len(cells) == 5 and cells[0] == kernel and cells[1] == workload and cells[2] == want:
             return int(cells[3]) + int(cells[4])
     return None
 
 
-def time_region(fn, iters, host_ahead=False):
-    """Average device time of fn over iters calls.  With host_ahead, a spin
-    kernel first covers the host's enqueueing so that the region measures
-    back-to-back device execution (used for the isolated kernel timings)."""
+def time_region(fn, iters):
+    """Average device time of fn over iters calls, between two events on the
+    current stream."""
     import torch
     torch.cuda.synchronize()
-    if host_ahead:
-        t0 = time.perf_counter()
-        fn(0)
-        torch.cuda.synchronize()
-        backlog(2.0 * (time.perf_counter() - t0) * iters + 2e-3)
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
     for i in range(iters):
@@ -368,27 +352,25 @@ def main():
     # the same step captured once in a HIP graph (torch's capture records the
     # library's launches on the capture stream) and replayed: the device work
     # is identical, without the host's per-launch cost
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        st.step()
-    torch.cuda.current_stream().wait_stream(side)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        st.step()
+    graph = capture(st.step)
     for _ in range(args.warmup):
         graph.replay()
     torch.cuda.synchronize()
     ms_step_graph = time_region(lambda i: graph.replay(), args.steps)
     ms_step = ms_step_eager if args.eager else ms_step_graph
 
-    # isolated kernels, on the stream they are launched on (torch's current)
+    # isolated kernels, each group captured in a HIP graph and replayed on
+    # torch's current stream (the stream the library launches on): the
+    # re-encode alternating between two source/destination copies so that
+    # back-to-back launches do not hit the LLC, the attention of every layer
+    # in one call each, and each attention stage over all layers
     it = args.kernel_iters
-    for i in range(2):
-        st.reencode(i)
-    re_ms = time_region(lambda i: st.reencode(i % 2), it, host_ahead=True)
-    at_ms = time_region(lambda i: [st.attend(l) for l in range(w.n_layers)], it,
-                        host_ahead=True) / w.n_layers
+    g_re = capture(lambda: (st.reencode(0), st.reencode(1)))
+    g_re.replay()
+    re_ms = time_region(lambda i: g_re.replay(), max(1, it // 2)) / 2
+    g_at = capture(lambda: [st.attend(l) for l in range(w.n_layers)])
+    g_at.replay()
+    at_ms = time_region(lambda i: g_at.replay(), it) / w.n_layers
     stage_ms = st.time_stages(max(1, it // 4))
 
     L = w.n_layers
