@@ -187,11 +187,14 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
  * packed per KV head as row = token * group + head-in-group (group =
  * n_q_heads / n_kv_heads) and cut into row blocks of row_block rows; a
  * (request, KV head, row block) unit walks the keys its last token sees in
- * 64-key tiles.  The tiles of all units, in unit order, are dealt out to
- * n_workgroups workgroups as equal contiguous ranges (the split-K of
- * flash-decoding with the splits balanced across units); each piece of a
- * unit that one workgroup covers is a segment, and a unit with several
- * segments has its partial results merged by a log-sum-exp combine.
+ * 64-key tiles.  The units' tiles are dealt out to n_workgroups persistent
+ * workgroups in contiguous pieces (the split-K of flash-decoding, balanced
+ * across units by a cost model): either each unit cut into pieces of equal
+ * cost, one per workgroup, or equal-cost ranges over all units in order;
+ * each piece of a unit that one workgroup covers is a segment, and a unit
+ * with several segments has its partial results merged by a log-sum-exp
+ * combine.  row_block is 16 for batches of at most 16 rows per request and
+ * KV head (a decoding step; fp32 batches always) and 256 otherwise.
  *
  * The table (int32, built on the host by kvlink_attend_make_plan, then
  * copied to the device by the caller) holds, in order:
@@ -217,7 +220,7 @@ typedef struct {
     int32_t n_workgroups;
     int32_t n_units;
     int32_t n_segments;
-    int32_t row_block;    /* rows per unit: 256 for bf16 (matrix-core kernel), 16 for fp32 */
+    int32_t row_block;    /* rows per unit: 256, or 16 (at most 16 rows per KV head; fp32) */
     int32_t n_seqs;
     int32_t n_split_units; /* units with more than one segment */
 } kvlink_attend_plan;
@@ -228,10 +231,11 @@ typedef struct {
  *   seq_new_ptr[n_seqs+1], seq_cached[n_seqs], new_visible[n_new]
  *                    host outputs of kvlink_build_layout for the batch
  *   n_compute_units  compute units of the device (sizes the schedule)
- *   n_workgroups     0: chosen by a cost model (every workgroup costs a fixed
- *                    set-up per segment plus a per-tile cost, the launch is
- *                    as long as its longest workgroup, and split partials
- *                    add a combine launch and their traffic); > 0: that many
+ *   n_workgroups     0: chosen by a cost model (a segment costs a set-up,
+ *                    a tile its K/V stream plus the products of the steps
+ *                    its wavefronts do not skip, the launch is as long as
+ *                    its longest workgroup, and split partials add a
+ *                    combine launch and their traffic); > 0: that many
  *                    workgroups (capped at the tile count)
  *   table, table_capacity  host array for the table; with table == NULL
  *                    only *plan is filled (to size the array)
