@@ -129,17 +129,20 @@ class Setup:
         layer gets its own workspace, so the RoPE stages of all layers, the
         split attentions of all layers and the combines of all layers can
         each be captured as one HIP graph (torch's capture records the
-        library's launches); each graph is replayed `iters` times between two
-        events on the replay stream, so the events bracket back-to-back
-        device execution with no host gaps."""
+        library's launches; a workload of few layers repeats them, so that a
+        replay holds at least 32 launches); each graph is replayed `iters`
+        times between two events on the replay stream, so the events bracket
+        back-to-back device execution with no host gaps."""
         import torch
         L = self.w.n_layers
         if not hasattr(self, "ws_layers"):
             self.ws_layers = [torch.empty_like(self.batch.workspace) for _ in range(L)]
 
+        reps = max(1, 32 // L)          # at least 32 launches per replay
+
         def group(stage):
             return lambda: [self.attend(l, stages=stage, workspace=self.ws_layers[l])
-                            for l in range(L)]
+                            for _ in range(reps) for l in range(L)]
         # every layer's partials and outputs exist before the stages run apart
         for l in range(L):
             self.attend(l, workspace=self.ws_layers[l])
@@ -154,7 +157,7 @@ class Setup:
                 g.replay()
             e.record()
             torch.cuda.synchronize()
-            out[name] = s.elapsed_time(e) / (iters * L)
+            out[name] = s.elapsed_time(e) / (iters * L * reps)
         return out
 
 
@@ -365,9 +368,10 @@ def main():
     # back-to-back launches do not hit the LLC, the attention of every layer
     # in one call each, and each attention stage over all layers
     it = args.kernel_iters
-    g_re = capture(lambda: (st.reencode(0), st.reencode(1)))
+    n_re = 16
+    g_re = capture(lambda: [st.reencode(i % 2) for i in range(n_re)])
     g_re.replay()
-    re_ms = time_region(lambda i: g_re.replay(), max(1, it // 2)) / 2
+    re_ms = time_region(lambda i: g_re.replay(), max(1, it // 4)) / n_re
     g_at = capture(lambda: [st.attend(l) for l in range(w.n_layers)])
     g_at.replay()
     at_ms = time_region(lambda i: g_at.replay(), it) / w.n_layers

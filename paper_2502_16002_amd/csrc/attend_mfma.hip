@@ -175,9 +175,10 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         }
     };
 
-    // Tile 0 goes out first; then the rows' data (visible prefixes, the Q
-    // operand), then tiles 1 and 2, so the first key tile's latency overlaps
-    // the queries' (loads complete in issue order).
+    // Tile 0 goes out first, then the rows' data (visible prefixes, the Q
+    // operand); tiles 1 and 2 follow once tile 0 has arrived and its first
+    // products are issued, so that when every workgroup starts at once tile 0
+    // is not queued behind them (its products are what the loop waits for).
     issue_tile(0);
 
     int tok[kRT], vis[kRT];
@@ -204,8 +205,6 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         for (int ds = 0; ds < DS; ++ds)
             qraw[rt][ds] = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
     }
-    if (n_tiles > 1) issue_tile(1);
-    if (n_tiles > 2) issue_tile(2);
 
     const float c2 = p.scale_log2;   // > 0
     // Row r may see virtual key v iff v < lo (cached rows up to its document,
@@ -468,12 +467,12 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // product over the current stage).  The barrier that makes tile t visible
     // sits in step 2t-1, after which the stage of tile t-2 (no longer read by
     // any wave) receives tile t+2; tile t-1's values stay until that step's
-    // P V.  The prologue issues tiles 0..2.
+    // P V.  The prologue issues tiles 0..2 (1 and 2 after tile 0's barrier).
     const int n_sub = (kend - kbeg + 31) / 32;
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
     constexpr std::integral_constant<int, 0> H0{};
     constexpr std::integral_constant<int, 1> H1{};
-    if (n_tiles >= 3) wait_vm<2 * LPW>(); else if (n_tiles == 2) wait_vm<LPW>(); else wait_vm<0>();
+    wait_vm<0>();
     __syncthreads();
 
     // a step whose two sub-tiles are both dead for the wave is skipped; a
@@ -483,6 +482,8 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         qk_half(stage_of(0), H0, H0, s_a);
         qk_half(stage_of(0), H0, H1, s_a);
     }
+    if (n_tiles > 1) issue_tile(1);
+    if (n_tiles > 2) issue_tile(2);
     for (int t = 0; t < n_tiles; ++t) {
         const unsigned char* st = stage_of(t);
         const int j0 = 2 * t;
