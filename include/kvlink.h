@@ -10,6 +10,9 @@
  *
  *   kvlink_build_layout       index maps of the concatenated sequence (host)
  *   kvlink_reencode_keys      K' = R(delta_i) K for every cached key (GPU)
+ *   kvlink_encode_keys_at_positions
+ *                             K' = R(g_i + t) K for keys cached without
+ *                             rotation (the paper's literal form, GPU)
  *   kvlink_attend_make_plan   balanced split-K schedule of a batch (host)
  *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
  *                             append of their keys/values to the cache and
@@ -180,6 +183,24 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
                                    int32_t head_dim, double rope_theta, int32_t n_spans,
                                    const kvlink_span* d_spans, int32_t max_span_len,
                                    kvlink_kv_view src, kvlink_kv_view dst, void* stream);
+
+/*
+ * kvlink_encode_keys_at_positions — the paper's literal storage form
+ * (Sec. 2.2): keys are cached without any positional rotation (K = W_k x)
+ * and the global rotation is applied at inference, per token:
+ *     dst(l, h, dst_seq_i, dst_row_i + t) = R(delta_i + t) src(l, h, src_seq_i, src_row_i + t)
+ * With the spans of kvlink_build_layout and doc_src_pos0 = 0, delta_i = g_i,
+ * so key t of document i lands at its global position g_i + t.  This equals
+ * kvlink_reencode_keys applied to keys stored rotated at local positions
+ * 0.. (rotations compose).  Arguments, layouts, aliasing rules and errors
+ * are those of kvlink_reencode_keys.
+ */
+kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_layers,
+                                              int32_t n_kv_heads, int32_t head_dim,
+                                              double rope_theta, int32_t n_spans,
+                                              const kvlink_span* d_spans, int32_t max_span_len,
+                                              kvlink_kv_view src, kvlink_kv_view dst,
+                                              void* stream);
 
 /*
  * Schedule of the split-K attention of a request batch (host-built once per

@@ -71,6 +71,8 @@ def _load():
     lib.kvlink_reencode_keys.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32,
                                          kvlink_kv_view, kvlink_kv_view, vp]
     lib.kvlink_reencode_keys.restype = ctypes.c_int
+    lib.kvlink_encode_keys_at_positions.argtypes = lib.kvlink_reencode_keys.argtypes
+    lib.kvlink_encode_keys_at_positions.restype = ctypes.c_int
     lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, i32,
                                             i32, vp, i64, ctypes.POINTER(kvlink_attend_plan)]
     lib.kvlink_attend_make_plan.restype = ctypes.c_int
@@ -181,6 +183,14 @@ def kvlink_reencode_keys(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_sp
     _check(_lib.kvlink_reencode_keys(int(dtype), int(n_layers), int(n_kv_heads), int(head_dim),
                                      float(rope_theta), int(n_spans), _ptr(d_spans),
                                      int(max_span_len), src, dst, _stream(stream)))
+
+
+def kvlink_encode_keys_at_positions(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_spans,
+                                    d_spans, max_span_len, src, dst, stream=None):
+    _check(_lib.kvlink_encode_keys_at_positions(int(dtype), int(n_layers), int(n_kv_heads),
+                                                int(head_dim), float(rope_theta), int(n_spans),
+                                                _ptr(d_spans), int(max_span_len), src, dst,
+                                                _stream(stream)))
 
 
 def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, seq_cached,

@@ -190,10 +190,11 @@ kvlink_status kvlink_build_layout(int32_t n_seqs, const int32_t* seq_doc_ptr,
     }
 }
 
-kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
-                                   int32_t head_dim, double rope_theta, int32_t n_spans,
-                                   const kvlink_span* d_spans, int32_t max_span_len,
-                                   kvlink_kv_view src, kvlink_kv_view dst, void* stream) {
+namespace {
+kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, int32_t n_layers,
+                          int32_t n_kv_heads, int32_t head_dim, double rope_theta, int32_t n_spans,
+                          const kvlink_span* d_spans, int32_t max_span_len, kvlink_kv_view src,
+                          kvlink_kv_view dst, void* stream) {
     try {
         if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
         if (head_dim != 64 && head_dim != 128)
@@ -215,12 +216,32 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
         hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads,
                                                kvlink::make_rope_freqs(rope_theta, head_dim),
                                                n_spans, d_spans, max_span_len, to_view(src),
-                                               to_view(dst), reinterpret_cast<hipStream_t>(stream));
-        if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "re-encode launch: %s", hipGetErrorString(e));
+                                               to_view(dst), per_token,
+                                               reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "%s launch: %s", name, hipGetErrorString(e));
         return ok();
     } catch (...) {
-        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_reencode_keys");
+        return fail(KVLINK_ERR_HIP, "unexpected exception in %s", name);
     }
+}
+}  // namespace
+
+kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
+                                   int32_t head_dim, double rope_theta, int32_t n_spans,
+                                   const kvlink_span* d_spans, int32_t max_span_len,
+                                   kvlink_kv_view src, kvlink_kv_view dst, void* stream) {
+    return rotate_keys("kvlink_reencode_keys", false, dtype, n_layers, n_kv_heads, head_dim,
+                       rope_theta, n_spans, d_spans, max_span_len, src, dst, stream);
+}
+
+kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_layers,
+                                              int32_t n_kv_heads, int32_t head_dim,
+                                              double rope_theta, int32_t n_spans,
+                                              const kvlink_span* d_spans, int32_t max_span_len,
+                                              kvlink_kv_view src, kvlink_kv_view dst,
+                                              void* stream) {
+    return rotate_keys("kvlink_encode_keys_at_positions", true, dtype, n_layers, n_kv_heads,
+                       head_dim, rope_theta, n_spans, d_spans, max_span_len, src, dst, stream);
 }
 
 kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,

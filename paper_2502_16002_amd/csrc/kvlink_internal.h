@@ -195,9 +195,11 @@ __device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, const RopeFreqs
 
 // ---------------------------------------------------------------- launchers
 
+// per_token: row t of a span is rotated by R(delta + t) (keys stored without
+// rotation), else every row by R(delta).
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
-                           int max_span_len, const View& src, const View& dst,
+                           int max_span_len, const View& src, const View& dst, bool per_token,
                            hipStream_t stream);
 
 // Sizes of one attention call, from the arguments and the schedule.

@@ -6,6 +6,11 @@
 // R(delta_i) with delta_i = g_i - (its stored start position); rotations
 // compose, R(delta) R(t) = R(delta + t).  Values are not touched.
 //
+// The paper's literal storage form keeps keys without any rotation and
+// applies the global rotation at inference: key t of document i is rotated
+// by R(delta_i + t) (delta_i = g_i for keys stored from position 0).  The same
+// kernel does this with a per-row cos/sin table (kPerToken).
+//
 // The pass is bound by HBM bandwidth (about 1.5 flop per byte moved):
 //   * one launch covers every layer and KV head, since delta does not depend
 //     on them;
@@ -43,7 +48,9 @@ __device__ __forceinline__ void store_stream(const uint4& v, void* p) {
     __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
 }
 
-template <typename T, int D>
+// kPerToken: row t of a span is rotated by R(delta + t) (keys stored without
+// rotation), else every row by R(delta).
+template <typename T, int D, bool kPerToken>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                                                             const kvlink_span* __restrict__ spans,
                                                             int n_lh, int n_kv_heads,
@@ -52,7 +59,8 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte access
     constexpr int TPV = H / E;               // threads per vector
     constexpr int VPP = kThreads / TPV;      // vectors per pass of the workgroup
-    __shared__ float s_cos[H], s_sin[H];
+    constexpr int TR = kPerToken ? kRows : 1;   // rows of the cos/sin table
+    __shared__ float s_cos[TR][H], s_sin[TR][H];
 
     const kvlink_span sp = spans[blockIdx.y];
     const int r0 = blockIdx.x * kRows;
@@ -61,16 +69,19 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     const int lh0 = blockIdx.z * kLH;
     const int nlh = min(kLH, n_lh - lh0);
 
-    for (int j = threadIdx.x; j < H; j += kThreads)
-        rope_cos_sin(sp.delta, j, freqs, &s_cos[j], &s_sin[j]);
+    for (int i = threadIdx.x; i < TR * H; i += kThreads) {
+        const int tr = i / H, j = i % H;
+        rope_cos_sin((int64_t)sp.delta + (kPerToken ? r0 + tr : 0), j, freqs, &s_cos[tr][j],
+                     &s_sin[tr][j]);
+    }
     __syncthreads();
 
     const int sub = threadIdx.x % TPV;
     float c[E], s[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        c[e] = s_cos[sub * E + e];
-        s[e] = s_sin[sub * E + e];
+        c[e] = s_cos[0][sub * E + e];
+        s[e] = s_sin[0][sub * E + e];
     }
 
     const int n_vec = rows * nlh;
@@ -99,6 +110,14 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                 float a[E], b[E], x[E], y[E];
                 unpack16<T>(lo[u], a);
                 unpack16<T>(hi[u], b);
+                if constexpr (kPerToken) {
+                    const int row = v % rows;
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        c[e] = s_cos[row][sub * E + e];
+                        s[e] = s_sin[row][sub * E + e];
+                    }
+                }
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
                     x[e] = a[e] * c[e] - b[e] * s[e];
@@ -115,11 +134,15 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 template <typename T, int D>
 hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_spans,
                   const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
-                  hipStream_t stream) {
+                  bool per_token, hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
     dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
-    hipLaunchKernelGGL((reencode_kernel<T, D>), grid, dim3(kThreads), 0, stream, src, dst, spans,
-                       n_lh, n_kv_heads, freqs);
+    if (per_token)
+        hipLaunchKernelGGL((reencode_kernel<T, D, true>), grid, dim3(kThreads), 0, stream, src,
+                           dst, spans, n_lh, n_kv_heads, freqs);
+    else
+        hipLaunchKernelGGL((reencode_kernel<T, D, false>), grid, dim3(kThreads), 0, stream, src,
+                           dst, spans, n_lh, n_kv_heads, freqs);
     return hipGetLastError();
 }
 
@@ -127,20 +150,20 @@ hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_sp
 
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
-                           int max_span_len, const View& src, const View& dst,
+                           int max_span_len, const View& src, const View& dst, bool per_token,
                            hipStream_t stream) {
     if (dt == KVLINK_BF16) {
         if (head_dim == 128)
             return launch<bf16_t, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len,
-                                       src, dst, stream);
+                                       src, dst, per_token, stream);
         return launch<bf16_t, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, stream);
+                                  dst, per_token, stream);
     }
     if (head_dim == 128)
         return launch<float, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, stream);
+                                  dst, per_token, stream);
     return launch<float, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src, dst,
-                             stream);
+                             per_token, stream);
 }
 
 }  // namespace kvlink

@@ -22,7 +22,8 @@ import torch
 
 from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_stages,
-               kvlink_attend_workspace_bytes, kvlink_build_layout, kvlink_reencode_keys)
+               kvlink_attend_workspace_bytes, kvlink_build_layout,
+               kvlink_encode_keys_at_positions, kvlink_reencode_keys)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
@@ -92,6 +93,13 @@ class Batch:
         kvlink_reencode_keys(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
                              self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
                              src_view, dst_view, stream)
+
+    def encode_at_positions(self, src_view, dst_view, stream=None):
+        """Rotate keys stored without RoPE to their global positions, all
+        layers (one launch)."""
+        kvlink_encode_keys_at_positions(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                                        self.rope_theta, self.n_docs, self.d_spans,
+                                        self.max_doc_len, src_view, dst_view, stream)
 
     def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None,
                stages=KVLINK_STAGE_ALL, workspace=None):

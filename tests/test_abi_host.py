@@ -154,22 +154,22 @@ def _view(kv, base=4096, **kw):
     (dict(rs=65), 1),                      # stride not a multiple of 16 bytes
     (dict(spans=None), 1),
 ])
-def test_reencode_validation(kv, change, status):
+@pytest.mark.parametrize("fn", ["kvlink_reencode_keys", "kvlink_encode_keys_at_positions"])
+def test_reencode_validation(kv, change, status, fn):
     a = dict(dtype=kv.KVLINK_BF16, n_layers=2, n_kv_heads=2, head_dim=64, theta=1e4, n_spans=1,
              spans=8192, max_len=4, src_base=4096, rs=64)
     a.update(change)
     src = _view(kv, a["src_base"], rs=a["rs"])
     dst = _view(kv, 8192)
     with pytest.raises(kv.KVLinkError) as e:
-        kv.kvlink_reencode_keys(a["dtype"], a["n_layers"], a["n_kv_heads"], a["head_dim"],
-                                a["theta"], a["n_spans"], a["spans"], a["max_len"], src, dst,
-                                stream=0)
+        getattr(kv, fn)(a["dtype"], a["n_layers"], a["n_kv_heads"], a["head_dim"], a["theta"],
+                        a["n_spans"], a["spans"], a["max_len"], src, dst, stream=0)
     assert e.value.status == status
 
 
-def test_reencode_empty_is_a_no_op(kv):
-    kv.kvlink_reencode_keys(kv.KVLINK_BF16, 1, 1, 64, 1e4, 0, None, 0, _view(kv), _view(kv),
-                            stream=0)
+@pytest.mark.parametrize("fn", ["kvlink_reencode_keys", "kvlink_encode_keys_at_positions"])
+def test_reencode_empty_is_a_no_op(kv, fn):
+    getattr(kv, fn)(kv.KVLINK_BF16, 1, 1, 64, 1e4, 0, None, 0, _view(kv), _view(kv), stream=0)
 
 
 def _plan(kv, dtype=None, hq=8, hkv=2, d=128, snp=(0, 10), vis=(100,) * 10, n_wg=0):

@@ -99,6 +99,79 @@ def test_reencode_first_document_is_bitwise_copy_and_in_place_matches():
     assert torch.equal(inplace.view(torch.int16), run.k_dst.view(torch.int16))
 
 
+# ------------------------------------------- keys stored without rotation
+
+
+def _check_encode_at_positions(run, layers, rows_sample=None):
+    """Keys of the stored caches taken as un-rotated (the paper's literal
+    storage form): key t of document i must come out as R(g_i + t) k."""
+    w = run.w
+    spans = run.batch.layout["spans"]
+    worst = 0.0
+    for l in layers:
+        kc, _ = workloads.request_cache(w, run.lds[l], 0)
+        kc = workloads.as_f64(w, kc)                              # [H][T_c][d]
+        got = to_f64(run.k_dst[l, :, 0, :kc.shape[1]])
+        for i, sp in enumerate(spans):
+            r0, n, delta = int(sp[3]), int(sp[4]), int(sp[5])
+            ts = np.arange(n) if rows_sample is None else np.unique(rows_sample % n)
+            ref = np.stack([oracle.reencode(kc[:, r0 + t], delta + int(t), w.rope_theta)
+                            for t in ts], axis=1)                 # [H][len(ts)][d]
+            worst = max(worst, check_close(w, got[:, r0 + ts], ref, f"literal layer {l} doc {i}"))
+            if w.dtype == "bf16":
+                check_bf16_rounding(got[:, r0 + ts], ref, f"literal layer {l} doc {i}")
+    return worst
+
+
+def test_encode_at_positions_tiny_f32():
+    w = workloads.tiny_f32()
+    run = ContiguousRun(w, layers=[])
+    run.batch.encode_at_positions(run.src_view, run.k_view)
+    _print("tiny literal worst", _check_encode_at_positions(run, [0]))
+
+
+def test_encode_at_positions_llama8b_all_layers():
+    w = workloads.llama8b_10doc()
+    run = ContiguousRun(w, layers=[])
+    run.batch.encode_at_positions(run.src_view, run.k_view)
+    worst = _check_encode_at_positions(run, [0, 31])
+    rng = np.random.default_rng(6)
+    worst = max(worst, _check_encode_at_positions(run, [4, 17], rows_sample=rng.integers(0, 300, 24)))
+    _print("8b literal worst", worst)
+
+
+def test_encode_at_positions_equals_reencode_of_locally_rotated_keys():
+    """R(g + t) k = R(g) R(t) k: the literal form of raw keys equals the
+    delta form of the same keys rotated at local positions 0.. (the local
+    rotation done by the oracle and rounded to the workload dtype)."""
+    import torch
+    from harness import to_torch
+    w = workloads.llama1b_layer()
+    run = ContiguousRun(w, layers=[])
+    run.batch.encode_at_positions(run.src_view, run.k_view)
+    literal = to_f64(run.k_dst[0, :, 0, :run.R])
+    # the stored keys rotated at their local positions, as a cache would hold them
+    ks = workloads.as_f64(w, run.lds[0].k_store)                 # [H][R][d]
+    row0 = workloads.doc_row0(w)
+    local = np.empty_like(ks)
+    for j, n in enumerate(w.doc_table_len):
+        for t in range(n):
+            local[:, row0[j] + t] = oracle.reencode(ks[:, row0[j] + t], t, w.rope_theta)
+    bits = workloads.f32_to_bf16_bits(local.astype(np.float32))
+    run.k_src[0] = to_torch(w, bits)
+    run.k_dst.zero_()
+    run.batch.reencode(run.src_view, run.k_view)
+    torch.cuda.synchronize()
+    delta_form = to_f64(run.k_dst[0, :, 0, :run.R])
+    # the delta path rounds the locally rotated keys to bf16 before the
+    # second rotation, which spreads that rounding over each rotation pair:
+    # the two results agree within a bf16 ulp of the pair's norm
+    h = literal.shape[-1] // 2
+    pair = np.sqrt(literal[..., :h] ** 2 + literal[..., h:] ** 2)
+    pair = np.concatenate([pair, pair], axis=-1)
+    assert np.all(np.abs(literal - delta_form) <= 2.0 ** -7 * pair + 1e-6)
+
+
 # ------------------------------------------------------------------ attention
 
 
