@@ -250,6 +250,63 @@ class PagedSetup(Setup):
         self.lse = b.new_lse()
 
 
+def host_load(st, iters=3):
+    """The stored caches in pinned host memory, loaded to the device with the
+    keys re-encoded (the first steps of the time-to-first-token path): the
+    plain copies alone, the kernels reading host memory directly, and the
+    staged copies with re-encodes on two streams or on one.  Milliseconds per
+    load of all layers."""
+    import torch
+    b, w = st.batch, st.w
+    h_k = st.k_src[0].cpu().pin_memory()
+    h_v = st.k_src[1].cpu().pin_memory()       # any stored-shape data serves as values
+    R = h_k.shape[2]
+    stage = torch.empty(b.load_stage_bytes(R), dtype=torch.uint8, device="cuda")
+    k_dst = torch.empty_like(st.k_dst[0])
+    v_dst = torch.empty_like(st.v_dst)
+    from paper_2502_16002_amd.runtime import contiguous_view
+    H, d = w.n_kv_heads, w.head_dim
+    kv_k = contiguous_view(k_dst, H, 1, st.cap, d)
+    kv_v = contiguous_view(v_dst, H, 1, st.cap, d)
+    dev_k = torch.empty_like(st.k_src[0])
+    dev_v = torch.empty_like(st.k_src[0])
+    copy = torch.cuda.Stream()
+    cur = torch.cuda.current_stream()
+
+    def timed(fn):
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        copy.wait_stream(cur)
+        for _ in range(iters):
+            fn()
+        cur.wait_stream(copy)
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / iters
+
+    def copies():
+        with torch.cuda.stream(copy):
+            dev_k.copy_(h_k, non_blocking=True)
+            dev_v.copy_(h_v, non_blocking=True)
+    direct = lambda: b.load_and_reencode(h_k, h_v, R, None, kv_k, kv_v, compute_stream=cur)
+    overlap = lambda: b.load_and_reencode(h_k, h_v, R, stage, kv_k, kv_v, copy_stream=copy,
+                                          compute_stream=cur)
+    serial = lambda: b.load_and_reencode(h_k, h_v, R, stage, kv_k, kv_v, copy_stream=cur,
+                                         compute_stream=cur)
+    direct()
+    overlap()
+    copy_ms, dir_ms = timed(copies), timed(direct)
+    over_ms, ser_ms = timed(overlap), timed(serial)
+    nbytes = 2 * h_k.numel() * h_k.element_size()
+    return {"bytes": nbytes, "copy_only_ms": round(copy_ms, 3),
+            "copy_gbps": round(nbytes / (copy_ms * 1e-3) / 1e9, 1),
+            "load_reencode_direct_ms": round(dir_ms, 3),
+            "direct_gbps": round(nbytes / (dir_ms * 1e-3) / 1e9, 1),
+            "load_reencode_staged_two_streams_ms": round(over_ms, 3),
+            "load_reencode_staged_one_stream_ms": round(ser_ms, 3)}
+
+
 def algorithmic(w, batch):
     """Bytes and flops the method itself moves (per the closed forms)."""
     es = 2 if w.dtype == "bf16" else 4
@@ -459,6 +516,8 @@ def main():
         "us_per_layer_eager_launch": round(ms_step_eager * 1000.0 / L, 3),
         "us_per_layer_graph_launch": round(ms_step_graph * 1000.0 / L, 3),
     }
+    if not w.pool and not w.decode:
+        res["host_load"] = host_load(st)
     if not args.no_cpu_baseline and w.n_seqs == 1:
         res["cpu_baseline"] = cpu_baseline(w, alg)
     print(json.dumps(res), flush=True)

@@ -13,6 +13,9 @@
  *   kvlink_encode_keys_at_positions
  *                             K' = R(g_i + t) K for keys cached without
  *                             rotation (the paper's literal form, GPU)
+ *   kvlink_load_and_reencode  the same, from caches held in host memory, the
+ *                             copy of each layer overlapping the re-encode of
+ *                             the one before (GPU copy and compute streams)
  *   kvlink_attend_make_plan   balanced split-K schedule of a batch (host)
  *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
  *                             append of their keys/values to the cache and
@@ -201,6 +204,59 @@ kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_laye
                                               const kvlink_span* d_spans, int32_t max_span_len,
                                               kvlink_kv_view src, kvlink_kv_view dst,
                                               void* stream);
+
+/*
+ * Bytes of the device staging area kvlink_load_and_reencode needs: two slots
+ * of one layer's stored keys and values (4 * n_kv_heads * stored_rows *
+ * head_dim elements).  Returns 0 for invalid sizes.
+ */
+size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t head_dim,
+                               int32_t stored_rows);
+
+/*
+ * kvlink_load_and_reencode — the first steps of the time-to-first-token path
+ * (Sec. 3.3 times it from caches held in CPU memory): the stored document
+ * caches of a batch are loaded from host memory, their keys re-encoded
+ * (Sec. 2.2, as kvlink_reencode_keys, or kvlink_encode_keys_at_positions
+ * with literal = 1) into k_dst and their values gathered into v_dst, both
+ * through the spans.  Two ways:
+ *   d_stage == NULL (direct): the kernels read the pinned host arrays over
+ *     the bus through their device mapping: one re-encode launch and one
+ *     value-gather launch for all layers on compute_stream (copy_stream is
+ *     not used).  The arrays must be pinned and mapped for the device
+ *     (hipHostMalloc with default flags); otherwise KVLINK_ERR_INVALID_ARG
+ *     and nothing is launched.
+ *   d_stage != NULL (staged): per layer l, copy_stream copies K_l and V_l to
+ *     staging slot l % 2 (once the re-encode of layer l - 2 has released
+ *     it) and compute_stream re-encodes from the slot; events order the two
+ *     streams.
+ * The call enqueues the work and returns.
+ *
+ *   h_k, h_v      host arrays [n_layers][n_kv_heads][stored_rows][head_dim],
+ *                 16-byte aligned, the stored caches of the batch's documents
+ *                 (span i's rows from src_row_i; src_seq is not used); they
+ *                 must stay valid until compute_stream has finished
+ *   d_stage, stage_bytes  NULL, or a device staging area of at least
+ *                 kvlink_load_stage_bytes(...) bytes, 256-byte aligned
+ *   k_dst, v_dst  destination views (K and V rows of every span land at
+ *                 dst_row_i.. of sequence dst_seq_i, layer l)
+ *   literal       0: keys cached rotated at local positions (R(delta_i));
+ *                 1: cached without rotation (R(delta_i + t))
+ *   copy_stream, compute_stream  hipStream_t as void* (the same stream
+ *                 serialises the copies and the re-encodes)
+ *
+ * Errors: those of kvlink_reencode_keys, and KVLINK_ERR_INVALID_ARG (null or
+ * misaligned host arrays, unmapped host memory on the direct way,
+ * stored_rows < 1, literal not 0 or 1), KVLINK_ERR_WORKSPACE (staging area
+ * misaligned or too small).
+ */
+kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
+                                       int32_t head_dim, double rope_theta, int32_t n_spans,
+                                       const kvlink_span* d_spans, int32_t max_span_len,
+                                       const void* h_k, const void* h_v, int32_t stored_rows,
+                                       void* d_stage, size_t stage_bytes, kvlink_kv_view k_dst,
+                                       kvlink_kv_view v_dst, int32_t literal, void* copy_stream,
+                                       void* compute_stream);
 
 /*
  * Schedule of the split-K attention of a request batch (host-built once per

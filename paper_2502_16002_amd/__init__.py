@@ -73,6 +73,12 @@ def _load():
     lib.kvlink_reencode_keys.restype = ctypes.c_int
     lib.kvlink_encode_keys_at_positions.argtypes = lib.kvlink_reencode_keys.argtypes
     lib.kvlink_encode_keys_at_positions.restype = ctypes.c_int
+    lib.kvlink_load_stage_bytes.argtypes = [ctypes.c_int, i32, i32, i32]
+    lib.kvlink_load_stage_bytes.restype = sz
+    lib.kvlink_load_and_reencode.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32, vp, vp,
+                                             i32, vp, sz, kvlink_kv_view, kvlink_kv_view, i32, vp,
+                                             vp]
+    lib.kvlink_load_and_reencode.restype = ctypes.c_int
     lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, i32,
                                             i32, vp, i64, ctypes.POINTER(kvlink_attend_plan)]
     lib.kvlink_attend_make_plan.restype = ctypes.c_int
@@ -191,6 +197,22 @@ def kvlink_encode_keys_at_positions(dtype, n_layers, n_kv_heads, head_dim, rope_
                                                 int(head_dim), float(rope_theta), int(n_spans),
                                                 _ptr(d_spans), int(max_span_len), src, dst,
                                                 _stream(stream)))
+
+
+def kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows):
+    return int(_lib.kvlink_load_stage_bytes(int(dtype), int(n_kv_heads), int(head_dim),
+                                            int(stored_rows)))
+
+
+def kvlink_load_and_reencode(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_spans, d_spans,
+                             max_span_len, h_k, h_v, stored_rows, d_stage, stage_bytes, k_dst,
+                             v_dst, literal=0, copy_stream=None, compute_stream=None):
+    _check(_lib.kvlink_load_and_reencode(int(dtype), int(n_layers), int(n_kv_heads),
+                                         int(head_dim), float(rope_theta), int(n_spans),
+                                         _ptr(d_spans), int(max_span_len), _ptr(h_k), _ptr(h_v),
+                                         int(stored_rows), _ptr(d_stage), int(stage_bytes),
+                                         k_dst, v_dst, int(literal), _stream(copy_stream),
+                                         _stream(compute_stream)))
 
 
 def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, seq_cached,

@@ -216,7 +216,9 @@ kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, 
         hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads,
                                                kvlink::make_rope_freqs(rope_theta, head_dim),
                                                n_spans, d_spans, max_span_len, to_view(src),
-                                               to_view(dst), per_token,
+                                               to_view(dst),
+                                               per_token ? kvlink::kReencodePerToken
+                                                         : kvlink::kReencodeDelta,
                                                reinterpret_cast<hipStream_t>(stream));
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "%s launch: %s", name, hipGetErrorString(e));
         return ok();
@@ -242,6 +244,159 @@ kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_laye
                                               void* stream) {
     return rotate_keys("kvlink_encode_keys_at_positions", true, dtype, n_layers, n_kv_heads,
                        head_dim, rope_theta, n_spans, d_spans, max_span_len, src, dst, stream);
+}
+
+size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t head_dim,
+                               int32_t stored_rows) {
+    if (!dtype_ok(dtype) || n_kv_heads < 1 || head_dim < 1 || stored_rows < 1) return 0;
+    return (size_t)4 * n_kv_heads * stored_rows * head_dim * elem_size(dtype);
+}
+
+kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
+                                       int32_t head_dim, double rope_theta, int32_t n_spans,
+                                       const kvlink_span* d_spans, int32_t max_span_len,
+                                       const void* h_k, const void* h_v, int32_t stored_rows,
+                                       void* d_stage, size_t stage_bytes, kvlink_kv_view k_dst,
+                                       kvlink_kv_view v_dst, int32_t literal, void* copy_stream,
+                                       void* compute_stream) {
+    try {
+        if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (n_layers < 1 || n_kv_heads < 1 || stored_rows < 1)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_layers, n_kv_heads and stored_rows must be >= 1");
+        if (n_spans < 0 || max_span_len < 0)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_spans and max_span_len must be >= 0");
+        if (n_spans > 65535) return fail(KVLINK_ERR_UNSUPPORTED, "more than 65535 spans");
+        if (n_kv_heads > 8 * 65535) return fail(KVLINK_ERR_UNSUPPORTED, "too many heads");
+        if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+            return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+        if (literal != 0 && literal != 1) return fail(KVLINK_ERR_INVALID_ARG, "literal must be 0 or 1");
+        if (!h_k || !h_v) return fail(KVLINK_ERR_INVALID_ARG, "h_k or h_v is NULL");
+        if (n_spans > 0 && max_span_len > 0 && !d_spans)
+            return fail(KVLINK_ERR_INVALID_ARG, "d_spans is NULL");
+        const size_t need = kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows);
+        if (d_stage && reinterpret_cast<uintptr_t>(d_stage) % 256)
+            return fail(KVLINK_ERR_WORKSPACE, "d_stage is not 256-byte aligned");
+        if (d_stage && stage_bytes < need)
+            return fail(KVLINK_ERR_WORKSPACE, "d_stage has %zu bytes, needs %zu", stage_bytes, need);
+        kvlink_status st = check_view(k_dst, dtype, "k_dst");
+        if (st != KVLINK_OK) return st;
+        if ((st = check_view(v_dst, dtype, "v_dst")) != KVLINK_OK) return st;
+        if (reinterpret_cast<uintptr_t>(h_k) % 16 || reinterpret_cast<uintptr_t>(h_v) % 16)
+            return fail(KVLINK_ERR_INVALID_ARG, "h_k or h_v is not 16-byte aligned");
+
+        const size_t es = elem_size(dtype);
+        const size_t layer_bytes = (size_t)n_kv_heads * stored_rows * head_dim * es;
+        hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
+        hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+        const kvlink::RopeFreqs freqs = kvlink::make_rope_freqs(rope_theta, head_dim);
+        const bool work = n_spans > 0 && max_span_len > 0;
+        const int rot = literal ? kvlink::kReencodePerToken : kvlink::kReencodeDelta;
+        // the stored caches as a view: [layer][n_kv_heads][stored_rows][head_dim]
+        auto stored_view = [&](const void* base, int64_t layer_stride) {
+            kvlink::View v;
+            v.base = reinterpret_cast<char*>(const_cast<void*>(base));
+            v.layer_stride = layer_stride;
+            v.head_stride = (int64_t)stored_rows * head_dim;
+            v.row_stride = head_dim;
+            v.seq_stride = 0;
+            v.page_stride = 0;
+            v.block_table = nullptr;
+            v.page_size = 1;
+            v.max_pages = 0;
+            return v;
+        };
+
+        if (!d_stage) {
+            // Direct: the kernels read the pinned host arrays over the bus
+            // (their device mapping), all layers in one re-encode launch and
+            // one value-gather launch on compute_stream.  Memory that is not
+            // mapped for the device is refused before any launch.
+            void* dk = nullptr;
+            void* dv = nullptr;
+            if (hipHostGetDevicePointer(&dk, const_cast<void*>(h_k), 0) != hipSuccess || !dk ||
+                hipHostGetDevicePointer(&dv, const_cast<void*>(h_v), 0) != hipSuccess || !dv) {
+                (void)hipGetLastError();
+                return fail(KVLINK_ERR_INVALID_ARG,
+                            "h_k or h_v is not pinned host memory mapped for the device "
+                            "(allocate it with hipHostMalloc) and no staging area was given");
+            }
+            if (!work) return ok();
+            const int64_t ls = (int64_t)n_kv_heads * stored_rows * head_dim;
+            hipError_t e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads, freqs,
+                                                   n_spans, d_spans, max_span_len,
+                                                   stored_view(dk, ls), to_view(k_dst), rot, ks);
+            if (e == hipSuccess)
+                e = kvlink::launch_reencode(dtype, head_dim, n_layers, n_kv_heads, freqs, n_spans,
+                                            d_spans, max_span_len, stored_view(dv, ls),
+                                            to_view(v_dst), kvlink::kReencodeCopy, ks);
+            if (e != hipSuccess)
+                return fail(KVLINK_ERR_HIP, "kvlink_load_and_reencode: %s", hipGetErrorString(e));
+            return ok();
+        }
+
+        // one stored layer in a staging slot: [n_kv_heads][stored_rows][head_dim]
+        auto slot_view = [&](char* base) {
+            kvlink::View v;
+            v.base = base;
+            v.layer_stride = 0;
+            v.head_stride = (int64_t)stored_rows * head_dim;
+            v.row_stride = head_dim;
+            v.seq_stride = 0;
+            v.page_stride = 0;
+            v.block_table = nullptr;
+            v.page_size = 1;
+            v.max_pages = 0;
+            return v;
+        };
+        auto layer_of = [&](const kvlink_kv_view& v, int l) {
+            kvlink::View d = to_view(v);
+            d.base += (int64_t)l * v.layer_stride * (int64_t)es;
+            return d;
+        };
+        hipEvent_t loaded[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
+        hipError_t e = hipSuccess;
+        for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+            e = hipEventCreateWithFlags(&loaded[i], hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&freed[i], hipEventDisableTiming);
+        }
+        for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+            const int slot = l & 1;
+            char* k_slot = reinterpret_cast<char*>(d_stage) + (size_t)slot * 2 * layer_bytes;
+            char* v_slot = k_slot + layer_bytes;
+            // the copy into a slot waits until the layer that used it two
+            // layers ago has been re-encoded
+            if (l >= 2) e = hipStreamWaitEvent(cs, freed[slot], 0);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(k_slot, reinterpret_cast<const char*>(h_k) + l * layer_bytes,
+                                   layer_bytes, hipMemcpyHostToDevice, cs);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(v_slot, reinterpret_cast<const char*>(h_v) + l * layer_bytes,
+                                   layer_bytes, hipMemcpyHostToDevice, cs);
+            if (e == hipSuccess) e = hipEventRecord(loaded[slot], cs);
+            if (e == hipSuccess) e = hipStreamWaitEvent(ks, loaded[slot], 0);
+            if (e == hipSuccess && work)
+                e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
+                                            d_spans, max_span_len, slot_view(k_slot),
+                                            layer_of(k_dst, l), rot, ks);
+            if (e == hipSuccess && work)
+                e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
+                                            d_spans, max_span_len, slot_view(v_slot),
+                                            layer_of(v_dst, l), kvlink::kReencodeCopy, ks);
+            if (e == hipSuccess) e = hipEventRecord(freed[slot], ks);
+        }
+        // destroying a recorded event is deferred by the runtime until it completes
+        for (int i = 0; i < 2; ++i) {
+            if (loaded[i]) (void)hipEventDestroy(loaded[i]);
+            if (freed[i]) (void)hipEventDestroy(freed[i]);
+        }
+        if (e != hipSuccess)
+            return fail(KVLINK_ERR_HIP, "kvlink_load_and_reencode: %s", hipGetErrorString(e));
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_load_and_reencode");
+    }
 }
 
 kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,

@@ -195,11 +195,13 @@ __device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, const RopeFreqs
 
 // ---------------------------------------------------------------- launchers
 
-// per_token: row t of a span is rotated by R(delta + t) (keys stored without
-// rotation), else every row by R(delta).
+// mode: kReencodeDelta rotates every row of a span by R(delta);
+// kReencodePerToken rotates row t by R(delta + t) (keys stored without
+// rotation); kReencodeCopy moves the rows unchanged (values).
+enum { kReencodeDelta = 0, kReencodePerToken = 1, kReencodeCopy = 2 };
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
-                           int max_span_len, const View& src, const View& dst, bool per_token,
+                           int max_span_len, const View& src, const View& dst, int mode,
                            hipStream_t stream);
 
 // Sizes of one attention call, from the arguments and the schedule.

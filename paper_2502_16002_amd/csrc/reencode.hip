@@ -48,9 +48,12 @@ __device__ __forceinline__ void store_stream(const uint4& v, void* p) {
     __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
 }
 
-// kPerToken: row t of a span is rotated by R(delta + t) (keys stored without
-// rotation), else every row by R(delta).
-template <typename T, int D, bool kPerToken>
+// Modes: kDelta rotates every row of a span by R(delta); kPerToken rotates
+// row t by R(delta + t) (keys stored without rotation); kCopy moves the rows
+// unchanged (values gathered through the same spans).
+enum { kDelta = 0, kPerToken = 1, kCopy = 2 };
+
+template <typename T, int D, int kMode>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                                                             const kvlink_span* __restrict__ spans,
                                                             int n_lh, int n_kv_heads,
@@ -59,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte access
     constexpr int TPV = H / E;               // threads per vector
     constexpr int VPP = kThreads / TPV;      // vectors per pass of the workgroup
-    constexpr int TR = kPerToken ? kRows : 1;   // rows of the cos/sin table
+    constexpr int TR = kMode == kPerToken ? kRows : 1;   // rows of the cos/sin table
     __shared__ float s_cos[TR][H], s_sin[TR][H];
 
     const kvlink_span sp = spans[blockIdx.y];
@@ -69,19 +72,21 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     const int lh0 = blockIdx.z * kLH;
     const int nlh = min(kLH, n_lh - lh0);
 
-    for (int i = threadIdx.x; i < TR * H; i += kThreads) {
-        const int tr = i / H, j = i % H;
-        rope_cos_sin((int64_t)sp.delta + (kPerToken ? r0 + tr : 0), j, freqs, &s_cos[tr][j],
-                     &s_sin[tr][j]);
+    if constexpr (kMode != kCopy) {
+        for (int i = threadIdx.x; i < TR * H; i += kThreads) {
+            const int tr = i / H, j = i % H;
+            rope_cos_sin((int64_t)sp.delta + (kMode == kPerToken ? r0 + tr : 0), j, freqs,
+                         &s_cos[tr][j], &s_sin[tr][j]);
+        }
+        __syncthreads();
     }
-    __syncthreads();
 
     const int sub = threadIdx.x % TPV;
     float c[E], s[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        c[e] = s_cos[0][sub * E + e];
-        s[e] = s_sin[0][sub * E + e];
+        c[e] = kMode == kCopy ? 1.f : s_cos[0][sub * E + e];
+        s[e] = kMode == kCopy ? 0.f : s_sin[0][sub * E + e];
     }
 
     const int n_vec = rows * nlh;
@@ -107,10 +112,16 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
         for (int u = 0; u < kUnroll; ++u) {
             const int v = v0 + u * VPP;
             if (v < n_vec) {
+                T* q = reinterpret_cast<T*>(dst.base) + doff[u];
+                if constexpr (kMode == kCopy) {
+                    store_stream(lo[u], q);
+                    store_stream(hi[u], q + H);
+                    continue;
+                }
                 float a[E], b[E], x[E], y[E];
                 unpack16<T>(lo[u], a);
                 unpack16<T>(hi[u], b);
-                if constexpr (kPerToken) {
+                if constexpr (kMode == kPerToken) {
                     const int row = v % rows;
 #pragma unroll
                     for (int e = 0; e < E; ++e) {
@@ -123,7 +134,6 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                     x[e] = a[e] * c[e] - b[e] * s[e];
                     y[e] = a[e] * s[e] + b[e] * c[e];
                 }
-                T* q = reinterpret_cast<T*>(dst.base) + doff[u];
                 store_stream(pack16<T>(x), q);
                 store_stream(pack16<T>(y), q + H);
             }
@@ -134,14 +144,17 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 template <typename T, int D>
 hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_spans,
                   const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
-                  bool per_token, hipStream_t stream) {
+                  int mode, hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
     dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
-    if (per_token)
-        hipLaunchKernelGGL((reencode_kernel<T, D, true>), grid, dim3(kThreads), 0, stream, src,
+    if (mode == kPerToken)
+        hipLaunchKernelGGL((reencode_kernel<T, D, kPerToken>), grid, dim3(kThreads), 0, stream,
+                           src, dst, spans, n_lh, n_kv_heads, freqs);
+    else if (mode == kCopy)
+        hipLaunchKernelGGL((reencode_kernel<T, D, kCopy>), grid, dim3(kThreads), 0, stream, src,
                            dst, spans, n_lh, n_kv_heads, freqs);
     else
-        hipLaunchKernelGGL((reencode_kernel<T, D, false>), grid, dim3(kThreads), 0, stream, src,
+        hipLaunchKernelGGL((reencode_kernel<T, D, kDelta>), grid, dim3(kThreads), 0, stream, src,
                            dst, spans, n_lh, n_kv_heads, freqs);
     return hipGetLastError();
 }
@@ -150,20 +163,20 @@ hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_sp
 
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
-                           int max_span_len, const View& src, const View& dst, bool per_token,
+                           int max_span_len, const View& src, const View& dst, int mode,
                            hipStream_t stream) {
     if (dt == KVLINK_BF16) {
         if (head_dim == 128)
             return launch<bf16_t, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len,
-                                       src, dst, per_token, stream);
+                                       src, dst, mode, stream);
         return launch<bf16_t, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, per_token, stream);
+                                  dst, mode, stream);
     }
     if (head_dim == 128)
         return launch<float, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, per_token, stream);
+                                  dst, mode, stream);
     return launch<float, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src, dst,
-                             per_token, stream);
+                             mode, stream);
 }
 
 }  // namespace kvlink

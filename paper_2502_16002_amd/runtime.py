@@ -23,7 +23,8 @@ import torch
 from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_stages,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
-               kvlink_encode_keys_at_positions, kvlink_reencode_keys)
+               kvlink_encode_keys_at_positions, kvlink_load_and_reencode,
+               kvlink_load_stage_bytes, kvlink_reencode_keys)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
@@ -100,6 +101,22 @@ class Batch:
         kvlink_encode_keys_at_positions(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
                                         self.rope_theta, self.n_docs, self.d_spans,
                                         self.max_doc_len, src_view, dst_view, stream)
+
+    def load_stage_bytes(self, stored_rows):
+        return kvlink_load_stage_bytes(self.dtype, self.n_kv_heads, self.head_dim, stored_rows)
+
+    def load_and_reencode(self, h_k, h_v, stored_rows, stage, k_view, v_view, literal=False,
+                          copy_stream=None, compute_stream=None):
+        """Stored caches in pinned host memory, [n_layers][H_kv][stored_rows][d]:
+        with stage None the kernels read them directly (one re-encode and one
+        value-gather launch for all layers); with a staging tensor they are
+        copied layer by layer on copy_stream while compute_stream (torch's
+        current stream when None) re-encodes the layer before."""
+        kvlink_load_and_reencode(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                                 self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
+                                 h_k, h_v, stored_rows, stage,
+                                 0 if stage is None else stage.numel() * stage.element_size(),
+                                 k_view, v_view, int(bool(literal)), copy_stream, compute_stream)
 
     def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None,
                stages=KVLINK_STAGE_ALL, workspace=None):

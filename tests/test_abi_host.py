@@ -172,6 +172,34 @@ def test_reencode_empty_is_a_no_op(kv, fn):
     getattr(kv, fn)(kv.KVLINK_BF16, 1, 1, 64, 1e4, 0, None, 0, _view(kv), _view(kv), stream=0)
 
 
+def test_load_stage_bytes(kv):
+    assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000) == 4 * 8 * 1000 * 128 * 2
+    assert kv.kvlink_load_stage_bytes(kv.KVLINK_F32, 2, 64, 10) == 4 * 2 * 10 * 64 * 4
+    assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 0) == 0
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(h_k=None), 1),
+    (dict(stored_rows=0), 1),
+    (dict(literal=2), 1),
+    (dict(head_dim=96), 2),
+    (dict(h_k=4096 + 8), 1),                # not 16-byte aligned
+    (dict(stage=4096 + 16), 4),             # not 256-byte aligned
+    (dict(stage_bytes=1024), 4),
+    (dict(spans=None), 1),
+])
+def test_load_and_reencode_validation(kv, change, status):
+    a = dict(dtype=kv.KVLINK_BF16, head_dim=64, h_k=4096, h_v=4096, stored_rows=8, literal=0,
+             stage=8192, stage_bytes=1 << 20, spans=8192)
+    a.update(change)
+    with pytest.raises(kv.KVLinkError) as e:
+        kv.kvlink_load_and_reencode(a["dtype"], 2, 2, a["head_dim"], 1e4, 1, a["spans"], 4,
+                                    a["h_k"], a["h_v"], a["stored_rows"], a["stage"],
+                                    a["stage_bytes"], _view(kv), _view(kv), a["literal"],
+                                    copy_stream=0, compute_stream=0)
+    assert e.value.status == status
+
+
 def _plan(kv, dtype=None, hq=8, hkv=2, d=128, snp=(0, 10), vis=(100,) * 10, n_wg=0):
     dtype = kv.KVLINK_BF16 if dtype is None else dtype
     tc = [max(vis)] * (len(snp) - 1)

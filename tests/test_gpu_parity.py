@@ -172,6 +172,61 @@ def test_encode_at_positions_equals_reencode_of_locally_rotated_keys():
     assert np.all(np.abs(literal - delta_form) <= 2.0 ** -7 * pair + 1e-6)
 
 
+# ------------------------------------------- caches loaded from host memory
+
+
+@pytest.mark.parametrize("literal,way", [(0, "direct"), (1, "direct"), (0, "staged"),
+                                         (1, "staged"), (0, "staged_one_stream")])
+def test_load_and_reencode_from_host_matches_device_path(literal, way):
+    """All 32 layers of the 10-document workload loaded from pinned host
+    memory, read directly by the kernels or copied through a staging area
+    (copies on one stream, re-encodes on another, or both on one): the keys
+    equal the device-resident entry point's bit for bit, the values equal
+    the stored ones."""
+    import torch
+    from harness import to_torch
+    w = workloads.llama8b_10doc()
+    run = ContiguousRun(w, layers=[])
+    b = run.batch
+    if literal:
+        b.encode_at_positions(run.src_view, run.k_view)
+    else:
+        b.reencode(run.src_view, run.k_view)
+    torch.cuda.synchronize()
+    h_k = run.k_src.cpu().pin_memory()                         # [L][H][R][d]
+    h_v = to_torch(w, np.stack([ld.v_store for ld in run.lds]), "cpu").pin_memory()
+    stage = None if way == "direct" else \
+        torch.empty(b.load_stage_bytes(run.R), dtype=torch.uint8, device="cuda")
+    k2 = torch.zeros_like(run.k_dst)
+    v2 = torch.zeros_like(run.v_dst)
+    from paper_2502_16002_amd.runtime import contiguous_view
+    H, d = w.n_kv_heads, w.head_dim
+    copy = torch.cuda.Stream() if way == "staged" else torch.cuda.current_stream()
+    b.load_and_reencode(h_k, h_v, run.R, stage, contiguous_view(k2, H, 1, run.cap, d),
+                        contiguous_view(v2, H, 1, run.cap, d), literal=literal,
+                        copy_stream=copy, compute_stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert torch.equal(k2.view(torch.int16), run.k_dst.view(torch.int16))
+    assert torch.equal(v2[:, :, 0, :run.R].view(torch.int16),
+                       run.v_dst[:, :, 0, :run.R].view(torch.int16))
+
+
+def test_load_and_reencode_direct_refuses_unpinned_host_memory():
+    """Reading host memory directly needs it pinned and mapped; a pageable
+    array is refused before any launch."""
+    import paper_2502_16002_amd as kv
+    from paper_2502_16002_amd.runtime import contiguous_view
+    import torch
+    w = workloads.tiny_f32()
+    run = ContiguousRun(w, layers=[])
+    h = np.zeros(run.k_src.numel() + 64, np.float32)
+    h = h[(-h.ctypes.data % 16) // 4:][:run.k_src.numel()]       # 16-byte aligned, pageable
+    with pytest.raises(kv.KVLinkError) as e:
+        run.batch.load_and_reencode(h, h, run.R, None, run.k_view, run.v_view)
+    assert e.value.status == 1
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------------ attention
 
 
