@@ -13,6 +13,9 @@
  *   kvlink_encode_keys_at_positions
  *                             K' = R(g_i + t) K for keys cached without
  *                             rotation (the paper's literal form, GPU)
+ *   kvlink_reencode_keys_mapped
+ *                             K' = R(g_i + t - p_t) K for compressed caches
+ *                             (kept tokens at original positions p_t, GPU)
  *   kvlink_load_and_reencode  the same, from caches held in host memory, the
  *                             copy of each layer overlapping the re-encode of
  *                             the one before (GPU copy and compute streams)
@@ -204,6 +207,31 @@ kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_laye
                                               const kvlink_span* d_spans, int32_t max_span_len,
                                               kvlink_kv_view src, kvlink_kv_view dst,
                                               void* stream);
+
+/*
+ * kvlink_reencode_keys_mapped — re-encoding of compressed caches (Sec. 2.4:
+ * only some tokens of a document are kept, e.g. its anchor tokens or the
+ * tokens a compressor keeps, each cached with RoPE at its original position
+ * p).  The kept keys take contiguous global positions after concatenation,
+ * so the rotation differs per key:
+ *     dst(l, h, dst_seq_i, dst_row_i + t) = R(delta_i + t - p) src(l, h, src_seq_i, src_row_i + t),
+ *     p = d_stored_pos[src_seq_i * stored_pos_stride + src_row_i + t]
+ * (p = t gives kvlink_reencode_keys, p = 0 kvlink_encode_keys_at_positions).
+ * The layout comes from kvlink_build_layout with the kept-token counts as
+ * document lengths; attention over the result needs nothing else.
+ *
+ *   d_stored_pos        device int32 array: the stored position of every
+ *                       source row, indexed by (src_seq, row)
+ *   stored_pos_stride   entries per source sequence in d_stored_pos
+ * Other arguments, layouts and errors as kvlink_reencode_keys; also
+ * KVLINK_ERR_INVALID_ARG for a NULL d_stored_pos or a negative stride.
+ */
+kvlink_status kvlink_reencode_keys_mapped(kvlink_dtype dtype, int32_t n_layers,
+                                          int32_t n_kv_heads, int32_t head_dim, double rope_theta,
+                                          int32_t n_spans, const kvlink_span* d_spans,
+                                          int32_t max_span_len, const int32_t* d_stored_pos,
+                                          int64_t stored_pos_stride, kvlink_kv_view src,
+                                          kvlink_kv_view dst, void* stream);
 
 /*
  * Bytes of the device staging area kvlink_load_and_reencode needs: two slots

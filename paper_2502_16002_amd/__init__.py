@@ -73,6 +73,10 @@ def _load():
     lib.kvlink_reencode_keys.restype = ctypes.c_int
     lib.kvlink_encode_keys_at_positions.argtypes = lib.kvlink_reencode_keys.argtypes
     lib.kvlink_encode_keys_at_positions.restype = ctypes.c_int
+    lib.kvlink_reencode_keys_mapped.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32,
+                                                vp, ctypes.c_int64, kvlink_kv_view,
+                                                kvlink_kv_view, vp]
+    lib.kvlink_reencode_keys_mapped.restype = ctypes.c_int
     lib.kvlink_load_stage_bytes.argtypes = [ctypes.c_int, i32, i32, i32]
     lib.kvlink_load_stage_bytes.restype = sz
     lib.kvlink_load_and_reencode.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32, vp, vp,
@@ -197,6 +201,15 @@ def kvlink_encode_keys_at_positions(dtype, n_layers, n_kv_heads, head_dim, rope_
                                                 int(head_dim), float(rope_theta), int(n_spans),
                                                 _ptr(d_spans), int(max_span_len), src, dst,
                                                 _stream(stream)))
+
+
+def kvlink_reencode_keys_mapped(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_spans,
+                                d_spans, max_span_len, d_stored_pos, stored_pos_stride, src, dst,
+                                stream=None):
+    _check(_lib.kvlink_reencode_keys_mapped(int(dtype), int(n_layers), int(n_kv_heads),
+                                            int(head_dim), float(rope_theta), int(n_spans),
+                                            _ptr(d_spans), int(max_span_len), _ptr(d_stored_pos),
+                                            int(stored_pos_stride), src, dst, _stream(stream)))
 
 
 def kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows):

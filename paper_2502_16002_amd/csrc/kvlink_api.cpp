@@ -194,7 +194,8 @@ namespace {
 kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, int32_t n_layers,
                           int32_t n_kv_heads, int32_t head_dim, double rope_theta, int32_t n_spans,
                           const kvlink_span* d_spans, int32_t max_span_len, kvlink_kv_view src,
-                          kvlink_kv_view dst, void* stream) {
+                          kvlink_kv_view dst, void* stream, const int32_t* pos_map = nullptr,
+                          int64_t pos_stride = 0) {
     try {
         if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
         if (head_dim != 64 && head_dim != 128)
@@ -219,7 +220,8 @@ kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, 
                                                to_view(dst),
                                                per_token ? kvlink::kReencodePerToken
                                                          : kvlink::kReencodeDelta,
-                                               reinterpret_cast<hipStream_t>(stream));
+                                               reinterpret_cast<hipStream_t>(stream), pos_map,
+                                               pos_stride);
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "%s launch: %s", name, hipGetErrorString(e));
         return ok();
     } catch (...) {
@@ -234,6 +236,21 @@ kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t
                                    kvlink_kv_view src, kvlink_kv_view dst, void* stream) {
     return rotate_keys("kvlink_reencode_keys", false, dtype, n_layers, n_kv_heads, head_dim,
                        rope_theta, n_spans, d_spans, max_span_len, src, dst, stream);
+}
+
+kvlink_status kvlink_reencode_keys_mapped(kvlink_dtype dtype, int32_t n_layers,
+                                          int32_t n_kv_heads, int32_t head_dim, double rope_theta,
+                                          int32_t n_spans, const kvlink_span* d_spans,
+                                          int32_t max_span_len, const int32_t* d_stored_pos,
+                                          int64_t stored_pos_stride, kvlink_kv_view src,
+                                          kvlink_kv_view dst, void* stream) {
+    if (n_spans > 0 && max_span_len > 0 && !d_stored_pos)
+        return fail(KVLINK_ERR_INVALID_ARG, "d_stored_pos is NULL");
+    if (stored_pos_stride < 0)
+        return fail(KVLINK_ERR_INVALID_ARG, "stored_pos_stride must be >= 0");
+    return rotate_keys("kvlink_reencode_keys_mapped", true, dtype, n_layers, n_kv_heads, head_dim,
+                       rope_theta, n_spans, d_spans, max_span_len, src, dst, stream, d_stored_pos,
+                       stored_pos_stride);
 }
 
 kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_layers,

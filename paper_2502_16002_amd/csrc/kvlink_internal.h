@@ -196,13 +196,16 @@ __device__ __forceinline__ void rope_cos_sin(int64_t pos, int j, const RopeFreqs
 // ---------------------------------------------------------------- launchers
 
 // mode: kReencodeDelta rotates every row of a span by R(delta);
-// kReencodePerToken rotates row t by R(delta + t) (keys stored without
-// rotation); kReencodeCopy moves the rows unchanged (values).
+// kReencodePerToken rotates row t by R(delta + t - p), p = 0 or, with
+// pos_map, the row's stored position pos_map[src_seq * pos_stride + row]
+// (keys stored without rotation, or a compressed cache); kReencodeCopy
+// moves the rows unchanged (values).
 enum { kReencodeDelta = 0, kReencodePerToken = 1, kReencodeCopy = 2 };
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
                            int max_span_len, const View& src, const View& dst, int mode,
-                           hipStream_t stream);
+                           hipStream_t stream, const int32_t* pos_map = nullptr,
+                           int64_t pos_stride = 0);
 
 // Sizes of one attention call, from the arguments and the schedule.
 struct AttendPlan {

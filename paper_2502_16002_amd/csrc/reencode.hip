@@ -9,7 +9,10 @@
 // The paper's literal storage form keeps keys without any rotation and
 // applies the global rotation at inference: key t of document i is rotated
 // by R(delta_i + t) (delta_i = g_i for keys stored from position 0).  The same
-// kernel does this with a per-row cos/sin table (kPerToken).
+// kernel does this with a per-row cos/sin table (kPerToken).  A compressed
+// cache (Sec. 2.4: only some tokens' keys kept, at their original positions
+// p_t) is re-encoded to contiguous global positions with R(delta_i + t - p_t),
+// p_t read from a per-row map of stored positions.
 //
 // The pass is bound by HBM bandwidth (about 1.5 flop per byte moved):
 //   * one launch covers every layer and KV head, since delta does not depend
@@ -53,11 +56,15 @@ __device__ __forceinline__ void store_stream(const uint4& v, void* p) {
 // unchanged (values gathered through the same spans).
 enum { kDelta = 0, kPerToken = 1, kCopy = 2 };
 
+// pos_map (kPerToken only, may be NULL): stored position of every source row,
+// entry src_seq * pos_stride + row; the angle of row t is delta + t - pos.
 template <typename T, int D, int kMode>
 __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                                                             const kvlink_span* __restrict__ spans,
                                                             int n_lh, int n_kv_heads,
-                                                            RopeFreqs freqs) {
+                                                            RopeFreqs freqs,
+                                                            const int32_t* __restrict__ pos_map,
+                                                            int64_t pos_stride) {
     constexpr int H = D / 2;                 // rotation pairs per vector
     constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte access
     constexpr int TPV = H / E;               // threads per vector
@@ -75,8 +82,13 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     if constexpr (kMode != kCopy) {
         for (int i = threadIdx.x; i < TR * H; i += kThreads) {
             const int tr = i / H, j = i % H;
-            rope_cos_sin((int64_t)sp.delta + (kMode == kPerToken ? r0 + tr : 0), j, freqs,
-                         &s_cos[tr][j], &s_sin[tr][j]);
+            int64_t pos = (int64_t)sp.delta;
+            if constexpr (kMode == kPerToken) {
+                pos += r0 + tr;
+                if (pos_map && r0 + tr < sp.len)
+                    pos -= pos_map[(int64_t)sp.src_seq * pos_stride + sp.src_row + r0 + tr];
+            }
+            rope_cos_sin(pos, j, freqs, &s_cos[tr][j], &s_sin[tr][j]);
         }
         __syncthreads();
     }
@@ -144,18 +156,18 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 template <typename T, int D>
 hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_spans,
                   const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
-                  int mode, hipStream_t stream) {
+                  int mode, const int32_t* pos_map, int64_t pos_stride, hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
     dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
     if (mode == kPerToken)
         hipLaunchKernelGGL((reencode_kernel<T, D, kPerToken>), grid, dim3(kThreads), 0, stream,
-                           src, dst, spans, n_lh, n_kv_heads, freqs);
+                           src, dst, spans, n_lh, n_kv_heads, freqs, pos_map, pos_stride);
     else if (mode == kCopy)
         hipLaunchKernelGGL((reencode_kernel<T, D, kCopy>), grid, dim3(kThreads), 0, stream, src,
-                           dst, spans, n_lh, n_kv_heads, freqs);
+                           dst, spans, n_lh, n_kv_heads, freqs, nullptr, (int64_t)0);
     else
         hipLaunchKernelGGL((reencode_kernel<T, D, kDelta>), grid, dim3(kThreads), 0, stream, src,
-                           dst, spans, n_lh, n_kv_heads, freqs);
+                           dst, spans, n_lh, n_kv_heads, freqs, nullptr, (int64_t)0);
     return hipGetLastError();
 }
 
@@ -164,19 +176,19 @@ hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_sp
 hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                            const RopeFreqs& freqs, int n_spans, const kvlink_span* spans,
                            int max_span_len, const View& src, const View& dst, int mode,
-                           hipStream_t stream) {
+                           hipStream_t stream, const int32_t* pos_map, int64_t pos_stride) {
     if (dt == KVLINK_BF16) {
         if (head_dim == 128)
             return launch<bf16_t, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len,
-                                       src, dst, mode, stream);
+                                       src, dst, mode, pos_map, pos_stride, stream);
         return launch<bf16_t, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, mode, stream);
+                                  dst, mode, pos_map, pos_stride, stream);
     }
     if (head_dim == 128)
         return launch<float, 128>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src,
-                                  dst, mode, stream);
+                                  dst, mode, pos_map, pos_stride, stream);
     return launch<float, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src, dst,
-                             mode, stream);
+                             mode, pos_map, pos_stride, stream);
 }
 
 }  // namespace kvlink

@@ -24,7 +24,7 @@ from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_stages,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
                kvlink_encode_keys_at_positions, kvlink_load_and_reencode,
-               kvlink_load_stage_bytes, kvlink_reencode_keys)
+               kvlink_load_stage_bytes, kvlink_reencode_keys, kvlink_reencode_keys_mapped)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
@@ -101,6 +101,13 @@ class Batch:
         kvlink_encode_keys_at_positions(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
                                         self.rope_theta, self.n_docs, self.d_spans,
                                         self.max_doc_len, src_view, dst_view, stream)
+
+    def reencode_mapped(self, src_view, dst_view, d_stored_pos, stored_pos_stride, stream=None):
+        """Re-encode a compressed cache: every stored row with its own stored
+        position (d_stored_pos, device int32, indexed (src_seq, row))."""
+        kvlink_reencode_keys_mapped(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                                    self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
+                                    d_stored_pos, stored_pos_stride, src_view, dst_view, stream)
 
     def load_stage_bytes(self, stored_rows):
         return kvlink_load_stage_bytes(self.dtype, self.n_kv_heads, self.head_dim, stored_rows)

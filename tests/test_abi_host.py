@@ -172,6 +172,14 @@ def test_reencode_empty_is_a_no_op(kv, fn):
     getattr(kv, fn)(kv.KVLINK_BF16, 1, 1, 64, 1e4, 0, None, 0, _view(kv), _view(kv), stream=0)
 
 
+@pytest.mark.parametrize("pos,stride", [(None, 0), (8192, -1)])
+def test_reencode_mapped_validation(kv, pos, stride):
+    with pytest.raises(kv.KVLinkError) as e:
+        kv.kvlink_reencode_keys_mapped(kv.KVLINK_BF16, 2, 2, 64, 1e4, 1, 8192, 4, pos, stride,
+                                       _view(kv), _view(kv, 8192), stream=0)
+    assert e.value.status == 1
+
+
 def test_load_stage_bytes(kv):
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000) == 4 * 8 * 1000 * 128 * 2
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_F32, 2, 64, 10) == 4 * 2 * 10 * 64 * 4

@@ -172,6 +172,50 @@ def test_encode_at_positions_equals_reencode_of_locally_rotated_keys():
     assert np.all(np.abs(literal - delta_form) <= 2.0 ** -7 * pair + 1e-6)
 
 
+# ------------------------------------------------------ compressed caches
+
+
+def test_compressed_cache_reencode_and_attention():
+    """A compressed cache (Sec. 2.4): each document keeps about a quarter of
+    its tokens, cached with RoPE at their original positions p_t; the kept
+    keys are re-encoded to contiguous global positions, R(g_i + t - p_t), and
+    the new tokens attend over them with the kept-token counts as document
+    lengths."""
+    import torch
+    rng = np.random.default_rng(29)
+    orig = rng.integers(300, 600, size=10, endpoint=True)
+    kept = [np.sort(rng.choice(n, size=n // 4, replace=False)) for n in orig]
+    w = workloads.custom([len(k) for k in kept], 5, 64, n_q_heads=32, n_kv_heads=8,
+                         head_dim=128, dtype="bf16", rope_theta=5e5, seed=31, n_layers=2)
+    run = ContiguousRun(w, layers=[0, 1])
+    b = run.batch
+    stored_pos = np.concatenate(kept).astype(np.int32)            # by stored row
+    d_pos = torch.from_numpy(stored_pos).cuda()
+    b.reencode_mapped(run.src_view, run.k_view, d_pos, 0)
+    for l in [0, 1]:
+        b.attend(l, run.q[l], run.kn[l], run.vn[l], run.k_view, run.v_view, run.out[l],
+                 run.lse[l])
+    torch.cuda.synchronize()
+    g = b.layout["doc_pos0"]
+    row0 = workloads.doc_row0(w)
+    for l in [0, 1]:
+        kc, vc, q, kn, vn = run.oracle_inputs(l)                  # stored keys as cached
+        enc = np.empty_like(kc)
+        for i, p in enumerate(kept):
+            for t, pt in enumerate(p):
+                r = int(row0[i]) + t
+                enc[:, r] = oracle.reencode(kc[:, r], int(g[i]) + t - int(pt), w.rope_theta)
+        got = to_f64(run.k_dst[l, :, 0, :kc.shape[1]])
+        check_close(w, got, enc, f"compressed re-encode layer {l}")
+        check_bf16_rounding(got, enc, f"compressed re-encode layer {l}")
+        # attention over the re-encoded keys: the oracle takes them as cached
+        # at their global positions (no further rotation)
+        ref, ref_lse = oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, enc,
+                                     vc, w.rope_theta, w.scale, src_pos0=[int(x) for x in g])
+        check_close(w, to_f64(run.out[l]), ref, f"compressed attention layer {l}")
+        assert float(np.max(np.abs(to_f64(run.lse[l]) - ref_lse))) <= 2e-2
+
+
 # ------------------------------------------- caches loaded from host memory
 
 
