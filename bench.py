@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--kernel-iters", type=int, default=20)
     ap.add_argument("--eager", action="store_true",
                     help="time steps launched from Python instead of a captured HIP graph")
+    ap.add_argument("--separate-rope", action="store_true",
+                    help="run the new tokens' RoPE as its own launch instead of inside the "
+                         "split attention (bf16)")
     return ap.parse_args()
 
 
@@ -73,7 +76,7 @@ class Setup:
     """Device buffers of a single-request workload (documents stored back to
     back, concatenated cache with room for the new tokens)."""
 
-    def __init__(self, w, n_workgroups, device="cuda"):
+    def __init__(self, w, n_workgroups, device="cuda", fused_rope=True):
         import torch
         import workloads
         from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
@@ -84,7 +87,7 @@ class Setup:
         self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                                [0, len(docs)], w.doc_len(0), w.link_count[0], w.n_query,
                                doc_src_row=[int(row0[j]) for j in docs], n_workgroups=n_workgroups,
-                               device=device)
+                               device=device, fused_rope=fused_rope)
         R = int(sum(w.doc_table_len))
         self.cap = cap = b.max_total
         self.k_src, self.k_dst = [], []
@@ -121,6 +124,8 @@ class Setup:
                           self.out, self.lse, stages=stages, workspace=workspace)
 
     def step(self):
+        # the batch's RoPE table (one launch; a no-op with the separate RoPE)
+        self.batch.build_rope_table()
         # a decoding step attends over a cache re-encoded at prefill
         if not self.w.decode:
             self.reencode(0)
@@ -149,8 +154,12 @@ class Setup:
         # every layer's partials and outputs exist before the stages run apart
         for l in range(L):
             self.attend(l, workspace=self.ws_layers[l])
-        out = {}
-        for name, stage in [("rope", 1), ("split", 2), ("combine", 4)]:
+        out = {"rope": None}
+        # with the fused RoPE the RoPE stage launches nothing
+        names = [("split", 2), ("combine", 4)]
+        if self.batch.rope_table is None:
+            names.insert(0, ("rope", 1))
+        for name, stage in names:
             g = capture(group(stage))
             g.replay()
             torch.cuda.synchronize()
@@ -187,7 +196,7 @@ class PagedSetup(Setup):
     through its V block table, with fresh pages after them for its new
     tokens."""
 
-    def __init__(self, w, n_workgroups, device="cuda", seed=11):
+    def __init__(self, w, n_workgroups, device="cuda", seed=11, fused_rope=True):
         import torch
         import workloads
         from paper_2502_16002_amd.runtime import Batch, dtype_code, paged_view
@@ -207,7 +216,7 @@ class PagedSetup(Setup):
         self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                                sdp, dl, lc, w.n_query, doc_src_seq=src_seq,
                                doc_src_row=[0] * len(dl), n_workgroups=n_workgroups,
-                               device=device)
+                               device=device, fused_rope=fused_rope)
         td = b.torch_dtype
         max_new_pages = (b.max_new + P - 1) // P
         n_fresh = w.n_seqs * max_new_pages
@@ -403,7 +412,7 @@ def main():
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workloads.get(args.workload)
-    st = (PagedSetup if w.pool else Setup)(w, args.workgroups)
+    st = (PagedSetup if w.pool else Setup)(w, args.workgroups, fused_rope=not args.separate_rope)
     alg = algorithmic(w, st.batch)
     print(f"# setup done: {w.name} cached={alg['cached_tokens']} new={alg['new_tokens']} "
           f"workgroups={st.batch.n_workgroups} segments={st.batch.plan.n_segments}", file=sys.stderr, flush=True)
@@ -476,7 +485,9 @@ def main():
     split_kernel = SPLIT_KERNEL[(w.dtype, st.batch.plan.row_block)]   # the library's own choice
     at_roof = attn_roof(split_kernel, stage_ms["split"])
     at_roof["traffic"] = traffic(split_kernel) if split_kernel in KERNEL_SOURCES else None
-    stages = {"rope_new_us": round(stage_ms["rope"] * 1000, 2),
+    fused = st.batch.rope_table is not None
+    stages = {"rope": "inside the split attention" if fused else "own launch",
+              "rope_new_us": None if fused else round(stage_ms["rope"] * 1000, 2),
               "split_attention_us": round(stage_ms["split"] * 1000, 2),
               "combine_us": round(stage_ms["combine"] * 1000, 2),
               "all_stages_one_call_us": round(at_ms * 1000, 2),

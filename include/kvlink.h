@@ -328,7 +328,31 @@ typedef struct {
     int32_t row_block;    /* rows per unit: 256, or 16 (at most 16 rows per KV head; fp32) */
     int32_t n_seqs;
     int32_t n_split_units; /* units with more than one segment */
+    /* device table of kvlink_attend_rope_table for the same batch, or NULL
+     * (then the RoPE stage runs as its own launch) */
+    const float* rope_table;
 } kvlink_attend_plan;
+
+/*
+ * kvlink_attend_rope_table — the cos/sin values of every new token's
+ * rotation (Sec. 2.2: the new tokens sit at their global positions), once per
+ * batch: table[n][j] = (cos(pos_n w_j), sin(pos_n w_j)), w_j =
+ * rope_theta^(-2j/head_dim), j < head_dim/2, angles in double precision
+ * rounded to float (as the RoPE stage computes them).  With plan.rope_table
+ * set to this table, kvlink_attend_new_tokens for bf16 batches rotates the
+ * new tokens inside the split-attention launch: the RoPE stage launches
+ * nothing, and the split stage rotates the queries it loads and appends the
+ * rotated keys and the values to the cache rows T_c + r itself (every
+ * workgroup whose keys include new rows writes the ones it reads; all write
+ * identical bytes).  fp32 batches always use the separate RoPE launch.
+ *
+ *   d_new_pos   device int32 [n_new_total] (the layout's new_pos)
+ *   d_table     device float [n_new_total][head_dim / 2][2]
+ * Errors: KVLINK_ERR_INVALID_ARG (null pointers, rope_theta <= 0,
+ * n_new_total < 0), KVLINK_ERR_UNSUPPORTED (head_dim), KVLINK_ERR_HIP.
+ */
+kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int32_t n_new_total,
+                                       const int32_t* d_new_pos, float* d_table, void* stream);
 
 /*
  * kvlink_attend_make_plan — build the schedule (pure host computation).
@@ -338,14 +362,19 @@ typedef struct {
  *   n_compute_units  compute units of the device (sizes the schedule)
  *   n_workgroups     0: chosen by a cost model (a segment costs a set-up,
  *                    a tile its K/V stream plus the products of the steps
- *                    its wavefronts do not skip, the launch is as long as
- *                    its longest workgroup, and split partials add a
- *                    combine launch and their traffic); > 0: that many
- *                    workgroups (capped at the tile count)
+ *                    its wavefronts do not skip and, for new rows among
+ *                    its keys, their RoPE and append as the fused form
+ *                    does them; the launch is as long as its longest
+ *                    workgroup, and split partials add a combine launch
+ *                    and their traffic); > 0: that many workgroups (capped
+ *                    at the tile count)
  *   table, table_capacity  host array for the table; with table == NULL
  *                    only *plan is filled (to size the array)
- *   plan             out: counts and row_block; plan->table is set to NULL
- *                    (the caller stores the device copy's address there)
+ *   plan             out: counts and row_block; plan->table and
+ *                    plan->rope_table are set to NULL (the caller stores
+ *                    the table's device copy in table and, for the fused
+ *                    RoPE, the batch's kvlink_attend_rope_table result in
+ *                    rope_table)
  *
  * The result of the attention does not depend on the schedule beyond float
  * rounding order.  Errors: KVLINK_ERR_INVALID_ARG (null required pointer,
@@ -395,6 +424,7 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *   d_new_visible[n_new_total] device copies of kvlink_build_layout outputs
  *   q_new  [n_new_total][n_q_heads][head_dim]   device, dtype, pre-RoPE
  *   k_new, v_new [n_new_total][n_kv_heads][head_dim]  device, dtype
+ *                              (q_new, k_new, v_new 16-byte aligned)
  *   k_cache, v_cache           views (see kvlink_kv_view) whose rows
  *                              0..T_c-1 of request s hold its re-encoded keys
  *                              and its values, with room for the new rows
@@ -404,7 +434,11 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *                              same batch, with plan.table pointing at the
  *                              device copy of its table (16-byte aligned).
  *                              Its row_block must match this call's path
- *                              (KVLINK_ERR_INVALID_ARG otherwise).
+ *                              (KVLINK_ERR_INVALID_ARG otherwise).  With
+ *                              plan.rope_table set (16-byte aligned, the
+ *                              batch's kvlink_attend_rope_table), a bf16
+ *                              call does steps 1 and 2 inside the split
+ *                              launch (same bytes as the separate launch)
  *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
  *                              device bytes, 256-byte aligned
  *
@@ -429,7 +463,9 @@ kvlink_status kvlink_attend_new_tokens(
  * kvlink_attend_stages — kvlink_attend_new_tokens run stage by stage, with
  * identical arguments plus a bit mask of the stages to launch:
  *   KVLINK_STAGE_ROPE     steps 1 and 2 (RoPE of the new tokens, append of
- *                         their keys and values, rotated q to the workspace)
+ *                         their keys and values, rotated q to the workspace);
+ *                         launches nothing when plan.rope_table is set for
+ *                         a bf16 call, whose SPLIT stage then does both
  *   KVLINK_STAGE_SPLIT    step 3 over every segment of the plan (a unit
  *                         with one segment writes out and lse directly, the
  *                         others write split partials to the workspace)

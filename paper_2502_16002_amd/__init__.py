@@ -56,7 +56,8 @@ class kvlink_attend_plan(ctypes.Structure):
                 ("n_segments", ctypes.c_int32),
                 ("row_block", ctypes.c_int32),
                 ("n_seqs", ctypes.c_int32),
-                ("n_split_units", ctypes.c_int32)]
+                ("n_split_units", ctypes.c_int32),
+                ("rope_table", ctypes.c_void_p)]
 
 
 def _load():
@@ -96,6 +97,8 @@ def _load():
     lib.kvlink_attend_new_tokens.restype = ctypes.c_int
     lib.kvlink_attend_stages.argtypes = lib.kvlink_attend_new_tokens.argtypes + [ctypes.c_uint32]
     lib.kvlink_attend_stages.restype = ctypes.c_int
+    lib.kvlink_attend_rope_table.argtypes = [i32, f64, i32, vp, vp, vp]
+    lib.kvlink_attend_rope_table.restype = ctypes.c_int
     lib.kvlink_last_error.restype = ctypes.c_char_p
     lib.kvlink_version.restype = ctypes.c_char_p
     return lib
@@ -245,6 +248,11 @@ def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr,
     table = np.zeros(max(plan.table_len, 1), np.int32)
     _check(_lib.kvlink_attend_make_plan(*args, _ptr(table), len(table), ctypes.byref(plan)))
     return plan, table[:plan.table_len]
+
+
+def kvlink_attend_rope_table(head_dim, rope_theta, n_new_total, d_new_pos, d_table, stream=None):
+    _check(_lib.kvlink_attend_rope_table(int(head_dim), float(rope_theta), int(n_new_total),
+                                         _ptr(d_new_pos), _ptr(d_table), _stream(stream)))
 
 
 def kvlink_attend_workspace_bytes(dtype, n_q_heads, n_kv_heads, head_dim, n_new_total, plan):

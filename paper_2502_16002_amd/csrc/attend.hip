@@ -90,16 +90,10 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
     auto rotate_store = [&](int hv, const uint4& l4, const uint4& h4) {
         T* dst = hv < n_q_heads ? q_rot + ((int64_t)n * n_q_heads + hv) * D
                                 : kb + view_offset(k, layer, hv - n_q_heads, s, row);
-        float a[E], b[E], x[E], y[E];
-        unpack16<T>(l4, a);
-        unpack16<T>(h4, b);
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            x[e] = a[e] * c[e] - b[e] * sn[e];
-            y[e] = a[e] * sn[e] + b[e] * c[e];
-        }
-        *reinterpret_cast<uint4*>(dst + sub * E) = pack16<T>(x);
-        *reinterpret_cast<uint4*>(dst + H + sub * E) = pack16<T>(y);
+        uint4 x, y;
+        rope_rotate16<T>(l4, h4, c, sn, x, y);
+        *reinterpret_cast<uint4*>(dst + sub * E) = x;
+        *reinterpret_cast<uint4*>(dst + H + sub * E) = y;
     };
 #pragma unroll
     for (int u = 0; u < kPre; ++u) {
@@ -119,6 +113,20 @@ __global__ __launch_bounds__(256) void rope_new_kernel(
         const int hk = i / VPH, cch = i % VPH;
         *reinterpret_cast<uint4*>(vb + view_offset(v, layer, hk, s, row) + cch * E) =
             *reinterpret_cast<const uint4*>(v_new + ((int64_t)n * n_kv_heads + hk) * D + cch * E);
+    }
+}
+
+// The batch's RoPE table: entry (n, j) = (cos, sin) of new token n's angle
+// for pair j, by the same routine as the RoPE stage.
+__global__ __launch_bounds__(64) void rope_table_kernel(const int32_t* __restrict__ new_pos,
+                                                        int half, RopeFreqs freqs,
+                                                        float2* __restrict__ table) {
+    const int n = blockIdx.x;
+    const int pos = new_pos[n];
+    for (int j = threadIdx.x; j < half; j += 64) {
+        float c, s;
+        rope_cos_sin(pos, j, freqs, &c, &s);
+        table[(int64_t)n * half + j] = make_float2(c, s);
     }
 }
 
@@ -431,9 +439,15 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
     p.out = a.out;
     p.lse = a.lse;
+    // the matrix-core kernels take the RoPE over when the batch's table is given
+    const bool fused = a.rope_table && pl.path != kPathValu;
+    p.rope = fused ? reinterpret_cast<const float2*>(a.rope_table) : nullptr;
+    p.q_new = a.q_new;
+    p.k_new = a.k_new;
+    p.v_new = a.v_new;
 
     hipError_t e = hipSuccess;
-    if (stages & KVLINK_STAGE_ROPE) {
+    if ((stages & KVLINK_STAGE_ROPE) && !fused) {
         hipLaunchKernelGGL((rope_new_kernel<T, D>), dim3(pl.n_new_total), dim3(256), 0, stream,
                            reinterpret_cast<const T*>(a.q_new), reinterpret_cast<const T*>(a.k_new),
                            reinterpret_cast<const T*>(a.v_new), q_rot, a.k, a.v, a.layer,
@@ -519,6 +533,14 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     }
     p->total_bytes = std::max<size_t>(256, p->q_rot_bytes + p->part_o_bytes + p->part_ml_bytes);
     return true;
+}
+
+hipError_t launch_rope_table(int head_dim, const RopeFreqs& freqs, int n_new_total,
+                             const int32_t* new_pos, float* table, hipStream_t stream) {
+    if (n_new_total == 0) return hipSuccess;
+    hipLaunchKernelGGL(rope_table_kernel, dim3(n_new_total), dim3(64), 0, stream, new_pos,
+                       head_dim / 2, freqs, reinterpret_cast<float2*>(table));
+    return hipGetLastError();
 }
 
 hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,

@@ -33,6 +33,40 @@ __device__ __forceinline__ int seq_of(const int32_t* seq_new_ptr, int n_seqs, in
     return lo;
 }
 
+// RoPE of 16 bytes of each half of a head vector (Sec. 2.2; dims j and
+// j + D/2 form a pair): lo holds dims j.., hi dims j + D/2.., c and s the
+// cos/sin of their angles.  Every kernel that rotates new tokens goes
+// through this one routine, so the fused and the separate RoPE produce the
+// same bytes.
+template <typename T>
+__device__ __forceinline__ void rope_rotate16(const uint4& lo, const uint4& hi, const float* c,
+                                              const float* s, uint4& x_out, uint4& y_out) {
+    constexpr int E = 16 / (int)sizeof(T);
+    float a[E], b[E], x[E], y[E];
+    unpack16<T>(lo, a);
+    unpack16<T>(hi, b);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        x[e] = __builtin_fmaf(a[e], c[e], -(b[e] * s[e]));
+        y[e] = __builtin_fmaf(a[e], s[e], b[e] * c[e]);
+    }
+    x_out = pack16<T>(x);
+    y_out = pack16<T>(y);
+}
+
+// Eight (cos, sin) pairs of a rope table row from entry j (64 bytes).
+__device__ __forceinline__ void rope_table8(const float2* row, int j, float* c, float* s) {
+    const float4* t = reinterpret_cast<const float4*>(row + j);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float4 v = t[i];
+        c[2 * i] = v.x;
+        s[2 * i] = v.y;
+        c[2 * i + 1] = v.z;
+        s[2 * i + 1] = v.w;
+    }
+}
+
 // Key range of a row block: cached rows seen by its last token (cmax) and
 // the virtual key count cmax + (last token + 1).
 struct BlockKeys {
@@ -70,6 +104,14 @@ struct KParams {
     float* part_ml;   // their (running max in log2 units, sum) pairs
     void* out;
     float* lse;
+    // With rope (the batch's cos/sin table, [n_new][D/2] (cos, sin)), the
+    // split kernels rotate the queries of q_new themselves and append the new
+    // tokens' rotated keys (k_new) and values (v_new) to the cache rows they
+    // read; q_rot is then unused.
+    const float2* rope;
+    const void* q_new;
+    const void* k_new;
+    const void* v_new;
 };
 
 static_assert(kSegRecord == 16, "segment records are read as four int4");
@@ -89,6 +131,72 @@ __device__ __forceinline__ bool record_ok(const KParams& p, const int4 (&rec)[4]
     return rec[0].x >= 0 && rec[0].x < p.n_seqs && rec[0].y >= 0 && rec[0].y < p.n_kv_heads &&
            rec[0].w >= 0 && rec[0].w <= p.row_block && nseg >= 1 && loc >= 0 && loc < nseg &&
            part >= 0 && part + nseg <= p.n_segments && (next < 0 || next > g);
+}
+
+// Wait until every memory access this wave issued has completed (stores
+// included), as a compiler barrier too, so no access moves across it.  With a
+// workgroup barrier after it, the stores are visible to the other waves.
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Fused RoPE: new rows [na, nb) of request token base n0 and KV head h are
+// written to the cache rows Tc + r of the views, keys rotated from k_new by
+// the table, values copied from v_new (bf16; a task is 16 bytes of each half
+// of one row, NT threads).  Workgroups whose key ranges overlap write the
+// same rows with the same bytes.  The caller makes the stores visible
+// (wait_vm_all, then a workgroup barrier) before loading those rows.
+template <int D, int NT>
+__device__ __forceinline__ void append_new_rows(const KParams& p, const RowPtr& kp,
+                                                const RowPtr& vp, int h, int n0, int Tc, int na,
+                                                int nb) {
+    constexpr int Hh = D / 2, TPR = Hh / 8;   // tasks per row
+    const bf16_t* kn = reinterpret_cast<const bf16_t*>(p.k_new);
+    const bf16_t* vn = reinterpret_cast<const bf16_t*>(p.v_new);
+    for (int i = threadIdx.x; i < (nb - na) * TPR; i += NT) {
+        const int r = na + i / TPR, c = 8 * (i % TPR);
+        const int64_t n = n0 + r;
+        const int64_t src = (n * p.n_kv_heads + h) * D + c;
+        const uint4 a = *reinterpret_cast<const uint4*>(kn + src);
+        const uint4 b = *reinterpret_cast<const uint4*>(kn + src + Hh);
+        const uint4 va = *reinterpret_cast<const uint4*>(vn + src);
+        const uint4 vb = *reinterpret_cast<const uint4*>(vn + src + Hh);
+        float cs[8], sn[8];
+        rope_table8(p.rope + n * Hh, c, cs, sn);
+        uint4 x, y;
+        rope_rotate16<bf16_t>(a, b, cs, sn, x, y);
+        char* kd = const_cast<char*>(kp.row(Tc + r)) + 2 * c;
+        char* vd = const_cast<char*>(vp.row(Tc + r)) + 2 * c;
+        *reinterpret_cast<uint4*>(kd) = x;
+        *reinterpret_cast<uint4*>(kd + 2 * Hh) = y;
+        *reinterpret_cast<uint4*>(vd) = va;
+        *reinterpret_cast<uint4*>(vd + 2 * Hh) = vb;
+    }
+}
+
+// Queries of one GQA row as the B operand pieces a lane holds (dims
+// 32ds + 8lg.. for each 32-dim step ds): loaded from the rotated-query
+// workspace, or, with the fused RoPE, from q_new and rotated here (the pairs
+// of a lane are steps ds and ds + D/64).
+template <int D>
+__device__ __forceinline__ void load_q_row(const KParams& p, int64_t n, int hq, int lg,
+                                           uint4 (&q)[D / 32]) {
+    constexpr int DS = D / 32;
+    const int64_t off = (n * p.n_q_heads + hq) * D + 8 * lg;
+    if (!p.rope) {
+        const bf16_t* src = reinterpret_cast<const bf16_t*>(p.q_rot) + off;
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) q[ds] = *reinterpret_cast<const uint4*>(src + 32 * ds);
+        return;
+    }
+    const bf16_t* src = reinterpret_cast<const bf16_t*>(p.q_new) + off;
+    uint4 raw[DS];
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) raw[ds] = *reinterpret_cast<const uint4*>(src + 32 * ds);
+#pragma unroll
+    for (int ds = 0; ds < DS / 2; ++ds) {
+        float cs[8], sn[8];
+        rope_table8(p.rope + n * (D / 2), 32 * ds + 8 * lg, cs, sn);
+        rope_rotate16<bf16_t>(raw[ds], raw[ds + DS / 2], cs, sn, q[ds], q[ds + DS / 2]);
+    }
 }
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);

@@ -192,6 +192,20 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
         return !cached_seen && !new_seen;
     };
 
+    // With the fused RoPE, the new rows among the segment's keys ([na, nb)
+    // of the request's new tokens) are appended to the cache, the stores
+    // waited for and the workgroup synchronised before any load that may
+    // read them: ahead of the prologue's loads when those reach the new rows,
+    // else right after them (the key loop has no barrier of its own).
+    const int na = max(kbeg, cmax) - cmax, nb = kend - cmax;
+    const bool has_new = p.rope != nullptr && nb > na;
+    const bool early_new = has_new && kbeg + 2 * kDW * kStep > cmax;
+    if (early_new) {
+        append_new_rows<D, 64 * kDW>(p, kp, vp, h, n0, Tc, na, nb);
+        wait_vm_all();
+        __syncthreads();
+    }
+
     StepRegs<D> R0, R1;
     int j = wave;
     if (j < n_steps) {
@@ -201,17 +215,19 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     // queries, B operand of S^T: row lr, dims 32ds + 8lg
     bf16x8 qB[DS];
     {
-        const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
-        const int64_t qrow = ((int64_t)(n0 + tok) * p.n_q_heads + h * G + rho % G) * D;
+        uint4 q[DS];
+        load_q_row<D>(p, n0 + tok, h * G + rho % G, lg, q);
 #pragma unroll
-        for (int ds = 0; ds < DS; ++ds) {
-            const uint4 q = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
-            qB[ds] = as_bf16x8(row_ok ? q : uint4{0u, 0u, 0u, 0u});
-        }
+        for (int ds = 0; ds < DS; ++ds) qB[ds] = as_bf16x8(row_ok ? q[ds] : uint4{0u, 0u, 0u, 0u});
     }
     if (j + kDW < n_steps) {
         issue_k(j + kDW, R1);
         issue_v(j + kDW, stage(1));
+    }
+    if (has_new && !early_new) {
+        append_new_rows<D, 64 * kDW>(p, kp, vp, h, n0, Tc, na, nb);
+        wait_vm_all();
+        __syncthreads();
     }
 
     const float c2 = p.scale_log2;

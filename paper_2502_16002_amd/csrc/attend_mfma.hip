@@ -175,6 +175,20 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         }
     };
 
+    // With the fused RoPE, the new rows among the segment's keys ([na, nb)
+    // of the request's new tokens) are appended to the cache before any tile
+    // holding them is loaded: ahead of tile 0 when it holds some, else while
+    // tile 0 is in flight (the prologue's full wait and barrier below then
+    // cover the stores before tiles 1.. go out).
+    const int na = max(kbeg, bk.cmax) - bk.cmax, nb = kend - bk.cmax;
+    const bool has_new = p.rope != nullptr && nb > na;
+    const bool tile0_new = has_new && kbeg + kTile > bk.cmax;
+    if (tile0_new) {
+        append_new_rows<D, 64 * kWaves>(p, kp, vp, h, n0, Tc, na, nb);
+        wait_vm_all();
+        __syncthreads();
+    }
+
     // Tile 0 goes out first, then the rows' data (visible prefixes, the Q
     // operand); tiles 1 and 2 follow once tile 0 has arrived and its first
     // products are issued, so that when every workgroup starts at once tile 0
@@ -195,16 +209,13 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     const int tok_max = (min(rho_w + kRT * 16, rho_end) - 1) / G;
     const int wave_vis_min = wave_active ? p.new_visible[n0 + tok_min] : 0;
     const int wave_vis_max = wave_active ? p.new_visible[n0 + tok_max] : 0;
-    const bf16_t* q_rot = reinterpret_cast<const bf16_t*>(p.q_rot);
     uint4 qraw[kRT][DS];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         const int rho = rho_w + 16 * rt + lr;
-        const int64_t qrow = ((int64_t)(n0 + max(tok[rt], 0)) * p.n_q_heads + h * G + rho % G) * D;
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
-            qraw[rt][ds] = *reinterpret_cast<const uint4*>(q_rot + qrow + 32 * ds + 8 * lg);
+        load_q_row<D>(p, n0 + max(tok[rt], 0), h * G + rho % G, lg, qraw[rt]);
     }
+    if (has_new && !tile0_new) append_new_rows<D, 64 * kWaves>(p, kp, vp, h, n0, Tc, na, nb);
 
     const float c2 = p.scale_log2;   // > 0
     // Row r may see virtual key v iff v < lo (cached rows up to its document,
@@ -472,7 +483,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
     constexpr std::integral_constant<int, 0> H0{};
     constexpr std::integral_constant<int, 1> H1{};
-    wait_vm<0>();
+    wait_vm_all();
     __syncthreads();
 
     // a step whose two sub-tiles are both dead for the wave is skipped; a

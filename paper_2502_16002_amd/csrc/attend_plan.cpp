@@ -23,11 +23,12 @@
 // The cheaper of the two, and the cheapest n, come from a cost model fitted
 // to MI355X timings of the Llama-8B-shaped workloads: a segment costs a
 // fixed set-up (its record, the first key tiles and queries, the partial
-// write), a tile costs a per-tile time, and a tile of a unit whose rows
-// fill at most half the wavefronts costs half (its other wavefronts sit
-// idle, and their SIMDs run one wavefront instead of two); the launch lasts
-// as long as its longest workgroup; split units add the combine launch and
-// the traffic of their partials.
+// write); a tile costs its K/V stream plus the products of the (wavefront,
+// step) pairs the kernel does not skip, more for steps that need the mask,
+// plus, for the new rows among its keys, their RoPE and append (which the
+// split launch does itself when the batch's RoPE table is given); the launch
+// lasts as long as its longest workgroup; split units add the combine launch
+// and the traffic of their partials.
 //
 // Segment records are numbered so that record w is workgroup w's first
 // segment; further segments of a workgroup follow the first n and are
@@ -66,6 +67,9 @@ struct CostModel {
     // fraction)
     double per_segment_us, first_us, tile_us, live_us, mask_us, combine_us, combine_bytes_per_us;
     int slots_per_cu;
+    // the RoPE and append of the new keys a segment reads (inside the split
+    // launch), per 64 new rows
+    double append_us;
 };
 
 // Wide-block kernel: fitted jointly to per-workgroup timelines of the 10-
@@ -77,7 +81,9 @@ struct CostModel {
 // tile.  A live step that some row of the wavefront sees only in part (it
 // runs the mask) costs about four times one seen whole.  A segment adds its
 // record and, for its first tile, the products that wait for the tile's
-// loads instead of overlapping them.  The combine costs about 6 us plus its partial
+// loads instead of overlapping them.  A segment whose keys include new rows
+// first rotates and appends them, one round of loads and stores per 64 rows
+// (about 0.9 us each).  The combine costs about 6 us plus its partial
 // traffic, written and read back at an effective ~6 TB/s.  Decode kernel: two
 // workgroups per compute unit sharing the unit's HBM stream, so a tile (64
 // keys of K and V) costs its bytes at an eighth of a compute unit's share of
@@ -87,9 +93,9 @@ CostModel cost_model(AttendPath path, int head_dim) {
     const bool d128 = head_dim == 128;
     const double f = d128 ? 1.0 : 0.63;   // head_dim 64: fewer bytes and products per key
     if (path == kPathWide)
-        return {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 6.0, 6.0e6, 1};
-    if (path == kPathDecode) return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 6.0, 6.0e6, 2};
-    return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 4.0, 6.0e6, d128 ? 2 : 4};
+        return {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 6.0, 6.0e6, 1, 0.9 * f};
+    if (path == kPathDecode) return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 6.0, 6.0e6, 2, 0.0};
+    return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 4.0, 6.0e6, d128 ? 2 : 4, 0.0};
 }
 
 // Live (wavefront, 32-key step) pairs of tile t of a wide-kernel unit, by the
@@ -330,8 +336,11 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             int masked = 0;
             const int live = path == kPathWide ? live_pairs(x, t, group, new_visible, &masked) : 16;
             x.live[t] = (float)(live / 16.0);
+            const int64_t new_rows =
+                std::max<int64_t>(0, std::min<int64_t>(x.nvirt, (int64_t)kTileKeys * (t + 1)) -
+                                         std::max<int64_t>(x.cmax, (int64_t)kTileKeys * t));
             x.prefix[t + 1] = x.prefix[t] + cm.tile_us + cm.live_us * live / 16.0 +
-                              cm.mask_us * masked / 16.0;
+                              cm.mask_us * masked / 16.0 + cm.append_us * new_rows / kTileKeys;
         }
     }
 

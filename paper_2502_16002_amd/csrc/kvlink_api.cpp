@@ -461,6 +461,7 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
         plan->row_block = c.row_block;
         plan->n_seqs = n_seqs;
         plan->n_split_units = c.n_split;
+        plan->rope_table = nullptr;
         return ok();
     } catch (...) {
         return fail(KVLINK_ERR_INVALID_ARG, "unexpected exception in kvlink_attend_make_plan");
@@ -522,6 +523,11 @@ kvlink_status kvlink_attend_stages(
             return fail(KVLINK_ERR_INVALID_ARG, "a layout descriptor pointer is NULL");
         if (!q_new || !k_new || !v_new || !out)
             return fail(KVLINK_ERR_INVALID_ARG, "q_new, k_new, v_new and out are required");
+        if ((reinterpret_cast<uintptr_t>(q_new) | reinterpret_cast<uintptr_t>(k_new) |
+             reinterpret_cast<uintptr_t>(v_new)) % 16)
+            return fail(KVLINK_ERR_INVALID_ARG, "q_new, k_new and v_new must be 16-byte aligned");
+        if (reinterpret_cast<uintptr_t>(sched.rope_table) % 16)
+            return fail(KVLINK_ERR_INVALID_ARG, "plan.rope_table is not 16-byte aligned");
         kvlink_status st = check_view(k_cache, dtype, "k_cache");
         if (st != KVLINK_OK) return st;
         if ((st = check_view(v_cache, dtype, "v_cache")) != KVLINK_OK) return st;
@@ -551,6 +557,7 @@ kvlink_status kvlink_attend_stages(
         a.out = out;
         a.lse = lse;
         a.workspace = workspace;
+        a.rope_table = sched.rope_table;
         hipError_t e =
             kvlink::launch_attend(dtype, plan, a, reinterpret_cast<hipStream_t>(stream), stages);
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
@@ -574,6 +581,29 @@ kvlink_status kvlink_attend_new_tokens(
                                 k_cache, v_cache, layer, out, lse, plan, workspace,
                                 workspace_bytes, stream,
                                 KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE);
+}
+
+kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int32_t n_new_total,
+                                       const int32_t* d_new_pos, float* d_table, void* stream) {
+    try {
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+            return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+        if (n_new_total < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_new_total < 0");
+        if (n_new_total == 0) return ok();
+        if (!d_new_pos || !d_table)
+            return fail(KVLINK_ERR_INVALID_ARG, "d_new_pos and d_table are required");
+        if (reinterpret_cast<uintptr_t>(d_table) % 16)
+            return fail(KVLINK_ERR_INVALID_ARG, "d_table is not 16-byte aligned");
+        hipError_t e = kvlink::launch_rope_table(head_dim, kvlink::make_rope_freqs(rope_theta, head_dim),
+                                                 n_new_total, d_new_pos, d_table,
+                                                 reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "rope table launch: %s", hipGetErrorString(e));
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_attend_rope_table");
+    }
 }
 
 const char* kvlink_last_error(void) { return g_error.c_str(); }

@@ -273,9 +273,13 @@ struct AttendArgs {
     void* out;
     float* lse;
     void* workspace;
+    const float* rope_table;   // the batch's cos/sin table, or NULL
 };
 
 hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,
                          hipStream_t stream, unsigned stages);
+// (cos, sin) of every new token's angles, [n_new_total][head_dim / 2]
+hipError_t launch_rope_table(int head_dim, const RopeFreqs& freqs, int n_new_total,
+                             const int32_t* new_pos, float* table, hipStream_t stream);
 
 }  // namespace kvlink

@@ -21,7 +21,8 @@ import numpy as np
 import torch
 
 from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
-               kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_stages,
+               kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_rope_table,
+               kvlink_attend_stages,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
                kvlink_encode_keys_at_positions, kvlink_load_and_reencode,
                kvlink_load_stage_bytes, kvlink_reencode_keys, kvlink_reencode_keys_mapped)
@@ -49,7 +50,7 @@ class Batch:
 
     def __init__(self, dtype, n_layers, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                  seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq=None, doc_src_row=None,
-                 doc_src_pos0=None, n_workgroups=0, device="cuda"):
+                 doc_src_pos0=None, n_workgroups=0, device="cuda", fused_rope=True):
         self.dtype = dtype
         self.torch_dtype = TORCH_DTYPE[dtype]
         self.n_layers, self.n_q_heads, self.n_kv_heads = n_layers, n_q_heads, n_kv_heads
@@ -70,7 +71,20 @@ class Batch:
         self.d_seq_cached = up(self.layout["seq_cached"])
         self.d_new_pos = up(self.layout["new_pos"])
         self.d_new_visible = up(self.layout["new_visible"])
+        # bf16 batches rotate their new tokens inside the split-attention
+        # launch, from a per-batch cos/sin table; fp32 keeps the RoPE launch
+        self.rope_table = None
+        if fused_rope and dtype == KVLINK_BF16:
+            self.rope_table = torch.empty((max(self.n_new, 1), head_dim // 2, 2),
+                                          dtype=torch.float32, device=device)
+            self.build_rope_table()
         self.set_schedule(n_workgroups)
+
+    def build_rope_table(self, stream=None):
+        """(Re)compute the batch's RoPE table (one launch)."""
+        if self.rope_table is not None:
+            kvlink_attend_rope_table(self.head_dim, self.rope_theta, self.n_new, self.d_new_pos,
+                                     self.rope_table, stream)
 
     def set_schedule(self, n_workgroups=0):
         """Build the split-K schedule (n_workgroups 0: the library's cost
@@ -82,6 +96,8 @@ class Batch:
                                                    self.layout["new_visible"], cus, n_workgroups)
         self.plan_table = torch.from_numpy(np.ascontiguousarray(table)).to(self.device)
         self.plan.table = self.plan_table.data_ptr()
+        if self.rope_table is not None:
+            self.plan.rope_table = self.rope_table.data_ptr()
         self.n_workgroups = self.plan.n_workgroups
         self.ws_bytes = kvlink_attend_workspace_bytes(self.dtype, self.n_q_heads, self.n_kv_heads,
                                                       self.head_dim, self.n_new, self.plan)

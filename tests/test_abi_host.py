@@ -41,6 +41,7 @@ def test_library_exports_every_declared_symbol(kv):
 def test_struct_sizes_match_header(kv):
     assert ctypes.sizeof(kv.kvlink_span) == 24
     assert ctypes.sizeof(kv.kvlink_kv_view) == 64
+    assert ctypes.sizeof(kv.kvlink_attend_plan) == 48
 
 
 # --------------------------------------------------------------- layout maps
@@ -263,7 +264,10 @@ def _bad_plan(kv, **fields):
     (dict(ws=1000), 4),                    # misaligned
     (dict(ws_bytes=16), 4),
     (dict(layer=-1), 1),
+    (dict(q=4100), 1),                     # misaligned new-token inputs
+    (dict(v=4104), 1),
     ("table", 1),                          # plan without a device table
+    ("rope_misaligned", 1),
     ("table_misaligned", 1),
     ("row_block", 1),                      # plan of the other path
     ("n_seqs", 1),
@@ -274,6 +278,7 @@ def test_attend_validation(kv, change, status):
     if isinstance(change, str):
         plan = {"table": lambda: _bad_plan(kv, table=None),
                 "table_misaligned": lambda: _bad_plan(kv, table=4100),
+                "rope_misaligned": lambda: _bad_plan(kv, rope_table=4100),
                 "row_block": lambda: _bad_plan(kv, row_block=16),
                 "n_seqs": lambda: _bad_plan(kv, n_seqs=2),
                 "table_len": lambda: _bad_plan(kv, table_len=3),
@@ -283,6 +288,25 @@ def test_attend_validation(kv, change, status):
         _call_attend(kv, _attend_args(kv, **change))
     assert e.value.status == status
     assert kv.kvlink_last_error()
+
+
+@pytest.mark.parametrize("args,status", [
+    ((80, 5e5, 4, 4096, 4096), 2),          # head_dim
+    ((128, 0.0, 4, 4096, 4096), 1),         # theta
+    ((128, float("nan"), 4, 4096, 4096), 1),
+    ((128, 5e5, -1, 4096, 4096), 1),
+    ((128, 5e5, 4, None, 4096), 1),
+    ((128, 5e5, 4, 4096, None), 1),
+    ((128, 5e5, 4, 4096, 4100), 1),         # misaligned table
+])
+def test_rope_table_validation(kv, args, status):
+    with pytest.raises(kv.KVLinkError) as e:
+        kv.kvlink_attend_rope_table(*args, stream=0)
+    assert e.value.status == status
+
+
+def test_rope_table_empty_is_a_no_op(kv):
+    kv.kvlink_attend_rope_table(128, 5e5, 0, None, None, stream=0)
 
 
 @pytest.mark.parametrize("stages", [0, 8, 15])

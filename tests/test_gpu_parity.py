@@ -356,7 +356,14 @@ def test_schedule_invariance(n_wg):
     other.run()
     a, b = to_f64(base.out[0]), to_f64(other.out[0])
     rowmax = np.maximum(np.max(np.abs(a), axis=-1), 1e-30)
-    assert float(np.max(np.max(np.abs(a - b), axis=-1) / rowmax)) <= 1e-2
+    # Two schedules round differently: their bf16 split partials (half an
+    # ulp, 2^-9 of the row maximum, on each side), the bf16 weights P under
+    # different running maxima, and the final bf16 rounding (one ulp apart,
+    # up to 2^-7 of the row maximum).  They must agree within the bf16
+    # tolerance each result meets against the oracle.
+    diff = float(np.max(np.max(np.abs(a - b), axis=-1) / rowmax))
+    _print("schedule", n_wg, "max diff / row max", diff)
+    assert diff <= 2e-2
     _check_attend(other, 0, tag=f"n_wg {n_wg}")
 
 
@@ -445,6 +452,85 @@ def test_graph_replay_matches_eager():
         assert torch.equal(run.k_dst.view(torch.int16), ref_k.view(torch.int16)), i
         run.run()                                  # eager work between replays
         assert torch.equal(run.out[0].view(torch.int16), ref_out.view(torch.int16)), i
+
+
+# ------------------------------------------------------------ fused RoPE
+
+
+def test_rope_table_matches_fp64_angles():
+    """Every entry of the batch's RoPE table is cos/sin of the fp64 angle
+    p_n * theta^(-2j/d) (Sec. 2.2), rounded to float."""
+    import torch
+    from paper_2502_16002_amd import kvlink_attend_rope_table
+    for d, theta, top in [(128, 5e5, 20808), (64, 1e4, 118)]:
+        pos = np.concatenate([np.arange(0, 40), np.arange(top - 40, top)]).astype(np.int32)
+        d_pos = torch.from_numpy(pos).cuda()
+        table = torch.empty((len(pos), d // 2, 2), dtype=torch.float32, device="cuda")
+        kvlink_attend_rope_table(d, theta, len(pos), d_pos, table)
+        torch.cuda.synchronize()
+        got = table.cpu().numpy().astype(np.float64)
+        ang = pos[:, None].astype(np.float64) * theta ** (-2.0 * np.arange(d // 2) / d)[None, :]
+        err = max(float(np.max(np.abs(got[..., 0] - np.cos(ang)))),
+                  float(np.max(np.abs(got[..., 1] - np.sin(ang)))))
+        _print("rope table", d, theta, err)
+        assert err <= 2.0 ** -24
+
+
+def _fused_vs_separate(make, layers):
+    """The same batch with the RoPE inside the split launch and as its own
+    launch: identical bytes in the outputs, the lse and both caches."""
+    import torch
+    a, b = make(True), make(False)
+    assert a.batch.plan.rope_table and not b.batch.plan.rope_table
+    a.run()
+    b.run()
+    for l in layers:
+        assert torch.equal(a.out[l].view(torch.int16), b.out[l].view(torch.int16)), l
+        assert torch.equal(a.lse[l], b.lse[l]), l
+    assert torch.equal(a.k_dst.view(torch.int16), b.k_dst.view(torch.int16))
+    v_a = a.v_dst if hasattr(a, "v_dst") else a.v_all
+    v_b = b.v_dst if hasattr(b, "v_dst") else b.v_all
+    assert torch.equal(v_a.view(torch.int16), v_b.view(torch.int16))
+    return a
+
+
+@pytest.mark.parametrize("name,n_wg", [("llama1b", 0), ("llama1b", 1), ("llama1b", 7),
+                                       ("llama1b", 1 << 20), ("8b-2layer", 0),
+                                       ("decode-2layer", 0), ("decode-2layer", 1 << 20)])
+def test_fused_rope_matches_separate_launch(name, n_wg):
+    w = {"llama1b": lambda: workloads.llama1b_layer(),
+         "8b-2layer": lambda: workloads.llama8b_10doc(n_layers=2),
+         "decode-2layer": lambda: workloads.llama8b_long_decode(n_layers=2)}[name]()
+    layers = list(range(w.n_layers))
+    run = _fused_vs_separate(lambda f: ContiguousRun(w, layers, n_workgroups=n_wg, fused_rope=f),
+                             layers)
+    _check_attend(run, layers[-1], rows=np.arange(min(run.batch.n_new, 24)), tag=f"fused {name}")
+    _check_append(run, layers[-1])
+
+
+@pytest.mark.parametrize("doc_len,link_count,n_query,head_dim", [
+    ([], [], 9, 128),                       # only new keys: tile 0 holds new rows
+    ([1, 1, 3, 1], [3, 0, 2, 1], 0, 64),    # ragged, no queries
+    ([130, 5, 260], [5, 5, 5], 33, 128),    # new rows across tile edges
+    ([37], [0], 1, 64),                     # decode kernel: one token
+    ([700, 2000], [0, 0], 1, 128),          # decode kernel: long cache, many segments
+])
+def test_fused_rope_edge_layouts(doc_len, link_count, n_query, head_dim):
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2,
+                         head_dim=head_dim, dtype="bf16", rope_theta=5e5, seed=29)
+    for n_wg in [0, 3, 1 << 20]:
+        run = _fused_vs_separate(lambda f: ContiguousRun(w, [0], n_workgroups=n_wg, fused_rope=f),
+                                 [0])
+        _check_attend(run, 0, tag=f"fused edge {doc_len}/{n_wg}")
+        _check_append(run, 0)
+
+
+def test_fused_rope_paged_pool():
+    """Fused RoPE with the new rows written through per-request block tables
+    (K into shuffled request pages, V into fresh pages after the pool's)."""
+    from harness import PagedRun
+    w = workloads.llama8b_paged()
+    _fused_vs_separate(lambda f: PagedRun(w, fused_rope=f), [0])
 
 
 # ---------------------------------------------------------------- decode step
