@@ -173,31 +173,50 @@ __device__ __forceinline__ void append_new_rows(const KParams& p, const RowPtr& 
 }
 
 // Queries of one GQA row as the B operand pieces a lane holds (dims
-// 32ds + 8lg.. for each 32-dim step ds): loaded from the rotated-query
-// workspace, or, with the fused RoPE, from q_new and rotated here (the pairs
-// of a lane are steps ds and ds + D/64).
+// 32ds + 8lg.. for each 32-dim step ds): from the rotated-query workspace,
+// or, with the fused RoPE, from q_new rotated by the table (the pairs of a
+// lane are steps ds and ds + D/64).  load() only issues the loads, get()
+// rotates, so a caller can let their latency overlap other loads.
 template <int D>
-__device__ __forceinline__ void load_q_row(const KParams& p, int64_t n, int hq, int lg,
-                                           uint4 (&q)[D / 32]) {
-    constexpr int DS = D / 32;
-    const int64_t off = (n * p.n_q_heads + hq) * D + 8 * lg;
-    if (!p.rope) {
-        const bf16_t* src = reinterpret_cast<const bf16_t*>(p.q_rot) + off;
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) q[ds] = *reinterpret_cast<const uint4*>(src + 32 * ds);
-        return;
-    }
-    const bf16_t* src = reinterpret_cast<const bf16_t*>(p.q_new) + off;
+struct QRow {
+    static constexpr int DS = D / 32;
     uint4 raw[DS];
+    float4 tab[DS / 2][4];
+
+    __device__ __forceinline__ void load(const KParams& p, int64_t n, int hq, int lg) {
+        const int64_t off = (n * p.n_q_heads + hq) * D + 8 * lg;
+        const bf16_t* src = reinterpret_cast<const bf16_t*>(p.rope ? p.q_new : p.q_rot) + off;
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) raw[ds] = *reinterpret_cast<const uint4*>(src + 32 * ds);
+        for (int ds = 0; ds < DS; ++ds) raw[ds] = *reinterpret_cast<const uint4*>(src + 32 * ds);
+        if (!p.rope) return;
 #pragma unroll
-    for (int ds = 0; ds < DS / 2; ++ds) {
-        float cs[8], sn[8];
-        rope_table8(p.rope + n * (D / 2), 32 * ds + 8 * lg, cs, sn);
-        rope_rotate16<bf16_t>(raw[ds], raw[ds + DS / 2], cs, sn, q[ds], q[ds + DS / 2]);
+        for (int ds = 0; ds < DS / 2; ++ds) {
+            const float4* t = reinterpret_cast<const float4*>(p.rope + n * (D / 2) + 32 * ds + 8 * lg);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) tab[ds][i] = t[i];
+        }
     }
-}
+
+    __device__ __forceinline__ void get(const KParams& p, uint4 (&q)[DS]) const {
+        if (!p.rope) {
+#pragma unroll
+            for (int ds = 0; ds < DS; ++ds) q[ds] = raw[ds];
+            return;
+        }
+#pragma unroll
+        for (int ds = 0; ds < DS / 2; ++ds) {
+            float cs[8], sn[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                cs[2 * i] = tab[ds][i].x;
+                sn[2 * i] = tab[ds][i].y;
+                cs[2 * i + 1] = tab[ds][i].z;
+                sn[2 * i + 1] = tab[ds][i].w;
+            }
+            rope_rotate16<bf16_t>(raw[ds], raw[ds + DS / 2], cs, sn, q[ds], q[ds + DS / 2]);
+        }
+    }
+};
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
 hipError_t launch_attend_decode(int head_dim, const KParams& p, int n_wg, hipStream_t stream);

@@ -213,16 +213,20 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
         issue_v(j, stage(0));
     }
     // queries, B operand of S^T: row lr, dims 32ds + 8lg
-    bf16x8 qB[DS];
-    {
-        uint4 q[DS];
-        load_q_row<D>(p, n0 + tok, h * G + rho % G, lg, q);
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) qB[ds] = as_bf16x8(row_ok ? q[ds] : uint4{0u, 0u, 0u, 0u});
-    }
+    // (their rotation, with the fused RoPE, after the next step's loads
+    // are issued)
+    QRow<D> qrow;
+    qrow.load(p, n0 + tok, h * G + rho % G, lg);
     if (j + kDW < n_steps) {
         issue_k(j + kDW, R1);
         issue_v(j + kDW, stage(1));
+    }
+    bf16x8 qB[DS];
+    {
+        uint4 q[DS];
+        qrow.get(p, q);
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) qB[ds] = as_bf16x8(row_ok ? q[ds] : uint4{0u, 0u, 0u, 0u});
     }
     if (has_new && !early_new) {
         append_new_rows<D, 64 * kDW>(p, kp, vp, h, n0, Tc, na, nb);

@@ -189,31 +189,45 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         __syncthreads();
     }
 
-    // Tile 0 goes out first, then the rows' data (visible prefixes, the Q
-    // operand); tiles 1 and 2 follow once tile 0 has arrived and its first
-    // products are issued, so that when every workgroup starts at once tile 0
-    // is not queued behind them (its products are what the loop waits for).
-    issue_tile(0);
-
-    int tok[kRT], vis[kRT];
+    // The queries go out first (they come from the L2: every segment of the
+    // unit reads them), then tile 0, then the rows' visible prefixes; the
+    // queries' rotation (fused RoPE) runs while tile 0 is in flight.  Tiles 1
+    // and 2 follow once tile 0 has arrived and its first products are
+    // issued, so that when every workgroup starts at once tile 0 is not
+    // queued behind them (its products are what the loop waits for).
+    int tok[kRT];
+    QRow<D> qrow[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
         const int rho = rho_w + 16 * rt + lr;
         tok[rt] = rho < rho_end ? rho / G : -1;
-        vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
+        qrow[rt].load(p, n0 + max(tok[rt], 0), h * G + rho % G, lg);
     }
+    issue_tile(0);
+    int vis[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
     // this wave's rows: the first and last tokens, the visible prefix of the
     // last (prefixes grow with the token)
+    // (scalar loads at clamped indices: a vector load here would make the
+    // compiler wait for every load in flight, tile 0's included, before the
+    // queries' rotation)
     const bool wave_active = rho_w < rho_end;
-    const int tok_min = rho_w / G;
+    const int tok_min = min(rho_w, rho_end - 1) / G;
     const int tok_max = (min(rho_w + kRT * 16, rho_end) - 1) / G;
-    const int wave_vis_min = wave_active ? p.new_visible[n0 + tok_min] : 0;
-    const int wave_vis_max = wave_active ? p.new_visible[n0 + tok_max] : 0;
-    uint4 qraw[kRT][DS];
+    const int vis_lo = load_uniform(p.new_visible + n0 + tok_min);
+    const int vis_hi = load_uniform(p.new_visible + n0 + tok_max);
+    const int wave_vis_min = wave_active ? vis_lo : 0;
+    const int wave_vis_max = wave_active ? vis_hi : 0;
+    // the Q operand (rows past the block end hold the request's first
+    // token's queries: finite values whose results are never written)
+    bf16x8 qB[kRT][DS];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
-        const int rho = rho_w + 16 * rt + lr;
-        load_q_row<D>(p, n0 + max(tok[rt], 0), h * G + rho % G, lg, qraw[rt]);
+        uint4 q[DS];
+        qrow[rt].get(p, q);
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) qB[rt][ds] = as_bf16x8(q[ds]);
     }
     if (has_new && !tile0_new) append_new_rows<D, 64 * kWaves>(p, kp, vp, h, n0, Tc, na, nb);
 
@@ -237,12 +251,6 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         const bool new_seen = v0 + 32 > bk.cmax && max(v0, bk.cmax) <= bk.cmax + tok_max;
         return !cached_seen && !new_seen;
     };
-    bf16x8 qB[kRT][DS];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
-            qB[rt][ds] = as_bf16x8(tok[rt] >= 0 ? qraw[rt][ds] : uint4{0u, 0u, 0u, 0u});
 
     floatx4 o[DT][kRT];
 #pragma unroll

@@ -58,14 +58,17 @@ __device__ __forceinline__ uint4 pack16<float>(const float* f) {
     return uint4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
                  __float_as_uint(f[3])};
 }
+// two floats to a packed bf16 pair, round to nearest even (one
+// v_cvt_pk_bf16_f32 on gfx950)
+typedef float f32x2_v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_v{lo, hi}, bf16x2_v));
+}
 template <>
 __device__ __forceinline__ uint4 pack16<bf16_t>(const float* f) {
-    uint32_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        w[i] = (uint32_t)from_f32<bf16_t>(f[2 * i]).bits |
-               ((uint32_t)from_f32<bf16_t>(f[2 * i + 1]).bits << 16);
-    return uint4{w[0], w[1], w[2], w[3]};
+    return uint4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                 pack_bf16x2(f[6], f[7])};
 }
 
 // ------------------------------------------------------------------- views
@@ -94,6 +97,12 @@ __device__ __forceinline__ int64_t view_offset(const View& v, int layer, int hea
 // Rows of one (layer, head, seq) slice of a view, with the slice's part of
 // the address hoisted: the per-row cost is one multiply-add (contiguous) or a
 // block-table lookup (paged).
+// A wavefront-uniform int32 read through the scalar cache (the address must
+// be the same in every lane and the memory not written during the kernel).
+__device__ __forceinline__ int32_t load_uniform(const int32_t* p) {
+    return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
 struct RowPtr {
     const char* base;          // bytes: contiguous: row 0 of the slice; paged: (layer, head)
     int64_t row_bytes;         // row stride in bytes
@@ -112,7 +121,7 @@ struct RowPtr {
     // (the same in every lane), read through the scalar cache, so that the
     // wavefront's vector loads in flight do not delay it.
     __device__ __forceinline__ int page_of(int r) const {
-        return *(const __attribute__((address_space(4))) int32_t*)(table + (r >> page_shift));
+        return load_uniform(table + (r >> page_shift));
     }
     // Row r of page pg (from page_of; ignored when contiguous); for r a
     // multiple of 16, rows r..r+15 follow it at row_bytes.
