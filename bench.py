@@ -316,6 +316,26 @@ def host_load(st, iters=3):
             "load_reencode_staged_one_stream_ms": round(ser_ms, 3)}
 
 
+def device_copy_gbps(nbytes=1 << 30, iters=10):
+    """A plain device-to-device copy of nbytes (larger than the 256 MB last
+    level cache), read + written bytes per second: the practical HBM ceiling
+    on this machine, as a sanity anchor for the nominal 8 TB/s."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / iters
+    del src, dst
+    return round(2 * nbytes / (ms * 1e-3) / 1e9, 1)
+
+
 def algorithmic(w, batch):
     """Bytes and flops the method itself moves (per the closed forms)."""
     es = 2 if w.dtype == "bf16" else 4
@@ -527,6 +547,7 @@ def main():
         "us_per_layer_eager_launch": round(ms_step_eager * 1000.0 / L, 3),
         "us_per_layer_graph_launch": round(ms_step_graph * 1000.0 / L, 3),
     }
+    res["device_copy_gbps"] = device_copy_gbps()
     if not w.pool and not w.decode:
         res["host_load"] = host_load(st)
     if not args.no_cpu_baseline and w.n_seqs == 1:
