@@ -350,20 +350,6 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
         issue_vt<DT, 32 * h * 2 * D, (32 * h + 16) * 2 * D>(va, vr);
     };
-    auto pv = [&](uint2 (&vr)[DT][2], const uint32_t (&pk)[kRT][4]) {
-        wait_vt(vr);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const uint2* half = vr[dt];
-            const bf16x8 a = as_bf16x8(uint4{half[0].x, half[0].y, half[1].x, half[1].y});
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt)
-                o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    a, as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]}), o[dt][rt],
-                    0, 0, 0);
-        }
-    };
-
     // One step of the pipeline: sub-tile `cur` (S in s_cur, keys from v0,
     // values in half hc of stage stc) becomes P and is added to O, while the
     // matrix cores compute S of the next sub-tile (half hn of stage stn) into
@@ -456,28 +442,52 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         uint2 vr[DT][2];
         v_issue(stc, hc, vr);
 
-        // second half: products of key half 1, with p = 2^x packed to bf16
-        // and the row sums (8 pairs over the 2 * DS products)
+        // second half: products of key half 1 with row tile 0's weights
+        // (p = 2^x packed to bf16, and the row sums); then P V of row tile 0
+        // with row tile 1's weights; then P V of row tile 1.  Every product is
+        // paired with about one exponential, the vector work one product's
+        // 16 matrix-core cycles hide.
         uint32_t pk[kRT][4];
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-        constexpr int PPC = 8 / NP;                // pairs per chunk
+        float e[kRT][8];
+        auto weights = [&](int r, int k) {   // weight k of row tile r; a pair when k is odd
+            e[r][k] = __builtin_amdgcn_exp2f(x[r][k]);
+            if (k & 1) {
+                pk[r][k / 2] = pack2(e[r][k - 1], e[r][k]);
+                lsum[r] = __builtin_amdgcn_fdot2_f32_bf16(
+                    __builtin_bit_cast(bf16x2, pk[r][k / 2]), ones, lsum[r], false);
+            }
+        };
+        constexpr int EB = 8 / NP;                 // row tile 0 weights per product
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
             const int ds = i / 2, rt = i % 2;
             s_nxt[1][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[1][ds], qB[rt][ds],
                                                                    s_nxt[1][rt], 0, 0, 0);
 #pragma unroll
-            for (int f = 0; f < PPC; ++f) {
-                const int idx = i * PPC + f, r = idx / 4, j = idx % 4;
-                pk[r][j] = pack2(__builtin_amdgcn_exp2f(x[r][2 * j]),
-                                 __builtin_amdgcn_exp2f(x[r][2 * j + 1]));
-                lsum[r] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[r][j]),
-                                                          ones, lsum[r], false);
-            }
+            for (int f = 0; f < EB; ++f) weights(0, i * EB + f);
             __builtin_amdgcn_sched_barrier(0);
         }
 
-        pv(vr, pk);
+        // O^T += V^T P^T (operands as laid out by v_issue)
+        wait_vt(vr);
+        bf16x8 va_op[DT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+            va_op[dt] = as_bf16x8(uint4{vr[dt][0].x, vr[dt][0].y, vr[dt][1].x, vr[dt][1].y});
+        const bf16x8 p0 = as_bf16x8(uint4{pk[0][0], pk[0][1], pk[0][2], pk[0][3]});
+        constexpr int EC = 8 / DT;                 // row tile 1 weights per product
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            o[dt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va_op[dt], p0, o[dt][0], 0, 0, 0);
+#pragma unroll
+            for (int f = 0; f < EC; ++f) weights(1, dt * EC + f);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const bf16x8 p1 = as_bf16x8(uint4{pk[1][0], pk[1][1], pk[1][2], pk[1][3]});
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+            o[dt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va_op[dt], p1, o[dt][1], 0, 0, 0);
     };
 
     // ---- software pipeline over 32-key sub-tiles j = 0, 1, ... (tile j/2,
