@@ -134,14 +134,17 @@ __global__ __launch_bounds__(64) void rope_table_kernel(const int32_t* __restric
 //
 // Used for fp32 and as the plain reference schedule: 16 GQA rows per
 // workgroup (4 per wavefront), 64-key tiles staged to LDS as float, one key
-// per lane for the scores, one or two head-dim columns per lane for P.V.
+// per lane for the scores (each K element read once for the wavefront's four
+// rows), then P V with one or two head-dim columns per lane.  The next tile's
+// K and V are loaded into registers (16-byte loads) while the current one is
+// used.
 
 constexpr int kValuRB = 16, kValuKT = 64;
 
 template <int D>
-struct ValuSmem {
+struct alignas(16) ValuSmem {
     float q[kValuRB][D];
-    float k[kValuKT][D + 1];
+    float k[kValuKT][D + 4];   // 16-byte aligned rows; float4 reads by key stay conflict-free
     float v[kValuKT][D];
 };
 
@@ -153,6 +156,10 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
                                              int seg_local) {
     const bool direct = nseg == 1;
     constexpr int RB = kValuRB, KT = kValuKT, RPW = 4, DPL = D / 64;
+    constexpr int E = 16 / (int)sizeof(T);          // elements per 16-byte chunk
+    constexpr int CPR = D / E;                      // chunks per K or V row
+    constexpr int U = KT * CPR / 256;               // chunks per thread per tile
+    static_assert(U * 256 == KT * CPR, "tile chunks");
     auto& s_q = sm.q;
     auto& s_k = sm.k;
     auto& s_v = sm.v;
@@ -165,6 +172,37 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
     if (kbeg >= bk.nvirt) return;
     const int kend = min(tile_b * KT, bk.nvirt);
     const int Tc = p.seq_cached[s];
+
+    const T* kb = reinterpret_cast<const T*>(p.k.base);
+    const T* vb = reinterpret_cast<const T*>(p.v.base);
+    // this thread's chunks of the tile from t0 (keys past the segment end
+    // read its last key; they are masked)
+    uint4 kr[U], vr[U];
+    auto fetch = [&](int t0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = threadIdx.x + 256 * u, key = c / CPR, col = (c % CPR) * E;
+            const int vk = min(t0 + key, kend - 1);
+            const int row = vk < bk.cmax ? vk : Tc + (vk - bk.cmax);
+            kr[u] = *reinterpret_cast<const uint4*>(kb + view_offset(p.k, p.layer, h, s, row) + col);
+            vr[u] = *reinterpret_cast<const uint4*>(vb + view_offset(p.v, p.layer, h, s, row) + col);
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = threadIdx.x + 256 * u, key = c / CPR, col = (c % CPR) * E;
+            float fk[E], fv[E];
+            unpack16<T>(kr[u], fk);
+            unpack16<T>(vr[u], fv);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                s_k[key][col + e] = fk[e];
+                s_v[key][col + e] = fv[e];
+            }
+        }
+    };
+    fetch(kbeg);
 
     const T* q_rot = reinterpret_cast<const T*>(p.q_rot);
     for (int i = threadIdx.x; i < RB * D; i += 256) {
@@ -194,46 +232,73 @@ __device__ __forceinline__ void valu_segment(const KParams& p, ValuSmem<D>& sm, 
         for (int dd = 0; dd < DPL; ++dd) o[i][dd] = 0.f;
     }
 
-    const T* kb = reinterpret_cast<const T*>(p.k.base);
-    const T* vb = reinterpret_cast<const T*>(p.v.base);
     for (int t0 = kbeg; t0 < kend; t0 += KT) {
+        __syncthreads();   // the previous tile's readers are done
+        stage();
         __syncthreads();
-        for (int i = threadIdx.x; i < KT * D; i += 256) {
-            const int key = i / D, d = i % D;
-            const int vk = t0 + key;
-            float kx = 0.f, vx = 0.f;
-            if (vk < kend) {
-                const int row = vk < bk.cmax ? vk : Tc + (vk - bk.cmax);
-                kx = to_f32(kb[view_offset(p.k, p.layer, h, s, row) + d]);
-                vx = to_f32(vb[view_offset(p.v, p.layer, h, s, row) + d]);
-            }
-            s_k[key][d] = kx;
-            s_v[key][d] = vx;
-        }
-        __syncthreads();
+        if (t0 + KT < kend) fetch(t0 + KT);
         const int vk = t0 + lane;
+        // scores of the wavefront's rows for key vk
+        float sc[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) sc[i] = 0.f;
+#pragma unroll 4
+        for (int d = 0; d < D; d += 4) {
+            const float4 k4 = *reinterpret_cast<const float4*>(&s_k[lane][d]);
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                const float4 q4 = *reinterpret_cast<const float4*>(&s_q[wave * RPW + i][d]);
+                sc[i] += q4.x * k4.x + q4.y * k4.y + q4.z * k4.z + q4.w * k4.w;
+            }
+        }
+        // online softmax of the four rows, their cross-lane reductions
+        // interleaved (independent chains of shuffles)
+        float x[RPW], mx[RPW], pr[RPW], ps[RPW];
+        bool ok[RPW];
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
-            if (!valid[i]) continue;
-            const int row = wave * RPW + i;
-            float sc = 0.f;
+            ok[i] = valid[i] && vk < kend &&
+                    (vk < bk.cmax ? vk < vis[i] : (vk - bk.cmax) <= tok[i]);
+            x[i] = ok[i] ? sc[i] * p.scale_log2 : -INFINITY;
+            mx[i] = x[i];
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) mx[i] = fmaxf(mx[i], __shfl_xor(mx[i], off));
+        float alpha[RPW];
+        bool live[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const float m_new = fmaxf(m[i], mx[i]);
+            live[i] = m_new != -INFINITY;   // some key of the row seen so far
+            alpha[i] = live[i] ? exp2f(m[i] - m_new) : 1.f;
+            pr[i] = ok[i] ? exp2f(x[i] - m_new) : 0.f;
+            ps[i] = pr[i];
+            if (live[i]) m[i] = m_new;
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) ps[i] += __shfl_xor(ps[i], off);
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            if (!live[i]) continue;
+            l[i] = l[i] * alpha[i] + ps[i];
+#pragma unroll
+            for (int dd = 0; dd < DPL; ++dd) o[i][dd] *= alpha[i];
+        }
+        // P V: each value read once for the four rows
 #pragma unroll 8
-            for (int d = 0; d < D; ++d) sc += s_q[row][d] * s_k[lane][d];
-            const bool ok = vk < kend && (vk < bk.cmax ? vk < vis[i] : (vk - bk.cmax) <= tok[i]);
-            sc = ok ? sc * p.scale_log2 : -INFINITY;
-            const float m_new = fmaxf(m[i], wave_max(sc));
-            if (m_new == -INFINITY) continue;
-            const float alpha = exp2f(m[i] - m_new);
-            const float pr = ok ? exp2f(sc - m_new) : 0.f;
-            l[i] = l[i] * alpha + wave_sum(pr);
-            m[i] = m_new;
+        for (int j = 0; j < KT; ++j) {
+            float vv[DPL];
 #pragma unroll
-            for (int dd = 0; dd < DPL; ++dd) o[i][dd] *= alpha;
+            for (int dd = 0; dd < DPL; ++dd) vv[dd] = s_v[j][lane + 64 * dd];
 #pragma unroll
-            for (int j = 0; j < KT; ++j) {
-                const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pr), j));
+            for (int i = 0; i < RPW; ++i) {
+                const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pr[i]), j));
 #pragma unroll
-                for (int dd = 0; dd < DPL; ++dd) o[i][dd] += pj * s_v[j][lane + 64 * dd];
+                for (int dd = 0; dd < DPL; ++dd) o[i][dd] += pj * vv[dd];
             }
         }
     }

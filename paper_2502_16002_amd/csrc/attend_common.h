@@ -12,16 +12,6 @@ constexpr float kLn2 = 0.6931471805599453f;
 // exceeds it, and masked scores (-inf) still give weight 0 without NaN.
 constexpr float kNoMax = -1.0e30f;
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-    return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
-}
 
 // Request of global new token n (binary search over seq_new_ptr).
 __device__ __forceinline__ int seq_of(const int32_t* seq_new_ptr, int n_seqs, int n) {
