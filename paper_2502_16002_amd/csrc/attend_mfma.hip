@@ -13,8 +13,10 @@
 //
 //   * the tiles are loaded straight from global memory into a four-stage
 //     LDS ring with 16-byte direct-to-LDS loads (each wave issues an eighth
-//     of a tile), so the loads of the next three tiles are in flight while the
-//     current one is used, at no register cost;
+//     of a tile), at no register cost.  The workgroup barrier of each tile
+//     waits for every load in flight (its fence covers the direct-to-LDS
+//     writes), so one tile is in flight while the next is used; a barrier
+//     that left two in flight measured the same;
 //   * K is stored in MFMA operand order (for each 16-key x 32-dim block,
 //     lane l's 16 bytes at l*16): the A operand of S^T = K Q^T is one
 //     conflict-free ds_read_b128 per lane;
@@ -493,10 +495,10 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // ---- software pipeline over 32-key sub-tiles j = 0, 1, ... (tile j/2,
     // half j%2).  Step j turns S of sub-tile j into P V while the matrix
     // cores compute S of sub-tile j+1 (for the last sub-tile, a discarded
-    // product over the current stage).  The barrier that makes tile t visible
-    // sits in step 2t-1, after which the stage of tile t-2 (no longer read by
-    // any wave) receives tile t+2; tile t-1's values stay until that step's
-    // P V.  The prologue issues tiles 0..2 (1 and 2 after tile 0's barrier).
+    // product over the current stage).  The barrier that makes tile t+1
+    // visible sits before the odd step of tile t, after which the stage of
+    // tile t-1 (last read in step 2t-1) receives tile t+3.  The prologue
+    // issues tiles 0..2 (1 and 2 after tile 0's barrier).
     const int n_sub = (kend - kbeg + 31) / 32;
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
     constexpr std::integral_constant<int, 0> H0{};
