@@ -533,6 +533,39 @@ def test_fused_rope_paged_pool():
     _fused_vs_separate(lambda f: PagedRun(w, fused_rope=f), [0])
 
 
+# ------------------------------------------------------------- GQA groups
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 4), (8, 4), (16, 2), (8, 8)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", ["prefill", "decode"])
+def test_gqa_groups(hq, hkv, dtype, layout):
+    """GQA groups 1, 2 and 8 (the workloads use 2 and 4): row packing
+    (row = token x group + head), unit sizes and the path choice (the decode
+    kernel when group x new tokens <= 16), against the oracle; for bf16 the
+    RoPE inside the split kernels against its separate launch, bit for bit."""
+    if layout == "prefill":
+        doc_len, link_count, n_query = [45, 130, 7], [3, 2, 1], 21
+    else:
+        doc_len, link_count, n_query = [300, 520], [0, 0], 16 // (hq // hkv) if hq // hkv > 1 else 2
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=hq, n_kv_heads=hkv,
+                         head_dim=128 if dtype == "bf16" else 64, dtype=dtype, rope_theta=5e5,
+                         seed=31)
+    for n_wg in [0, 5]:
+        if dtype == "bf16":
+            run = _fused_vs_separate(
+                lambda f: ContiguousRun(w, [0], n_workgroups=n_wg, fused_rope=f), [0])
+        else:
+            run = ContiguousRun(w, [0], n_workgroups=n_wg)
+            run.run()
+        g = hq // hkv
+        if dtype == "bf16":
+            expect = 16 if g * max(run.batch.max_new, 1) <= 16 else 256
+            assert run.batch.plan.row_block == expect
+        _check_attend(run, 0, tag=f"gqa {hq}/{hkv} {dtype} {layout} {n_wg}")
+        _check_append(run, 0)
+
+
 # ---------------------------------------------------------------- decode step
 
 
