@@ -533,6 +533,123 @@ def test_fused_rope_paged_pool():
     _fused_vs_separate(lambda f: PagedRun(w, fused_rope=f), [0])
 
 
+# ------------------------------------------------- batches of several requests
+
+
+class _BatchRun:
+    """Several requests in one batch over contiguous caches: stored documents
+    back to back in one source sequence, each request's re-encoded keys and
+    its values in its own sequence of [layer][head][request][row][d] views."""
+
+    def __init__(self, w, n_workgroups=0, fused_rope=True):
+        import torch
+        from harness import to_torch
+        from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
+        self.w = w
+        L, H, d = w.n_layers, w.n_kv_heads, w.head_dim
+        self.ld = workloads.layer_data(w, 0)
+        row0 = workloads.doc_row0(w)
+        sdp = np.concatenate([[0], np.cumsum([len(x) for x in w.docs])]).astype(np.int32)
+        dl = [w.doc_table_len[j] for x in w.docs for j in x]
+        lc = [k for x in w.link_count for k in x]
+        self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
+                               sdp, dl, lc, w.n_query, doc_src_seq=[0] * len(dl),
+                               doc_src_row=[int(row0[j]) for x in w.docs for j in x],
+                               n_workgroups=n_workgroups, fused_rope=fused_rope)
+        R = max(int(sum(w.doc_table_len)), 1)
+        S, cap = w.n_seqs, max(b.max_total, 1)
+        self.k_src = torch.zeros((L, H, 1, R, d), dtype=b.torch_dtype, device="cuda")
+        if sum(w.doc_table_len):
+            self.k_src[0, :, 0] = to_torch(w, self.ld.k_store)
+        self.k_dst = torch.zeros((L, H, S, cap, d), dtype=b.torch_dtype, device="cuda")
+        self.v_dst = torch.zeros((L, H, S, cap, d), dtype=b.torch_dtype, device="cuda")
+        for q in range(S):
+            _, vc = workloads.request_cache(w, self.ld, q)
+            if vc.shape[1]:
+                self.v_dst[0, :, q, :vc.shape[1]] = to_torch(w, vc)
+        self.src_view = contiguous_view(self.k_src, H, 1, R, d)
+        self.k_view = contiguous_view(self.k_dst, H, S, cap, d)
+        self.v_view = contiguous_view(self.v_dst, H, S, cap, d)
+        self.q, self.kn, self.vn = (to_torch(w, x) for x in (self.ld.q_new, self.ld.k_new,
+                                                             self.ld.v_new))
+        self.out = {0: b.new_out()}
+        self.lse = {0: b.new_lse()}
+
+    def run(self):
+        import torch
+        self.batch.reencode(self.src_view, self.k_view)
+        self.batch.attend(0, self.q, self.kn, self.vn, self.k_view, self.v_view, self.out[0],
+                          self.lse[0])
+        torch.cuda.synchronize()
+
+
+def _check_batch(run, tag):
+    w, b = run.w, run.batch
+    got, lse = to_f64(run.out[0]), to_f64(run.lse[0])
+    k_dst, v_dst = to_f64(run.k_dst[0]), to_f64(run.v_dst[0])
+    for q in range(w.n_seqs):
+        kc, vc = workloads.request_cache(w, run.ld, q)
+        qn, kn, vn = workloads.request_new(w, run.ld, q)
+        f = lambda x: workloads.as_f64(w, x)
+        kc, vc, qn, kn, vn = f(kc), f(vc), f(qn), f(kn), f(vn)
+        n0, n1 = int(b.layout["seq_new_ptr"][q]), int(b.layout["seq_new_ptr"][q + 1])
+        Tc = int(b.layout["seq_cached"][q])
+        assert Tc == kc.shape[1]
+        if n1 > n0:
+            ref, ref_lse = oracle.attend(w.doc_len(q), w.link_count[q], w.n_query[q], qn, kn, vn,
+                                         kc, vc, w.rope_theta, w.scale)
+            check_close(w, got[n0:n1], ref, f"{tag} request {q}")
+            assert float(np.max(np.abs(lse[n0:n1] - ref_lse))) <= (1e-5 if w.dtype == "f32"
+                                                                    else 2e-2)
+            # the appended new rows, after the request's cached rows
+            pos = b.layout["new_pos"][n0:n1]
+            ref_k = np.stack([[oracle.rope(kn[r, h], int(pos[r]), w.rope_theta)
+                               for r in range(n1 - n0)] for h in range(w.n_kv_heads)])
+            check_close(w, k_dst[:, q, Tc:Tc + n1 - n0], ref_k, f"{tag} appended keys {q}")
+            assert np.array_equal(v_dst[:, q, Tc:Tc + n1 - n0], vn.transpose(1, 0, 2))
+        # the re-encoded documents of the request
+        spans = b.layout["spans"][int(np.sum([len(x) for x in w.docs[:q]])):][:len(w.docs[q])]
+        for sp in spans:
+            rows = np.arange(int(sp[3]), int(sp[3]) + int(sp[4]))
+            ref = oracle.reencode(kc[:, rows], int(sp[5]), w.rope_theta)
+            check_close(w, k_dst[:, q, rows], ref, f"{tag} re-encode request {q}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", ["prefill", "decode"])
+def test_batch_of_requests_contiguous(dtype, kind):
+    """Four requests of different shapes in one batch over contiguous caches
+    (a request without documents, one document, several, one reused by two
+    requests): every request's output, LSE, appended rows and re-encoded keys
+    against the oracle; for bf16 also the RoPE inside the split kernels
+    against its separate launch, bit for bit."""
+    table = [130, 7, 64, 300, 1, 45]
+    docs = [[], [3], [0, 1, 2], [4, 5, 0]]
+    if kind == "prefill":
+        links = [[], [5], [2, 0, 3], [1, 1, 4]]
+        nq = [9, 33, 1, 17]
+    else:
+        links = [[], [0], [0, 0, 0], [0, 0, 0]]
+        nq = [1, 2, 1, 4]
+    w = workloads.Workload(name="batch4", dtype=dtype, n_layers=1, n_q_heads=8, n_kv_heads=2,
+                           head_dim=128 if dtype == "bf16" else 64, rope_theta=5e5, seed=37,
+                           doc_table_len=table, docs=docs, link_count=links, n_query=nq)
+    for n_wg in [0, 3]:
+        if dtype == "bf16":
+            a, b = _BatchRun(w, n_wg, True), _BatchRun(w, n_wg, False)
+            a.run()
+            b.run()
+            import torch
+            assert torch.equal(a.out[0].view(torch.int16), b.out[0].view(torch.int16))
+            assert torch.equal(a.k_dst.view(torch.int16), b.k_dst.view(torch.int16))
+            run = a
+            assert run.batch.plan.row_block == (16 if kind == "decode" else 256)
+        else:
+            run = _BatchRun(w, n_wg)
+            run.run()
+        _check_batch(run, f"batch {dtype} {kind} {n_wg}")
+
+
 # ------------------------------------------------------------- GQA groups
 
 
