@@ -7,6 +7,7 @@ import re
 
 import numpy as np
 import pytest
+from hypothesis import given, settings, strategies as st
 
 import oracle
 import workloads
@@ -389,7 +390,7 @@ def _check_schedule(kv, w, n_wg_req):
                                              256, n_wg_req)
     G = w.n_q_heads // w.n_kv_heads
     max_new = int(np.max(np.diff(L["seq_new_ptr"])))
-    mfma = w.dtype == "bf16" and max_new * G >= 32
+    mfma = w.dtype == "bf16" and max_new * G > 16
     assert plan.row_block == (256 if mfma else 16)
     recs, unit_recs, split = _decode(plan, table, w.n_seqs)
     units, _ = _expected_units(L, G, w.n_kv_heads, plan.row_block)
@@ -457,6 +458,33 @@ def test_attend_schedule(kv, name):
         assert chosen.row_block == (16 if rows <= 16 else 256)
     if w.decode:
         assert chosen.n_workgroups >= 256     # two workgroups per compute unit fit
+
+
+@settings(max_examples=80, deadline=None)
+@given(st.data())
+def test_attend_schedule_random_batches(kv, data):
+    """The schedule invariants over random batches: 1-4 requests of 0-5
+    documents (1-400 tokens, documents shared between requests), 0-5 link
+    tokens each, 0-40 queries (at least one new token per request), GQA
+    groups 1-8, both dtypes, chosen and forced workgroup counts."""
+    n_seqs = data.draw(st.integers(1, 4))
+    table = data.draw(st.lists(st.integers(1, 400), min_size=1, max_size=6))
+    docs, links, nq = [], [], []
+    for _ in range(n_seqs):
+        d = data.draw(st.lists(st.integers(0, len(table) - 1), min_size=0, max_size=5))
+        lc = data.draw(st.lists(st.integers(0, 5), min_size=len(d), max_size=len(d)))
+        q = data.draw(st.integers(0 if sum(lc) else 1, 40))
+        docs.append(d)
+        links.append(lc)
+        nq.append(q)
+    hkv = data.draw(st.sampled_from([1, 2, 8]))
+    g = data.draw(st.sampled_from([1, 2, 4, 8]))
+    dtype = data.draw(st.sampled_from(["bf16", "f32"]))
+    w = workloads.Workload(name="random", dtype=dtype, n_layers=1, n_q_heads=hkv * g,
+                           n_kv_heads=hkv, head_dim=data.draw(st.sampled_from([64, 128])),
+                           rope_theta=1e4, seed=1, doc_table_len=table, docs=docs,
+                           link_count=links, n_query=nq)
+    _check_schedule(kv, w, data.draw(st.sampled_from([0, 0, 1, 2, 7, 300])))
 
 
 def test_attend_schedule_errors(kv):

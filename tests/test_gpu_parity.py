@@ -650,6 +650,36 @@ def test_batch_of_requests_contiguous(dtype, kind):
         _check_batch(run, f"batch {dtype} {kind} {n_wg}")
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_random_batches(seed):
+    """Seeded random batches: 1-4 requests of 0-5 documents (1-300 tokens,
+    shared between requests), 0-5 link tokens each, 0-40 queries, GQA groups
+    1-8, head_dim 64 or 128, both dtypes, a random workgroup count: every
+    request against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    table = [int(x) for x in rng.integers(1, 301, size=int(rng.integers(1, 7)))]
+    docs, links, nq = [], [], []
+    for _ in range(int(rng.integers(1, 5))):
+        d = [int(x) for x in rng.integers(0, len(table), size=int(rng.integers(0, 6)))]
+        lc = [int(x) for x in rng.integers(0, 6, size=len(d))]
+        docs.append(d)
+        links.append(lc)
+        nq.append(int(rng.integers(0 if sum(lc) else 1, 41)))
+    hkv = int(rng.choice([1, 2, 8]))
+    g = int(rng.choice([1, 2, 4, 8]))
+    dtype = ["bf16", "f32"][seed % 2]
+    w = workloads.Workload(name=f"random{seed}", dtype=dtype, n_layers=1, n_q_heads=hkv * g,
+                           n_kv_heads=hkv, head_dim=int(rng.choice([64, 128])),
+                           rope_theta=float(rng.choice([1e4, 5e5])), seed=41 + seed,
+                           doc_table_len=table, docs=docs, link_count=links, n_query=nq)
+    n_wg = int(rng.choice([0, 1, 5, 300]))
+    _print("random batch", seed, dtype, "heads", hkv * g, hkv, "d", w.head_dim, "docs", docs,
+           "links", links, "queries", nq, "n_wg", n_wg)
+    run = _BatchRun(w, n_wg)
+    run.run()
+    _check_batch(run, f"random {seed}")
+
+
 # ------------------------------------------------------------- GQA groups
 
 
