@@ -342,7 +342,13 @@ def algorithmic(w, batch):
     Tc = int(batch.layout["seq_cached"].astype(np.int64).sum())
     n_new = batch.n_new
     H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
-    re_bytes = 2 * w.n_layers * H * Tc * d * es
+    # re-encode: every destination row written, every stored row read once
+    # (a document reused by several spans is read once for all of them)
+    from paper_2502_16002_amd import kvlink_group_spans
+    spans = batch.layout["spans"]
+    order, gptr = kvlink_group_spans(spans)
+    stored_rows = int(sum(int(spans[order[gptr[g]], 4]) for g in range(len(gptr) - 1)))
+    re_bytes = w.n_layers * H * (Tc + stored_rows) * d * es
     pairs = int((batch.layout["new_pos"].astype(np.int64) + 1).sum())
     at_bytes = (2 * H * Tc * d + n_new * (Hq + 2 * H) * d + n_new * Hq * d) * es
     at_flops = 4 * d * Hq * pairs

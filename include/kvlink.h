@@ -234,6 +234,48 @@ kvlink_status kvlink_reencode_keys_mapped(kvlink_dtype dtype, int32_t n_layers,
                                           kvlink_kv_view dst, void* stream);
 
 /*
+ * kvlink_group_spans — group the spans that read the same stored rows (host,
+ * integer).  A document reused by several requests of a batch (the cache
+ * reuse of Sec. 1 and Sec. 3.3: one precomputed cache per document, shared by
+ * every request that retrieves it) appears in one span per use, all with the
+ * same (src_seq, src_row, len) and each with its own destination and delta.
+ *
+ *   h_spans[n_spans]        host spans (e.g. kvlink_build_layout's)
+ *   h_order[n_spans]        out: span indices, grouped, each group in span
+ *                           order, groups by (src_seq, src_row, len)
+ *   h_group_ptr[n_spans+1]  out: group g is h_order[h_group_ptr[g] ..
+ *                           h_group_ptr[g+1])
+ *   n_groups                out
+ * Errors: KVLINK_ERR_INVALID_ARG (n_spans < 0, NULL pointers).
+ */
+kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t* h_order,
+                                 int32_t* h_group_ptr, int32_t* n_groups);
+
+/*
+ * kvlink_reencode_keys_shared — kvlink_reencode_keys, document-major: the
+ * stored rows of each group of spans are read once and written, rotated by
+ * each span's delta, to every span's destination (Sec. 2.2; the bytes moved
+ * are the group's rows once plus every destination, instead of every span's
+ * rows twice).  The result is the same, byte for byte, as
+ * kvlink_reencode_keys over the same spans.
+ *
+ *   n_groups, d_group_ptr   device int32 [n_groups + 1]: group g's spans are
+ *                           d_spans[d_group_ptr[g] .. d_group_ptr[g+1])
+ *   d_spans                 device spans in group order (kvlink_group_spans'
+ *                           h_order applied); all spans of a group must
+ *                           share src_seq, src_row and len (the first span's
+ *                           are used); max_span_len as kvlink_reencode_keys
+ * src and dst must be different buffers (no in-place form).  Other
+ * arguments, layouts and errors as kvlink_reencode_keys, with n_groups in
+ * place of n_spans; also KVLINK_ERR_INVALID_ARG for src.base == dst.base.
+ */
+kvlink_status kvlink_reencode_keys_shared(kvlink_dtype dtype, int32_t n_layers,
+                                          int32_t n_kv_heads, int32_t head_dim, double rope_theta,
+                                          int32_t n_groups, const int32_t* d_group_ptr,
+                                          const kvlink_span* d_spans, int32_t max_span_len,
+                                          kvlink_kv_view src, kvlink_kv_view dst, void* stream);
+
+/*
  * Bytes of the device staging area kvlink_load_and_reencode needs: two slots
  * of one layer's stored keys and values (4 * n_kv_heads * stored_rows *
  * head_dim elements).  Returns 0 for invalid sizes.

@@ -78,6 +78,11 @@ def _load():
                                                 vp, ctypes.c_int64, kvlink_kv_view,
                                                 kvlink_kv_view, vp]
     lib.kvlink_reencode_keys_mapped.restype = ctypes.c_int
+    lib.kvlink_group_spans.argtypes = [i32, vp, vp, vp, ctypes.POINTER(i32)]
+    lib.kvlink_group_spans.restype = ctypes.c_int
+    lib.kvlink_reencode_keys_shared.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, vp, i32,
+                                                kvlink_kv_view, kvlink_kv_view, vp]
+    lib.kvlink_reencode_keys_shared.restype = ctypes.c_int
     lib.kvlink_load_stage_bytes.argtypes = [ctypes.c_int, i32, i32, i32]
     lib.kvlink_load_stage_bytes.restype = sz
     lib.kvlink_load_and_reencode.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32, vp, vp,
@@ -213,6 +218,26 @@ def kvlink_reencode_keys_mapped(dtype, n_layers, n_kv_heads, head_dim, rope_thet
                                             int(head_dim), float(rope_theta), int(n_spans),
                                             _ptr(d_spans), int(max_span_len), _ptr(d_stored_pos),
                                             int(stored_pos_stride), src, dst, _stream(stream)))
+
+
+def kvlink_group_spans(spans):
+    """Group spans [n, 6] int32 (kvlink_span fields) that read the same stored
+    rows: returns (order, group_ptr) int32 arrays."""
+    sp = np.ascontiguousarray(np.asarray(spans, dtype=np.int32).reshape(-1, SPAN_FIELDS))
+    n = len(sp)
+    order = np.zeros(max(n, 1), np.int32)
+    gptr = np.zeros(n + 1, np.int32)
+    ng = ctypes.c_int32(0)
+    _check(_lib.kvlink_group_spans(n, _ptr(sp), _ptr(order), _ptr(gptr), ctypes.byref(ng)))
+    return order[:n], gptr[:ng.value + 1]
+
+
+def kvlink_reencode_keys_shared(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_groups,
+                                d_group_ptr, d_spans, max_span_len, src, dst, stream=None):
+    _check(_lib.kvlink_reencode_keys_shared(int(dtype), int(n_layers), int(n_kv_heads),
+                                            int(head_dim), float(rope_theta), int(n_groups),
+                                            _ptr(d_group_ptr), _ptr(d_spans), int(max_span_len),
+                                            src, dst, _stream(stream)))
 
 
 def kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows):

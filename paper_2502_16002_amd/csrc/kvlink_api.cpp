@@ -1,6 +1,7 @@
 // kvlink_api.cpp — the C ABI of include/kvlink.h: host-side layout, argument
 // validation (before any HIP call) and the launches.
 #include <algorithm>
+#include <tuple>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -229,6 +230,75 @@ kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, 
     }
 }
 }  // namespace
+
+kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t* h_order,
+                                 int32_t* h_group_ptr, int32_t* n_groups) {
+    try {
+        if (n_spans < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_spans < 0");
+        if (!n_groups || (n_spans > 0 && (!h_spans || !h_order || !h_group_ptr)))
+            return fail(KVLINK_ERR_INVALID_ARG, "a required pointer is NULL");
+        // stable order by (src_seq, src_row, len): spans reading the same
+        // stored rows become neighbours, each group in span order
+        std::vector<int32_t> order((size_t)n_spans);
+        for (int32_t i = 0; i < n_spans; ++i) order[(size_t)i] = i;
+        auto key = [&](int32_t i) {
+            const kvlink_span& sp = h_spans[i];
+            return std::make_tuple(sp.src_seq, sp.src_row, sp.len);
+        };
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int32_t a, int32_t b) { return key(a) < key(b); });
+        int32_t g = 0;
+        if (h_group_ptr) h_group_ptr[0] = 0;
+        for (int32_t i = 0; i < n_spans; ++i) {
+            h_order[i] = order[(size_t)i];
+            if (i > 0 && key(order[(size_t)i]) != key(order[(size_t)i - 1])) h_group_ptr[++g] = i;
+        }
+        if (n_spans > 0) h_group_ptr[++g] = n_spans;
+        *n_groups = g;
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_INVALID_ARG, "unexpected exception in kvlink_group_spans");
+    }
+}
+
+kvlink_status kvlink_reencode_keys_shared(kvlink_dtype dtype, int32_t n_layers,
+                                          int32_t n_kv_heads, int32_t head_dim, double rope_theta,
+                                          int32_t n_groups, const int32_t* d_group_ptr,
+                                          const kvlink_span* d_spans, int32_t max_span_len,
+                                          kvlink_kv_view src, kvlink_kv_view dst, void* stream) {
+    try {
+        if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+        if (head_dim != 64 && head_dim != 128)
+            return fail(KVLINK_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", head_dim);
+        if (n_layers < 1 || n_kv_heads < 1)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_layers and n_kv_heads must be >= 1");
+        if (n_groups < 0 || max_span_len < 0)
+            return fail(KVLINK_ERR_INVALID_ARG, "n_groups and max_span_len must be >= 0");
+        if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+            return fail(KVLINK_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+        if (n_groups > 65535) return fail(KVLINK_ERR_UNSUPPORTED, "more than 65535 groups");
+        if ((int64_t)n_layers * n_kv_heads > (int64_t)8 * 65535)
+            return fail(KVLINK_ERR_UNSUPPORTED, "too many layers x heads");
+        if (n_groups == 0 || max_span_len == 0) return ok();
+        if (!d_spans || !d_group_ptr)
+            return fail(KVLINK_ERR_INVALID_ARG, "d_spans and d_group_ptr are required");
+        kvlink_status st = check_view(src, dtype, "src");
+        if (st != KVLINK_OK) return st;
+        if ((st = check_view(dst, dtype, "dst")) != KVLINK_OK) return st;
+        if (src.base == dst.base)
+            return fail(KVLINK_ERR_INVALID_ARG, "src and dst must be different buffers");
+        hipError_t e = kvlink::launch_reencode_shared(
+            dtype, head_dim, n_layers, n_kv_heads, kvlink::make_rope_freqs(rope_theta, head_dim),
+            n_groups, d_group_ptr, d_spans, max_span_len, to_view(src), to_view(dst),
+            reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess)
+            return fail(KVLINK_ERR_HIP, "kvlink_reencode_keys_shared launch: %s",
+                        hipGetErrorString(e));
+        return ok();
+    } catch (...) {
+        return fail(KVLINK_ERR_HIP, "unexpected exception in kvlink_reencode_keys_shared");
+    }
+}
 
 kvlink_status kvlink_reencode_keys(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
                                    int32_t head_dim, double rope_theta, int32_t n_spans,

@@ -216,6 +216,13 @@ hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv
                            hipStream_t stream, const int32_t* pos_map = nullptr,
                            int64_t pos_stride = 0);
 
+// Document-major re-encode: group g's spans (spans[group_ptr[g] ..
+// group_ptr[g+1])) share their stored rows, read once for all of them.
+hipError_t launch_reencode_shared(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                                  const RopeFreqs& freqs, int n_groups, const int32_t* group_ptr,
+                                  const kvlink_span* spans, int max_span_len, const View& src,
+                                  const View& dst, hipStream_t stream);
+
 // Sizes of one attention call, from the arguments and the schedule.
 struct AttendPlan {
     int n_q_heads, n_kv_heads, group, head_dim;

@@ -51,6 +51,26 @@ __device__ __forceinline__ void store_stream(const uint4& v, void* p) {
     __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
 }
 
+// Rotation of one 16-byte slice pair (dims j.. and j + D/2..) by (c, s) and
+// its non-temporal store at q (the slice) and q + D/2 (its partner); the
+// per-span and the shared kernels both go through it, so they write the same
+// bytes.
+template <typename T, int D>
+__device__ __forceinline__ void rotate_store(const uint4& lo, const uint4& hi, const float* c,
+                                             const float* s, T* q) {
+    constexpr int E = 16 / (int)sizeof(T);
+    float a[E], b[E], x[E], y[E];
+    unpack16<T>(lo, a);
+    unpack16<T>(hi, b);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        x[e] = a[e] * c[e] - b[e] * s[e];
+        y[e] = a[e] * s[e] + b[e] * c[e];
+    }
+    store_stream(pack16<T>(x), q);
+    store_stream(pack16<T>(y), q + D / 2);
+}
+
 // Modes: kDelta rotates every row of a span by R(delta); kPerToken rotates
 // row t by R(delta + t) (keys stored without rotation); kCopy moves the rows
 // unchanged (values gathered through the same spans).
@@ -130,9 +150,6 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                     store_stream(hi[u], q + H);
                     continue;
                 }
-                float a[E], b[E], x[E], y[E];
-                unpack16<T>(lo[u], a);
-                unpack16<T>(hi[u], b);
                 if constexpr (kMode == kPerToken) {
                     const int row = v % rows;
 #pragma unroll
@@ -141,16 +158,119 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                         s[e] = s_sin[row][sub * E + e];
                     }
                 }
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    x[e] = a[e] * c[e] - b[e] * s[e];
-                    y[e] = a[e] * s[e] + b[e] * c[e];
-                }
-                store_stream(pack16<T>(x), q);
-                store_stream(pack16<T>(y), q + H);
+                rotate_store<T, D>(lo[u], hi[u], c, s, q);
             }
         }
     }
+}
+
+// Document-major re-encode: the spans of group g (spans[group_ptr[g] ..
+// group_ptr[g+1])) all read the same stored rows (one document reused by
+// several requests, each at its own global offset).  A workgroup loads its
+// kRows rows x kLH (layer, head) pairs of the group's document once, then
+// for each span rotates them by that span's delta and stores them at the
+// span's destination: the stored rows are read once per group instead of
+// once per span.  The cos/sin tables of up to kMaxDst spans are built per
+// round (double-precision angles, in LDS); the first round's table work
+// overlaps the loads.
+constexpr int kMaxDst = 32;
+constexpr int kLHS = 4;   // (layer, head) pairs per workgroup of the shared kernel
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
+    View src, View dst, const kvlink_span* __restrict__ spans,
+    const int32_t* __restrict__ group_ptr, int n_lh, int n_kv_heads, RopeFreqs freqs) {
+    constexpr int H = D / 2;
+    constexpr int E = 16 / (int)sizeof(T);
+    constexpr int TPV = H / E;
+    constexpr int VPP = kThreads / TPV;
+    constexpr int NB = (kRows * kLHS + VPP - 1) / VPP;  // vectors per thread
+    __shared__ float s_cos[kMaxDst][H], s_sin[kMaxDst][H];
+
+    const int sp0 = group_ptr[blockIdx.y], sp1 = group_ptr[blockIdx.y + 1];
+    if (sp1 <= sp0) return;
+    const kvlink_span first = spans[sp0];
+    const int r0 = blockIdx.x * kRows;
+    if (r0 >= first.len) return;
+    const int rows = min(kRows, first.len - r0);
+    const int lh0 = blockIdx.z * kLHS;
+    const int nlh = min(kLHS, n_lh - lh0);
+    const int sub = threadIdx.x % TPV;
+    const int n_vec = rows * nlh;
+
+    uint4 lo[NB], hi[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const int v = threadIdx.x / TPV + u * VPP;
+        if (v < n_vec) {
+            const int lh = lh0 + v / rows, row = v % rows;
+            const T* p = reinterpret_cast<const T*>(src.base) +
+                         view_offset(src, lh / n_kv_heads, lh % n_kv_heads, first.src_seq,
+                                     first.src_row + r0 + row) +
+                         sub * E;
+            lo[u] = load_stream(p);
+            hi[u] = load_stream(p + H);
+        }
+    }
+
+    for (int c0 = sp0; c0 < sp1; c0 += kMaxDst) {
+        const int nd = min(kMaxDst, sp1 - c0);
+        __syncthreads();   // the previous round's tables are no longer read
+        for (int i = threadIdx.x; i < nd * H; i += kThreads) {
+            const int k = i / H, j = i % H;
+            rope_cos_sin((int64_t)spans[c0 + k].delta, j, freqs, &s_cos[k][j], &s_sin[k][j]);
+        }
+        __syncthreads();
+        for (int k = 0; k < nd; ++k) {
+            const kvlink_span sp = spans[c0 + k];
+            float c[E], s[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                c[e] = s_cos[k][sub * E + e];
+                s[e] = s_sin[k][sub * E + e];
+            }
+            // the destination rows, when they lie in one page (or the view
+            // is contiguous), from one scalar read of the block table
+            const int drow0 = sp.dst_row + r0;
+            bool one_page = true;
+            int64_t base = 0;
+            if (dst.block_table) {
+                one_page = drow0 % dst.page_size + rows <= dst.page_size;
+                if (one_page)
+                    base = (int64_t)load_uniform(dst.block_table + (int64_t)sp.dst_seq * dst.max_pages +
+                                                 drow0 / dst.page_size) * dst.page_stride +
+                           (int64_t)(drow0 % dst.page_size) * dst.row_stride;
+            } else {
+                base = (int64_t)sp.dst_seq * dst.seq_stride + (int64_t)drow0 * dst.row_stride;
+            }
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int v = threadIdx.x / TPV + u * VPP;
+                if (v < n_vec) {
+                    const int lh = lh0 + v / rows, row = v % rows;
+                    const int layer = lh / n_kv_heads, head = lh % n_kv_heads;
+                    const int64_t off =
+                        one_page ? (int64_t)layer * dst.layer_stride +
+                                       (int64_t)head * dst.head_stride + base +
+                                       (int64_t)row * dst.row_stride
+                                 : view_offset(dst, layer, head, sp.dst_seq, drow0 + row);
+                    rotate_store<T, D>(lo[u], hi[u], c, s,
+                                       reinterpret_cast<T*>(dst.base) + off + sub * E);
+                }
+            }
+        }
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_shared(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_groups,
+                         const int32_t* group_ptr, const kvlink_span* spans, int max_span_len,
+                         const View& src, const View& dst, hipStream_t stream) {
+    const int n_lh = n_layers * n_kv_heads;
+    dim3 grid((max_span_len + kRows - 1) / kRows, n_groups, (n_lh + kLHS - 1) / kLHS);
+    hipLaunchKernelGGL((reencode_shared_kernel<T, D>), grid, dim3(kThreads), 0, stream, src, dst,
+                       spans, group_ptr, n_lh, n_kv_heads, freqs);
+    return hipGetLastError();
 }
 
 template <typename T, int D>
@@ -189,6 +309,24 @@ hipError_t launch_reencode(kvlink_dtype dt, int head_dim, int n_layers, int n_kv
                                   dst, mode, pos_map, pos_stride, stream);
     return launch<float, 64>(n_layers, n_kv_heads, freqs, n_spans, spans, max_span_len, src, dst,
                              mode, pos_map, pos_stride, stream);
+}
+
+hipError_t launch_reencode_shared(kvlink_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                                  const RopeFreqs& freqs, int n_groups, const int32_t* group_ptr,
+                                  const kvlink_span* spans, int max_span_len, const View& src,
+                                  const View& dst, hipStream_t stream) {
+    if (dt == KVLINK_BF16) {
+        if (head_dim == 128)
+            return launch_shared<bf16_t, 128>(n_layers, n_kv_heads, freqs, n_groups, group_ptr,
+                                              spans, max_span_len, src, dst, stream);
+        return launch_shared<bf16_t, 64>(n_layers, n_kv_heads, freqs, n_groups, group_ptr, spans,
+                                         max_span_len, src, dst, stream);
+    }
+    if (head_dim == 128)
+        return launch_shared<float, 128>(n_layers, n_kv_heads, freqs, n_groups, group_ptr, spans,
+                                         max_span_len, src, dst, stream);
+    return launch_shared<float, 64>(n_layers, n_kv_heads, freqs, n_groups, group_ptr, spans,
+                                    max_span_len, src, dst, stream);
 }
 
 }  // namespace kvlink

@@ -22,7 +22,7 @@ import torch
 
 from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_rope_table,
-               kvlink_attend_stages,
+               kvlink_attend_stages, kvlink_group_spans, kvlink_reencode_keys_shared,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
                kvlink_encode_keys_at_positions, kvlink_load_and_reencode,
                kvlink_load_stage_bytes, kvlink_reencode_keys, kvlink_reencode_keys_mapped)
@@ -67,6 +67,14 @@ class Batch:
         def up(a):
             return torch.from_numpy(np.ascontiguousarray(a)).to(device)
         self.d_spans = up(self.layout["spans"].reshape(-1, SPAN_FIELDS))
+        # documents reused within the batch: their stored rows are re-encoded
+        # document-major (read once for all their spans)
+        order, gptr = kvlink_group_spans(self.layout["spans"])
+        self.n_groups = len(gptr) - 1
+        self.shared_docs = self.n_groups < self.n_docs
+        if self.shared_docs:
+            self.d_spans_grouped = up(self.layout["spans"].reshape(-1, SPAN_FIELDS)[order])
+            self.d_group_ptr = up(gptr)
         self.d_seq_new_ptr = up(self.layout["seq_new_ptr"])
         self.d_seq_cached = up(self.layout["seq_cached"])
         self.d_new_pos = up(self.layout["new_pos"])
@@ -105,11 +113,28 @@ class Batch:
             raise ValueError("invalid attention sizes")
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
 
-    def reencode(self, src_view, dst_view, stream=None):
-        """Re-encode every cached key of the batch, all layers (one launch)."""
-        kvlink_reencode_keys(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
-                             self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
-                             src_view, dst_view, stream)
+    def reencode(self, src_view, dst_view, stream=None, shared=None):
+        """Re-encode every cached key of the batch, all layers (one launch);
+        document-major when some document serves several spans (shared None:
+        then; True / False force either form; the document-major form needs
+        distinct source and destination buffers)."""
+        if shared is None:
+            shared = self.shared_docs
+        if shared:
+            gp = self.d_group_ptr if self.shared_docs else None
+            if gp is None:
+                order, gptr = kvlink_group_spans(self.layout["spans"])
+                self.d_spans_grouped = torch.from_numpy(np.ascontiguousarray(
+                    self.layout["spans"].reshape(-1, SPAN_FIELDS)[order])).to(self.device)
+                self.d_group_ptr = gp = torch.from_numpy(gptr).to(self.device)
+            kvlink_reencode_keys_shared(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                                        self.rope_theta, self.n_groups, gp,
+                                        self.d_spans_grouped, self.max_doc_len, src_view,
+                                        dst_view, stream)
+        else:
+            kvlink_reencode_keys(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
+                                 self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
+                                 src_view, dst_view, stream)
 
     def encode_at_positions(self, src_view, dst_view, stream=None):
         """Rotate keys stored without RoPE to their global positions, all

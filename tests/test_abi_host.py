@@ -182,6 +182,63 @@ def test_reencode_mapped_validation(kv, pos, stride):
     assert e.value.status == 1
 
 
+@pytest.mark.parametrize("change,status", [
+    (dict(head_dim=96), 2),
+    (dict(dtype=7), 2),
+    (dict(n_layers=0), 1),
+    (dict(n_groups=-1), 1),
+    (dict(theta=0.0), 1),
+    (dict(gptr=None), 1),
+    (dict(spans=None), 1),
+    (dict(src_base=8192), 1),          # src and dst are one buffer
+    (dict(src_base=0), 1),
+    (dict(rs=63), 1),
+])
+def test_reencode_shared_validation(kv, change, status):
+    a = dict(dtype=kv.KVLINK_BF16, n_layers=2, n_kv_heads=2, head_dim=64, theta=1e4, n_groups=1,
+             gptr=12288, spans=8192, max_len=4, src_base=4096, rs=64)
+    a.update(change)
+    src = _view(kv, a["src_base"], rs=a["rs"])
+    dst = _view(kv, 8192)
+    with pytest.raises(kv.KVLinkError) as e:
+        kv.kvlink_reencode_keys_shared(a["dtype"], a["n_layers"], a["n_kv_heads"], a["head_dim"],
+                                       a["theta"], a["n_groups"], a["gptr"], a["spans"],
+                                       a["max_len"], src, dst, stream=0)
+    assert e.value.status == status
+
+
+def test_reencode_shared_empty_is_a_no_op(kv):
+    kv.kvlink_reencode_keys_shared(kv.KVLINK_BF16, 2, 2, 64, 1e4, 0, None, None, 4, _view(kv),
+                                   _view(kv, 8192), stream=0)
+
+
+def test_group_spans(kv):
+    """Spans reading the same stored rows (same source sequence, row and
+    length) form one group, each group in span order; every span appears
+    once."""
+    rng = np.random.default_rng(5)
+    for n in [0, 1, 7, 200]:
+        src = rng.integers(0, 4, size=(n, 3))     # few distinct sources
+        spans = np.zeros((n, 6), np.int32)
+        spans[:, 0] = src[:, 0] % 2
+        spans[:, 1] = src[:, 1] * 100
+        spans[:, 4] = 1 + src[:, 2] % 2
+        spans[:, 2] = np.arange(n)
+        spans[:, 3] = rng.integers(0, 1000, size=n)
+        spans[:, 5] = rng.integers(0, 5000, size=n)
+        order, gptr = kv.kvlink_group_spans(spans)
+        assert sorted(order.tolist()) == list(range(n))
+        assert gptr[0] == 0 and gptr[-1] == n and np.all(np.diff(gptr) >= 1)
+        keys = [tuple(spans[i, [0, 1, 4]]) for i in order]
+        for g in range(len(gptr) - 1):
+            grp = order[gptr[g]:gptr[g + 1]]
+            assert len({keys[i] for i in range(gptr[g], gptr[g + 1])}) == 1
+            assert list(grp) == sorted(grp)
+            if g:
+                assert keys[gptr[g]] > keys[gptr[g] - 1]
+        assert len(gptr) - 1 == len({tuple(r) for r in spans[:, [0, 1, 4]]})
+
+
 def test_load_stage_bytes(kv):
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000) == 4 * 8 * 1000 * 128 * 2
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_F32, 2, 64, 10) == 4 * 2 * 10 * 64 * 4

@@ -766,6 +766,51 @@ def test_decode_step_paged_pool():
         assert float(np.max(np.abs(lse_all[n0:n0 + 1] - ref_lse))) <= 2e-2
 
 
+# ------------------------------------------------- document-major re-encode
+
+
+def test_shared_reencode_equals_per_span_pool():
+    """The shared pool (every document used by about five of the sixteen
+    requests): the document-major re-encode writes the same bytes as the
+    per-span one, and is what the batch runs by default."""
+    import torch
+    from harness import PagedRun
+    w = workloads.llama8b_paged()
+    run = PagedRun(w)
+    b = run.batch
+    assert b.shared_docs and b.n_groups == len(w.doc_table_len) < b.n_docs
+    run.k_dst.zero_()
+    b.reencode(run.src_view, run.k_view, shared=False)
+    per_span = run.k_dst.clone()
+    run.k_dst.zero_()
+    b.reencode(run.src_view, run.k_view)
+    torch.cuda.synchronize()
+    assert torch.equal(per_span.view(torch.int16), run.k_dst.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_shared_reencode_equals_per_span_batch(dtype):
+    """A contiguous batch where one document serves three spans and another
+    two (one of them twice in one request), both dtypes and head_dims."""
+    import torch
+    for d in [64, 128]:
+        w = workloads.Workload(name="shared", dtype=dtype, n_layers=3, n_q_heads=8, n_kv_heads=2,
+                               head_dim=d, rope_theta=5e5, seed=43, doc_table_len=[70, 1, 300],
+                               docs=[[0, 2], [2, 0, 2], [0, 1]], link_count=[[1, 2], [0, 0, 3],
+                                                                              [2, 2]],
+                               n_query=[5, 9, 1])
+        run = _BatchRun(w)
+        assert run.batch.shared_docs
+        run.batch.reencode(run.src_view, run.k_view, shared=False)
+        per_span = run.k_dst.clone()
+        run.k_dst.zero_()
+        run.batch.reencode(run.src_view, run.k_view, shared=True)
+        torch.cuda.synchronize()
+        assert torch.equal(per_span, run.k_dst)
+        run.run()                                  # the default path, then the attention
+        _check_batch(run, f"shared {dtype} {d}")
+
+
 # ---------------------------------------------------------------- paged pool
 
 
