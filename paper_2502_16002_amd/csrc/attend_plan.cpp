@@ -347,25 +347,48 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     std::vector<Seg> segs, cand;
     if (T > 0) {
         const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
-        double best = 1e300;
+        // every cut's estimate, then the cut that keeps the most workgroups
+        // busy among those within kNearTie of the best estimate: the
+        // estimate leaves out the launch and prologue costs that do not
+        // shrink with more workgroups, and measured near ties favour filling
+        // every compute unit
+        constexpr double kNearTie = 0.02;
+        struct Est {
+            double t;
+            int c, way, used;
+        };
+        std::vector<Est> est;
+        auto cut = [&](int c, int way) {
+            cand.clear();
+            if (way == 0) cut_unit_aligned(units, c, &cand);
+            else cut_equal_ranges(units, c, &cand);
+        };
         auto consider = [&](int c, bool any_cost) {
             for (int way = 0; way < 2; ++way) {
-                cand.clear();
-                if (way == 0) cut_unit_aligned(units, c, &cand);
-                else cut_equal_ranges(units, c, &cand);
+                cut(c, way);
+                const int used = compact_workgroups(&cand);
                 // a forced count takes only cuts that use every workgroup
-                if (compact_workgroups(&cand) < c && any_cost) continue;
-                const double t = estimate_us(units, cand, cm, head_dim, dt == KVLINK_BF16 ? 2 : 4);
-                if (t < best * 0.99) {   // fewer workgroups, unit-aligned cuts on near ties
-                    best = t;
-                    segs = cand;
-                }
+                if (used < c && any_cost) continue;
+                est.push_back({estimate_us(units, cand, cm, head_dim, dt == KVLINK_BF16 ? 2 : 4), c,
+                               way, used});
             }
         };
         if (n_workgroups > 0) {
             consider((int)std::min<int64_t>(n_workgroups, T), true);
         } else {
             for (int c = 1; c <= max_n; ++c) consider(c, false);
+        }
+        double best = 1e300;
+        for (const Est& e : est) best = std::min(best, e.t);
+        const Est* pick = nullptr;
+        for (const Est& e : est)   // most workgroups, then lowest estimate, then unit-aligned
+            if (e.t <= best * (1.0 + kNearTie) &&
+                (!pick || e.used > pick->used || (e.used == pick->used && e.t < pick->t)))
+                pick = &e;
+        if (pick) {
+            cut(pick->c, pick->way);
+            compact_workgroups(&cand);
+            segs = cand;
         }
     }
     const int n = used_workgroups(segs);
