@@ -408,8 +408,9 @@ kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int3
  *                    its keys, their RoPE and append as the fused form
  *                    does them; the launch is as long as its longest
  *                    workgroup, and split partials add a combine launch
- *                    and their traffic); > 0: that many workgroups (capped
- *                    at the tile count)
+ *                    and their traffic; of the cuts within 2% of the best
+ *                    estimate, the one with the most workgroups is taken);
+ *                    > 0: that many workgroups (capped at the tile count)
  *   table, table_capacity  host array for the table; with table == NULL
  *                    only *plan is filled (to size the array)
  *   plan             out: counts and row_block; plan->table and
