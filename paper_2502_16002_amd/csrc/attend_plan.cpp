@@ -20,7 +20,7 @@
 //     ranges of equal cost, crossing unit boundaries (perfect balance, but a
 //     workgroup whose range crosses a boundary pays a second segment).
 //
-// The cheaper of the two, and the cheapest n, come from a cost model fitted
+// Each cut is priced by a cost model fitted
 // to MI355X timings of the Llama-8B-shaped workloads: a segment costs a
 // fixed set-up (its record, the first key tiles and queries, the partial
 // write); a tile costs its K/V stream plus the products of the (wavefront,
@@ -28,7 +28,10 @@
 // plus, for the new rows among its keys, their RoPE and append (which the
 // split launch does itself when the batch's RoPE table is given); the launch
 // lasts as long as its longest workgroup; split units add the combine launch
-// and the traffic of their partials.
+// and the traffic of their partials.  Of the cuts priced within 2% of the
+// cheapest, the one with the most workgroups is taken (the model leaves out
+// costs that more workgroups do not shrink, and measured near ties favour
+// filling the chip).
 //
 // Segment records are numbered so that record w is workgroup w's first
 // segment; further segments of a workgroup follow the first n and are
