@@ -16,9 +16,9 @@
  *   kvlink_reencode_keys_mapped
  *                             K' = R(g_i + t - p_t) K for compressed caches
  *                             (kept tokens at original positions p_t, GPU)
- *   kvlink_load_and_reencode  the same, from caches held in host memory, the
- *                             copy of each layer overlapping the re-encode of
- *                             the one before (GPU copy and compute streams)
+ *   kvlink_load_and_reencode  the same, from caches held in host memory: read
+ *                             by the kernels over the bus, or copied layer by
+ *                             layer through a device staging ring (GPU)
  *   kvlink_attend_make_plan   balanced split-K schedule of a batch (host)
  *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
  *                             append of their keys/values to the cache and
@@ -35,8 +35,10 @@
  *    failed; the message holds HIP's error string.
  *  * GPU calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *    NULL means the null stream).  The library allocates no device memory and
- *    keeps no state between calls; the caller owns every buffer, including
- *    the workspace.  Host arrays are only read during the call.
+ *    keeps no state between calls (except the HIP events that the staged
+ *    kvlink_load_and_reencode keeps for reuse); the caller owns every
+ *    buffer, including the workspace.  Host arrays are only read during the
+ *    call.
  *  * Positions are 0-based.  RoPE (Sec. 2.2) rotates each pair
  *    (x_j, x_{j + d/2}), j < d/2, by pos * theta^(-2j/d): the half-split
  *    pairing of the Llama family the paper fine-tunes (Sec. 3.1).  Angles are
@@ -276,12 +278,13 @@ kvlink_status kvlink_reencode_keys_shared(kvlink_dtype dtype, int32_t n_layers,
                                           kvlink_kv_view src, kvlink_kv_view dst, void* stream);
 
 /*
- * Bytes of the device staging area kvlink_load_and_reencode needs: two slots
- * of one layer's stored keys and values (4 * n_kv_heads * stored_rows *
- * head_dim elements).  Returns 0 for invalid sizes.
+ * Bytes of a device staging area of n_slots slots for kvlink_load_and_reencode:
+ * a slot holds one layer's stored keys and values (2 * n_kv_heads *
+ * stored_rows * head_dim elements).  Returns 0 for invalid sizes or
+ * n_slots < 2.
  */
 size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t head_dim,
-                               int32_t stored_rows);
+                               int32_t stored_rows, int32_t n_slots);
 
 /*
  * kvlink_load_and_reencode — the first steps of the time-to-first-token path
@@ -296,10 +299,17 @@ size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t h
  *     not used).  The arrays must be pinned and mapped for the device
  *     (hipHostMalloc with default flags); otherwise KVLINK_ERR_INVALID_ARG
  *     and nothing is launched.
- *   d_stage != NULL (staged): per layer l, copy_stream copies K_l and V_l to
- *     staging slot l % 2 (once the re-encode of layer l - 2 has released
- *     it) and compute_stream re-encodes from the slot; events order the two
- *     streams.
+ *   d_stage != NULL (staged): the staging area is a ring of
+ *     min(n_layers, stage_bytes / slot) one-layer slots (slot as
+ *     kvlink_load_stage_bytes).  Layer l is copied to slot l % n_slots on
+ *     copy_stream and re-encoded from it on compute_stream.  With two
+ *     streams, events order them: the re-encode of layer l waits for its
+ *     copy, the copy waits for the re-encode that last read its slot, and the
+ *     first copies wait for the work compute_stream held when the call was
+ *     made (an earlier call's re-encodes may still read the slots).  With
+ *     copy_stream == compute_stream the stream itself orders everything.
+ *     The events are created on a thread's first staged call on a device
+ *     and kept for reuse by later calls of that thread.
  * The call enqueues the work and returns.
  *
  *   h_k, h_v      host arrays [n_layers][n_kv_heads][stored_rows][head_dim],
@@ -307,18 +317,17 @@ size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t h
  *                 (span i's rows from src_row_i; src_seq is not used); they
  *                 must stay valid until compute_stream has finished
  *   d_stage, stage_bytes  NULL, or a device staging area of at least
- *                 kvlink_load_stage_bytes(...) bytes, 256-byte aligned
+ *                 kvlink_load_stage_bytes(..., 2) bytes, 256-byte aligned
  *   k_dst, v_dst  destination views (K and V rows of every span land at
  *                 dst_row_i.. of sequence dst_seq_i, layer l)
  *   literal       0: keys cached rotated at local positions (R(delta_i));
  *                 1: cached without rotation (R(delta_i + t))
- *   copy_stream, compute_stream  hipStream_t as void* (the same stream
- *                 serialises the copies and the re-encodes)
+ *   copy_stream, compute_stream  hipStream_t as void*
  *
  * Errors: those of kvlink_reencode_keys, and KVLINK_ERR_INVALID_ARG (null or
  * misaligned host arrays, unmapped host memory on the direct way,
  * stored_rows < 1, literal not 0 or 1), KVLINK_ERR_WORKSPACE (staging area
- * misaligned or too small).
+ * misaligned or smaller than two slots).
  */
 kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
                                        int32_t head_dim, double rope_theta, int32_t n_spans,

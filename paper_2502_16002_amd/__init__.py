@@ -83,7 +83,7 @@ def _load():
     lib.kvlink_reencode_keys_shared.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, vp, i32,
                                                 kvlink_kv_view, kvlink_kv_view, vp]
     lib.kvlink_reencode_keys_shared.restype = ctypes.c_int
-    lib.kvlink_load_stage_bytes.argtypes = [ctypes.c_int, i32, i32, i32]
+    lib.kvlink_load_stage_bytes.argtypes = [ctypes.c_int, i32, i32, i32, i32]
     lib.kvlink_load_stage_bytes.restype = sz
     lib.kvlink_load_and_reencode.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, i32, vp, vp,
                                              i32, vp, sz, kvlink_kv_view, kvlink_kv_view, i32, vp,
@@ -240,9 +240,9 @@ def kvlink_reencode_keys_shared(dtype, n_layers, n_kv_heads, head_dim, rope_thet
                                             src, dst, _stream(stream)))
 
 
-def kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows):
+def kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows, n_slots=2):
     return int(_lib.kvlink_load_stage_bytes(int(dtype), int(n_kv_heads), int(head_dim),
-                                            int(stored_rows)))
+                                            int(stored_rows), int(n_slots)))
 
 
 def kvlink_load_and_reencode(dtype, n_layers, n_kv_heads, head_dim, rope_theta, n_spans, d_spans,

@@ -334,10 +334,52 @@ kvlink_status kvlink_encode_keys_at_positions(kvlink_dtype dtype, int32_t n_laye
 }
 
 size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t head_dim,
-                               int32_t stored_rows) {
-    if (!dtype_ok(dtype) || n_kv_heads < 1 || head_dim < 1 || stored_rows < 1) return 0;
-    return (size_t)4 * n_kv_heads * stored_rows * head_dim * elem_size(dtype);
+                               int32_t stored_rows, int32_t n_slots) {
+    if (!dtype_ok(dtype) || n_kv_heads < 1 || head_dim < 1 || stored_rows < 1 || n_slots < 2)
+        return 0;
+    return (size_t)n_slots * 2 * n_kv_heads * stored_rows * head_dim * elem_size(dtype);
 }
+
+}  // extern "C"
+
+namespace {
+
+// HIP events of the staged load, created on first use and kept for the life
+// of the calling thread, one set per device.  Re-recording an event is safe
+// while earlier waits on it are pending: a wait takes the record that was
+// current when it was enqueued.
+struct StageEvents {
+    int device = -1;
+    std::vector<hipEvent_t> ev;   // [0]: entry; then loaded[k], freed[k] for each slot k
+};
+
+hipError_t stage_events(int n_slots, hipEvent_t** out) {
+    thread_local std::vector<StageEvents> pools;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    StageEvents* pool = nullptr;
+    for (StageEvents& p : pools)
+        if (p.device == dev) pool = &p;
+    if (!pool) {
+        pools.push_back(StageEvents());
+        pool = &pools.back();
+        pool->device = dev;
+    }
+    const size_t need = 1 + 2 * (size_t)n_slots;
+    while (pool->ev.size() < need) {
+        hipEvent_t ev = nullptr;
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) return e;
+        pool->ev.push_back(ev);
+    }
+    *out = pool->ev.data();
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
 
 kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int32_t n_kv_heads,
                                        int32_t head_dim, double rope_theta, int32_t n_spans,
@@ -362,11 +404,13 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
         if (!h_k || !h_v) return fail(KVLINK_ERR_INVALID_ARG, "h_k or h_v is NULL");
         if (n_spans > 0 && max_span_len > 0 && !d_spans)
             return fail(KVLINK_ERR_INVALID_ARG, "d_spans is NULL");
-        const size_t need = kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows);
+        // a slot holds one layer's stored keys and values
+        const size_t slot_bytes = kvlink_load_stage_bytes(dtype, n_kv_heads, head_dim, stored_rows, 2) / 2;
         if (d_stage && reinterpret_cast<uintptr_t>(d_stage) % 256)
             return fail(KVLINK_ERR_WORKSPACE, "d_stage is not 256-byte aligned");
-        if (d_stage && stage_bytes < need)
-            return fail(KVLINK_ERR_WORKSPACE, "d_stage has %zu bytes, needs %zu", stage_bytes, need);
+        if (d_stage && stage_bytes < 2 * slot_bytes)
+            return fail(KVLINK_ERR_WORKSPACE, "d_stage has %zu bytes, needs at least %zu (two slots)",
+                        stage_bytes, 2 * slot_bytes);
         kvlink_status st = check_view(k_dst, dtype, "k_dst");
         if (st != KVLINK_OK) return st;
         if ((st = check_view(v_dst, dtype, "v_dst")) != KVLINK_OK) return st;
@@ -374,7 +418,7 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
             return fail(KVLINK_ERR_INVALID_ARG, "h_k or h_v is not 16-byte aligned");
 
         const size_t es = elem_size(dtype);
-        const size_t layer_bytes = (size_t)n_kv_heads * stored_rows * head_dim * es;
+        const size_t layer_bytes = slot_bytes / 2;
         hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
         hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
         const kvlink::RopeFreqs freqs = kvlink::make_rope_freqs(rope_theta, head_dim);
@@ -423,18 +467,13 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
             return ok();
         }
 
-        // one stored layer in a staging slot: [n_kv_heads][stored_rows][head_dim]
+        // Staged: a ring of as many one-layer slots as the staging area holds
+        // (at most one per layer).  Layer l goes to slot l % n_slots; its
+        // copy waits until the re-encode of layer l - n_slots has released
+        // the slot, and its re-encode waits for its copy.
+        const int n_slots = (int)std::min<size_t>((size_t)n_layers, stage_bytes / slot_bytes);
         auto slot_view = [&](char* base) {
-            kvlink::View v;
-            v.base = base;
-            v.layer_stride = 0;
-            v.head_stride = (int64_t)stored_rows * head_dim;
-            v.row_stride = head_dim;
-            v.seq_stride = 0;
-            v.page_stride = 0;
-            v.block_table = nullptr;
-            v.page_size = 1;
-            v.max_pages = 0;
+            kvlink::View v = stored_view(base, 0);
             return v;
         };
         auto layer_of = [&](const kvlink_kv_view& v, int l) {
@@ -442,27 +481,28 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
             d.base += (int64_t)l * v.layer_stride * (int64_t)es;
             return d;
         };
-        hipEvent_t loaded[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
-        hipError_t e = hipSuccess;
-        for (int i = 0; i < 2 && e == hipSuccess; ++i) {
-            e = hipEventCreateWithFlags(&loaded[i], hipEventDisableTiming);
-            if (e == hipSuccess) e = hipEventCreateWithFlags(&freed[i], hipEventDisableTiming);
-        }
+        const bool two = cs != ks;
+        hipEvent_t* ev = nullptr;
+        hipError_t e = two ? stage_events(n_slots, &ev) : hipSuccess;
+        // the first copies reuse slots that the re-encodes of an earlier call
+        // on compute_stream may still be reading
+        if (two && e == hipSuccess) e = hipEventRecord(ev[0], ks);
+        if (two && e == hipSuccess) e = hipStreamWaitEvent(cs, ev[0], 0);
         for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
-            const int slot = l & 1;
-            char* k_slot = reinterpret_cast<char*>(d_stage) + (size_t)slot * 2 * layer_bytes;
+            const int slot = l % n_slots;
+            hipEvent_t loaded = two ? ev[1 + 2 * slot] : nullptr;
+            hipEvent_t freed = two ? ev[2 + 2 * slot] : nullptr;
+            char* k_slot = reinterpret_cast<char*>(d_stage) + (size_t)slot * slot_bytes;
             char* v_slot = k_slot + layer_bytes;
-            // the copy into a slot waits until the layer that used it two
-            // layers ago has been re-encoded
-            if (l >= 2) e = hipStreamWaitEvent(cs, freed[slot], 0);
+            if (two && l >= n_slots) e = hipStreamWaitEvent(cs, freed, 0);
             if (e == hipSuccess)
                 e = hipMemcpyAsync(k_slot, reinterpret_cast<const char*>(h_k) + l * layer_bytes,
                                    layer_bytes, hipMemcpyHostToDevice, cs);
             if (e == hipSuccess)
                 e = hipMemcpyAsync(v_slot, reinterpret_cast<const char*>(h_v) + l * layer_bytes,
                                    layer_bytes, hipMemcpyHostToDevice, cs);
-            if (e == hipSuccess) e = hipEventRecord(loaded[slot], cs);
-            if (e == hipSuccess) e = hipStreamWaitEvent(ks, loaded[slot], 0);
+            if (two && e == hipSuccess) e = hipEventRecord(loaded, cs);
+            if (two && e == hipSuccess) e = hipStreamWaitEvent(ks, loaded, 0);
             if (e == hipSuccess && work)
                 e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
                                             d_spans, max_span_len, slot_view(k_slot),
@@ -471,12 +511,7 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
                 e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
                                             d_spans, max_span_len, slot_view(v_slot),
                                             layer_of(v_dst, l), kvlink::kReencodeCopy, ks);
-            if (e == hipSuccess) e = hipEventRecord(freed[slot], ks);
-        }
-        // destroying a recorded event is deferred by the runtime until it completes
-        for (int i = 0; i < 2; ++i) {
-            if (loaded[i]) (void)hipEventDestroy(loaded[i]);
-            if (freed[i]) (void)hipEventDestroy(freed[i]);
+            if (two && e == hipSuccess) e = hipEventRecord(freed, ks);
         }
         if (e != hipSuccess)
             return fail(KVLINK_ERR_HIP, "kvlink_load_and_reencode: %s", hipGetErrorString(e));

@@ -242,7 +242,9 @@ def test_group_spans(kv):
 def test_load_stage_bytes(kv):
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000) == 4 * 8 * 1000 * 128 * 2
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_F32, 2, 64, 10) == 4 * 2 * 10 * 64 * 4
+    assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000, 6) == 12 * 8 * 1000 * 128 * 2
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 0) == 0
+    assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000, 1) == 0
 
 
 @pytest.mark.parametrize("change,status", [

@@ -68,13 +68,36 @@ def test_reencode_llama8b_all_layers():
     _print("8b re-encode worst", _check_reencode(run, range(w.n_layers)))
 
 
-def test_reencode_long_sampled_layers():
+@pytest.fixture(scope="module")
+def long_run():
+    """The 40 x 512-token workload, all 32 layers re-encoded and attended
+    once (shared by the re-encode and attention checks below)."""
     w = workloads.llama8b_long()
-    run = ContiguousRun(w, layers=[])
-    run.batch.reencode(run.src_view, run.k_view)
+    run = ContiguousRun(w, layers=list(range(w.n_layers)))
+    run.run()
+    return run
+
+
+def _long_token_sample(n_new, seed):
+    """About 5% of the new tokens (seeded) plus the first and last token of
+    every 64-token block (one 256-row unit of the wide kernel at group 4)."""
+    rng = np.random.default_rng(seed)
+    edges = [t for b in range(0, n_new, 64) for t in (b, min(b + 63, n_new - 1))]
+    pick = rng.choice(n_new, size=max(1, round(0.05 * n_new)), replace=False)
+    return np.unique(np.concatenate([edges, pick]))
+
+
+def test_reencode_long(long_run):
+    """Every key of layers 0, 15 and 31; on every other layer about 5% of
+    each document's rows (seeded) plus its first and last row."""
+    run = long_run
     worst = _check_reencode(run, [0, 15, 31])
     rng = np.random.default_rng(5)
-    worst = max(worst, _check_reencode(run, [3, 22], rows_sample=rng.integers(0, 512, 48)))
+    for l in range(run.w.n_layers):
+        if l in (0, 15, 31):
+            continue
+        rows = np.concatenate([[0, 511], rng.integers(0, 512, 26)])
+        worst = max(worst, _check_reencode(run, [l], rows_sample=rows))
     _print("long re-encode worst", worst)
 
 
@@ -219,40 +242,92 @@ def test_compressed_cache_reencode_and_attention():
 # ------------------------------------------- caches loaded from host memory
 
 
-@pytest.mark.parametrize("literal,way", [(0, "direct"), (1, "direct"), (0, "staged"),
-                                         (1, "staged"), (0, "staged_one_stream")])
-def test_load_and_reencode_from_host_matches_device_path(literal, way):
-    """All 32 layers of the 10-document workload loaded from pinned host
-    memory, read directly by the kernels or copied through a staging area
-    (copies on one stream, re-encodes on another, or both on one): the keys
-    equal the device-resident entry point's bit for bit, the values equal
-    the stored ones."""
+def _load_setup(w):
     import torch
     from harness import to_torch
-    w = workloads.llama8b_10doc()
     run = ContiguousRun(w, layers=[])
-    b = run.batch
-    if literal:
-        b.encode_at_positions(run.src_view, run.k_view)
-    else:
-        b.reencode(run.src_view, run.k_view)
-    torch.cuda.synchronize()
     h_k = run.k_src.cpu().pin_memory()                         # [L][H][R][d]
     h_v = to_torch(w, np.stack([ld.v_store for ld in run.lds]), "cpu").pin_memory()
-    stage = None if way == "direct" else \
-        torch.empty(b.load_stage_bytes(run.R), dtype=torch.uint8, device="cuda")
-    k2 = torch.zeros_like(run.k_dst)
-    v2 = torch.zeros_like(run.v_dst)
+    return run, h_k, h_v
+
+
+def _load(run, h_k, h_v, way, literal, n_slots=2, k2=None, v2=None, copy=None):
+    import torch
     from paper_2502_16002_amd.runtime import contiguous_view
+    w, b = run.w, run.batch
+    stage = None if way == "direct" else \
+        torch.empty(b.load_stage_bytes(run.R, n_slots), dtype=torch.uint8, device="cuda")
+    k2 = torch.zeros_like(run.k_dst) if k2 is None else k2
+    v2 = torch.zeros_like(run.v_dst) if v2 is None else v2
     H, d = w.n_kv_heads, w.head_dim
-    copy = torch.cuda.Stream() if way == "staged" else torch.cuda.current_stream()
+    if copy is None:
+        copy = torch.cuda.Stream() if way == "staged" else torch.cuda.current_stream()
     b.load_and_reencode(h_k, h_v, run.R, stage, contiguous_view(k2, H, 1, run.cap, d),
                         contiguous_view(v2, H, 1, run.cap, d), literal=literal,
                         copy_stream=copy, compute_stream=torch.cuda.current_stream())
+    return k2, v2, stage
+
+
+@pytest.mark.parametrize("literal,way,n_slots", [(0, "direct", 2), (1, "direct", 2),
+                                                 (0, "staged", 2), (1, "staged", 2),
+                                                 (0, "staged", 5), (0, "staged_one_stream", 2)])
+def test_load_and_reencode_from_host(literal, way, n_slots):
+    """All 32 layers of the 10-document workload loaded from pinned host
+    memory, read directly by the kernels or copied through a staging ring
+    (copies on one stream, re-encodes on another, or both on one): the keys
+    against the oracle (every key of four layers: R(delta_i), or R(g_i + t)
+    for keys cached without rotation), bit for bit equal to the
+    device-resident entry point on every layer; the values equal the stored
+    ones."""
+    import torch
+    w = workloads.llama8b_10doc()
+    run, h_k, h_v = _load_setup(w)
+    k2, v2, _ = _load(run, h_k, h_v, way, literal, n_slots)
+    torch.cuda.synchronize()
+    check = _check_encode_at_positions if literal else _check_reencode
+    run_k = run.k_dst
+    run.k_dst = k2
+    worst = check(run, [0, 9, 22, 31])
+    run.k_dst = run_k
+    _print(f"load {way} literal={literal} slots={n_slots}: oracle worst {worst:.3e}")
+    if literal:
+        run.batch.encode_at_positions(run.src_view, run.k_view)
+    else:
+        run.batch.reencode(run.src_view, run.k_view)
     torch.cuda.synchronize()
     assert torch.equal(k2.view(torch.int16), run.k_dst.view(torch.int16))
     assert torch.equal(v2[:, :, 0, :run.R].view(torch.int16),
                        run.v_dst[:, :, 0, :run.R].view(torch.int16))
+
+
+def test_load_and_reencode_staged_back_to_back():
+    """Two staged loads on two streams, one right after the other with no
+    synchronisation, through the same two-slot staging area and with
+    different stored caches: the second call's first copies must wait for
+    the first call's last re-encodes, which still read those slots.  Both
+    results equal the device-resident re-encode of their own inputs."""
+    import torch
+    w = workloads.llama8b_10doc()
+    run, h_k, h_v = _load_setup(w)
+    h_k2 = (h_k.float() * -0.5).to(h_k.dtype).pin_memory()     # other keys, same shape
+    h_v2 = (h_v.float() * 2.0).to(h_v.dtype).pin_memory()
+    copy = torch.cuda.Stream()
+    ka, va, stage = _load(run, h_k, h_v, "staged", 0, copy=copy)
+    from paper_2502_16002_amd.runtime import contiguous_view
+    H, d = w.n_kv_heads, w.head_dim
+    kb, vb = torch.zeros_like(run.k_dst), torch.zeros_like(run.v_dst)
+    run.batch.load_and_reencode(h_k2, h_v2, run.R, stage, contiguous_view(kb, H, 1, run.cap, d),
+                                contiguous_view(vb, H, 1, run.cap, d), copy_stream=copy,
+                                compute_stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for hk, hv, k_got, v_got in [(h_k, h_v, ka, va), (h_k2, h_v2, kb, vb)]:
+        run.k_src.copy_(hk)
+        run.k_dst.zero_()
+        run.batch.reencode(run.src_view, run.k_view)
+        torch.cuda.synchronize()
+        assert torch.equal(k_got.view(torch.int16), run.k_dst.view(torch.int16))
+        assert torch.equal(v_got[:, :, 0, :run.R].cpu().view(torch.int16),
+                           hv.view(torch.int16)[:, :, :run.R])
 
 
 def test_load_and_reencode_direct_refuses_unpinned_host_memory():
@@ -321,27 +396,40 @@ def test_attend_llama1b():
 
 
 def test_attend_llama8b_32_layers():
+    """Every new token and head of every one of the 32 layers."""
     w = workloads.llama8b_10doc()
     run = ContiguousRun(w, layers=list(range(w.n_layers)))
     run.run()
-    rng = np.random.default_rng(3)
-    for l in [0, 31]:
-        _print("8b attend layer", l, _check_attend(run, l, tag="8b"))
-    for l in [7, 15, 24]:
-        rows = np.sort(rng.choice(run.batch.n_new, 16, replace=False))
-        _print("8b attend layer", l, "sampled", _check_attend(run, l, rows=rows, tag="8b"))
+    worst = (0.0, 0.0)
+    for l in range(w.n_layers):
+        e = _check_attend(run, l, tag="8b")
+        worst = (max(worst[0], e[0]), max(worst[1], e[1]))
+    _print("8b attend worst (row rel, lse abs) over 32 layers", worst)
     _check_append(run, 31)
 
 
-def test_attend_long_sampled():
-    w = workloads.llama8b_long()
-    run = ContiguousRun(w, layers=list(range(w.n_layers)))
-    run.run()
-    n_new = run.batch.n_new
-    # early and late link tokens, and first / last queries
-    rows = np.array([0, 1, 4, 5, 99, 100, 199, 200, 201, n_new - 2, n_new - 1])
+def test_attend_long_full_layers(long_run):
+    """Layers 0, 15 and 31 of the 20,808-position workload: all 328 new
+    tokens x 32 heads, i.e. every row of the six row blocks of every KV
+    head; and the appended rows of layer 31."""
     for l in [0, 15, 31]:
-        _print("long attend layer", l, _check_attend(run, l, rows=rows, tag="long"))
+        _print("long attend layer", l, _check_attend(long_run, l, tag="long"))
+    _check_append(long_run, 31)
+
+
+def test_attend_long_other_layers_sampled(long_run):
+    """The other 29 layers: about 5% of the new tokens of each (seeded, a
+    new sample per layer) plus the first and last token of every row block."""
+    run = long_run
+    n_new = run.batch.n_new
+    worst = (0.0, 0.0)
+    for l in range(run.w.n_layers):
+        if l in (0, 15, 31):
+            continue
+        rows = _long_token_sample(n_new, 100 + l)
+        e = _check_attend(run, l, rows=rows, tag="long sampled")
+        worst = (max(worst[0], e[0]), max(worst[1], e[1]))
+    _print("long attend sampled layers worst (row rel, lse abs)", worst)
 
 
 @pytest.mark.parametrize("n_wg", [1, 5, 64, 1 << 20])
@@ -816,33 +904,37 @@ def test_shared_reencode_equals_per_span_batch(dtype):
 
 def test_paged_pool_reencode_and_attention():
     """Shared 64-document pool in 16-token pages, 16 requests: per-request
-    re-encoded K copies in shuffled pages, V read from the pool pages."""
+    re-encoded K copies in shuffled pages, V read from the pool pages.  Every
+    request: the re-encoded keys of all 20 of its spans, and the output and
+    LSE of all of its new tokens and heads."""
     from harness import PagedRun
     w = workloads.llama8b_paged()
     run = PagedRun(w)
     run.run()
     b = run.batch
     k_dst = to_f64(run.k_dst[0])                       # [pages][H][P][d]
-    rng = np.random.default_rng(9)
-    for s in [0, 5, 15]:
+    out_all, lse_all = to_f64(run.out[0]), to_f64(run.lse[0])
+    worst_k, worst_o, worst_lse = 0.0, 0.0, 0.0
+    d0 = 0
+    for s in range(w.n_seqs):
         kc, vc, q, kn, vn = run.oracle_inputs(0, s)
-        d0, d1 = int(np.sum([len(x) for x in w.docs[:s]])), None
         spans = b.layout["spans"][d0:d0 + len(w.docs[s])]
-        for sp in spans[[0, 7, 19]]:
+        d0 += len(w.docs[s])
+        for i, sp in enumerate(spans):
             rows = np.arange(sp[3], sp[3] + sp[4])
             pg, slot = run.request_rows(run.k_table_np, s, rows)
             got = k_dst[pg, :, slot, :].transpose(1, 0, 2)      # [H][n][d]
             ref = oracle.reencode(kc[:, rows], int(sp[5]), w.rope_theta)
-            check_close(w, got, ref, f"paged re-encode request {s}")
-            check_bf16_rounding(got, ref, f"paged re-encode request {s}")
+            worst_k = max(worst_k, check_close(w, got, ref, f"paged re-encode request {s} span {i}"))
+            check_bf16_rounding(got, ref, f"paged re-encode request {s} span {i}")
         n0, n1 = int(b.layout["seq_new_ptr"][s]), int(b.layout["seq_new_ptr"][s + 1])
-        rows = np.sort(rng.choice(n1 - n0, 12, replace=False))
         ref, ref_lse = oracle.attend(w.doc_len(s), w.link_count[s], w.n_query[s], q, kn, vn, kc,
-                                     vc, w.rope_theta, w.scale, rows=rows)
-        got = to_f64(run.out[0])[n0 + rows]
-        check_close(w, got, ref, f"paged attention request {s}")
-        lse = to_f64(run.lse[0])[n0 + rows]
-        assert float(np.max(np.abs(lse - ref_lse))) <= 2e-2
+                                     vc, w.rope_theta, w.scale)
+        worst_o = max(worst_o, check_close(w, out_all[n0:n1], ref, f"paged attention request {s}"))
+        lse_err = float(np.max(np.abs(lse_all[n0:n1] - ref_lse)))
+        assert lse_err <= 2e-2, f"paged lse request {s}: {lse_err}"
+        worst_lse = max(worst_lse, lse_err)
+    _print("paged pool worst: re-encode", worst_k, "attention", worst_o, "lse", worst_lse)
     # values in the pool pages are untouched
     ld = run.lds[0]
     assert np.array_equal(to_f64(run.v_all[0, int(run.pool_table[3, 2])]),

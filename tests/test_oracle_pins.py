@@ -236,11 +236,10 @@ def _tiny_inputs(seed=3, doc_len=(32, 32, 32), links=2, nq=16, hq=4, hkv=2, d=64
         kn.astype(np.float64), vn.astype(np.float64)
 
 
-def test_attend_matches_brute_force_full_matrix():
+def _brute_force(w, kc, vc, q, kn, vn):
     """Full T x T masked softmax in numpy (scipy softmax) over the whole
-    sequence, keys built with the complex-form RoPE, equals the oracle's
-    streaming rows of the link and query tokens."""
-    w, kc, vc, q, kn, vn = _tiny_inputs()
+    sequence, keys built with the complex-form RoPE: the softmax rows P[h] of
+    the link and query tokens, their outputs and LSE."""
     theta, scale = w.rope_theta, w.scale
     dl, lc, nq = w.doc_len(0), w.link_count[0], w.n_query[0]
     kind, seg, idx = oracle.layout(dl, lc, nq)
@@ -268,16 +267,45 @@ def test_attend_matches_brute_force_full_matrix():
     new_rows = np.nonzero(kind != oracle.KIND_DOC)[0]
     out_bf = np.zeros((len(new_rows), hq, d))
     lse_bf = np.zeros((len(new_rows), hq))
+    probs = np.zeros((hq, len(new_rows), T))
     group = hq // hkv
     for h in range(hq):
         S = scale * (Q[:, h, :] @ K[:, h // group, :].T)
         S = np.where(mask, S, -np.inf)
         P = scipy.special.softmax(S[new_rows], axis=1)
+        probs[h] = P
         out_bf[:, h, :] = P @ V[:, h // group, :]
         lse_bf[:, h] = scipy.special.logsumexp(S[new_rows], axis=1)
-    out, lse = oracle.attend(dl, lc, nq, q, kn, vn, kc, vc, theta, scale)
+    return new_rows, probs, out_bf, lse_bf
+
+
+def test_attend_matches_brute_force_full_matrix():
+    """The brute-force full-matrix masked softmax equals the oracle's
+    streaming rows of the link and query tokens."""
+    w, kc, vc, q, kn, vn = _tiny_inputs()
+    _, _, out_bf, lse_bf = _brute_force(w, kc, vc, q, kn, vn)
+    out, lse = oracle.attend(w.doc_len(0), w.link_count[0], w.n_query[0], q, kn, vn, kc, vc,
+                             w.rope_theta, w.scale)
     assert np.max(np.abs(out - out_bf)) <= 1e-12
     assert np.max(np.abs(lse - lse_bf)) <= 1e-12
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 2), (8, 2)])
+def test_attend_probs_matches_brute_force_softmax_row(hq, hkv):
+    """attend_probs, element by element, equals the brute-force softmax row
+    (same token, same query head) for heads of every KV group, the last
+    included (h // group = hkv - 1), on link tokens of the first and later
+    documents and on query tokens."""
+    w, kc, vc, q, kn, vn = _tiny_inputs(seed=13, hq=hq, hkv=hkv)
+    new_rows, probs, _, _ = _brute_force(w, kc, vc, q, kn, vn)
+    dl, lc, nq = w.doc_len(0), w.link_count[0], w.n_query[0]
+    group = hq // hkv
+    heads = [0, group - 1, group, hq - 1]       # KV groups 0, 0, 1 and the last
+    for r in [0, 1, 2, 3, 5, len(new_rows) - 1]:
+        for h in heads:
+            p = oracle.attend_probs(dl, lc, nq, q, kn, kc, w.rope_theta, w.scale, r, h)
+            assert p.shape == probs[h, r].shape
+            assert np.max(np.abs(p - probs[h, r])) <= 1e-13, (r, h)
 
 
 def test_attend_one_document_no_links_equals_torch_sdpa():
