@@ -539,6 +539,40 @@ kvlink_status kvlink_attend_stages(
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
     void* workspace, size_t workspace_bytes, void* stream, uint32_t stages);
 
+/*
+ * kvlink_attend_new_tokens_noalloc — kvlink_attend_new_tokens for callers
+ * that cannot allocate device memory or own a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments and result (the same kernels, the same schedule: the outputs are
+ * bit for bit those of kvlink_attend_new_tokens), without the workspace.
+ *
+ * The rotated queries and split partials go to a scratch area inside the
+ * library: a static device array of KVLINK_NOALLOC_SCRATCH_BYTES bytes, one
+ * copy per GPU, held from the library's load until the process ends.  Its
+ * address on a device is looked up once, on the first call with that device
+ * current.  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).  Every call on one GPU uses that GPU's single copy: calls that
+ * overlap on one GPU (different streams, or host threads without ordering)
+ * race and give wrong results; calls ordered on one stream do not.  Nothing
+ * in the scratch has to start at zero: every byte a call reads was written
+ * earlier in the same call.
+ *
+ * Errors: those of kvlink_attend_new_tokens; KVLINK_ERR_WORKSPACE when the
+ * call needs more than KVLINK_NOALLOC_SCRATCH_BYTES (kvlink_attend_workspace_bytes
+ * of the same arguments), before any HIP call; KVLINK_ERR_HIP if the scratch
+ * address cannot be looked up.
+ */
+#define KVLINK_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+kvlink_status kvlink_attend_new_tokens_noalloc(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
+    void* stream);
+
 /* Message of the last non-OK status on the calling thread ("" if none). */
 const char* kvlink_last_error(void);
 

@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -583,14 +584,48 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
     return p.total_bytes;
 }
 
-kvlink_status kvlink_attend_stages(
+}  // extern "C"
+
+namespace {
+
+// ------------------------------------------------ allocation-free attention
+
+// Device memory of kvlink_attend_new_tokens_noalloc: one copy per GPU, held
+// from the library's load until the process ends.  In host code `scratch`
+// names a host-side stand-in; the device address of each GPU's copy comes
+// from hipGetSymbolAddress and is the only form passed to kernels.
+__device__ __align__(256) unsigned char scratch[KVLINK_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_dev;   // per device id: its copy of scratch, NULL until looked up
+
+// The current device's copy of scratch, looked up on the first call on that
+// device (with it current) and kept.
+hipError_t current_scratch(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if ((int)g_scratch_dev.size() <= dev) g_scratch_dev.resize((size_t)dev + 1, nullptr);
+    if (!g_scratch_dev[(size_t)dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_dev[(size_t)dev] = p;
+    }
+    *out = g_scratch_dev[(size_t)dev];
+    return hipSuccess;
+}
+
+kvlink_status attend_impl(
     kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
     double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
     int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan sched,
-    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages) {
+    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages, bool noalloc) {
     try {
         const uint32_t all = KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE;
         if (stages == 0 || (stages & ~all))
@@ -640,6 +675,19 @@ kvlink_status kvlink_attend_stages(
         if (!kvlink::make_attend_plan(dtype, n_q_heads, n_kv_heads, head_dim, n_new_total, sched,
                                       &plan))
             return fail(KVLINK_ERR_INVALID_ARG, "invalid attention sizes or plan counts");
+        if (noalloc) {
+            // the library's scratch instead of a workspace: refused before any
+            // HIP call when the call needs more than it holds
+            if (plan.total_bytes > (size_t)KVLINK_NOALLOC_SCRATCH_BYTES)
+                return fail(KVLINK_ERR_WORKSPACE,
+                            "the call needs %zu bytes of scratch; the allocation-free entry "
+                            "point holds %zu (use kvlink_attend_new_tokens with a workspace)",
+                            plan.total_bytes, (size_t)KVLINK_NOALLOC_SCRATCH_BYTES);
+            hipError_t e = current_scratch(&workspace);
+            if (e != hipSuccess)
+                return fail(KVLINK_ERR_HIP, "scratch lookup: %s", hipGetErrorString(e));
+            workspace_bytes = (size_t)KVLINK_NOALLOC_SCRATCH_BYTES;
+        }
         if (!workspace) return fail(KVLINK_ERR_WORKSPACE, "workspace is NULL");
         if (reinterpret_cast<uintptr_t>(workspace) % 256)
             return fail(KVLINK_ERR_WORKSPACE, "workspace is not 256-byte aligned");
@@ -672,6 +720,24 @@ kvlink_status kvlink_attend_stages(
     }
 }
 
+}  // namespace
+
+extern "C" {
+
+kvlink_status kvlink_attend_stages(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan sched,
+    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages) {
+    return attend_impl(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale, n_seqs,
+                       n_new_total, max_new, max_cached, d_seq_new_ptr, d_seq_cached, d_new_pos,
+                       d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer, out, lse,
+                       sched, workspace, workspace_bytes, stream, stages, false);
+}
+
 kvlink_status kvlink_attend_new_tokens(
     kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
     double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
@@ -686,6 +752,21 @@ kvlink_status kvlink_attend_new_tokens(
                                 k_cache, v_cache, layer, out, lse, plan, workspace,
                                 workspace_bytes, stream,
                                 KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE);
+}
+
+kvlink_status kvlink_attend_new_tokens_noalloc(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
+    void* stream) {
+    return attend_impl(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale, n_seqs,
+                       n_new_total, max_new, max_cached, d_seq_new_ptr, d_seq_cached, d_new_pos,
+                       d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer, out, lse,
+                       plan, nullptr, 0, stream,
+                       KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE, true);
 }
 
 kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int32_t n_new_total,

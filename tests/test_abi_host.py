@@ -569,3 +569,44 @@ def test_attend_schedule_errors(kv):
         with pytest.raises(kv.KVLinkError) as e:
             mk(*args)
         assert e.value.status == status, args
+
+
+def _call_noalloc(kv, a):
+    kv.kvlink_attend_new_tokens_noalloc(
+        a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"], a["n_seqs"], a["n_new"],
+        a["max_new"], a["max_cached"], a["snp"], a["sc"], a["pos"], a["vis"], a["q"], a["k"],
+        a["v"], a["kview"], a["vview"], a["layer"], a["out"], a["lse"], a["plan"], stream=0)
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(d=80), 2),
+    (dict(n_seqs=0), 1),
+    (dict(scale=0.0), 1),
+    (dict(q=None), 1),
+    ("table", 1),
+])
+def test_attend_noalloc_validation(kv, change, status):
+    """The allocation-free entry point validates like the workspace one,
+    before any HIP call (the scratch lookup included)."""
+    if change == "table":
+        change = dict(plan=_bad_plan(kv, table=None))
+    with pytest.raises(kv.KVLinkError) as e:
+        _call_noalloc(kv, _attend_args(kv, **change))
+    assert e.value.status == status
+
+
+def test_attend_noalloc_refuses_calls_beyond_its_scratch(kv):
+    """A schedule whose split partials need more than the library's scratch
+    (one 64-key tile per segment over a 100,000-row cache) is refused with
+    KVLINK_ERR_WORKSPACE before any HIP call."""
+    plan = _plan(kv, snp=(0, 64), vis=(100000,) * 64, n_wg=1 << 20)
+    need = kv.kvlink_attend_workspace_bytes(kv.KVLINK_BF16, 8, 2, 128, 64, plan)
+    assert need > kv.KVLINK_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(kv.KVLinkError) as e:
+        _call_noalloc(kv, _attend_args(kv, plan=plan, n_new=64, max_new=64, max_cached=100000))
+    assert e.value.status == 4
+    assert "scratch" in kv.kvlink_last_error()
+
+
+def test_attend_noalloc_no_new_tokens_is_a_no_op(kv):
+    _call_noalloc(kv, _attend_args(kv, n_new=0, max_new=0))
