@@ -42,7 +42,8 @@ KERNEL_SOURCES = {
     "reencode_shared_kernel": ["reencode.hip", "kvlink_internal.h"],
 }
 # split-attention kernel by (dtype, the schedule's row block)
-SPLIT_KERNEL = {("bf16", 256): "attend_mfma_kernel", ("bf16", 16): "attend_decode_kernel",
+SPLIT_KERNEL = {("bf16", 256): "attend_mfma_kernel", ("bf16", 128): "attend_mfma_kernel",
+                ("bf16", 64): "attend_mfma_kernel", ("bf16", 16): "attend_decode_kernel",
                 ("f32", 16): "attend_valu_kernel"}
 # committed counter summaries, one per workload
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_{workload}.md")
@@ -56,6 +57,10 @@ def parse():
     ap.add_argument("--workload", default="llama8b-32layer-10doc")
     ap.add_argument("--workgroups", type=int, default=0,
                     help="workgroups of the split attention (0: the library's schedule)")
+    ap.add_argument("--row-block", type=int, default=0,
+                    help="rows per unit of the split attention (0: the library's schedule)")
+    ap.add_argument("--plan-flags", type=int, default=None,
+                    help="kvlink_attend_make_plan flags (default: the runtime's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-iters", type=int, default=20)
     ap.add_argument("--eager", action="store_true",
@@ -77,7 +82,7 @@ class Setup:
     """Device buffers of a single-request workload (documents stored back to
     back, concatenated cache with room for the new tokens)."""
 
-    def __init__(self, w, n_workgroups, device="cuda", fused_rope=True):
+    def __init__(self, w, n_workgroups, device="cuda", fused_rope=True, row_block=0, flags=None):
         import torch
         import workloads
         from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
@@ -88,7 +93,8 @@ class Setup:
         self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                                [0, len(docs)], w.doc_len(0), w.link_count[0], w.n_query,
                                doc_src_row=[int(row0[j]) for j in docs], n_workgroups=n_workgroups,
-                               device=device, fused_rope=fused_rope)
+                               device=device, fused_rope=fused_rope, row_block=row_block,
+                               plan_flags=flags)
         R = int(sum(w.doc_table_len))
         self.cap = cap = b.max_total
         self.k_src, self.k_dst = [], []
@@ -145,7 +151,7 @@ class Setup:
         import torch
         L = self.w.n_layers
         if not hasattr(self, "ws_layers"):
-            self.ws_layers = [torch.empty_like(self.batch.workspace) for _ in range(L)]
+            self.ws_layers = [torch.zeros_like(self.batch.workspace) for _ in range(L)]
 
         reps = max(1, 32 // L)          # at least 32 launches per replay
 
@@ -197,7 +203,8 @@ class PagedSetup(Setup):
     through its V block table, with fresh pages after them for its new
     tokens."""
 
-    def __init__(self, w, n_workgroups, device="cuda", seed=11, fused_rope=True):
+    def __init__(self, w, n_workgroups, device="cuda", seed=11, fused_rope=True, row_block=0,
+                 flags=None):
         import torch
         import workloads
         from paper_2502_16002_amd.runtime import Batch, dtype_code, paged_view
@@ -217,7 +224,8 @@ class PagedSetup(Setup):
         self.batch = b = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                                sdp, dl, lc, w.n_query, doc_src_seq=src_seq,
                                doc_src_row=[0] * len(dl), n_workgroups=n_workgroups,
-                               device=device, fused_rope=fused_rope)
+                               device=device, fused_rope=fused_rope, row_block=row_block,
+                               plan_flags=flags)
         td = b.torch_dtype
         max_new_pages = (b.max_new + P - 1) // P
         n_fresh = w.n_seqs * max_new_pages
@@ -439,7 +447,8 @@ def main():
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workloads.get(args.workload)
-    st = (PagedSetup if w.pool else Setup)(w, args.workgroups, fused_rope=not args.separate_rope)
+    st = (PagedSetup if w.pool else Setup)(w, args.workgroups, fused_rope=not args.separate_rope,
+                                           row_block=args.row_block, flags=args.plan_flags)
     alg = algorithmic(w, st.batch)
     print(f"# setup done: {w.name} cached={alg['cached_tokens']} new={alg['new_tokens']} "
           f"workgroups={st.batch.n_workgroups} segments={st.batch.plan.n_segments}", file=sys.stderr, flush=True)
@@ -447,6 +456,9 @@ def main():
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
+    # the last layer's output of a step, to check that every later replay
+    # reproduces it bit for bit (the schedule's merge order is fixed)
+    first_out = st.out.clone()
     ms_step_eager = time_region(lambda i: st.step(), args.steps)
     # the same step captured once in a HIP graph (torch's capture records the
     # library's launches on the capture stream) and replayed: the device work
@@ -457,6 +469,9 @@ def main():
     torch.cuda.synchronize()
     ms_step_graph = time_region(lambda i: graph.replay(), args.steps)
     ms_step = ms_step_eager if args.eager else ms_step_graph
+    torch.cuda.synchronize()
+    assert torch.equal(st.out.view(torch.int16), first_out.view(torch.int16)), \
+        "a replayed step changed the output"
 
     # isolated kernels, each group captured in a HIP graph and replayed on
     # torch's current stream (the stream the library launches on): the
@@ -543,6 +558,8 @@ def main():
                    "cached_tokens": alg["cached_tokens"], "new_tokens": alg["new_tokens"],
                    "attention_workgroups": st.batch.n_workgroups,
                    "attention_segments": st.batch.plan.n_segments,
+                   "attention_row_block": st.batch.plan.row_block,
+                   "attention_plan_flags": st.batch.plan.flags,
                    "step": "decode: attention only" if w.decode else "re-encode + attention"},
         "hbm_gbps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 3),

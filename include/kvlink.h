@@ -347,10 +347,11 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
  * workgroups in contiguous pieces (the split-K of flash-decoding, balanced
  * across units by a cost model): either each unit cut into pieces of equal
  * cost, one per workgroup, or equal-cost ranges over all units in order;
- * each piece of a unit that one workgroup covers is a segment, and a unit
- * with several segments has its partial results merged by a log-sum-exp
- * combine.  row_block is 16 for batches of at most 16 rows per request and
- * KV head (a decoding step; fp32 batches always) and 256 otherwise.
+ * each piece of a unit that one workgroup covers is a segment.  A unit with
+ * several segments has its partial results merged by a log-sum-exp merge:
+ * by a combine launch, or (row blocks 256, 128 and 64: batches with more than
+ * 16 rows per request and KV head, when the schedule chooses it) inside the
+ * split launch by the unit's last-arriving workgroup.
  *
  * The table (int32, built on the host by kvlink_attend_make_plan, then
  * copied to the device by the caller) holds, in order:
@@ -366,7 +367,7 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
  *   n_units x 8        unit records {request, KV head, first row of the
  *                      block, rows in the block, first new token of the
  *                      request, first segment in unit order, segments, 0}
- *   n_split_units      the units with more than one segment (combined)
+ *   n_split_units      the units with more than one segment (merged)
  * Like the layout arrays, the device copy is trusted: it must be the
  * unmodified table built for the same batch.
  */
@@ -376,9 +377,13 @@ typedef struct {
     int32_t n_workgroups;
     int32_t n_units;
     int32_t n_segments;
-    int32_t row_block;    /* rows per unit: 256, or 16 (at most 16 rows per KV head; fp32) */
+    int32_t row_block;    /* rows per unit: 256, 128 or 64, or 16 (at most 16 rows per KV
+                             head; fp32) */
     int32_t n_seqs;
     int32_t n_split_units; /* units with more than one segment */
+    uint32_t flags;       /* the kvlink_attend_make_plan flags the schedule was built
+                             with, with KVLINK_PLAN_COMBINE or KVLINK_PLAN_IN_LAUNCH
+                             set to the merge it uses */
     /* device table of kvlink_attend_rope_table for the same batch, or NULL
      * (then the RoPE stage runs as its own launch) */
     const float* rope_table;
@@ -416,10 +421,26 @@ kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int3
  *                    its wavefronts do not skip and, for new rows among
  *                    its keys, their RoPE and append as the fused form
  *                    does them; the launch is as long as its longest
- *                    workgroup, and split partials add a combine launch
- *                    and their traffic; of the cuts within 2% of the best
- *                    estimate, the one with the most workgroups is taken);
+ *                    workgroup, and split units add their merge; of the
+ *                    cuts within 2% of the best estimate, the one with the
+ *                    most workgroups is taken);
  *                    > 0: that many workgroups (capped at the tile count)
+ *   row_block        0: chosen by the same cost model among the row blocks
+ *                    of the batch's kernel (256, 128, 64 for batches with
+ *                    more than 16 rows per request and KV head, else 16);
+ *                    else that row block (KVLINK_ERR_UNSUPPORTED if it is
+ *                    not one of them)
+ *   flags            a combination of
+ *                    KVLINK_PLAN_XCD: number the workgroups so that those
+ *                      whose first segment shares a request and KV head run
+ *                      on one XCD (workgroup w runs on XCD w % 8 on MI355X),
+ *                      sharing one L2;
+ *                    KVLINK_PLAN_COMBINE or KVLINK_PLAN_IN_LAUNCH (not
+ *                      both): merge split units by the combine launch, or
+ *                      inside the split launch (wide kernel only); without
+ *                      either the cost model chooses, and plan->flags
+ *                      reports the choice;
+ *                    none changes the result beyond float rounding order
  *   table, table_capacity  host array for the table; with table == NULL
  *                    only *plan is filled (to size the array)
  *   plan             out: counts and row_block; plan->table and
@@ -430,23 +451,35 @@ kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int3
  *
  * The result of the attention does not depend on the schedule beyond float
  * rounding order.  Errors: KVLINK_ERR_INVALID_ARG (null required pointer,
- * n_seqs < 1, n_compute_units < 1, n_workgroups < 0, table too small),
- * KVLINK_ERR_UNSUPPORTED (head_dim, dtype, group), KVLINK_ERR_LAYOUT
- * (seq_new_ptr not non-decreasing from 0, seq_cached or new_visible
- * negative, a key range beyond 2^30).
+ * n_seqs < 1, n_compute_units < 1, n_workgroups < 0, row_block < 0, unknown
+ * flags, table too small), KVLINK_ERR_UNSUPPORTED (head_dim, dtype, group,
+ * row_block, more than 16384 units), KVLINK_ERR_LAYOUT (seq_new_ptr not
+ * non-decreasing from 0, seq_cached or new_visible negative, a key range
+ * beyond 2^30).
  */
+enum {
+    KVLINK_PLAN_XCD = 1,
+    KVLINK_PLAN_COMBINE = 4,
+    KVLINK_PLAN_IN_LAUNCH = 8
+};
+
 kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
                                       int32_t head_dim, int32_t n_seqs,
                                       const int32_t* seq_new_ptr, const int32_t* seq_cached,
                                       const int32_t* new_visible,
                                       int32_t n_compute_units, int32_t n_workgroups,
-                                      int32_t* table, int64_t table_capacity,
-                                      kvlink_attend_plan* plan);
+                                      int32_t row_block, uint32_t flags, int32_t* table,
+                                      int64_t table_capacity, kvlink_attend_plan* plan);
 
 /*
- * Workspace bytes kvlink_attend_new_tokens needs (rotated queries, plus the
- * split partials when some unit has several segments).  Returns 0 for
- * invalid sizes or a null plan.
+ * Workspace bytes kvlink_attend_new_tokens needs: 64 KiB of merge counters,
+ * then the rotated queries and, when some unit has several segments, the
+ * split partials.  Returns 0 for invalid sizes or a null plan.
+ *
+ * The counters (the workspace's first 64 KiB) must be zero before a
+ * workspace is first used, with any plan: fill them with zeros once after
+ * allocating it.  Every call that completes leaves them zero again, so a
+ * workspace is reused without clearing.
  */
 size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads,
                                      int32_t head_dim, int32_t n_new_total,
@@ -492,7 +525,8 @@ size_t kvlink_attend_workspace_bytes(kvlink_dtype dtype, int32_t n_q_heads, int3
  *                              call does steps 1 and 2 inside the split
  *                              launch (same bytes as the separate launch)
  *   workspace, workspace_bytes at least kvlink_attend_workspace_bytes(...)
- *                              device bytes, 256-byte aligned
+ *                              device bytes, 256-byte aligned, its first
+ *                              64 KiB zero (see kvlink_attend_workspace_bytes)
  *
  * softmax_scale must be positive and finite (1/sqrt(head_dim) for the Llama
  * family).  Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in {1, 2, 4, 8};
@@ -553,9 +587,11 @@ kvlink_status kvlink_attend_stages(
  * current.  The call allocates nothing (no hipMalloc, no allocating library
  * routine).  Every call on one GPU uses that GPU's single copy: calls that
  * overlap on one GPU (different streams, or host threads without ordering)
- * race and give wrong results; calls ordered on one stream do not.  Nothing
- * in the scratch has to start at zero: every byte a call reads was written
- * earlier in the same call.
+ * race and give wrong results; calls ordered on one stream do not.  The
+ * scratch needs no clearing: its merge counters (its first 64 KiB, as in a
+ * workspace) are zero when the library is loaded and every completed call
+ * leaves them zero; every other byte a call reads was written earlier in the
+ * same call.
  *
  * Errors: those of kvlink_attend_new_tokens; KVLINK_ERR_WORKSPACE when the
  * call needs more than KVLINK_NOALLOC_SCRATCH_BYTES (kvlink_attend_workspace_bytes

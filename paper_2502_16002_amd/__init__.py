@@ -17,6 +17,9 @@ LIB_PATH = os.path.join(HERE, "libkvlink.so")
 KVLINK_F32, KVLINK_BF16 = 0, 1
 KVLINK_STAGE_ROPE, KVLINK_STAGE_SPLIT, KVLINK_STAGE_COMBINE = 1, 2, 4
 KVLINK_STAGE_ALL = 7
+KVLINK_PLAN_XCD = 1
+KVLINK_PLAN_COMBINE = 4
+KVLINK_PLAN_IN_LAUNCH = 8
 STATUS = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_UNSUPPORTED", 3: "ERR_LAYOUT",
           4: "ERR_WORKSPACE", 5: "ERR_HIP"}
 
@@ -57,6 +60,7 @@ class kvlink_attend_plan(ctypes.Structure):
                 ("row_block", ctypes.c_int32),
                 ("n_seqs", ctypes.c_int32),
                 ("n_split_units", ctypes.c_int32),
+                ("flags", ctypes.c_uint32),
                 ("rope_table", ctypes.c_void_p)]
 
 
@@ -90,7 +94,8 @@ def _load():
                                              vp]
     lib.kvlink_load_and_reencode.restype = ctypes.c_int
     lib.kvlink_attend_make_plan.argtypes = [ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, i32,
-                                            i32, vp, i64, ctypes.POINTER(kvlink_attend_plan)]
+                                            i32, i32, ctypes.c_uint32, vp, i64,
+                                            ctypes.POINTER(kvlink_attend_plan)]
     lib.kvlink_attend_make_plan.restype = ctypes.c_int
     lib.kvlink_attend_workspace_bytes.argtypes = [ctypes.c_int, i32, i32, i32, i32,
                                                   ctypes.POINTER(kvlink_attend_plan)]
@@ -259,7 +264,7 @@ def kvlink_load_and_reencode(dtype, n_layers, n_kv_heads, head_dim, rope_theta, 
 
 
 def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr, seq_cached,
-                            new_visible, n_compute_units, n_workgroups=0):
+                            new_visible, n_compute_units, n_workgroups=0, row_block=0, flags=0):
     """Host-built split-K schedule: returns (plan, table) with table an int32
     numpy array; plan.table is None until the caller sets it to the address
     of a device copy of the table."""
@@ -270,7 +275,8 @@ def kvlink_attend_make_plan(dtype, n_q_heads, n_kv_heads, head_dim, seq_new_ptr,
         raise ValueError("seq_cached must have n_seqs entries")
     plan = kvlink_attend_plan()
     args = (int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), len(snp) - 1, _ptr(snp),
-            _ptr(sc), _ptr(vis), int(n_compute_units), int(n_workgroups))
+            _ptr(sc), _ptr(vis), int(n_compute_units), int(n_workgroups), int(row_block),
+            int(flags))
     _check(_lib.kvlink_attend_make_plan(*args, None, 0, ctypes.byref(plan)))
     table = np.zeros(max(plan.table_len, 1), np.int32)
     _check(_lib.kvlink_attend_make_plan(*args, _ptr(table), len(table), ctypes.byref(plan)))

@@ -479,7 +479,7 @@ template <typename T, int D>
 hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t stream,
                         unsigned stages) {
     char* ws = reinterpret_cast<char*>(a.workspace);
-    T* q_rot = reinterpret_cast<T*>(ws);
+    T* q_rot = reinterpret_cast<T*>(ws + kCounterBytes);
     KParams p;
     p.q_rot = q_rot;
     p.k = a.k;
@@ -500,13 +500,15 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.unit = reinterpret_cast<const int4*>(pl.table + (size_t)kSegRecord * pl.n_segments);
     p.split_units = pl.table + (size_t)kSegRecord * pl.n_segments + (size_t)kUnitRecord * pl.n_units;
     p.n_split = pl.n_split;
-    p.part_o = ws + pl.q_rot_bytes;
-    p.part_ml = reinterpret_cast<float*>(ws + pl.q_rot_bytes + pl.part_o_bytes);
+    p.counters = reinterpret_cast<uint32_t*>(ws);
+    p.part_o = ws + kCounterBytes + pl.q_rot_bytes;
+    p.part_ml = reinterpret_cast<float*>(ws + kCounterBytes + pl.q_rot_bytes + pl.part_o_bytes);
     p.out = a.out;
     p.lse = a.lse;
     // the matrix-core kernels take the RoPE over when the batch's table is given
     const bool fused = a.rope_table && pl.path != kPathValu;
     p.rope = fused ? reinterpret_cast<const float2*>(a.rope_table) : nullptr;
+    p.merge_in_launch = pl.merge_in_launch ? 1 : 0;
     p.q_new = a.q_new;
     p.k_new = a.k_new;
     p.v_new = a.v_new;
@@ -533,11 +535,12 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
         }
         if (e != hipSuccess) return e;
     }
-    if (!(stages & KVLINK_STAGE_COMBINE) || !pl.partials) return hipSuccess;
+    // the wide kernel may merge its split units itself
+    if (!(stages & KVLINK_STAGE_COMBINE) || !pl.partials || pl.merge_in_launch) return hipSuccess;
 
     constexpr int rpb = combine_rows_per_block<T, D>();
     const dim3 grid((pl.row_block + rpb - 1) / rpb, std::min(pl.n_split, 65535));
-    if (pl.row_block == kValuRB || pl.path == kPathDecode)
+    if (pl.path != kPathWide)
         hipLaunchKernelGGL((combine_kernel<T, D, true>), grid, dim3(256), 0, stream, p);
     else
         hipLaunchKernelGGL((combine_kernel<T, D, false>), grid, dim3(256), 0, stream, p);
@@ -546,9 +549,9 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
 
 }  // namespace
 
-int attend_row_block(AttendPath path) {
-    return path == kPathWide ? attn::attend_mfma_row_block()
-                             : path == kPathDecode ? attn::attend_decode_row_block() : kValuRB;
+bool attend_row_block_ok(AttendPath path, int row_block) {
+    if (path == kPathWide) return attn::attend_mfma_row_block_ok(row_block);
+    return row_block == (path == kPathDecode ? attn::attend_decode_row_block() : kValuRB);
 }
 
 bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
@@ -558,10 +561,11 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     if (n_new_total < 0 || sched.n_seqs < 1) return false;
     // the kernel is fixed by the dtype and the schedule's row block
     int path = -1;
-    if (dt == KVLINK_BF16 && sched.row_block == attend_row_block(kPathWide)) path = kPathWide;
-    if (dt == KVLINK_BF16 && sched.row_block == attend_row_block(kPathDecode)) path = kPathDecode;
-    if (dt == KVLINK_F32 && sched.row_block == attend_row_block(kPathValu)) path = kPathValu;
+    if (dt == KVLINK_BF16 && attend_row_block_ok(kPathWide, sched.row_block)) path = kPathWide;
+    if (dt == KVLINK_BF16 && attend_row_block_ok(kPathDecode, sched.row_block)) path = kPathDecode;
+    if (dt == KVLINK_F32 && attend_row_block_ok(kPathValu, sched.row_block)) path = kPathValu;
     if (path < 0) return false;
+    if (sched.n_units > kMaxUnits) return false;
     if (sched.n_workgroups < 0 || sched.n_units < 0 || sched.n_segments < sched.n_units)
         return false;
     if ((int64_t)sched.n_segments * kSegRecord > INT32_MAX) return false;
@@ -586,6 +590,8 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->n_segments = sched.n_segments;
     p->table = sched.table;
     p->partials = sched.n_split_units > 0;
+    p->merge_in_launch = path == kPathWide && (sched.flags & KVLINK_PLAN_IN_LAUNCH) != 0;
+    if ((sched.flags & KVLINK_PLAN_IN_LAUNCH) && (sched.flags & KVLINK_PLAN_COMBINE)) return false;
     p->n_split = sched.n_split_units;
     const int64_t rows = (int64_t)n_new_total * n_q_heads;
     p->q_rot_bytes = align256((size_t)rows * head_dim * elem);
@@ -593,10 +599,12 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
         const size_t prow = (size_t)sched.n_segments * sched.row_block;
         p->part_o_bytes = align256(prow * head_dim * elem);
         p->part_ml_bytes = align256(prow * 2 * sizeof(float));
+        // the in-launch merge addresses the partials with 32-bit offsets
+        if (p->part_o_bytes >= ((size_t)1 << 31)) return false;
     } else {
         p->part_o_bytes = p->part_ml_bytes = 0;
     }
-    p->total_bytes = std::max<size_t>(256, p->q_rot_bytes + p->part_o_bytes + p->part_ml_bytes);
+    p->total_bytes = kCounterBytes + p->q_rot_bytes + p->part_o_bytes + p->part_ml_bytes;
     return true;
 }
 

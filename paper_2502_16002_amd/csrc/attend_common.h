@@ -92,6 +92,12 @@ struct KParams {
     int n_split;
     void* part_o;     // split partials O / l, in the workload dtype
     float* part_ml;   // their (running max in log2 units, sum) pairs
+    // arrival counters of the units whose segments the wide kernel merges in
+    // the same launch, one per unit; zero before the launch and after it
+    uint32_t* counters;
+    // wide kernel, 128- and 64-row units: split units merged in the launch by
+    // their last-arriving workgroup (1), or left to the combine launch (0)
+    int merge_in_launch;
     void* out;
     float* lse;
     // With rope (the batch's cos/sin table, [n_new][D/2] (cos, sin)), the
@@ -117,10 +123,11 @@ __device__ __forceinline__ void load_record(const KParams& p, int g, int4 (&rec)
 // segment numbering within the unit's partials, and a chain that only moves
 // forward (so a workgroup's walk ends).
 __device__ __forceinline__ bool record_ok(const KParams& p, const int4 (&rec)[4], int g) {
-    const int nseg = rec[1].z, loc = rec[1].w, part = rec[3].x, next = rec[3].y;
+    const int nseg = rec[1].z, loc = rec[1].w, part = rec[3].x, next = rec[3].y, unit = rec[3].z;
     return rec[0].x >= 0 && rec[0].x < p.n_seqs && rec[0].y >= 0 && rec[0].y < p.n_kv_heads &&
            rec[0].w >= 0 && rec[0].w <= p.row_block && nseg >= 1 && loc >= 0 && loc < nseg &&
-           part >= 0 && part + nseg <= p.n_segments && (next < 0 || next > g);
+           part >= 0 && part + nseg <= p.n_segments && (next < 0 || next > g) && unit >= 0 &&
+           unit < p.n_units;
 }
 
 // Wait until every memory access this wave issued has completed (stores
@@ -210,8 +217,8 @@ struct QRow {
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
 hipError_t launch_attend_decode(int head_dim, const KParams& p, int n_wg, hipStream_t stream);
-// GQA rows per unit of the wide-block and decode kernels
-int attend_mfma_row_block();
+// GQA rows per unit of the wide-block (256, 128 or 64) and decode kernels
+bool attend_mfma_row_block_ok(int row_block);
 int attend_decode_row_block();
 
 }  // namespace attn

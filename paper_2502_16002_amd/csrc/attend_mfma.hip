@@ -1,15 +1,23 @@
 // attend_mfma.hip — bf16 split-K attention of the new tokens on gfx950 matrix
 // cores (v_mfma_f32_16x16x32_bf16, float accumulation).
 //
-// A unit is one KV head's kRB = 256 GQA-packed rows (64 tokens x 4 heads for
-// a group of 4) of one request; its keys are walked in 64-key tiles.  The
-// workgroups are persistent: each owns an equal contiguous range of the
-// schedule's tiles, which may cover the end of one unit and the start of the
-// next (one segment per unit touched).  Each of the eight wavefronts owns 32
-// of the unit's rows and walks every key of the segment (two wavefronts per
-// SIMD, so one's softmax can overlap the other's matrix products); K and V
-// tiles are brought into LDS once per workgroup and shared by the eight
-// waves:
+// A unit is one KV head's GQA-packed rows of one request (a block of 256,
+// 128 or 64 rows: 64, 32 or 16 tokens x 4 heads for a group of 4); its keys
+// are walked in 64-key tiles.  The workgroups are persistent: each owns a
+// contiguous range of the schedule's tiles, which may cover the end of one
+// unit and the start of the next (one segment per unit touched).  The eight
+// wavefronts (two per SIMD, so one's softmax can overlap the other's matrix
+// products) split a unit two ways, by a template choice:
+//
+//   * 256-row units: each wavefront owns 32 rows and walks every key of the
+//     segment;
+//   * 128- and 64-row units: the wavefronts form two key groups of four; in
+//     each group a wavefront owns 32 (or 16) rows, and group g takes the
+//     32-key half g of every tile.  The two groups' online-softmax states of
+//     a row are merged through LDS at the end of the segment.
+//
+// K and V tiles are brought into LDS once per workgroup and shared by the
+// eight waves:
 //
 //   * the tiles are loaded straight from global memory into a four-stage
 //     LDS ring with 16-byte direct-to-LDS loads (each wave issues an eighth
@@ -38,6 +46,16 @@
 // The running row maximum is raised lazily (only when a score exceeds it by
 // more than 2^kTau), so the rescale of O and l and the cross-lane reduction
 // are off the common path.
+//
+// A unit cut into several segments stores one partial result per segment
+// (O / l in bf16, (m, l) in float).  The partials are merged either by the
+// combine launch that follows, or, by the schedule's choice, inside the same
+// launch: each segment then stores its partial with agent-coherent stores,
+// waits for them, and increments the unit's arrival counter; the workgroup
+// that arrives last reads every segment's partial back with agent-coherent
+// loads and writes the unit's output and LSE.  The counter wraps to zero on
+// the last arrival, so a counter array that starts at zero is left at zero
+// by every launch.
 #include <algorithm>
 #include <type_traits>
 
@@ -50,8 +68,6 @@ namespace attn {
 namespace {
 
 constexpr int kWaves = 8;
-constexpr int kRT = 2;                    // 16-row tiles per wave
-constexpr int kRB = kWaves * kRT * 16;    // GQA rows per workgroup
 constexpr int kTile = 64;                 // keys per LDS stage
 constexpr int kStages = 4;
 // Rescale threshold of the online softmax, in log2 units: p = 2^(s - m)
@@ -69,12 +85,156 @@ struct Smem {
     static constexpr int bytes = base + kStages * stage;
 };
 
+// Shape of a unit: kRT 16-row tiles per wavefront and kKG key groups; the
+// wavefronts of a group own kRB rows between them.
+template <int kRT_, int kKG_>
+struct Shape {
+    static constexpr int kRT = kRT_;
+    static constexpr int kKG = kKG_;
+    static constexpr int kRW = kWaves / kKG;        // wavefronts per key group
+    static constexpr int kRB = kRW * kRT * 16;      // GQA rows per unit
+    static constexpr bool kMergeInLaunch = kKG == 2;
+    static_assert(kKG == 1 || kKG == 2, "one or two key groups");
+    static_assert(kRT == 1 || kRT == 2, "one or two row tiles per wavefront");
+};
+
+// 8-byte loads and stores coherent at agent scope (they bypass the
+// non-coherent caches), for the partials one workgroup writes and another,
+// possibly on another XCD, reads in the same launch.
+__device__ __forceinline__ void store_agent(void* p, uint32_t lo, uint32_t hi) {
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(p), ((uint64_t)hi << 32) | lo,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint2 load_agent(const void* p) {
+    const uint64_t v = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<void*>(p)),
+                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return uint2{(uint32_t)v, (uint32_t)(v >> 32)};
+}
+
+// 16-byte loads coherent at agent scope, through a buffer resource over the
+// partials (sc1: they do not take stale lines from a non-coherent cache);
+// plain loads to the compiler, so a batch of them goes out together.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base) {
+    // descriptor word 3 of gfx9 buffer resources (32-bit data format)
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ uint4 load_coherent16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16);
+    return uint4{v.x, v.y, v.z, v.w};
+#else
+    return uint4{0u, 0u, 0u, 0u};
+#endif
+}
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint2 load_coherent8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 16);
+    return uint2{v.x, v.y};
+#else
+    return uint2{0u, 0u};
+#endif
+}
+
+// The last-arriving workgroup of a split unit merges its partials: rows
+// [0, rows) of the unit, each with nseg partials from entry part * kRB +
+// row * nseg on (O / l bf16, (m, l) float).  A row is handled by LPS = D / 8
+// lanes, each holding 16 bytes (8 dims) of every partial vector; the
+// workgroup's lane groups take RPP rows per pass, P passes.  The segments
+// are taken in chunks of SC, each chunk's loads for every pass issued
+// together (at most 32 vectors per lane in flight) before any is used; a
+// row's state (running maximum M, sum L, 8 accumulators) carries across
+// chunks.  out = sum_s w_s (O/l)_s / sum_s w_s, w_s = 2^(m_s - M) l_s; the
+// running maximum starts finite, so a segment that saw no key of a row
+// weighs 0.
+template <int D, int kRB>
+__device__ void merge_unit(const KParams& p, int part, int rows, int nseg, int h, int rho0,
+                           int n0) {
+    constexpr int LPS = D / 8;                     // lanes per row
+    constexpr int RPP = 64 * kWaves / LPS;         // rows per pass of the workgroup
+    constexpr int P = (kRB + RPP - 1) / RPP;       // passes
+    constexpr int SC = (32 / P < LPS) ? 32 / P : LPS;   // segments per chunk
+    static_assert(SC >= 1 && P * SC <= 32, "merge chunk");
+    const int lane = threadIdx.x & 63;
+    const int grp = threadIdx.x / LPS, gl = threadIdx.x % LPS;
+    const int lane0 = lane & ~(LPS - 1);           // first lane of this row's group
+    const __amdgpu_buffer_rsrc_t ro = coherent_rsrc(p.part_o);
+    const __amdgpu_buffer_rsrc_t rm = coherent_rsrc(p.part_ml);
+    float M[P], L[P], acc[P][8];
+    int64_t base[P];
+#pragma unroll
+    for (int k = 0; k < P; ++k) {
+        const int r = min(grp + RPP * k, rows - 1);   // in-bounds addresses for spare lanes
+        base[k] = (int64_t)part * kRB + (int64_t)r * nseg;
+        M[k] = kNoMax;
+        L[k] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[k][e] = 0.f;
+    }
+    for (int cb = 0; cb < nseg; cb += SC) {
+        const int nb = min(SC, nseg - cb);
+        uint4 v[P][SC];
+        uint2 mine[P];
+#pragma unroll
+        for (int k = 0; k < P; ++k) {
+            if (k * RPP >= rows) continue;            // uniform: no row of this pass
+            mine[k] = load_coherent8(rm, (uint32_t)((base[k] + cb + min(gl, nb - 1)) * 8));
+#pragma unroll
+            for (int i = 0; i < SC; ++i)
+                v[k][i] = i < nb ? load_coherent16(ro, (uint32_t)(((base[k] + cb + i) * D + 8 * gl) * 2))
+                                 : uint4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int k = 0; k < P; ++k) {
+            if (k * RPP >= rows) continue;
+            const float mm = __uint_as_float(mine[k].x), ll = __uint_as_float(mine[k].y);
+            float mb = gl < nb ? mm : kNoMax;
+#pragma unroll
+            for (int off = 1; off < LPS; off *= 2) mb = fmaxf(mb, __shfl_xor(mb, off));
+            const float Mn = fmaxf(M[k], mb);
+            const float a = __builtin_amdgcn_exp2f(M[k] - Mn);
+            const float w_mine = gl < nb ? __builtin_amdgcn_exp2f(mm - Mn) * ll : 0.f;
+            float ws = w_mine;
+#pragma unroll
+            for (int off = 1; off < LPS; off *= 2) ws += __shfl_xor(ws, off);
+            L[k] = L[k] * a + ws;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[k][e] *= a;
+#pragma unroll
+            for (int i = 0; i < SC; ++i) {
+                const float w = __shfl(w_mine, lane0 + i);   // 0 past the chunk's last segment
+                float x[8];
+                unpack16<bf16_t>(v[k][i], x);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[k][e] += w * x[e];
+            }
+            M[k] = Mn;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < P; ++k) {
+        const int r = grp + RPP * k;
+        if (r >= rows) continue;
+        const int rho = rho0 + r;
+        const int64_t orow =
+            (int64_t)(n0 + rho / p.group) * p.n_q_heads + h * p.group + rho % p.group;
+        const float inv = 1.f / L[k];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[k][e] *= inv;
+        *reinterpret_cast<uint4*>(reinterpret_cast<bf16_t*>(p.out) + orow * D + 8 * gl) =
+            pack16<bf16_t>(acc[k]);
+        if (p.lse && gl == 0) p.lse[orow] = (M[k] + log2f(L[k])) * kLn2;
+    }
+}
+
 // One segment of a unit: tiles [tile_a, tile_b) of the key range of KV head
 // h's rows [rho0, rho0 + rows) of request s, from its schedule record.
 // Every early return is uniform over the workgroup.
-template <int D>
+template <int D, class S>
 __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem,
                                                const int4 (&rec)[4]) {
+    constexpr int kRT = S::kRT, kKG = S::kKG, kRW = S::kRW, kRB = S::kRB;
     constexpr int DT = D / 16;         // 16-dim tiles of O^T
     constexpr int DS = D / 32;         // 32-dim steps of S^T = K Q^T
     constexpr int KB = 4 * DS;         // 1 KB operand blocks of a K tile
@@ -85,7 +245,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
     const int s = rec[0].x, h = rec[0].y, rho0 = rec[0].z, rows = rec[0].w;
     const int tile_a = rec[1].x, tile_b = rec[1].y;
-    const int nseg = rec[1].z, seg_local = rec[1].w, part = rec[3].x;
+    const int nseg = rec[1].z, seg_local = rec[1].w, part = rec[3].x, unit = rec[3].z;
     const bool direct = nseg == 1;
     const int n0 = rec[2].x, Tc = rec[2].y;
     BlockKeys bk;
@@ -100,7 +260,8 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
-    const int rho_w = rho0 + wave * kRT * 16;      // first row of this wave
+    const int rw = wave % kRW, kg = wave / kRW;    // row wave and key group
+    const int rho_w = rho0 + rw * kRT * 16;        // first row of this wave
 
     const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
     const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
@@ -196,7 +357,8 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // queries' rotation (fused RoPE) runs while tile 0 is in flight.  Tiles 1
     // and 2 follow once tile 0 has arrived and its first products are
     // issued, so that when every workgroup starts at once tile 0 is not
-    // queued behind them (its products are what the loop waits for).
+    // queued behind them (its products are what the loop waits for; issuing
+    // tiles 1..3 with tile 0 measured no faster on any workload).
     int tok[kRT];
     QRow<D> qrow[kRT];
 #pragma unroll
@@ -276,18 +438,24 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         v_rel[dt] = key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
     }
 
-    // ---- pieces of a 32-key sub-tile (stage st, half h of its tile)
+    // ---- pieces of a 32-key sub-tile.  A sub-tile is addressed by the
+    // start of its K blocks (ks: half h of a stage's K area starts
+    // h * 2 * DS KB in) and of its V rows (vs: half h starts 32 h rows into
+    // the stage's V area).
+    auto k_sub = [&](const unsigned char* st, int h) { return st + h * 2 * DS * 1024; };
+    auto v_sub = [&](const unsigned char* st, int h) {
+        return st + Smem<D>::k_bytes + h * 32 * 2 * D;
+    };
 
     // one 16-key half kt of S^T = K Q^T
-    auto qk_half = [&](const unsigned char* st, auto h_const, auto kt_const,
-                       floatx4 (&sacc)[2][kRT]) {
-        constexpr int h = decltype(h_const)::value, kt = decltype(kt_const)::value;
+    auto qk_half = [&](const unsigned char* ks, auto kt_const, floatx4 (&sacc)[2][kRT]) {
+        constexpr int kt = decltype(kt_const)::value;
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) sacc[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) {
-            const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(
-                st + ((h * 2 + kt) * DS + ds) * 1024 + lane * 16));
+            const bf16x8 a = as_bf16x8(
+                *reinterpret_cast<const uint4*>(ks + (kt * DS + ds) * 1024 + lane * 16));
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt)
                 sacc[kt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qB[rt][ds],
@@ -340,37 +508,33 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
     // O^T += V^T P^T.  For a 16-lane block, the transpose read gives lane i
     // element i%4 of the 4-element rows supplied by lanes 4k + i/4 (k =
-    // 0..3); lane j therefore supplies key 32h + 16e + 4lg + j/4 (e: key
-    // half), dims 16dt + 4(j%4).., so that lane i receives keys 4lg+k (k =
-    // 0..3) of dim 16dt + i.  The sub-tile and key-half parts of the
-    // addresses are immediate offsets.
-    auto v_issue = [&](const unsigned char* st, auto h_const, uint2 (&vr)[DT][2]) {
-        constexpr int h = decltype(h_const)::value;
-        const uint32_t vt = lds_addr(st + Smem<D>::k_bytes);
+    // 0..3); lane j therefore supplies key 16e + 4lg + j/4 of the sub-tile
+    // (e: key half), dims 16dt + 4(j%4).., so that lane i receives keys
+    // 4lg+k (k = 0..3) of dim 16dt + i.  The key-half part of the addresses
+    // is an immediate offset.
+    auto v_issue = [&](const unsigned char* vs, uint2 (&vr)[DT][2]) {
+        const uint32_t vt = lds_addr(vs);
         uint32_t va[DT];
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) va[dt] = vt + v_rel[dt];
-        issue_vt<DT, 32 * h * 2 * D, (32 * h + 16) * 2 * D>(va, vr);
+        issue_vt<DT, 0, 16 * 2 * D>(va, vr);
     };
-    // One step of the pipeline: sub-tile `cur` (S in s_cur, keys from v0,
-    // values in half hc of stage stc) becomes P and is added to O, while the
-    // matrix cores compute S of the next sub-tile (half hn of stage stn) into
-    // s_nxt.  The online softmax works in base 2 on x = s * scale_log2 - m
-    // with a lazily raised maximum: the slow path (cross-lane maximum,
-    // rescale of O and l) runs only if some x exceeds kTau; the maximum is
-    // taken over x, the result of a fused multiply-add, so no NaN-quieting is
-    // needed in front of it.  P is packed to bf16 pairs; the row sum adds the
-    // rounded pairs (the weights the product uses) with dot products against
-    // (1, 1).
+    // One step of the pipeline: the current sub-tile (S in s_cur, keys from
+    // v0, values at vc) becomes P and is added to O, while the matrix cores
+    // compute S of the next sub-tile (K at kn) into s_nxt.  The online
+    // softmax works in base 2 on x = s * scale_log2 - m with a lazily raised
+    // maximum: the slow path (cross-lane maximum, rescale of O and l) runs
+    // only if some x exceeds kTau; the maximum is taken over x, the result of
+    // a fused multiply-add, so no NaN-quieting is needed in front of it.  P
+    // is packed to bf16 pairs; the row sum adds the rounded pairs (the
+    // weights the product uses) with dot products against (1, 1).
     //
-    // The vector work is written out in chunks, one per product of the next
-    // S (d-step ds, row tile rt), each chunk fenced by a scheduling barrier:
-    // a product occupies the matrix core for 16 cycles, during which the
-    // wave issues the chunk's independent vector instructions.
+    // The vector work is written out in chunks, one per matrix product, each
+    // chunk fenced by a scheduling barrier: a product occupies the matrix
+    // core for 16 cycles, during which the wave issues the chunk's
+    // independent vector instructions.
     auto step = [&](floatx4 (&s_cur)[2][kRT], floatx4 (&s_nxt)[2][kRT], int v0,
-                    const unsigned char* stc, auto hc, const unsigned char* stn, auto hn) {
-        constexpr int h_n = decltype(hn)::value;
-        static_assert(kRT == 2, "chunking assumes two row tiles");
+                    const unsigned char* vc, const unsigned char* kn) {
         mask(s_cur, v0);
 
         // K operands of the next sub-tile (both key halves)
@@ -379,21 +543,22 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int ds = 0; ds < DS; ++ds)
-                ka[kt][ds] = as_bf16x8(*reinterpret_cast<const uint4*>(
-                    stn + ((h_n * 2 + kt) * DS + ds) * 1024 + lane * 16));
+                ka[kt][ds] = as_bf16x8(
+                    *reinterpret_cast<const uint4*>(kn + (kt * DS + ds) * 1024 + lane * 16));
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt) s_nxt[kt][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
         // first half: products of key half 0, with x = s * c2 - m and the
-        // maxima (16 fused multiply-adds over the 2 * DS products)
+        // maxima (8 fused multiply-adds per row tile over the products)
         float x[kRT][8];
-        constexpr int NP = 2 * DS;                 // products per key half
-        constexpr int FPC = 16 / NP;               // multiply-adds per chunk
+        constexpr int NP = kRT * DS;               // products per key half
+        constexpr int FPC = 8 / DS;                // multiply-adds per chunk
+        static_assert(NP <= 8 && 8 % NP == 0, "chunking");
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const int ds = i / 2, rt = i % 2;
+            const int ds = i / kRT, rt = i % kRT;
             s_nxt[0][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[0][ds], qB[rt][ds],
                                                                    s_nxt[0][rt], 0, 0, 0);
 #pragma unroll
@@ -442,13 +607,13 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         for (int ds = 0; ds < DS; ++ds) asm volatile("" ::"v"(ka[1][ds]));
 #endif
         uint2 vr[DT][2];
-        v_issue(stc, hc, vr);
+        v_issue(vc, vr);
 
         // second half: products of key half 1 with row tile 0's weights
-        // (p = 2^x packed to bf16, and the row sums); then P V of row tile 0
-        // with row tile 1's weights; then P V of row tile 1.  Every product is
-        // paired with about one exponential, the vector work one product's
-        // 16 matrix-core cycles hide.
+        // (p = 2^x packed to bf16, and the row sums); then the P V products
+        // of each row tile with the next row tile's weights.  Every product
+        // is paired with about one exponential, the vector work one
+        // product's 16 matrix-core cycles hide.
         uint32_t pk[kRT][4];
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
         float e[kRT][8];
@@ -463,7 +628,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         constexpr int EB = 8 / NP;                 // row tile 0 weights per product
 #pragma unroll
         for (int i = 0; i < NP; ++i) {
-            const int ds = i / 2, rt = i % 2;
+            const int ds = i / kRT, rt = i % kRT;
             s_nxt[1][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[1][ds], qB[rt][ds],
                                                                    s_nxt[1][rt], 0, 0, 0);
 #pragma unroll
@@ -477,62 +642,87 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
             va_op[dt] = as_bf16x8(uint4{vr[dt][0].x, vr[dt][0].y, vr[dt][1].x, vr[dt][1].y});
-        const bf16x8 p0 = as_bf16x8(uint4{pk[0][0], pk[0][1], pk[0][2], pk[0][3]});
-        constexpr int EC = 8 / DT;                 // row tile 1 weights per product
+        constexpr int EC = 8 / DT;                 // next row tile's weights per product
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            o[dt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va_op[dt], p0, o[dt][0], 0, 0, 0);
+        for (int rt = 0; rt < kRT; ++rt) {
+            const bf16x8 pb = as_bf16x8(uint4{pk[rt][0], pk[rt][1], pk[rt][2], pk[rt][3]});
 #pragma unroll
-            for (int f = 0; f < EC; ++f) weights(1, dt * EC + f);
-            __builtin_amdgcn_sched_barrier(0);
+            for (int dt = 0; dt < DT; ++dt) {
+                o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va_op[dt], pb, o[dt][rt], 0,
+                                                                    0, 0);
+                if (rt + 1 < kRT) {
+#pragma unroll
+                    for (int f = 0; f < EC; ++f) weights(rt + 1, dt * EC + f);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
         }
-        const bf16x8 p1 = as_bf16x8(uint4{pk[1][0], pk[1][1], pk[1][2], pk[1][3]});
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-            o[dt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va_op[dt], p1, o[dt][1], 0, 0, 0);
     };
 
-    // ---- software pipeline over 32-key sub-tiles j = 0, 1, ... (tile j/2,
-    // half j%2).  Step j turns S of sub-tile j into P V while the matrix
-    // cores compute S of sub-tile j+1 (for the last sub-tile, a discarded
-    // product over the current stage).  The barrier that makes tile t+1
-    // visible sits before the odd step of tile t, after which the stage of
-    // tile t-1 (last read in step 2t-1) receives tile t+3.  The prologue
+    // ---- software pipeline over this wave's 32-key sub-tiles.  A step turns
+    // S of one sub-tile into P V while the matrix cores compute S of the
+    // wave's next sub-tile (for the last, a discarded product over the
+    // current stage).  With one key group a wave takes both halves of every
+    // tile (the barrier that makes tile t+1 visible sits before the step of
+    // half 1 of tile t); with two, group g takes half g of every tile (the
+    // barrier sits before the step of tile t).  After the barrier, the stage
+    // of tile t-1, last read before it, receives tile t+3.  The prologue
     // issues tiles 0..2 (1 and 2 after tile 0's barrier).
-    const int n_sub = (kend - kbeg + 31) / 32;
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
-    constexpr std::integral_constant<int, 0> H0{};
-    constexpr std::integral_constant<int, 1> H1{};
+    constexpr std::integral_constant<int, 0> K0{};
+    constexpr std::integral_constant<int, 1> K1{};
     wait_vm_all();
     __syncthreads();
 
-    // a step whose two sub-tiles are both dead for the wave is skipped; a
-    // step that runs on a dead sub-tile's never-computed S masks all of it
+    // a step whose current and next sub-tiles are both dead for the wave is
+    // skipped; a step that runs on a dead sub-tile's never-computed S masks
+    // all of it
+    const int h0 = kKG == 2 ? kg : 0;      // this wave's first half
     floatx4 s_a[2][kRT], s_b[2][kRT];
-    if (!dead(kbeg)) {
-        qk_half(stage_of(0), H0, H0, s_a);
-        qk_half(stage_of(0), H0, H1, s_a);
+    if (!dead(kbeg + 32 * h0)) {
+        qk_half(k_sub(stage_of(0), h0), K0, s_a);
+        qk_half(k_sub(stage_of(0), h0), K1, s_a);
     }
     if (n_tiles > 1) issue_tile(1);
     if (n_tiles > 2) issue_tile(2);
-    for (int t = 0; t < n_tiles; ++t) {
-        const unsigned char* st = stage_of(t);
-        const int j0 = 2 * t;
-        const int v0 = kbeg + 32 * j0;
-        // even step: sub-tile (t, 0) -> next (t, 1), same stage
-        if (!(dead(v0) && dead(v0 + 32))) step(s_a, s_b, v0, st, H0, st, H1);
-        if (j0 + 1 >= n_sub) break;
-        // odd step: sub-tile (t, 1) -> next (t+1, 0), behind tile t+1's barrier
-        const bool more = t + 1 < n_tiles;
-        if (more) {
-            // this wave's loads of tile t+1 are done when at most those of
-            // tile t+2 are outstanding
-            if (t + 2 < n_tiles) wait_vm<LPW>(); else wait_vm<0>();
-            __syncthreads();
-            if (t + 3 < n_tiles) issue_tile(t + 3);
+    // tile t+1 resident and visible, and the stage of tile t-1 refilled
+    auto next_tile_barrier = [&](int t) {
+        // this wave's loads of tile t+1 are done when at most those of
+        // tile t+2 are outstanding
+        if (t + 2 < n_tiles) wait_vm<LPW>(); else wait_vm<0>();
+        __syncthreads();
+        if (t + 3 < n_tiles) issue_tile(t + 3);
+    };
+    if constexpr (kKG == 1) {
+        const int n_sub = (kend - kbeg + 31) / 32;
+        for (int t = 0; t < n_tiles; ++t) {
+            const unsigned char* st = stage_of(t);
+            const int v0 = kbeg + 64 * t;
+            // half 0 of tile t -> half 1, same stage
+            if (!(dead(v0) && dead(v0 + 32))) step(s_a, s_b, v0, v_sub(st, 0), k_sub(st, 1));
+            if (2 * t + 1 >= n_sub) break;
+            // half 1 of tile t -> half 0 of tile t+1, behind its barrier
+            const bool more = t + 1 < n_tiles;
+            if (more) next_tile_barrier(t);
+            if (!(dead(v0 + 32) && dead(v0 + 64)))
+                step(s_b, s_a, v0 + 32, v_sub(st, 1), k_sub(more ? stage_of(t + 1) : st, 0));
         }
-        if (!(dead(v0 + 32) && dead(v0 + 64)))
-            step(s_b, s_a, v0 + 32, st, H1, more ? stage_of(t + 1) : st, H0);
+    } else {
+        // half kg of tile t -> half kg of tile t+1, behind its barrier (every
+        // wave takes every barrier, whether or not its steps run)
+        auto tile_step = [&](int t, floatx4 (&cur)[2][kRT], floatx4 (&nxt)[2][kRT]) {
+            const bool more = t + 1 < n_tiles;
+            if (more) next_tile_barrier(t);
+            const int v0 = kbeg + 64 * t + 32 * kg;
+            if (!(dead(v0) && dead(v0 + 64)))
+                step(cur, nxt, v0, v_sub(stage_of(t), kg),
+                     k_sub(stage_of(more ? t + 1 : t), kg));
+        };
+        for (int t = 0; t < n_tiles; t += 2) {
+            tile_step(t, s_a, s_b);
+            if (t + 1 >= n_tiles) break;
+            tile_step(t + 1, s_b, s_a);
+        }
     }
 
     // row sums: add the four lane groups that hold each row
@@ -542,40 +732,120 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         lsum[rt] += __shfl_xor(lsum[rt], 32);
     }
 
-    // each wave writes its own rows
+    // two key groups: group 1 hands its (m, l, O) of every row to group 0
+    // through LDS (in the ring, free once every wave has left the loop);
+    // lane (lg, lr) holds dims 16dt + 4lg.. of row 16rt + lr in both groups
+    if constexpr (kKG == 2) {
+        constexpr int OS = D + 4;                               // floats per row (bank skew)
+        float* xo = reinterpret_cast<float*>(smem + Smem<D>::base) + rw * kRT * 16 * OS;
+        float* xml = reinterpret_cast<float*>(smem + Smem<D>::base) + kRW * kRT * 16 * OS +
+                     rw * kRT * 16 * 2;
+        static_assert(kRW * kRT * 16 * (OS + 2) * 4 <= kStages * Smem<D>::stage, "merge area");
+        __syncthreads();
+        if (kg == 1) {
 #pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        if (tok[rt] < 0) continue;
-        const int rho = rho_w + 16 * rt + lr;
-        const int64_t orow = (int64_t)(n0 + tok[rt]) * p.n_q_heads + h * G + rho % G;
-        // the output, or this segment's partial: O / l in bf16 (0 for a row
-        // that saw no key of the segment) with (m, l) in float.  A unit's
-        // partials are row-major over its segments, so the combine reads one
-        // contiguous run per row.
-        const float inv = lsum[rt] > 0.f ? 1.f / lsum[rt] : 0.f;
-        const int64_t pi = (int64_t)part * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
-        bf16_t* dst = direct ? reinterpret_cast<bf16_t*>(p.out) + orow * D
-                             : reinterpret_cast<bf16_t*>(p.part_o) + pi * D;
+            for (int rt = 0; rt < kRT; ++rt) {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const floatx4 v = o[dt][rt];
-            *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
-                uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
+                for (int dt = 0; dt < DT; ++dt)
+                    *reinterpret_cast<floatx4*>(xo + (16 * rt + lr) * OS + 16 * dt + 4 * lg) =
+                        o[dt][rt];
+                if (lg == 0) {
+                    xml[(16 * rt + lr) * 2] = m[rt];
+                    xml[(16 * rt + lr) * 2 + 1] = lsum[rt];
+                }
+            }
         }
-        if (lg == 0) {
-            if (direct) {
-                if (p.lse) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
-            } else {
-                p.part_ml[pi * 2] = m[rt];
-                p.part_ml[pi * 2 + 1] = lsum[rt];
+        __syncthreads();
+        if (kg == 0) {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const float m1 = xml[(16 * rt + lr) * 2], l1 = xml[(16 * rt + lr) * 2 + 1];
+                const float M = fmaxf(m[rt], m1);
+                const float a0 = __builtin_amdgcn_exp2f(m[rt] - M);
+                const float a1 = __builtin_amdgcn_exp2f(m1 - M);
+                m[rt] = M;
+                lsum[rt] = lsum[rt] * a0 + l1 * a1;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+                    o[dt][rt] = o[dt][rt] * a0 +
+                                *reinterpret_cast<const floatx4*>(
+                                    xo + (16 * rt + lr) * OS + 16 * dt + 4 * lg) * a1;
             }
         }
     }
+
+    // the waves of key group 0 write their rows: the output, or this
+    // segment's partial (O / l in bf16, 0 for a row that saw no key of the
+    // segment, with (m, l) in float; a unit's partials are row-major over its
+    // segments, so the merge reads one contiguous run per row)
+    if (kg == 0) {
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            if (tok[rt] < 0) continue;
+            const int rho = rho_w + 16 * rt + lr;
+            const int64_t orow = (int64_t)(n0 + tok[rt]) * p.n_q_heads + h * G + rho % G;
+            const float inv = lsum[rt] > 0.f ? 1.f / lsum[rt] : 0.f;
+            if (direct) {
+                bf16_t* dst = reinterpret_cast<bf16_t*>(p.out) + orow * D;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const floatx4 v = o[dt][rt];
+                    *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
+                        uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
+                }
+                if (lg == 0 && p.lse) p.lse[orow] = (m[rt] + log2f(lsum[rt])) * kLn2;
+            } else {
+                const int64_t pi = (int64_t)part * kRB + (int64_t)(rho - rho0) * nseg + seg_local;
+                bf16_t* dst = reinterpret_cast<bf16_t*>(p.part_o) + pi * D;
+                if (S::kMergeInLaunch && p.merge_in_launch) {
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) {
+                        const floatx4 v = o[dt][rt];
+                        store_agent(dst + 16 * dt + 4 * lg, pack2(v[0] * inv, v[1] * inv),
+                                    pack2(v[2] * inv, v[3] * inv));
+                    }
+                    if (lg == 0)
+                        store_agent(p.part_ml + pi * 2, __float_as_uint(m[rt]),
+                                    __float_as_uint(lsum[rt]));
+                } else {
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) {
+                        const floatx4 v = o[dt][rt];
+                        *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * lg) =
+                            uint2{pack2(v[0] * inv, v[1] * inv), pack2(v[2] * inv, v[3] * inv)};
+                    }
+                    if (lg == 0) {
+                        p.part_ml[pi * 2] = m[rt];
+                        p.part_ml[pi * 2 + 1] = lsum[rt];
+                    }
+                }
+            }
+        }
+    }
+    // (256-row units always leave their partials to the combine launch: the
+    // merge's registers would crowd the eight-wavefront loop)
+    if constexpr (!S::kMergeInLaunch) return;
+    if (direct || !p.merge_in_launch) return;
+
+    // arrival: every partial store of the workgroup has completed (each wave
+    // waits for its own, then the barrier), then one increment of the unit's
+    // counter; it wraps to 0 when the last segment arrives, which merges
+    wait_vm_all();
+    __syncthreads();
+    int* flag = reinterpret_cast<int*>(smem);     // below the ring
+    if (threadIdx.x == 0) {
+        const unsigned old = __builtin_amdgcn_atomic_inc32(p.counters + unit, (unsigned)(nseg - 1),
+                                                           __ATOMIC_RELAXED, "agent");
+        *flag = old == (unsigned)(nseg - 1);
+    }
+    __syncthreads();
+    const bool last = *flag != 0;
+    if (last) merge_unit<D, kRB>(p, part, rows, nseg, h, rho0, n0);
 }
 
 // A persistent workgroup runs its chain of segments of the schedule: record
 // blockIdx.x first, then the records its `next` fields name.
-template <int D>
+template <int D, class S>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
     for (int g = blockIdx.x, first = 1; g >= 0 && g < p.n_segments; first = 0) {
@@ -584,21 +854,35 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         if (!record_ok(p, rec, g)) break;
         // the previous segment's waves are done with every LDS stage
         if (!first) __syncthreads();
-        attend_segment<D>(p, smem, rec);
+        attend_segment<D, S>(p, smem, rec);
         g = rec[3].y;
     }
 }
 
+template <int D>
+void launch_d(const KParams& p, int n_wg, hipStream_t stream) {
+    const dim3 grid(n_wg), block(64 * kWaves);
+    if (p.row_block == Shape<2, 1>::kRB)
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 1>>), grid, block, 0, stream, p);
+    else if (p.row_block == Shape<2, 2>::kRB)
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 2>>), grid, block, 0, stream, p);
+    else
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<1, 2>>), grid, block, 0, stream, p);
+}
+
 }  // namespace
 
-int attend_mfma_row_block() { return kRB; }
+bool attend_mfma_row_block_ok(int row_block) {
+    return row_block == Shape<2, 1>::kRB || row_block == Shape<2, 2>::kRB ||
+           row_block == Shape<1, 2>::kRB;
+}
 
 hipError_t launch_attend_mfma(int head_dim, const KParams& p, int n_wg, hipStream_t stream) {
-    const dim3 grid(n_wg);
+    if (!attend_mfma_row_block_ok(p.row_block)) return hipErrorInvalidValue;
     if (head_dim == 128)
-        hipLaunchKernelGGL(attend_mfma_kernel<128>, grid, dim3(64 * kWaves), 0, stream, p);
+        launch_d<128>(p, n_wg, stream);
     else
-        hipLaunchKernelGGL(attend_mfma_kernel<64>, grid, dim3(64 * kWaves), 0, stream, p);
+        launch_d<64>(p, n_wg, stream);
     return hipGetLastError();
 }
 

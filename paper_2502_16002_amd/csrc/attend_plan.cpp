@@ -66,53 +66,97 @@ struct Seg {
 
 struct CostModel {
     // a segment costs per_segment_us + first_us * (live fraction of its first
-    // tile); a tile tile_us + live_us * (live fraction) + mask_us * (masked
-    // fraction)
-    double per_segment_us, first_us, tile_us, live_us, mask_us, combine_us, combine_bytes_per_us;
+    // tile), plus split_us when its unit has several segments; a tile
+    // tile_us + live_us * (live fraction) + mask_us * (masked fraction)
+    double per_segment_us, first_us, tile_us, live_us, mask_us;
+    double split_us;
     int slots_per_cu;
     // the RoPE and append of the new keys a segment reads (inside the split
     // launch), per 64 new rows
     double append_us;
+    // split units merged in the launch (merge_bytes_per_us > 0): the slowest
+    // last-arriving workgroup's merge follows, merge_us plus the unit's
+    // partial bytes at merge_bytes_per_us; else by the combine launch:
+    // combine_us plus all partial bytes, written and read, at
+    // combine_bytes_per_us
+    double merge_us, merge_bytes_per_us, combine_us, combine_bytes_per_us;
 };
 
-// Wide-block kernel: fitted jointly to per-workgroup timelines of the 10-
-// and 40-document workloads.  A tile costs its stream of K and V (about
-// 1.6 us at the share of HBM a workgroup gets while all stream) plus its
-// products, which scale with the fraction of (wavefront, 32-key step) pairs
-// that are live: a wavefront skips a step none of its rows sees (link tokens
-// see only the documents before them), but the workgroup still streams the
-// tile.  A live step that some row of the wavefront sees only in part (it
-// runs the mask) costs about four times one seen whole.  A segment adds its
-// record and, for its first tile, the products that wait for the tile's
-// loads instead of overlapping them.  A segment whose keys include new rows
-// first rotates and appends them, one round of loads and stores per 64 rows
-// (about 0.9 us each).  The combine costs about 6 us plus its partial
-// traffic, written and read back at an effective ~6 TB/s.  Decode kernel: two
-// workgroups per compute unit sharing the unit's HBM stream, so a tile (64
-// keys of K and V) costs its bytes at an eighth of a compute unit's share of
-// ~6 TB/s, plus the start of a segment (its first loads' latency).  VALU
-// kernel: fp32, a fixed cost per tile.
-CostModel cost_model(AttendPath path, int head_dim) {
+// Constants fitted to per-workgroup timelines (probe builds stamping each
+// workgroup's phases with the 100 MHz real-time counter) of the Llama-8B
+// workloads on MI355X.
+//
+// Wide kernel, 256-row units (fitted jointly on the 10- and 40-document
+// workloads): a tile costs its stream of K and V (about 1.6 us at the share
+// of HBM a workgroup gets while all stream) plus its products, which scale
+// with the fraction of (wavefront, 32-key step) pairs that are live: a
+// wavefront skips a step none of its rows sees (link tokens see only the
+// documents before them), but the workgroup still streams the tile.  A live
+// step that some row of the wavefront sees only in part (it runs the mask)
+// costs about four times one seen whole.  A segment adds its record and, for
+// its first tile, the products that wait for the tile's loads.  A segment
+// whose keys include new rows first rotates and appends them, one round of
+// loads and stores per 64 rows (about 0.9 us each).
+//
+// 128- and 64-row units: a segment's record and prologue (queries and the
+// first tile) take about 5.1 and 3.6 us; a tile about 1.5 and 1.1 us when all
+// its steps are live.  A split segment merged in the launch adds its
+// partial's coherent stores and the arrival (about 4.2 and 2.6 us; 3 us for
+// 256 rows); the last arrival's merge reads the unit's partials at about
+// 0.1 MB/us after 2 us.  Merged by the combine launch instead, a split
+// segment's partial stores add about 1.5 us and the combine about 6 us plus
+// the partial traffic at an effective ~6 TB/s.
+//
+// Decode kernel: two workgroups per compute unit sharing the unit's HBM
+// stream, so a tile (64 keys of K and V) costs its bytes at an eighth of a
+// compute unit's share of ~6 TB/s, plus the start of a segment (its first
+// loads' latency).  VALU kernel: fp32, a fixed cost per tile.
+CostModel cost_model(AttendPath path, int head_dim, int row_block, bool in_launch) {
     const bool d128 = head_dim == 128;
     const double f = d128 ? 1.0 : 0.63;   // head_dim 64: fewer bytes and products per key
-    if (path == kPathWide)
-        return {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 6.0, 6.0e6, 1, 0.9 * f};
-    if (path == kPathDecode) return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 6.0, 6.0e6, 2, 0.0};
-    return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 4.0, 6.0e6, d128 ? 2 : 4, 0.0};
+    CostModel cm;
+    if (path == kPathWide) {
+        if (row_block == 256)
+            cm = {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
+        else if (row_block == 128)
+            cm = {5.1, 0.0, 0.9 * f, 0.6 * f, 0.5 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
+        else
+            cm = {3.6, 0.0, 0.7 * f, 0.4 * f, 0.3 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
+        if (in_launch) {
+            cm.split_us = row_block == 256 ? 3.0 : row_block == 128 ? 4.2 : 2.6;
+            cm.merge_us = 2.0;
+            cm.merge_bytes_per_us = 1.0e5;
+        } else {
+            cm.split_us = row_block == 256 ? 0.0 : 1.5;
+            cm.combine_us = 6.0;
+            cm.combine_bytes_per_us = 6.0e6;
+        }
+        return cm;
+    }
+    if (path == kPathDecode)
+        return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 0.0, 2, 0.0, 0, 0, 6.0, 6.0e6};
+    return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 0.0, d128 ? 2 : 4, 0.0, 0, 0, 4.0, 6.0e6};
 }
 
 // Live (wavefront, 32-key step) pairs of tile t of a wide-kernel unit, by the
-// rule the kernel skips a step with: step j of wavefront w is dead when none
-// of the wavefront's rows sees a key of sub-tiles j or j+1 (32 rows per
-// wavefront, eight wavefronts); *masked counts the live pairs whose
-// sub-tile is not wholly below the wavefront's smallest visible prefix.
-int live_pairs(const Unit& x, int t, int group, const int32_t* new_visible, int* masked) {
+// rule the kernel skips a step with.  The unit's rows are split over kRW row
+// wavefronts of rpw rows (kRW * rpw = row block); with one key group a
+// wavefront takes both 32-key halves of the tile and skips the step of half
+// j when neither that half nor the next one it would compute is seen by any
+// of its rows; with two, the wavefronts of group j take half j and the next
+// half they compute is 64 keys on.  Returns the live pairs out of 2 * kRW;
+// *masked counts the live ones whose half is not wholly below the
+// wavefront's smallest visible prefix.
+int live_pairs(const Unit& x, int t, int group, int row_block, const int32_t* new_visible,
+               int* masked) {
+    const int kg = row_block == 256 ? 1 : 2;
+    const int rw_n = 8 / kg, rpw = row_block / rw_n;
     int cnt = 0;
     *masked = 0;
-    for (int w = 0; w < 8; ++w) {
-        const int rw = x.rho0 + 32 * w;
+    for (int w = 0; w < rw_n; ++w) {
+        const int rw = x.rho0 + rpw * w;
         if (rw >= x.rho0 + x.rows) continue;
-        const int tok_max = (std::min(rw + 32, x.rho0 + x.rows) - 1) / group;
+        const int tok_max = (std::min(rw + rpw, x.rho0 + x.rows) - 1) / group;
         const int vis_max = new_visible[x.n0 + tok_max];
         const int vis_min = new_visible[x.n0 + rw / group];
         auto dead = [&](int64_t v0) {
@@ -123,7 +167,7 @@ int live_pairs(const Unit& x, int t, int group, const int32_t* new_visible, int*
         };
         for (int j = 0; j < 2; ++j) {
             const int64_t v0 = (int64_t)kTileKeys * t + 32 * j;
-            if (!(dead(v0) && dead(v0 + 32))) {
+            if (!(dead(v0) && dead(v0 + 32 * kg))) {
                 ++cnt;
                 if (v0 + 32 > vis_min) ++*masked;
             }
@@ -258,33 +302,79 @@ int used_workgroups(const std::vector<Seg>& segs) {
 
 double estimate_us(const std::vector<Unit>& units, const std::vector<Seg>& segs,
                    const CostModel& cm, int head_dim, int elem) {
-    std::vector<double> wg(used_workgroups(segs), 0.0);
     std::vector<int> pieces(units.size(), 0);
-    for (const Seg& g : segs) {
+    for (const Seg& g : segs) ++pieces[g.u];
+    std::vector<double> wg(used_workgroups(segs), 0.0);
+    for (const Seg& g : segs)
         wg[g.w] += cm.per_segment_us + cm.first_us * units[g.u].live[g.t0] +
-                   units[g.u].cost(g.t0, g.len);
-        ++pieces[g.u];
-    }
+                   units[g.u].cost(g.t0, g.len) + (pieces[g.u] > 1 ? cm.split_us : 0.0);
     double t = *std::max_element(wg.begin(), wg.end());
+    const double row_bytes = head_dim * elem + 8.0;
+    if (cm.merge_bytes_per_us > 0.0) {
+        double merge = 0.0;
+        for (size_t u = 0; u < units.size(); ++u)
+            if (pieces[u] > 1)
+                merge = std::max(merge, cm.merge_us + pieces[u] * units[u].rows * row_bytes /
+                                                          cm.merge_bytes_per_us);
+        return t + merge;
+    }
     double bytes = 0.0;
     for (size_t u = 0; u < units.size(); ++u)
-        if (pieces[u] > 1)
-            bytes += 2.0 * pieces[u] * units[u].rows * (head_dim * elem + 8.0);   // write + read
+        if (pieces[u] > 1) bytes += 2.0 * pieces[u] * units[u].rows * row_bytes;   // write + read
     if (bytes > 0.0) t += cm.combine_us + bytes / cm.combine_bytes_per_us;
     return t;
+}
+
+// XCD-aware numbering: workgroup w of a launch runs on XCD w % kXcds on
+// MI355X, and the XCDs have separate L2 caches.  Workgroups whose first
+// segment belongs to the same (request, KV head) are given ids on one XCD
+// where the ids allow, so that they share that KV head's keys and values and
+// the unit's queries through one L2.
+constexpr int kXcds = 8;
+void number_by_xcd(const std::vector<Unit>& units, int n_kv_heads, std::vector<Seg>* segs) {
+    const int n = used_workgroups(*segs);
+    // the workgroup's first segment in (unit, tile) order decides
+    std::vector<int> pref(n, 0);
+    std::vector<int64_t> first_t(n, INT64_MAX);
+    for (const Seg& g : *segs) {
+        const int64_t key = (int64_t)g.u << 32 | g.t0;
+        if (key < first_t[g.w]) {
+            first_t[g.w] = key;
+            pref[g.w] = (units[g.u].s * n_kv_heads + units[g.u].h) % kXcds;
+        }
+    }
+    std::vector<std::vector<int>> free_ids(kXcds);
+    for (int id = n - 1; id >= 0; --id) free_ids[id % kXcds].push_back(id);   // smallest last
+    std::vector<int> new_id(n, -1), deferred;
+    for (int w = 0; w < n; ++w) {
+        auto& f = free_ids[pref[w]];
+        if (!f.empty()) {
+            new_id[w] = f.back();
+            f.pop_back();
+        } else {
+            deferred.push_back(w);
+        }
+    }
+    std::vector<int> rest;
+    for (int x = 0; x < kXcds; ++x)
+        for (int id : free_ids[x]) rest.push_back(id);
+    std::sort(rest.begin(), rest.end());
+    for (size_t i = 0; i < deferred.size(); ++i) new_id[deferred[i]] = rest[i];
+    for (Seg& g : *segs) g.w = new_id[g.w];
 }
 
 }  // namespace
 
 AttendPath attend_path(kvlink_dtype dt, int group, int max_new) {
     if (dt != KVLINK_BF16) return kPathValu;
-    return (int64_t)group * max_new <= attend_row_block(kPathDecode) ? kPathDecode : kPathWide;
+    return (int64_t)group * max_new <= 16 ? kPathDecode : kPathWide;
 }
 
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                           int n_seqs, const int32_t* seq_new_ptr, const int32_t* seq_cached,
                           const int32_t* new_visible, int n_compute_units, int n_workgroups,
-                          std::vector<int32_t>* table, PlanCounts* counts, const char** why) {
+                          int row_block, unsigned flags, std::vector<int32_t>* table,
+                          PlanCounts* counts, const char** why) {
     const int group = n_q_heads / n_kv_heads;
     if (seq_new_ptr[0] != 0) {
         *why = "seq_new_ptr[0] must be 0";
@@ -309,91 +399,142 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
             return KVLINK_ERR_LAYOUT;
         }
     const AttendPath path = attend_path(dt, group, max_new);
-    const int rb = attend_row_block(path);
+    // row blocks to consider: the wide kernel's three unit shapes, or the
+    // 16-row units of the decode and vector kernels
+    std::vector<int> rbs;
+    if (path == kPathWide) rbs = {256, 128, 64};
+    else rbs = {16};
+    if (row_block != 0) {
+        if (!attend_row_block_ok(path, row_block)) {
+            *why = "row_block is not one of this batch's kernel (wide: 256, 128, 64; else 16)";
+            return KVLINK_ERR_UNSUPPORTED;
+        }
+        rbs = {row_block};
+    }
+    const int elem = dt == KVLINK_BF16 ? 2 : 4;
+    // merge of split units: in the split launch (wide kernel only) or by the
+    // combine launch; the flags may force one
+    std::vector<bool> modes;
+    if (path != kPathWide || (flags & KVLINK_PLAN_COMBINE)) modes = {false};
+    else if (flags & KVLINK_PLAN_IN_LAUNCH) modes = {true};
+    else modes = {true, false};
+    if ((flags & KVLINK_PLAN_IN_LAUNCH) && row_block == 256) {
+        *why = "256-row units merge by the combine launch only";
+        return KVLINK_ERR_UNSUPPORTED;
+    }
 
     std::vector<Unit> units;
-    for (int s = 0; s < n_seqs; ++s) {
-        const int n0 = seq_new_ptr[s];
-        const int rows_s = (seq_new_ptr[s + 1] - n0) * group;
-        for (int h = 0; h < n_kv_heads; ++h)
-            for (int rho0 = 0; rho0 < rows_s; rho0 += rb) {
-                const int rows = std::min(rb, rows_s - rho0);
-                const int r_last = (rho0 + rows - 1) / group;
-                const int vis = new_visible[n0 + r_last];
-                const int64_t nvirt = (int64_t)vis + r_last + 1;
-                if (nvirt > INT32_MAX / 2) {
-                    *why = "key range too long";
-                    return KVLINK_ERR_LAYOUT;
+    std::vector<Seg> segs;
+    int rb = rbs[0];
+    bool in_launch = false;
+    double best_rb_est = 1e300;
+    for (int cand_rb : rbs)
+      for (bool mode : modes) {
+        if (mode && cand_rb == 256) continue;   // 256-row units: combine launch only
+        const CostModel cm = cost_model(path, head_dim, cand_rb, mode);
+        std::vector<Unit> us;
+        for (int s = 0; s < n_seqs; ++s) {
+            const int n0 = seq_new_ptr[s];
+            const int rows_s = (seq_new_ptr[s + 1] - n0) * group;
+            for (int h = 0; h < n_kv_heads; ++h)
+                for (int rho0 = 0; rho0 < rows_s; rho0 += cand_rb) {
+                    const int rows = std::min(cand_rb, rows_s - rho0);
+                    const int r_last = (rho0 + rows - 1) / group;
+                    const int vis = new_visible[n0 + r_last];
+                    const int64_t nvirt = (int64_t)vis + r_last + 1;
+                    if (nvirt > INT32_MAX / 2) {
+                        *why = "key range too long";
+                        return KVLINK_ERR_LAYOUT;
+                    }
+                    us.push_back({s, h, rho0, (int)((nvirt + kTileKeys - 1) / kTileKeys), rows,
+                                  n0, seq_cached[s], vis, (int)nvirt, {}});
                 }
-                units.push_back({s, h, rho0, (int)((nvirt + kTileKeys - 1) / kTileKeys), rows, n0,
-                                 seq_cached[s], vis, (int)nvirt, {}});
-            }
-    }
-    int64_t T = 0;
-    for (const Unit& x : units) T += x.tiles;
-    const CostModel cm = cost_model(path, head_dim);
-    for (Unit& x : units) {
-        x.prefix.assign((size_t)x.tiles + 1, 0.0);
-        x.live.assign((size_t)x.tiles, 1.0f);
-        for (int t = 0; t < x.tiles; ++t) {
-            int masked = 0;
-            const int live = path == kPathWide ? live_pairs(x, t, group, new_visible, &masked) : 16;
-            x.live[t] = (float)(live / 16.0);
-            const int64_t new_rows =
-                std::max<int64_t>(0, std::min<int64_t>(x.nvirt, (int64_t)kTileKeys * (t + 1)) -
-                                         std::max<int64_t>(x.cmax, (int64_t)kTileKeys * t));
-            x.prefix[t + 1] = x.prefix[t] + cm.tile_us + cm.live_us * live / 16.0 +
-                              cm.mask_us * masked / 16.0 + cm.append_us * new_rows / kTileKeys;
         }
-    }
+        if ((int64_t)us.size() > kMaxUnits) continue;   // too many for the merge counters
+        int64_t T = 0;
+        for (const Unit& x : us) T += x.tiles;
+        for (Unit& x : us) {
+            x.prefix.assign((size_t)x.tiles + 1, 0.0);
+            x.live.assign((size_t)x.tiles, 1.0f);
+            const int pairs = path == kPathWide ? (cand_rb == 256 ? 16 : 8) : 16;
+            for (int t = 0; t < x.tiles; ++t) {
+                int masked = 0;
+                const int live = path == kPathWide
+                                     ? live_pairs(x, t, group, cand_rb, new_visible, &masked)
+                                     : pairs;
+                const double lf = (double)live / pairs, mf = (double)masked / pairs;
+                x.live[t] = (float)lf;
+                const int64_t new_rows =
+                    std::max<int64_t>(0, std::min<int64_t>(x.nvirt, (int64_t)kTileKeys * (t + 1)) -
+                                             std::max<int64_t>(x.cmax, (int64_t)kTileKeys * t));
+                x.prefix[t + 1] = x.prefix[t] + cm.tile_us + cm.live_us * lf + cm.mask_us * mf +
+                                  cm.append_us * new_rows / kTileKeys;
+            }
+        }
 
-    std::vector<Seg> segs, cand;
-    if (T > 0) {
-        const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
-        // every cut's estimate, then the cut that keeps the most workgroups
-        // busy among those within kNearTie of the best estimate: the
-        // estimate leaves out the launch and prologue costs that do not
-        // shrink with more workgroups, and measured near ties favour filling
-        // every compute unit
-        constexpr double kNearTie = 0.02;
-        struct Est {
-            double t;
-            int c, way, used;
-        };
-        std::vector<Est> est;
-        auto cut = [&](int c, int way) {
-            cand.clear();
-            if (way == 0) cut_unit_aligned(units, c, &cand);
-            else cut_equal_ranges(units, c, &cand);
-        };
-        auto consider = [&](int c, bool any_cost) {
-            for (int way = 0; way < 2; ++way) {
-                cut(c, way);
-                const int used = compact_workgroups(&cand);
-                // a forced count takes only cuts that use every workgroup
-                if (used < c && any_cost) continue;
-                est.push_back({estimate_us(units, cand, cm, head_dim, dt == KVLINK_BF16 ? 2 : 4), c,
-                               way, used});
+        std::vector<Seg> best_segs, cand;
+        double best_est = 1e300;
+        if (T > 0) {
+            const int64_t max_n = std::min<int64_t>(T, (int64_t)cm.slots_per_cu * n_compute_units);
+            // every cut's estimate, then the cut that keeps the most
+            // workgroups busy among those within kNearTie of the best
+            // estimate: the estimate leaves out the launch and prologue costs
+            // that do not shrink with more workgroups, and measured near ties
+            // favour filling every compute unit
+            constexpr double kNearTie = 0.02;
+            struct Est {
+                double t;
+                int c, way, used;
+            };
+            std::vector<Est> est;
+            auto cut = [&](int c, int way) {
+                cand.clear();
+                if (way == 0) cut_unit_aligned(us, c, &cand);
+                else cut_equal_ranges(us, c, &cand);
+            };
+            auto consider = [&](int c, bool any_cost) {
+                for (int way = 0; way < 2; ++way) {
+                    cut(c, way);
+                    const int used = compact_workgroups(&cand);
+                    // a forced count takes only cuts that use every workgroup
+                    if (used < c && any_cost) continue;
+                    est.push_back({estimate_us(us, cand, cm, head_dim, elem), c, way, used});
+                }
+            };
+            if (n_workgroups > 0) {
+                consider((int)std::min<int64_t>(n_workgroups, T), true);
+            } else {
+                for (int c = 1; c <= max_n; ++c) consider(c, false);
             }
-        };
-        if (n_workgroups > 0) {
-            consider((int)std::min<int64_t>(n_workgroups, T), true);
+            double best = 1e300;
+            for (const Est& e : est) best = std::min(best, e.t);
+            const Est* pick = nullptr;
+            for (const Est& e : est)   // most workgroups, then lowest estimate, then unit-aligned
+                if (e.t <= best * (1.0 + kNearTie) &&
+                    (!pick || e.used > pick->used || (e.used == pick->used && e.t < pick->t)))
+                    pick = &e;
+            if (pick) {
+                cut(pick->c, pick->way);
+                compact_workgroups(&cand);
+                best_segs = cand;
+                best_est = pick->t;
+            }
         } else {
-            for (int c = 1; c <= max_n; ++c) consider(c, false);
+            best_est = 0.0;
         }
-        double best = 1e300;
-        for (const Est& e : est) best = std::min(best, e.t);
-        const Est* pick = nullptr;
-        for (const Est& e : est)   // most workgroups, then lowest estimate, then unit-aligned
-            if (e.t <= best * (1.0 + kNearTie) &&
-                (!pick || e.used > pick->used || (e.used == pick->used && e.t < pick->t)))
-                pick = &e;
-        if (pick) {
-            cut(pick->c, pick->way);
-            compact_workgroups(&cand);
-            segs = cand;
+        if (best_est < best_rb_est) {
+            best_rb_est = best_est;
+            rb = cand_rb;
+            in_launch = mode;
+            units = std::move(us);
+            segs = std::move(best_segs);
         }
+      }
+    if (best_rb_est == 1e300) {
+        *why = "more units than the merge counters hold";
+        return KVLINK_ERR_UNSUPPORTED;
     }
+    if ((flags & KVLINK_PLAN_XCD) && !segs.empty()) number_by_xcd(units, n_kv_heads, &segs);
     const int n = used_workgroups(segs);
 
     // segments per unit, in tile order, and the unit-order numbering used
@@ -436,6 +577,7 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
     counts->n_units = (int)units.size();
     counts->n_segments = n_seg;
     counts->row_block = rb;
+    counts->in_launch = in_launch;
     std::vector<int32_t> split;
     for (size_t u = 0; u < units.size(); ++u)
         if (unit_seg[u + 1] - unit_seg[u] > 1) split.push_back((int32_t)u);

@@ -527,8 +527,8 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
                                       const int32_t* seq_new_ptr, const int32_t* seq_cached,
                                       const int32_t* new_visible,
                                       int32_t n_compute_units, int32_t n_workgroups,
-                                      int32_t* table, int64_t table_capacity,
-                                      kvlink_attend_plan* plan) {
+                                      int32_t row_block, uint32_t flags, int32_t* table,
+                                      int64_t table_capacity, kvlink_attend_plan* plan) {
     try {
         if (!dtype_ok(dtype)) return fail(KVLINK_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
         if (head_dim != 64 && head_dim != 128)
@@ -544,13 +544,18 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
                         "seq_new_ptr, seq_cached, new_visible and plan are required");
         if (n_compute_units < 1) return fail(KVLINK_ERR_INVALID_ARG, "n_compute_units must be >= 1");
         if (n_workgroups < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_workgroups must be >= 0");
+        if (row_block < 0) return fail(KVLINK_ERR_INVALID_ARG, "row_block must be >= 0");
+        if (flags & ~(uint32_t)(KVLINK_PLAN_XCD | KVLINK_PLAN_COMBINE | KVLINK_PLAN_IN_LAUNCH))
+            return fail(KVLINK_ERR_INVALID_ARG, "unknown plan flags 0x%x", (unsigned)flags);
+        if ((flags & KVLINK_PLAN_COMBINE) && (flags & KVLINK_PLAN_IN_LAUNCH))
+            return fail(KVLINK_ERR_INVALID_ARG, "KVLINK_PLAN_COMBINE and KVLINK_PLAN_IN_LAUNCH exclude each other");
         std::vector<int32_t> tab;
         kvlink::PlanCounts c;
         const char* why = "";
         const int st = kvlink::build_attend_schedule(dtype, n_q_heads, n_kv_heads, head_dim, n_seqs,
                                                      seq_new_ptr, seq_cached, new_visible,
-                                                     n_compute_units, n_workgroups,
-                                                     table ? &tab : nullptr, &c, &why);
+                                                     n_compute_units, n_workgroups, row_block,
+                                                     flags, table ? &tab : nullptr, &c, &why);
         if (st != KVLINK_OK) return fail((kvlink_status)st, "%s", why);
         if (c.table_len > INT32_MAX) return fail(KVLINK_ERR_LAYOUT, "schedule table too large");
         if (table) {
@@ -567,6 +572,8 @@ kvlink_status kvlink_attend_make_plan(kvlink_dtype dtype, int32_t n_q_heads, int
         plan->row_block = c.row_block;
         plan->n_seqs = n_seqs;
         plan->n_split_units = c.n_split;
+        plan->flags = (flags & ~(uint32_t)(KVLINK_PLAN_COMBINE | KVLINK_PLAN_IN_LAUNCH)) |
+                      (c.in_launch ? KVLINK_PLAN_IN_LAUNCH : KVLINK_PLAN_COMBINE);
         plan->rope_table = nullptr;
         return ok();
     } catch (...) {
@@ -655,10 +662,9 @@ kvlink_status attend_impl(
         if (sched.n_seqs != n_seqs)
             return fail(KVLINK_ERR_INVALID_ARG, "plan is for %d requests, call has %d", sched.n_seqs,
                         n_seqs);
-        const int rb = kvlink::attend_row_block(kvlink::attend_path(dtype, group, max_new));
-        if (sched.row_block != rb)
-            return fail(KVLINK_ERR_INVALID_ARG, "plan row_block %d does not match this call's path (%d)",
-                        sched.row_block, rb);
+        if (!kvlink::attend_row_block_ok(kvlink::attend_path(dtype, group, max_new), sched.row_block))
+            return fail(KVLINK_ERR_INVALID_ARG, "plan row_block %d does not match this call's path",
+                        sched.row_block);
         if (!d_seq_new_ptr || !d_seq_cached || !d_new_pos || !d_new_visible)
             return fail(KVLINK_ERR_INVALID_ARG, "a layout descriptor pointer is NULL");
         if (!q_new || !k_new || !v_new || !out)

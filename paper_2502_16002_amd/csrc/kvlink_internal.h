@@ -232,6 +232,7 @@ struct AttendPlan {
     int n_wg, n_units, n_segments, n_split;
     const int32_t* table;   // device copy of the schedule table
     bool partials;          // some unit has several segments
+    bool merge_in_launch;   // wide kernel: split units merged inside the split launch
     size_t q_rot_bytes, part_o_bytes, part_ml_bytes, total_bytes;
 };
 
@@ -244,7 +245,16 @@ struct AttendPlan {
 // runs on the VALU kernel (16-row units).
 enum AttendPath { kPathWide = 0, kPathDecode = 1, kPathValu = 2 };
 AttendPath attend_path(kvlink_dtype dt, int group, int max_new);
-int attend_row_block(AttendPath path);
+// whether a schedule's row block belongs to a path (wide: 256, 128 or 64;
+// decode and vector: 16)
+bool attend_row_block_ok(AttendPath path, int row_block);
+
+// The workspace starts with the arrival counters of the units the wide
+// kernel merges in its own launch (one uint32 per unit, at most kMaxUnits):
+// they must be zero before a workspace's first use, and every completed call
+// leaves them zero.  The rotated queries and the split partials follow.
+constexpr size_t kCounterBytes = 64 * 1024;
+constexpr int kMaxUnits = (int)(kCounterBytes / 4);
 
 // Fills every field from the sizes and the schedule's counts; returns false
 // on invalid sizes or counts.
@@ -267,12 +277,14 @@ enum {
 // and, on failure, a message in *why.
 struct PlanCounts {
     int n_wg, n_units, n_segments, row_block, n_split;
+    bool in_launch;   // split units merged inside the split launch
     int64_t table_len;
 };
 int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_dim,
                           int n_seqs, const int32_t* seq_new_ptr, const int32_t* seq_cached,
                           const int32_t* new_visible, int n_compute_units, int n_workgroups,
-                          std::vector<int32_t>* table, PlanCounts* counts, const char** why);
+                          int row_block, unsigned flags, std::vector<int32_t>* table,
+                          PlanCounts* counts, const char** why);
 
 struct AttendArgs {
     const void* q_new;

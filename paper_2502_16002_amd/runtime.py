@@ -20,7 +20,8 @@ innermost):
 import numpy as np
 import torch
 
-from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
+from . import (KVLINK_BF16, KVLINK_F32, KVLINK_PLAN_XCD,
+               KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_rope_table,
                kvlink_attend_stages, kvlink_group_spans, kvlink_reencode_keys_shared,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
@@ -28,6 +29,9 @@ from . import (KVLINK_BF16, KVLINK_F32, KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_load_stage_bytes, kvlink_reencode_keys, kvlink_reencode_keys_mapped)
 
 TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
+
+# schedule options used unless a caller names others
+DEFAULT_PLAN_FLAGS = KVLINK_PLAN_XCD
 
 
 def dtype_code(name):
@@ -50,7 +54,8 @@ class Batch:
 
     def __init__(self, dtype, n_layers, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale,
                  seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq=None, doc_src_row=None,
-                 doc_src_pos0=None, n_workgroups=0, device="cuda", fused_rope=True):
+                 doc_src_pos0=None, n_workgroups=0, device="cuda", fused_rope=True, row_block=0,
+                 plan_flags=None):
         self.dtype = dtype
         self.torch_dtype = TORCH_DTYPE[dtype]
         self.n_layers, self.n_q_heads, self.n_kv_heads = n_layers, n_q_heads, n_kv_heads
@@ -86,7 +91,7 @@ class Batch:
             self.rope_table = torch.empty((max(self.n_new, 1), head_dim // 2, 2),
                                           dtype=torch.float32, device=device)
             self.build_rope_table()
-        self.set_schedule(n_workgroups)
+        self.set_schedule(n_workgroups, row_block, plan_flags)
 
     def build_rope_table(self, stream=None):
         """(Re)compute the batch's RoPE table (one launch)."""
@@ -94,14 +99,20 @@ class Batch:
             kvlink_attend_rope_table(self.head_dim, self.rope_theta, self.n_new, self.d_new_pos,
                                      self.rope_table, stream)
 
-    def set_schedule(self, n_workgroups=0):
-        """Build the split-K schedule (n_workgroups 0: the library's cost
-        model for this device), upload its table and size the workspace."""
+    def set_schedule(self, n_workgroups=0, row_block=0, flags=None):
+        """Build the split-K schedule (n_workgroups and row_block 0: the
+        library's cost model for this device; flags: kvlink_attend_make_plan
+        flags, None for DEFAULT_PLAN_FLAGS),
+        upload its table and allocate the workspace (zeroed: its merge
+        counters must start at zero; every call leaves them zero)."""
         cus = torch.cuda.get_device_properties(torch.device(self.device)).multi_processor_count
+        if flags is None:
+            flags = DEFAULT_PLAN_FLAGS
         self.plan, table = kvlink_attend_make_plan(self.dtype, self.n_q_heads, self.n_kv_heads,
                                                    self.head_dim, self.layout["seq_new_ptr"],
                                                    self.layout["seq_cached"],
-                                                   self.layout["new_visible"], cus, n_workgroups)
+                                                   self.layout["new_visible"], cus, n_workgroups,
+                                                   row_block, flags)
         self.plan_table = torch.from_numpy(np.ascontiguousarray(table)).to(self.device)
         self.plan.table = self.plan_table.data_ptr()
         if self.rope_table is not None:
@@ -111,7 +122,7 @@ class Batch:
                                                       self.head_dim, self.n_new, self.plan)
         if self.ws_bytes == 0:
             raise ValueError("invalid attention sizes")
-        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.workspace = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=self.device)
 
     def reencode(self, src_view, dst_view, stream=None, shared=None):
         """Re-encode every cached key of the batch, all layers (one launch);
@@ -173,7 +184,8 @@ class Batch:
                stages=KVLINK_STAGE_ALL, workspace=None):
         """RoPE + append of the new tokens and their attention, one layer
         (all stages, or the ones named by the stage mask).  `workspace`
-        replaces the batch's own (at least ws_bytes, 256-byte aligned)."""
+        replaces the batch's own (at least ws_bytes, 256-byte aligned, zeroed
+        before its first use)."""
         ws = self.workspace if workspace is None else workspace
         if ws.numel() * ws.element_size() < self.ws_bytes:
             raise ValueError("workspace smaller than ws_bytes")

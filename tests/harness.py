@@ -64,7 +64,8 @@ class ContiguousRun:
     """A single-request workload whose stored caches are the request's
     documents back to back (the tiny, 1B and 8B workloads)."""
 
-    def __init__(self, w, layers, n_workgroups=0, device="cuda", fused_rope=True):
+    def __init__(self, w, layers, n_workgroups=0, device="cuda", fused_rope=True, row_block=0,
+                 plan_flags=None):
         import torch
         from paper_2502_16002_amd.runtime import Batch, contiguous_view, dtype_code
         assert w.n_seqs == 1 and not w.pool
@@ -76,7 +77,8 @@ class ContiguousRun:
         self.batch = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                            [0, len(docs)], w.doc_len(0), w.link_count[0], w.n_query,
                            doc_src_row=[int(row0[j]) for j in docs], n_workgroups=n_workgroups,
-                           device=device, fused_rope=fused_rope)
+                           device=device, fused_rope=fused_rope, row_block=row_block,
+                           plan_flags=plan_flags)
         b = self.batch
         R = int(sum(w.doc_table_len))
         self.cap = max(b.max_total, 1)
@@ -125,7 +127,8 @@ class PagedRun:
     pages of its documents through its V block table (values are never
     rewritten), with fresh pages after them for its new tokens."""
 
-    def __init__(self, w, n_workgroups=0, device="cuda", seed=11, fused_rope=True):
+    def __init__(self, w, n_workgroups=0, device="cuda", seed=11, fused_rope=True, row_block=0,
+                 plan_flags=None):
         import torch
         from paper_2502_16002_amd.runtime import Batch, dtype_code, paged_view
         assert w.pool
@@ -151,7 +154,7 @@ class PagedRun:
         self.batch = Batch(dtype_code(w.dtype), L, w.n_q_heads, H, d, w.rope_theta, w.scale,
                            sdp, dl, lc, w.n_query, doc_src_seq=src_seq,
                            doc_src_row=[0] * len(dl), n_workgroups=n_workgroups, device=device,
-                           fused_rope=fused_rope)
+                           fused_rope=fused_rope, row_block=row_block, plan_flags=plan_flags)
         b = self.batch
         td = b.torch_dtype
         # pool tensors [L][page][H][P][d]; V gets extra fresh pages for new tokens

@@ -383,15 +383,17 @@ def test_attend_no_new_tokens_is_a_no_op(kv):
 def test_workspace_bytes(kv):
     f = kv.kvlink_attend_workspace_bytes
     bf, f32 = kv.KVLINK_BF16, kv.KVLINK_F32
+    counters = 64 * 1024                      # the merge counters come first
     one = _plan(kv, n_wg=1)                   # one segment per unit: no partials
     assert one.n_segments == one.n_units
-    assert f(bf, 8, 2, 128, 10, one) == _align(10 * 8 * 128 * 2)
+    assert f(bf, 8, 2, 128, 10, one) == counters + _align(10 * 8 * 128 * 2)
     assert f(bf, 8, 2, 96, 10, one) == 0
     many = _plan(kv, n_wg=1 << 20)            # one tile per segment
     assert many.n_segments > many.n_units
-    assert f(bf, 8, 2, 128, 10, many) == (_align(10 * 8 * 128 * 2) +
-                                           _align(many.n_segments * 256 * 128 * 2) +
-                                           _align(many.n_segments * 256 * 2 * 4))
+    rb = many.row_block
+    assert f(bf, 8, 2, 128, 10, many) == (counters + _align(10 * 8 * 128 * 2) +
+                                           _align(many.n_segments * rb * 128 * 2) +
+                                           _align(many.n_segments * rb * 2 * 4))
     thin = _plan(kv, f32, 4, 2, 64, (0, 22), [200] * 22, n_wg=12)
     assert thin.row_block == 16 and thin.n_segments > thin.n_units
     assert f(f32, 4, 2, 64, 22, thin) > f(f32, 4, 2, 64, 22, _plan(kv, f32, 4, 2, 64, (0, 22),
@@ -438,7 +440,7 @@ def _expected_units(L, G, hkv, rb):
     return np.array(out, np.int64).reshape(-1, 9), np.array(seq_unit)
 
 
-def _check_schedule(kv, w, n_wg_req):
+def _check_schedule(kv, w, n_wg_req, row_block=0, flags=0):
     sdp = np.concatenate([[0], np.cumsum([len(d) for d in w.docs])])
     dl = [w.doc_table_len[j] for s in range(w.n_seqs) for j in w.docs[s]]
     lc = [k for s in range(w.n_seqs) for k in w.link_count[s]]
@@ -446,11 +448,13 @@ def _check_schedule(kv, w, n_wg_req):
     dt = kv.KVLINK_F32 if w.dtype == "f32" else kv.KVLINK_BF16
     plan, table = kv.kvlink_attend_make_plan(dt, w.n_q_heads, w.n_kv_heads, w.head_dim,
                                              L["seq_new_ptr"], L["seq_cached"], L["new_visible"],
-                                             256, n_wg_req)
+                                             256, n_wg_req, row_block, flags)
     G = w.n_q_heads // w.n_kv_heads
     max_new = int(np.max(np.diff(L["seq_new_ptr"])))
     mfma = w.dtype == "bf16" and max_new * G > 16
-    assert plan.row_block == (256 if mfma else 16)
+    assert plan.row_block in ((256, 128, 64) if mfma else (16,))
+    if row_block:
+        assert plan.row_block == row_block
     recs, unit_recs, split = _decode(plan, table, w.n_seqs)
     units, _ = _expected_units(L, G, w.n_kv_heads, plan.row_block)
     assert plan.n_units == len(units)
@@ -507,6 +511,12 @@ def test_attend_schedule(kv, name):
     chosen = _check_schedule(kv, w, 0)
     for n in [1, 3, 64, 1 << 20]:
         _check_schedule(kv, w, n)
+    rows = max(w.n_new(s) for s in range(w.n_seqs)) * (w.n_q_heads // w.n_kv_heads)
+    wide = w.dtype == "bf16" and rows > 16
+    for rb in ((256, 128, 64) if wide else (16,)):
+        for flags in (0, kv.KVLINK_PLAN_XCD):
+            _check_schedule(kv, w, 0, rb, flags)
+            _check_schedule(kv, w, 7, rb, flags)
     # the long-context workload's tile count keeps the whole chip busy
     if name == "llama8b-32layer-40x512":
         assert chosen.n_workgroups >= 200
@@ -520,8 +530,7 @@ def test_attend_schedule(kv, name):
     # the kernel: 16-row units for bf16 batches of at most 16 rows per KV
     # head (decoding steps), 256-row units for the other bf16 batches
     if w.dtype == "bf16":
-        rows = max(w.n_new(s) for s in range(w.n_seqs)) * (w.n_q_heads // w.n_kv_heads)
-        assert chosen.row_block == (16 if rows <= 16 else 256)
+        assert chosen.row_block in ((256, 128, 64) if wide else (16,))
     if w.decode:
         assert chosen.n_workgroups >= 256     # two workgroups per compute unit fit
 
@@ -550,7 +559,10 @@ def test_attend_schedule_random_batches(kv, data):
                            n_kv_heads=hkv, head_dim=data.draw(st.sampled_from([64, 128])),
                            rope_theta=1e4, seed=1, doc_table_len=table, docs=docs,
                            link_count=links, n_query=nq)
-    _check_schedule(kv, w, data.draw(st.sampled_from([0, 0, 1, 2, 7, 300])))
+    rows = max(w.n_new(s) for s in range(w.n_seqs)) * g
+    rb = data.draw(st.sampled_from([0, 256, 128, 64])) if dtype == "bf16" and rows > 16 else 0
+    _check_schedule(kv, w, data.draw(st.sampled_from([0, 0, 1, 2, 7, 300])), rb,
+                    data.draw(st.sampled_from([0, kv.KVLINK_PLAN_XCD])))
 
 
 def test_attend_schedule_errors(kv):

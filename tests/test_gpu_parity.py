@@ -80,9 +80,10 @@ def long_run():
 
 def _long_token_sample(n_new, seed):
     """About 5% of the new tokens (seeded) plus the first and last token of
-    every 64-token block (one 256-row unit of the wide kernel at group 4)."""
+    every 16-token block (at group 4 the smallest unit of the wide kernel,
+    64 rows; a 128- or 256-row unit is two or four such blocks)."""
     rng = np.random.default_rng(seed)
-    edges = [t for b in range(0, n_new, 64) for t in (b, min(b + 63, n_new - 1))]
+    edges = [t for b in range(0, n_new, 16) for t in (b, min(b + 15, n_new - 1))]
     pick = rng.choice(n_new, size=max(1, round(0.05 * n_new)), replace=False)
     return np.unique(np.concatenate([edges, pick]))
 
@@ -731,7 +732,7 @@ def test_batch_of_requests_contiguous(dtype, kind):
             assert torch.equal(a.out[0].view(torch.int16), b.out[0].view(torch.int16))
             assert torch.equal(a.k_dst.view(torch.int16), b.k_dst.view(torch.int16))
             run = a
-            assert run.batch.plan.row_block == (16 if kind == "decode" else 256)
+            assert run.batch.plan.row_block in ((16,) if kind == "decode" else (256, 128, 64))
         else:
             run = _BatchRun(w, n_wg)
             run.run()
@@ -795,8 +796,8 @@ def test_gqa_groups(hq, hkv, dtype, layout):
             run.run()
         g = hq // hkv
         if dtype == "bf16":
-            expect = 16 if g * max(run.batch.max_new, 1) <= 16 else 256
-            assert run.batch.plan.row_block == expect
+            expect = (16,) if g * max(run.batch.max_new, 1) <= 16 else (256, 128, 64)
+            assert run.batch.plan.row_block in expect
         _check_attend(run, 0, tag=f"gqa {hq}/{hkv} {dtype} {layout} {n_wg}")
         _check_append(run, 0)
 
@@ -939,3 +940,83 @@ def test_paged_pool_reencode_and_attention():
     ld = run.lds[0]
     assert np.array_equal(to_f64(run.v_all[0, int(run.pool_table[3, 2])]),
                           workloads.as_f64(w, ld.v_store[:, 3 * 256 + 32:3 * 256 + 48]).reshape(8, 16, 128))
+
+
+# ------------------------------------- wide-kernel unit shapes and the merge
+
+
+def _counters_zero(run):
+    import torch
+    torch.cuda.synchronize()
+    assert int(run.batch.workspace[:64 * 1024].count_nonzero()) == 0, "merge counters not reset"
+
+
+# plan flags: the cost model's merge; XCD numbering with the combine launch;
+# XCD numbering with the merge in the launch; the merge in the launch alone
+@pytest.mark.parametrize("flags", [0, 1 | 4, 1 | 8, 8])
+@pytest.mark.parametrize("row_block", [256, 128, 64])
+def test_wide_unit_shapes_against_oracle(row_block, flags):
+    if row_block == 256 and flags & 8:
+        pytest.skip("256-row units merge by the combine launch only")
+    """Each unit shape of the wide kernel (256 rows on eight wavefronts; 128
+    and 64 rows on two key groups of four wavefronts), with and without the
+    XCD-aware numbering, split units merged by the combine
+    launch or inside the split launch: the 10-document Llama-8B workload (two
+    layers, every row) and the Llama-1B one (head_dim 64) under the
+    schedule's own cut and under forced workgroup counts that split every
+    unit into one-tile segments; the merge counters are zero afterwards."""
+    worst = 0.0
+    for w, n_wgs in [(workloads.llama8b_10doc(n_layers=2), [0]),
+                     (workloads.llama1b_layer(), [0, 1, 7, 1 << 20])]:
+        for n_wg in n_wgs:
+            run = ContiguousRun(w, layers=list(range(w.n_layers)), n_workgroups=n_wg,
+                                row_block=row_block, plan_flags=flags)
+            assert run.batch.plan.row_block == row_block
+            run.run()
+            for l in range(w.n_layers):
+                worst = max(worst, _check_attend(run, l, tag=f"rb{row_block}/{n_wg}/{flags}")[0])
+            _counters_zero(run)
+            if n_wg == 1 << 20:
+                assert run.batch.plan.n_split_units == run.batch.plan.n_units
+    _print(f"row block {row_block} flags {flags}: worst row rel {worst:.3e}")
+
+
+@pytest.mark.parametrize("row_block", [128, 64])
+@pytest.mark.parametrize("doc_len,link_count,n_query", [
+    ([5], [0], 7),                          # K = 0: causal queries
+    ([1, 1, 1], [3, 3, 3], 0),              # 1-token documents, no queries
+    ([63, 64, 65], [1, 2, 3], 5),           # lengths across tile edges
+    ([], [], 40),                           # no documents
+    ([300, 700], [5, 5], 64),               # a longer cache cut into segments
+])
+def test_wide_unit_shapes_edge_layouts(row_block, doc_len, link_count, n_query):
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                         dtype="bf16", rope_theta=5e5, seed=17)
+    for n_wg in [0, 3, 1 << 20]:
+        run = ContiguousRun(w, layers=[0], n_workgroups=n_wg, row_block=row_block)
+        run.run()
+        _check_attend(run, 0, tag=f"edge rb{row_block}/{n_wg}")
+        _check_append(run, 0)
+        _counters_zero(run)
+
+
+@pytest.mark.parametrize("row_block", [128, 64])
+def test_wide_unit_shapes_paged_pool(row_block):
+    """The 16-request shared pool through block tables with the smaller unit
+    shapes and the XCD-aware numbering: every request's output and LSE."""
+    from harness import PagedRun
+    w = workloads.llama8b_paged()
+    run = PagedRun(w, row_block=row_block, plan_flags=1 | 8)
+    run.run()
+    b = run.batch
+    out_all, lse_all = to_f64(run.out[0]), to_f64(run.lse[0])
+    worst = 0.0
+    for s in range(w.n_seqs):
+        kc, vc, q, kn, vn = run.oracle_inputs(0, s)
+        ref, ref_lse = oracle.attend(w.doc_len(s), w.link_count[s], w.n_query[s], q, kn, vn, kc,
+                                     vc, w.rope_theta, w.scale)
+        n0, n1 = int(b.layout["seq_new_ptr"][s]), int(b.layout["seq_new_ptr"][s + 1])
+        worst = max(worst, check_close(w, out_all[n0:n1], ref, f"paged rb{row_block} request {s}"))
+        assert float(np.max(np.abs(lse_all[n0:n1] - ref_lse))) <= 2e-2
+    _counters_zero(run)
+    _print(f"paged pool row block {row_block}: worst {worst:.3e}")
