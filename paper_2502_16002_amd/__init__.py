@@ -10,6 +10,10 @@ import ctypes
 import os
 
 import numpy as np
+# torch first: libkvlink.so then binds to the HIP runtime torch has loaded
+# (loading the library first would bring in a second HIP runtime beside
+# torch's, and the two do not share devices)
+import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkvlink.so")

@@ -17,28 +17,44 @@
 // The pass is bound by HBM bandwidth (about 1.5 flop per byte moved):
 //   * one launch covers every layer and KV head, since delta does not depend
 //     on them;
-//   * a workgroup owns up to kRows rows of one document for kLH (layer, head)
-//     pairs, so the document's cos/sin table is built once (double-precision
-//     angles reduced and evaluated in registers, stored to LDS) and then held
-//     in registers: each thread always handles the same slice of the rotation
-//     pairs;
+//   * a workgroup owns up to kRows rows of one document for lh_per_wg(D)
+//     (layer, head) pairs (8 KiB of bf16 keys at head_dim 128, one 16-byte
+//     vector pair per thread), so the document's cos/sin table is built once
+//     (double-precision angles reduced and evaluated in registers, stored to
+//     LDS) and then held in registers: each thread always handles the same
+//     slice of the rotation pairs; the first loads are issued before the table
+//     is built, so that its work overlaps their latency;
 //   * each thread moves 16-byte vectors: the slice [j0, j0+E) and its partner
 //     slice [j0+d/2, j0+d/2+E), consecutive threads cover one row, then the
 //     next row, so a wavefront reads and writes whole contiguous rows;
 //   * kUnroll vectors are loaded before any is stored, to keep enough bytes in
 //     flight per wavefront;
 //   * loads and stores are non-temporal (every byte is touched once), and a
-//     workgroup covers 16 rows, so the many short documents of a request
-//     spread evenly over the compute units.
+//     workgroup covers 8 rows, so the many short documents of a request
+//     spread evenly over the compute units;
+//   * a grid of at least kLongGrid workgroups (a long-context batch: a
+//     steady stream, ramp and tail negligible) runs with at most
+//     kLongResident workgroups resident per CU, capped through their LDS
+//     allocation: on MI355X fewer concurrent streams then sustain a higher
+//     HBM rate (79-80% of peak against 76-77% at full residency, 40 x 512
+//     tokens x 32 layers x 8 heads), while short grids keep full residency
+//     (there ramp and tail dominate and the cap costs 3-15%).
 #include "kvlink_internal.h"
 
 namespace kvlink {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRows = 16;
-constexpr int kLH = 8;
-constexpr int kUnroll = 4;
+constexpr int kRows = 8;
+constexpr int kUnroll = 2;
+constexpr int kLongGrid = 65536;
+constexpr int kLongResident = 6;
+constexpr int kLdsPerCu = 160 * 1024;
+
+// (layer, head) pairs per workgroup of the per-span kernel: 32 rows of
+// head_dim 128 (4 pairs x 8 rows), scaled so a workgroup always holds 32 x 128
+// elements.
+__host__ __device__ constexpr int lh_per_wg(int D) { return 4 * 128 / D; }
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -96,35 +112,15 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
     const int r0 = blockIdx.x * kRows;
     if (r0 >= sp.len) return;
     const int rows = min(kRows, sp.len - r0);
+    constexpr int kLH = lh_per_wg(D);
     const int lh0 = blockIdx.z * kLH;
     const int nlh = min(kLH, n_lh - lh0);
 
-    if constexpr (kMode != kCopy) {
-        for (int i = threadIdx.x; i < TR * H; i += kThreads) {
-            const int tr = i / H, j = i % H;
-            int64_t pos = (int64_t)sp.delta;
-            if constexpr (kMode == kPerToken) {
-                pos += r0 + tr;
-                if (pos_map && r0 + tr < sp.len)
-                    pos -= pos_map[(int64_t)sp.src_seq * pos_stride + sp.src_row + r0 + tr];
-            }
-            rope_cos_sin(pos, j, freqs, &s_cos[tr][j], &s_sin[tr][j]);
-        }
-        __syncthreads();
-    }
-
     const int sub = threadIdx.x % TPV;
-    float c[E], s[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        c[e] = kMode == kCopy ? 1.f : s_cos[0][sub * E + e];
-        s[e] = kMode == kCopy ? 0.f : s_sin[0][sub * E + e];
-    }
-
     const int n_vec = rows * nlh;
-    for (int v0 = threadIdx.x / TPV; v0 < n_vec; v0 += VPP * kUnroll) {
-        uint4 lo[kUnroll], hi[kUnroll];
-        int64_t doff[kUnroll];
+    uint4 lo[kUnroll], hi[kUnroll];
+    int64_t doff[kUnroll];
+    auto load_round = [&](int v0) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int v = v0 + u * VPP;
@@ -140,6 +136,35 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
                 doff[u] = view_offset(dst, layer, head, sp.dst_seq, sp.dst_row + r0 + row) + sub * E;
             }
         }
+    };
+    // the first round of loads goes out before the cos/sin table is built,
+    // so that the table's double-precision work overlaps their latency
+    const int v_first = threadIdx.x / TPV;
+    load_round(v_first);
+
+    if constexpr (kMode != kCopy) {
+        for (int i = threadIdx.x; i < TR * H; i += kThreads) {
+            const int tr = i / H, j = i % H;
+            int64_t pos = (int64_t)sp.delta;
+            if constexpr (kMode == kPerToken) {
+                pos += r0 + tr;
+                if (pos_map && r0 + tr < sp.len)
+                    pos -= pos_map[(int64_t)sp.src_seq * pos_stride + sp.src_row + r0 + tr];
+            }
+            rope_cos_sin(pos, j, freqs, &s_cos[tr][j], &s_sin[tr][j]);
+        }
+        __syncthreads();
+    }
+
+    float c[E], s[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        c[e] = kMode == kCopy ? 1.f : s_cos[0][sub * E + e];
+        s[e] = kMode == kCopy ? 0.f : s_sin[0][sub * E + e];
+    }
+
+    for (int v0 = v_first; v0 < n_vec; v0 += VPP * kUnroll) {
+        if (v0 != v_first) load_round(v0);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int v = v0 + u * VPP;
@@ -167,14 +192,15 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 // Document-major re-encode: the spans of group g (spans[group_ptr[g] ..
 // group_ptr[g+1])) all read the same stored rows (one document reused by
 // several requests, each at its own global offset).  A workgroup loads its
-// kRows rows x kLH (layer, head) pairs of the group's document once, then
+// kRowsS rows x kLHS (layer, head) pairs of the group's document once, then
 // for each span rotates them by that span's delta and stores them at the
 // span's destination: the stored rows are read once per group instead of
 // once per span.  The cos/sin tables of up to kMaxDst spans are built per
 // round (double-precision angles, in LDS); the first round's table work
 // overlaps the loads.
 constexpr int kMaxDst = 32;
-constexpr int kLHS = 4;   // (layer, head) pairs per workgroup of the shared kernel
+constexpr int kRowsS = 16;  // rows per workgroup of the shared kernel
+constexpr int kLHS = 4;     // (layer, head) pairs per workgroup of the shared kernel
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
@@ -184,15 +210,15 @@ __global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
     constexpr int E = 16 / (int)sizeof(T);
     constexpr int TPV = H / E;
     constexpr int VPP = kThreads / TPV;
-    constexpr int NB = (kRows * kLHS + VPP - 1) / VPP;  // vectors per thread
+    constexpr int NB = (kRowsS * kLHS + VPP - 1) / VPP;  // vectors per thread
     __shared__ float s_cos[kMaxDst][H], s_sin[kMaxDst][H];
 
     const int sp0 = group_ptr[blockIdx.y], sp1 = group_ptr[blockIdx.y + 1];
     if (sp1 <= sp0) return;
     const kvlink_span first = spans[sp0];
-    const int r0 = blockIdx.x * kRows;
+    const int r0 = blockIdx.x * kRowsS;
     if (r0 >= first.len) return;
-    const int rows = min(kRows, first.len - r0);
+    const int rows = min(kRowsS, first.len - r0);
     const int lh0 = blockIdx.z * kLHS;
     const int nlh = min(kLHS, n_lh - lh0);
     const int sub = threadIdx.x % TPV;
@@ -267,7 +293,7 @@ hipError_t launch_shared(int n_layers, int n_kv_heads, const RopeFreqs& freqs, i
                          const int32_t* group_ptr, const kvlink_span* spans, int max_span_len,
                          const View& src, const View& dst, hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
-    dim3 grid((max_span_len + kRows - 1) / kRows, n_groups, (n_lh + kLHS - 1) / kLHS);
+    dim3 grid((max_span_len + kRowsS - 1) / kRowsS, n_groups, (n_lh + kLHS - 1) / kLHS);
     hipLaunchKernelGGL((reencode_shared_kernel<T, D>), grid, dim3(kThreads), 0, stream, src, dst,
                        spans, group_ptr, n_lh, n_kv_heads, freqs);
     return hipGetLastError();
@@ -278,15 +304,22 @@ hipError_t launch(int n_layers, int n_kv_heads, const RopeFreqs& freqs, int n_sp
                   const kvlink_span* spans, int max_span_len, const View& src, const View& dst,
                   int mode, const int32_t* pos_map, int64_t pos_stride, hipStream_t stream) {
     const int n_lh = n_layers * n_kv_heads;
+    constexpr int kLH = lh_per_wg(D);
     dim3 grid((max_span_len + kRows - 1) / kRows, n_spans, (n_lh + kLH - 1) / kLH);
+    // residency cap of long grids: dynamic LDS that, with the kernel's own
+    // cos/sin table, fills kLdsPerCu / kLongResident per workgroup
+    const unsigned table = 2u * (mode == kPerToken ? kRows : 1) * (D / 2) * (unsigned)sizeof(float);
+    const unsigned lds = (int64_t)grid.x * grid.y * grid.z >= kLongGrid
+                             ? kLdsPerCu / kLongResident - table
+                             : 0u;
     if (mode == kPerToken)
-        hipLaunchKernelGGL((reencode_kernel<T, D, kPerToken>), grid, dim3(kThreads), 0, stream,
+        hipLaunchKernelGGL((reencode_kernel<T, D, kPerToken>), grid, dim3(kThreads), lds, stream,
                            src, dst, spans, n_lh, n_kv_heads, freqs, pos_map, pos_stride);
     else if (mode == kCopy)
-        hipLaunchKernelGGL((reencode_kernel<T, D, kCopy>), grid, dim3(kThreads), 0, stream, src,
+        hipLaunchKernelGGL((reencode_kernel<T, D, kCopy>), grid, dim3(kThreads), lds, stream, src,
                            dst, spans, n_lh, n_kv_heads, freqs, nullptr, (int64_t)0);
     else
-        hipLaunchKernelGGL((reencode_kernel<T, D, kDelta>), grid, dim3(kThreads), 0, stream, src,
+        hipLaunchKernelGGL((reencode_kernel<T, D, kDelta>), grid, dim3(kThreads), lds, stream, src,
                            dst, spans, n_lh, n_kv_heads, freqs, nullptr, (int64_t)0);
     return hipGetLastError();
 }
