@@ -243,15 +243,22 @@ kvlink_status kvlink_reencode_keys_mapped(kvlink_dtype dtype, int32_t n_layers,
  * same (src_seq, src_row, len) and each with its own destination and delta.
  *
  *   h_spans[n_spans]        host spans (e.g. kvlink_build_layout's)
+ *   max_group               0: one group per distinct (src_seq, src_row,
+ *                           len); > 0: such a run of n spans is cut into
+ *                           ceil(n / max_group) consecutive groups whose
+ *                           sizes differ by at most one (kvlink_reencode_keys_
+ *                           shared then reads those stored rows once per
+ *                           group, and a workgroup's work is bounded by
+ *                           max_group destinations)
  *   h_order[n_spans]        out: span indices, grouped, each group in span
  *                           order, groups by (src_seq, src_row, len)
  *   h_group_ptr[n_spans+1]  out: group g is h_order[h_group_ptr[g] ..
  *                           h_group_ptr[g+1])
  *   n_groups                out
- * Errors: KVLINK_ERR_INVALID_ARG (n_spans < 0, NULL pointers).
+ * Errors: KVLINK_ERR_INVALID_ARG (n_spans < 0, max_group < 0, NULL pointers).
  */
-kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t* h_order,
-                                 int32_t* h_group_ptr, int32_t* n_groups);
+kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t max_group,
+                                 int32_t* h_order, int32_t* h_group_ptr, int32_t* n_groups);
 
 /*
  * kvlink_reencode_keys_shared — kvlink_reencode_keys, document-major: the

@@ -86,7 +86,7 @@ def _load():
                                                 vp, ctypes.c_int64, kvlink_kv_view,
                                                 kvlink_kv_view, vp]
     lib.kvlink_reencode_keys_mapped.restype = ctypes.c_int
-    lib.kvlink_group_spans.argtypes = [i32, vp, vp, vp, ctypes.POINTER(i32)]
+    lib.kvlink_group_spans.argtypes = [i32, vp, i32, vp, vp, ctypes.POINTER(i32)]
     lib.kvlink_group_spans.restype = ctypes.c_int
     lib.kvlink_reencode_keys_shared.argtypes = [ctypes.c_int, i32, i32, i32, f64, i32, vp, vp, i32,
                                                 kvlink_kv_view, kvlink_kv_view, vp]
@@ -231,15 +231,17 @@ def kvlink_reencode_keys_mapped(dtype, n_layers, n_kv_heads, head_dim, rope_thet
                                             int(stored_pos_stride), src, dst, _stream(stream)))
 
 
-def kvlink_group_spans(spans):
+def kvlink_group_spans(spans, max_group=0):
     """Group spans [n, 6] int32 (kvlink_span fields) that read the same stored
-    rows: returns (order, group_ptr) int32 arrays."""
+    rows, runs longer than max_group (> 0) cut into near-equal groups:
+    returns (order, group_ptr) int32 arrays."""
     sp = np.ascontiguousarray(np.asarray(spans, dtype=np.int32).reshape(-1, SPAN_FIELDS))
     n = len(sp)
     order = np.zeros(max(n, 1), np.int32)
     gptr = np.zeros(n + 1, np.int32)
     ng = ctypes.c_int32(0)
-    _check(_lib.kvlink_group_spans(n, _ptr(sp), _ptr(order), _ptr(gptr), ctypes.byref(ng)))
+    _check(_lib.kvlink_group_spans(n, _ptr(sp), int(max_group), _ptr(order), _ptr(gptr),
+                                   ctypes.byref(ng)))
     return order[:n], gptr[:ng.value + 1]
 
 

@@ -232,10 +232,11 @@ kvlink_status rotate_keys(const char* name, bool per_token, kvlink_dtype dtype, 
 }
 }  // namespace
 
-kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t* h_order,
-                                 int32_t* h_group_ptr, int32_t* n_groups) {
+kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, int32_t max_group,
+                                 int32_t* h_order, int32_t* h_group_ptr, int32_t* n_groups) {
     try {
         if (n_spans < 0) return fail(KVLINK_ERR_INVALID_ARG, "n_spans < 0");
+        if (max_group < 0) return fail(KVLINK_ERR_INVALID_ARG, "max_group < 0");
         if (!n_groups || (n_spans > 0 && (!h_spans || !h_order || !h_group_ptr)))
             return fail(KVLINK_ERR_INVALID_ARG, "a required pointer is NULL");
         // stable order by (src_seq, src_row, len): spans reading the same
@@ -248,13 +249,20 @@ kvlink_status kvlink_group_spans(int32_t n_spans, const kvlink_span* h_spans, in
         };
         std::stable_sort(order.begin(), order.end(),
                          [&](int32_t a, int32_t b) { return key(a) < key(b); });
+        for (int32_t i = 0; i < n_spans; ++i) h_order[i] = order[(size_t)i];
+        // runs of equal keys, each cut into ceil(n / max_group) groups whose
+        // sizes differ by at most one
         int32_t g = 0;
         if (h_group_ptr) h_group_ptr[0] = 0;
-        for (int32_t i = 0; i < n_spans; ++i) {
-            h_order[i] = order[(size_t)i];
-            if (i > 0 && key(order[(size_t)i]) != key(order[(size_t)i - 1])) h_group_ptr[++g] = i;
+        for (int32_t i = 0; i < n_spans;) {
+            int32_t j = i + 1;
+            while (j < n_spans && key(order[(size_t)j]) == key(order[(size_t)i])) ++j;
+            const int32_t n = j - i;
+            const int32_t parts = max_group > 0 ? (n + max_group - 1) / max_group : 1;
+            for (int32_t k = 1; k <= parts; ++k)
+                h_group_ptr[++g] = i + (int32_t)((int64_t)n * k / parts);
+            i = j;
         }
-        if (n_spans > 0) h_group_ptr[++g] = n_spans;
         *n_groups = g;
         return ok();
     } catch (...) {

@@ -196,8 +196,9 @@ __global__ __launch_bounds__(kThreads) void reencode_kernel(View src, View dst,
 // for each span rotates them by that span's delta and stores them at the
 // span's destination: the stored rows are read once per group instead of
 // once per span.  The cos/sin tables of up to kMaxDst spans are built per
-// round (double-precision angles, in LDS); the first round's table work
-// overlaps the loads.
+// round (double-precision angles, in LDS), together with the destinations'
+// span records and page offsets; the first round's table work overlaps the
+// loads.
 constexpr int kMaxDst = 32;
 constexpr int kRowsS = 16;  // rows per workgroup of the shared kernel
 constexpr int kLHS = 4;     // (layer, head) pairs per workgroup of the shared kernel
@@ -212,6 +213,8 @@ __global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
     constexpr int VPP = kThreads / TPV;
     constexpr int NB = (kRowsS * kLHS + VPP - 1) / VPP;  // vectors per thread
     __shared__ float s_cos[kMaxDst][H], s_sin[kMaxDst][H];
+    __shared__ kvlink_span s_dst[kMaxDst];
+    __shared__ int64_t s_base[kMaxDst];
 
     const int sp0 = group_ptr[blockIdx.y], sp1 = group_ptr[blockIdx.y + 1];
     if (sp1 <= sp0) return;
@@ -242,33 +245,38 @@ __global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
     for (int c0 = sp0; c0 < sp1; c0 += kMaxDst) {
         const int nd = min(kMaxDst, sp1 - c0);
         __syncthreads();   // the previous round's tables are no longer read
+        // one thread per destination fetches its span record and, when its
+        // rows lie in one page (or the view is contiguous), the element offset
+        // of its first row from one block-table read: all destinations' reads
+        // are in flight together, not one dependent chain per destination
+        if (threadIdx.x < nd) {
+            const kvlink_span sp = spans[c0 + threadIdx.x];
+            const int drow0 = sp.dst_row + r0;
+            int64_t base = -1;
+            if (dst.block_table) {
+                if (drow0 % dst.page_size + rows <= dst.page_size)
+                    base = (int64_t)dst.block_table[(int64_t)sp.dst_seq * dst.max_pages +
+                                                    drow0 / dst.page_size] * dst.page_stride +
+                           (int64_t)(drow0 % dst.page_size) * dst.row_stride;
+            } else {
+                base = (int64_t)sp.dst_seq * dst.seq_stride + (int64_t)drow0 * dst.row_stride;
+            }
+            s_dst[threadIdx.x] = sp;
+            s_base[threadIdx.x] = base;
+        }
         for (int i = threadIdx.x; i < nd * H; i += kThreads) {
             const int k = i / H, j = i % H;
             rope_cos_sin((int64_t)spans[c0 + k].delta, j, freqs, &s_cos[k][j], &s_sin[k][j]);
         }
         __syncthreads();
         for (int k = 0; k < nd; ++k) {
-            const kvlink_span sp = spans[c0 + k];
             float c[E], s[E];
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 c[e] = s_cos[k][sub * E + e];
                 s[e] = s_sin[k][sub * E + e];
             }
-            // the destination rows, when they lie in one page (or the view
-            // is contiguous), from one scalar read of the block table
-            const int drow0 = sp.dst_row + r0;
-            bool one_page = true;
-            int64_t base = 0;
-            if (dst.block_table) {
-                one_page = drow0 % dst.page_size + rows <= dst.page_size;
-                if (one_page)
-                    base = (int64_t)load_uniform(dst.block_table + (int64_t)sp.dst_seq * dst.max_pages +
-                                                 drow0 / dst.page_size) * dst.page_stride +
-                           (int64_t)(drow0 % dst.page_size) * dst.row_stride;
-            } else {
-                base = (int64_t)sp.dst_seq * dst.seq_stride + (int64_t)drow0 * dst.row_stride;
-            }
+            const int64_t base = s_base[k];
 #pragma unroll
             for (int u = 0; u < NB; ++u) {
                 const int v = threadIdx.x / TPV + u * VPP;
@@ -276,10 +284,11 @@ __global__ __launch_bounds__(kThreads) void reencode_shared_kernel(
                     const int lh = lh0 + v / rows, row = v % rows;
                     const int layer = lh / n_kv_heads, head = lh % n_kv_heads;
                     const int64_t off =
-                        one_page ? (int64_t)layer * dst.layer_stride +
-                                       (int64_t)head * dst.head_stride + base +
-                                       (int64_t)row * dst.row_stride
-                                 : view_offset(dst, layer, head, sp.dst_seq, drow0 + row);
+                        base >= 0 ? (int64_t)layer * dst.layer_stride +
+                                        (int64_t)head * dst.head_stride + base +
+                                        (int64_t)row * dst.row_stride
+                                  : view_offset(dst, layer, head, s_dst[k].dst_seq,
+                                                s_dst[k].dst_row + r0 + row);
                     rotate_store<T, D>(lo[u], hi[u], c, s,
                                        reinterpret_cast<T*>(dst.base) + off + sub * E);
                 }

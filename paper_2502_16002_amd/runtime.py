@@ -32,6 +32,13 @@ TORCH_DTYPE = {KVLINK_F32: torch.float32, KVLINK_BF16: torch.bfloat16}
 
 # schedule options used unless a caller names others
 DEFAULT_PLAN_FLAGS = KVLINK_PLAN_XCD
+# destinations per group of the document-major re-encode: a document reused
+# by more spans is read once per group of at most this many, which bounds the
+# work of one workgroup (a document serving hundreds of requests would
+# otherwise set the launch's duration alone).  Cutting smaller groups costs
+# more than it balances: on the 16-request pool (up to 9 uses per document)
+# groups of at most 2, 3, 4 or 6 all measured slower than whole documents.
+SHARED_MAX_GROUP = 16
 
 
 def dtype_code(name):
@@ -73,10 +80,12 @@ class Batch:
             return torch.from_numpy(np.ascontiguousarray(a)).to(device)
         self.d_spans = up(self.layout["spans"].reshape(-1, SPAN_FIELDS))
         # documents reused within the batch: their stored rows are re-encoded
-        # document-major (read once for all their spans)
-        order, gptr = kvlink_group_spans(self.layout["spans"])
+        # document-major (read once per group of at most SHARED_MAX_GROUP of
+        # their spans)
+        _, gptr = kvlink_group_spans(self.layout["spans"])
+        self.shared_docs = len(gptr) - 1 < self.n_docs
+        order, gptr = kvlink_group_spans(self.layout["spans"], SHARED_MAX_GROUP)
         self.n_groups = len(gptr) - 1
-        self.shared_docs = self.n_groups < self.n_docs
         if self.shared_docs:
             self.d_spans_grouped = up(self.layout["spans"].reshape(-1, SPAN_FIELDS)[order])
             self.d_group_ptr = up(gptr)
@@ -134,7 +143,7 @@ class Batch:
         if shared:
             gp = self.d_group_ptr if self.shared_docs else None
             if gp is None:
-                order, gptr = kvlink_group_spans(self.layout["spans"])
+                order, gptr = kvlink_group_spans(self.layout["spans"], SHARED_MAX_GROUP)
                 self.d_spans_grouped = torch.from_numpy(np.ascontiguousarray(
                     self.layout["spans"].reshape(-1, SPAN_FIELDS)[order])).to(self.device)
                 self.d_group_ptr = gp = torch.from_numpy(gptr).to(self.device)

@@ -239,6 +239,31 @@ def test_group_spans(kv):
         assert len(gptr) - 1 == len({tuple(r) for r in spans[:, [0, 1, 4]]})
 
 
+def test_group_spans_max_group(kv):
+    """With max_group > 0 a run of n spans reading the same rows is cut into
+    ceil(n / max_group) consecutive groups of near-equal size, in the same
+    order as the uncut grouping; max_group < 0 is refused."""
+    rng = np.random.default_rng(6)
+    n = 300
+    spans = np.zeros((n, 6), np.int32)
+    spans[:, 0] = rng.integers(0, 7, size=n)
+    spans[:, 4] = 16
+    spans[:, 2] = np.arange(n)
+    full_order, full_ptr = kv.kvlink_group_spans(spans)
+    for mg in [1, 2, 3, 4, 10, 1000]:
+        order, gptr = kv.kvlink_group_spans(spans, max_group=mg)
+        assert np.array_equal(order, full_order)
+        assert set(full_ptr.tolist()) <= set(gptr.tolist())
+        for g in range(len(full_ptr) - 1):
+            a, b = full_ptr[g], full_ptr[g + 1]
+            cuts = [c for c in gptr.tolist() if a <= c <= b]
+            sizes = np.diff(cuts)
+            assert len(sizes) == -(-(b - a) // mg)
+            assert sizes.max() <= mg and sizes.max() - sizes.min() <= 1
+    with pytest.raises(kv.KVLinkError):
+        kv.kvlink_group_spans(spans, max_group=-1)
+
+
 def test_load_stage_bytes(kv):
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_BF16, 8, 128, 1000) == 4 * 8 * 1000 * 128 * 2
     assert kv.kvlink_load_stage_bytes(kv.KVLINK_F32, 2, 64, 10) == 4 * 2 * 10 * 64 * 4

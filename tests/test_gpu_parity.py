@@ -863,11 +863,12 @@ def test_shared_reencode_equals_per_span_pool():
     requests): the document-major re-encode writes the same bytes as the
     per-span one, and is what the batch runs by default."""
     import torch
+    import paper_2502_16002_amd as kv
     from harness import PagedRun
     w = workloads.llama8b_paged()
     run = PagedRun(w)
     b = run.batch
-    assert b.shared_docs and b.n_groups == len(w.doc_table_len) < b.n_docs
+    assert b.shared_docs and len(w.doc_table_len) <= b.n_groups < b.n_docs
     run.k_dst.zero_()
     b.reencode(run.src_view, run.k_view, shared=False)
     per_span = run.k_dst.clone()
@@ -875,6 +876,19 @@ def test_shared_reencode_equals_per_span_pool():
     b.reencode(run.src_view, run.k_view)
     torch.cuda.synchronize()
     assert torch.equal(per_span.view(torch.int16), run.k_dst.view(torch.int16))
+    # every cut of the documents' runs of spans (one group per document, one
+    # span per group, groups of up to 2 or 3) writes the same bytes
+    spans = b.layout["spans"].reshape(-1, 6)
+    for mg in [0, 1, 2, 3]:
+        order, gptr = kv.kvlink_group_spans(spans, mg)
+        d_sp = torch.from_numpy(np.ascontiguousarray(spans[order])).cuda()
+        d_gp = torch.from_numpy(gptr).cuda()
+        run.k_dst.zero_()
+        kv.kvlink_reencode_keys_shared(b.dtype, b.n_layers, b.n_kv_heads, b.head_dim,
+                                       b.rope_theta, len(gptr) - 1, d_gp, d_sp, b.max_doc_len,
+                                       run.src_view, run.k_view)
+        torch.cuda.synchronize()
+        assert torch.equal(per_span.view(torch.int16), run.k_dst.view(torch.int16)), mg
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
