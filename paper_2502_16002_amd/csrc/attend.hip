@@ -590,7 +590,7 @@ bool make_attend_plan(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int head_d
     p->n_segments = sched.n_segments;
     p->table = sched.table;
     p->partials = sched.n_split_units > 0;
-    p->merge_in_launch = path == kPathWide && (sched.flags & KVLINK_PLAN_IN_LAUNCH) != 0;
+    p->merge_in_launch = path != kPathValu && (sched.flags & KVLINK_PLAN_IN_LAUNCH) != 0;
     if ((sched.flags & KVLINK_PLAN_IN_LAUNCH) && (sched.flags & KVLINK_PLAN_COMBINE)) return false;
     p->n_split = sched.n_split_units;
     const int64_t rows = (int64_t)n_new_total * n_q_heads;

@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "attend_common.h"
+#include "merge_launch.h"
 #include "mfma_ops.h"
 
 namespace kvlink {
@@ -52,8 +53,9 @@ struct DecodeSmem {
     static constexpr int wave = 2 * v_bytes;
     static_assert(o_bytes <= wave, "merge area inside the wave's stages");
     static constexpr int ml = 0;
+    static constexpr int flag = 1020;                      // the last-arrival flag
     static constexpr int base = 1024;
-    static_assert(kDW * kDR * 2 * 4 <= base, "(m, l) block");
+    static_assert(kDW * kDR * 2 * 4 <= flag, "(m, l) block");
     static constexpr int bytes = base + kDW * wave;
 };
 
@@ -76,8 +78,11 @@ __device__ __forceinline__ uint4 load16(const char* p) {
 }
 
 // One segment: tiles [tile_a, tile_b) of the keys of KV head h for rows
-// [rho0, rho0 + rows) of request s.  Every early return is uniform over the
-// workgroup.
+// [rho0, rho0 + rows) of request s, each wavefront taking every kDW-th
+// 32-key step.  A split unit's segment stores its partial, either for the
+// combine launch or, merged in this launch, with agent-coherent stores
+// followed by its arrival on the unit's counter; the last arrival merges the
+// unit's partials.  Every early return is uniform over the workgroup.
 template <int D, int kPolK, int kPolV>
 __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* smem,
                                                const int4 (&rec)[4]) {
@@ -90,19 +95,28 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
 
     const int s = rec[0].x, h = rec[0].y, rho0 = rec[0].z, rows = rec[0].w;
     const int tile_a = rec[1].x, tile_b = rec[1].y;
-    const int nseg = rec[1].z, seg_local = rec[1].w, part = rec[3].x;
+    const int nseg = rec[1].z, seg_local = rec[1].w, part = rec[3].x, unit = rec[3].z;
     const bool direct = nseg == 1;
+    const bool in_launch = !direct && p.merge_in_launch;
     const int n0 = rec[2].x, Tc = rec[2].y, cmax = rec[2].z, nvirt = rec[2].w;
     const int G = p.group;
     const int kbeg = tile_a * kTile;
-    if (kbeg >= nvirt || rows < 1) return;
+    // (a split segment merged in the launch must still arrive)
+    if (kbeg >= nvirt && !in_launch) return;
     const int kend = min(tile_b * kTile, nvirt);
-    const int n_steps = (kend - kbeg + kStep - 1) / kStep;
 
     constexpr int LPS = 2 * DS + VL;   // loads per step
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     unsigned char* vs = smem + DecodeSmem<D>::base + wave * DecodeSmem<D>::wave;
+
+    // the wavefront's steps, as key offsets v0 (-1: none left)
+    int stat_t = wave;
+    auto next_step = [&]() -> int {
+        const int v0 = kbeg + stat_t * kStep;
+        stat_t += kDW;
+        return v0 < kend ? v0 : -1;
+    };
 
     const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
     const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
@@ -121,11 +135,10 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     auto v_key = [&](int i) { return (64 * i + lane) / CH; };
     auto v_off = [&](int i) { return 16 * ((lane % CH) ^ (v_key(i) & (CH - 1))); };
 
-    // Loads of step j: K into r, then V into LDS stage st, with the cache
-    // policies the launch chose for the two views.
-    auto issue_k_as = [&](int j, StepRegs<D>& r, auto policy) {
+    // Loads of the step at v0: K into r, then V into LDS stage st, with the
+    // cache policies the launch chose for the two views.
+    auto issue_k_as = [&](int v0, StepRegs<D>& r, auto policy) {
         constexpr int pol = decltype(policy)::value;
-        const int v0 = kbeg + j * kStep;
         if (v0 + kStep <= fast_end) {
             int pg[2] = {0, 0};
             if (kp.table) {
@@ -147,9 +160,8 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
             }
         }
     };
-    auto issue_v_as = [&](int j, unsigned char* st, auto policy) {
+    auto issue_v_as = [&](int v0, unsigned char* st, auto policy) {
         constexpr int pol = decltype(policy)::value;
-        const int v0 = kbeg + j * kStep;
         if (v0 + kStep <= fast_end) {
             int pg[2] = {0, 0};
             if (vp.table) {
@@ -171,8 +183,8 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     };
     constexpr std::integral_constant<int, kPolK> pol_k{};
     constexpr std::integral_constant<int, kPolV> pol_v{};
-    auto issue_k = [&](int j, StepRegs<D>& r) { issue_k_as(j, r, pol_k); };
-    auto issue_v = [&](int j, unsigned char* st) { issue_v_as(j, st, pol_v); };
+    auto issue_k = [&](int v0, StepRegs<D>& r) { issue_k_as(v0, r, pol_k); };
+    auto issue_v = [&](int v0, unsigned char* st) { issue_v_as(v0, st, pol_v); };
     auto stage = [&](int parity) { return vs + parity * DecodeSmem<D>::v_bytes; };
 
     // rows of the unit: lane row lr (padding rows past `rows` see no key)
@@ -182,7 +194,7 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     const int vis = p.new_visible[n0 + tok];
     const int lo = row_ok ? min(vis, kend) : 0;              // cached keys v < lo
     const int hi = row_ok ? min(cmax + tok, kend - 1) : -1;  // new keys cmax <= v <= hi
-    const int tok_max = (rho0 + rows - 1) / G;
+    const int tok_max = (rho0 + max(rows, 1) - 1) / G;
     const int vis_min = p.new_visible[n0 + rho0 / G];
     const int vis_max = p.new_visible[n0 + tok_max];
     // a step no row sees (only possible at a unit's ends)
@@ -195,8 +207,8 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     // With the fused RoPE, the new rows among the segment's keys ([na, nb)
     // of the request's new tokens) are appended to the cache, the stores
     // waited for and the workgroup synchronised before any load that may
-    // read them: ahead of the prologue's loads when those reach the new rows,
-    // else right after them (the key loop has no barrier of its own).
+    // read them: ahead of the prologue's loads when those reach the new
+    // rows, else right after them (the key loop has no barrier of its own).
     const int na = max(kbeg, cmax) - cmax, nb = kend - cmax;
     const bool has_new = p.rope != nullptr && nb > na;
     const bool early_new = has_new && kbeg + 2 * kDW * kStep > cmax;
@@ -207,19 +219,20 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     }
 
     StepRegs<D> R0, R1;
-    int j = wave;
-    if (j < n_steps) {
-        issue_k(j, R0);
-        issue_v(j, stage(0));
+    int va = next_step();
+    if (va >= 0) {
+        issue_k(va, R0);
+        issue_v(va, stage(0));
     }
     // queries, B operand of S^T: row lr, dims 32ds + 8lg
     // (their rotation, with the fused RoPE, after the next step's loads
     // are issued)
     QRow<D> qrow;
     qrow.load(p, n0 + tok, h * G + rho % G, lg);
-    if (j + kDW < n_steps) {
-        issue_k(j + kDW, R1);
-        issue_v(j + kDW, stage(1));
+    int vb = va >= 0 ? next_step() : -1;
+    if (vb >= 0) {
+        issue_k(vb, R1);
+        issue_v(vb, stage(1));
     }
     bf16x8 qB[DS];
     {
@@ -244,26 +257,27 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     // wide-block kernel): lane (lg, lr) reads key 4lg + lr/4, chunk
     // 2dt + (lr/2)%2, half lr%2; the keys 16.. of the step sit 16 rows
     // further, stage 1 v_bytes further
-    uint32_t va[DT];
+    uint32_t va_lds[DT];
     {
         const uint32_t base = lds_addr(vs);
         const int key = 4 * lg + (lr >> 2);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             const int c = 2 * dt + ((lr >> 1) & 1);
-            va[dt] = base + key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
+            va_lds[dt] = base + key * (2 * D) + 16 * (c ^ (key & (CH - 1))) + 8 * (lr & 1);
         }
     }
 
-    // step jj from registers r and LDS stage `parity`; the loads of step
-    // j_next go into r once K has fed the products, and into the stage once
-    // its V has been read
-    auto run_step = [&](int jj, StepRegs<D>& r, auto parity, int j_next) {
+    // the step at v0 from registers r and LDS stage `parity`; `more`: the
+    // wavefront's following step is in flight behind it.  The loads of the
+    // step after that go into r once K has fed the products and into the
+    // stage once its V has been read; returns its v0 (-1: none).
+    auto run_step = [&](int v0, StepRegs<D>& r, auto parity, bool more) -> int {
         constexpr int par = decltype(parity)::value;
         // this step's loads are done when at most the next step's are
-        // outstanding (more loads after them only make the wait stricter)
-        if (jj + kDW < n_steps) wait_vm<LPS>(); else wait_vm<0>();
-        const int v0 = kbeg + jj * kStep;
+        // outstanding
+        if (more) wait_vm<LPS>(); else wait_vm<0>();
+        const int v_next = next_step();
         const bool live = !dead(v0);
         floatx4 sacc[2];
         if (live) {
@@ -276,21 +290,21 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
                                                                        qB[ds], sacc[kh], 0, 0, 0);
             }
         }
-        const bool more = j_next < n_steps;
-        if (more) issue_k(j_next, r);
+        const bool next_ok = v_next >= 0;
+        if (next_ok) issue_k(v_next, r);
         if (!live) {
-            if (more) issue_v(j_next, stage(par));
-            return;
+            if (next_ok) issue_v(v_next, stage(par));
+            return v_next;
         }
 
         // mask: lane group lg holds keys 16kh + 4lg + i of the step
-        const int vb = v0 + 4 * lg;
+        const int vb4 = v0 + 4 * lg;
         if (v0 + kStep > vis_min || v0 + kStep > cmax) {
 #pragma unroll
             for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int v = vb + 16 * kh + i;
+                    const int v = vb4 + 16 * kh + i;
                     const bool ok = v < lo || (v >= cmax && v <= hi);
                     sacc[kh][i] = ok ? sacc[kh][i] : -INFINITY;
                 }
@@ -325,26 +339,28 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
             lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[t]), ones, lsum,
                                                    false);
         }
-        // O^T += V^T P^T; the stage is free for step j_next once the reads
+        // O^T += V^T P^T; the stage is free for the next step once the reads
         // have returned
         uint2 vr[DT][2];
-        issue_vt<DT, par * DecodeSmem<D>::v_bytes, par * DecodeSmem<D>::v_bytes + 16 * 2 * D>(va, vr);
+        issue_vt<DT, par * DecodeSmem<D>::v_bytes, par * DecodeSmem<D>::v_bytes + 16 * 2 * D>(va_lds,
+                                                                                              vr);
         wait_vt(vr);
-        if (more) issue_v(j_next, stage(par));
+        if (next_ok) issue_v(v_next, stage(par));
         const bf16x8 b = as_bf16x8(uint4{pk[0], pk[1], pk[2], pk[3]});
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             const bf16x8 a = as_bf16x8(uint4{vr[dt][0].x, vr[dt][0].y, vr[dt][1].x, vr[dt][1].y});
             o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, o[dt], 0, 0, 0);
         }
+        return v_next;
     };
 
     constexpr std::integral_constant<int, 0> P0{};
     constexpr std::integral_constant<int, 1> P1{};
-    for (; j < n_steps; j += 2 * kDW) {
-        run_step(j, R0, P0, j + 2 * kDW);
-        if (j + kDW >= n_steps) break;
-        run_step(j + kDW, R1, P1, j + 3 * kDW);
+    while (va >= 0) {
+        va = run_step(va, R0, P0, vb >= 0);
+        if (vb < 0) break;
+        vb = run_step(vb, R1, P1, va >= 0);
     }
 
     // this wave's state: row sums over the four lane groups, then O, m and l
@@ -386,22 +402,42 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
         const int64_t orow = (int64_t)(n0 + rr / G) * p.n_q_heads + h * G + rr % G;
         // the output, or this segment's partial: O / l in bf16 (0 for a row
         // that saw no key of the segment) with (m, l) in float, row-major over
-        // the unit's segments
+        // the unit's segments; stored coherently when merged in this launch
         const float inv = L > 0.f ? 1.f / L : 0.f;
+        const uint32_t o01 = pack2(acc[0] * inv, acc[1] * inv);
+        const uint32_t o23 = pack2(acc[2] * inv, acc[3] * inv);
         const int64_t pi = (int64_t)part * kDR + (int64_t)r * nseg + seg_local;
-        bf16_t* dst = direct ? reinterpret_cast<bf16_t*>(p.out) + orow * D
-                             : reinterpret_cast<bf16_t*>(p.part_o) + pi * D;
-        *reinterpret_cast<uint2*>(dst + 4 * c) =
-            uint2{pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
-        if (c == 0) {
-            if (direct) {
-                if (p.lse) p.lse[orow] = (M + log2f(L)) * kLn2;
-            } else {
+        if (direct) {
+            *reinterpret_cast<uint2*>(reinterpret_cast<bf16_t*>(p.out) + orow * D + 4 * c) =
+                uint2{o01, o23};
+            if (c == 0 && p.lse) p.lse[orow] = (M + log2f(L)) * kLn2;
+        } else if (in_launch) {
+            store_agent(reinterpret_cast<bf16_t*>(p.part_o) + pi * D + 4 * c, o01, o23);
+            if (c == 0) store_agent(p.part_ml + pi * 2, __float_as_uint(M), __float_as_uint(L));
+        } else {
+            *reinterpret_cast<uint2*>(reinterpret_cast<bf16_t*>(p.part_o) + pi * D + 4 * c) =
+                uint2{o01, o23};
+            if (c == 0) {
                 p.part_ml[pi * 2] = M;
                 p.part_ml[pi * 2 + 1] = L;
             }
         }
     }
+    if (!in_launch) return;
+
+    // arrival: every partial store of the workgroup has completed (each wave
+    // waits for its own, then the barrier), then one increment of the unit's
+    // arrival counter, which wraps to 0 on the last arrival, which merges
+    wait_vm_all();
+    __syncthreads();
+    int* flag = reinterpret_cast<int*>(smem + DecodeSmem<D>::flag);
+    if (threadIdx.x == 0) {
+        const unsigned old = __builtin_amdgcn_atomic_inc32(p.counters + unit, (unsigned)(nseg - 1),
+                                                           __ATOMIC_RELAXED, "agent");
+        *flag = old == (unsigned)(nseg - 1);
+    }
+    __syncthreads();
+    if (*flag) merge_unit<D, kDR, 64 * kDW>(p, part, rows, nseg, h, rho0, n0);
 }
 
 // A persistent workgroup runs its chain of segments: record blockIdx.x
@@ -411,7 +447,7 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
 // through the caches, since its pages may be shared between requests (the
 // values of a shared document pool).
 template <int D, int kPolK, int kPolV>
-__global__ __launch_bounds__(64 * kDW, 2) void attend_decode_kernel(KParams p) {
+__global__ __launch_bounds__(64 * kDW, 1) void attend_decode_kernel(KParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[DecodeSmem<D>::bytes];
     for (int g = blockIdx.x, first = 1; g >= 0 && g < p.n_segments; first = 0) {
         int4 rec[4];

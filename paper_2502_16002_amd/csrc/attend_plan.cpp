@@ -107,10 +107,14 @@ struct CostModel {
 // segment's partial stores add about 1.5 us and the combine about 6 us plus
 // the partial traffic at an effective ~6 TB/s.
 //
-// Decode kernel: two workgroups per compute unit sharing the unit's HBM
-// stream, so a tile (64 keys of K and V) costs its bytes at an eighth of a
-// compute unit's share of ~6 TB/s, plus the start of a segment (its first
-// loads' latency).  VALU kernel: fp32, a fixed cost per tile.
+// Decode kernel: one workgroup per compute unit (two would share its HBM
+// stream and measured slower), a tile (64 keys of K and V) costing its bytes
+// at a compute unit's share of ~6 TB/s, plus the start of a segment (its
+// first loads' latency).  Split units: the combine launch costs about 3.4 us
+// plus the partials' traffic; merged in the launch, a split segment's
+// coherent stores and arrival add about 0.9 us and the last arrival's merge
+// 1 us plus the unit's partials at ~0.013 MB/us (a 32-segment unit: 4.6 us in
+// all, two segments: 2.1 us).  VALU kernel: fp32, a fixed cost per tile.
 CostModel cost_model(AttendPath path, int head_dim, int row_block, bool in_launch) {
     const bool d128 = head_dim == 128;
     const double f = d128 ? 1.0 : 0.63;   // head_dim 64: fewer bytes and products per key
@@ -133,8 +137,11 @@ CostModel cost_model(AttendPath path, int head_dim, int row_block, bool in_launc
         }
         return cm;
     }
-    if (path == kPathDecode)
-        return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 0.0, 2, 0.0, 0, 0, 6.0, 6.0e6};
+    if (path == kPathDecode) {
+        if (in_launch)
+            return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 0.9, 1, 0.0, 1.0, 1.27e4, 0, 0};
+        return {3.0, 0.0, d128 ? 2.8 : 1.5, 0.0, 0.0, 0.0, 1, 0.0, 0, 0, 3.4, 6.0e6};
+    }
     return {4.0, 0.0, d128 ? 1.0 : 0.6, 0.0, 0.0, 0.0, d128 ? 2 : 4, 0.0, 0, 0, 4.0, 6.0e6};
 }
 
@@ -412,10 +419,10 @@ int build_attend_schedule(kvlink_dtype dt, int n_q_heads, int n_kv_heads, int he
         rbs = {row_block};
     }
     const int elem = dt == KVLINK_BF16 ? 2 : 4;
-    // merge of split units: in the split launch (wide kernel only) or by the
-    // combine launch; the flags may force one
+    // merge of split units: in the split launch (wide and decode kernels) or
+    // by the combine launch; the flags may force one
     std::vector<bool> modes;
-    if (path != kPathWide || (flags & KVLINK_PLAN_COMBINE)) modes = {false};
+    if (path == kPathValu || (flags & KVLINK_PLAN_COMBINE)) modes = {false};
     else if (flags & KVLINK_PLAN_IN_LAUNCH) modes = {true};
     else modes = {true, false};
     if ((flags & KVLINK_PLAN_IN_LAUNCH) && row_block == 256) {

@@ -547,17 +547,22 @@ def test_attend_schedule(kv, name):
         assert chosen.n_workgroups >= 200
     # near ties of the estimate go to the cut with the most workgroups: the
     # 10-document workload fills every compute unit (measured faster than
-    # the 208 workgroups of the lowest estimate), a decoding step all slots
-    if name in ("llama8b-32layer-10doc", "llama8b-paged-16req"):
+    # the 208 workgroups of the lowest estimate), a decoding step takes one
+    # workgroup per compute unit
+    if name in ("llama8b-32layer-10doc", "llama8b-paged-16req", "llama8b-decode-40x512"):
         assert chosen.n_workgroups == 256
+    # split units of a decoding step: 32 segments each over the long cache
+    # merge faster in the combine launch, the pool's two each in the launch
     if name == "llama8b-decode-40x512":
-        assert chosen.n_workgroups == 512
+        assert chosen.flags & kv.KVLINK_PLAN_COMBINE
+    if name == "llama8b-paged-decode-16req":
+        assert chosen.flags & kv.KVLINK_PLAN_IN_LAUNCH
     # the kernel: 16-row units for bf16 batches of at most 16 rows per KV
     # head (decoding steps), 256-row units for the other bf16 batches
     if w.dtype == "bf16":
         assert chosen.row_block in ((256, 128, 64) if wide else (16,))
     if w.decode:
-        assert chosen.n_workgroups >= 256     # two workgroups per compute unit fit
+        assert chosen.n_workgroups >= 256     # every compute unit busy
 
 
 @settings(max_examples=80, deadline=None)

@@ -827,14 +827,23 @@ def test_decode_step_long_cache():
 @pytest.mark.parametrize("head_dim", [64, 128])
 def test_decode_kernel_layouts(doc_len, link_count, n_query, head_dim):
     """Units of at most 16 rows (group 4, up to 4 new tokens) on the decode
-    kernel, for several workgroup counts."""
+    kernel, for several workgroup counts, split units merged in the launch
+    or by the combine launch, with the new rows' RoPE and append inside the
+    split launch or before it."""
+    import paper_2502_16002_amd as kv
     w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2,
                          head_dim=head_dim, dtype="bf16", rope_theta=5e5, seed=23)
-    for n_wg in [0, 1, 3, 1 << 20]:
-        run = ContiguousRun(w, layers=[0], n_workgroups=n_wg)
-        assert run.batch.plan.row_block == 16
-        run.run()
-        _check_attend(run, 0, tag=f"decode{doc_len}/{head_dim}/{n_wg}")
+    for flags in [kv.KVLINK_PLAN_XCD | kv.KVLINK_PLAN_IN_LAUNCH, kv.KVLINK_PLAN_COMBINE]:
+        for fused in [True, False]:
+            for n_wg in [0, 1, 3, 1 << 20]:
+                run = ContiguousRun(w, layers=[0], n_workgroups=n_wg, plan_flags=flags,
+                                    fused_rope=fused)
+                assert run.batch.plan.row_block == 16
+                run.run()
+                tag = f"decode{doc_len}/{head_dim}/{n_wg}/{flags}/{fused}"
+                _check_attend(run, 0, tag=tag)
+                _check_append(run, 0)
+                _counters_zero(run)
 
 
 def test_decode_step_paged_pool():
