@@ -77,6 +77,9 @@ def parse():
                     help="kvlink_attend_make_plan flags (default: the runtime's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-host-load", action="store_true")
+    ap.add_argument("--host-load-only", action="store_true",
+                    help="only the host-to-device load of the workload's stored caches "
+                         "(copies, direct and staged forms), for a trace")
     ap.add_argument("--kernel-iters", type=int, default=20)
     ap.add_argument("--eager", action="store_true",
                     help="time steps launched from Python instead of a captured HIP graph")
@@ -647,6 +650,10 @@ def main():
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workloads.get(args.workload)
+    if args.host_load_only:
+        st = Setup(w, args.workgroups)
+        print(json.dumps({"workload": w.name, "host_load": host_load(st)}), flush=True)
+        return
     head = measure(w, args, headline=True)
     res = {
         "metric": METRIC,

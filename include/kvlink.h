@@ -306,15 +306,21 @@ size_t kvlink_load_stage_bytes(kvlink_dtype dtype, int32_t n_kv_heads, int32_t h
  *     not used).  The arrays must be pinned and mapped for the device
  *     (hipHostMalloc with default flags); otherwise KVLINK_ERR_INVALID_ARG
  *     and nothing is launched.
- *   d_stage != NULL (staged): the staging area is a ring of
- *     min(n_layers, stage_bytes / slot) one-layer slots (slot as
- *     kvlink_load_stage_bytes).  Layer l is copied to slot l % n_slots on
- *     copy_stream and re-encoded from it on compute_stream.  With two
- *     streams, events order them: the re-encode of layer l waits for its
- *     copy, the copy waits for the re-encode that last read its slot, and the
- *     first copies wait for the work compute_stream held when the call was
- *     made (an earlier call's re-encodes may still read the slots).  With
- *     copy_stream == compute_stream the stream itself orders everything.
+ *   d_stage != NULL (staged): the staging area holds cap =
+ *     min(n_layers, stage_bytes / slot) layers (slot as
+ *     kvlink_load_stage_bytes: one layer's keys and values), used as a ring
+ *     of floor(cap / G) chunks of G consecutive layers, G the fewest layers
+ *     whose keys reach 64 MiB, at most cap / 2 (so the ring has two chunks
+ *     or more).  Chunk c is copied (one copy for its keys, one for its
+ *     values) to ring entry c % n_ring on copy_stream and re-encoded from it
+ *     on compute_stream.  With two streams, events order them: the
+ *     re-encode of a chunk waits for its copy, the copy waits for the
+ *     re-encode that last read its entry, and the first copies wait for the
+ *     work compute_stream held when the call was made (an earlier call's
+ *     re-encodes may still read the entries).  With copy_stream ==
+ *     compute_stream the stream itself orders everything.  Copies and
+ *     cross-stream waits carry a fixed cost each; a staging area of many
+ *     layers keeps them few (with two slots every layer is a chunk).
  *     The events are created on a thread's first staged call on a device
  *     and kept for reuse by later calls of that thread.
  * The call enqueues the work and returns.

@@ -476,15 +476,24 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
             return ok();
         }
 
-        // Staged: a ring of as many one-layer slots as the staging area holds
-        // (at most one per layer).  Layer l goes to slot l % n_slots; its
-        // copy waits until the re-encode of layer l - n_slots has released
-        // the slot, and its re-encode waits for its copy.
-        const int n_slots = (int)std::min<size_t>((size_t)n_layers, stage_bytes / slot_bytes);
-        auto slot_view = [&](char* base) {
-            kvlink::View v = stored_view(base, 0);
-            return v;
-        };
+        // Staged: the staging area holds `cap` layers (at least two); they
+        // form a ring of chunks of G consecutive layers, G as large as a
+        // copy of at least kMinCopyBytes of keys needs while the ring keeps
+        // at least two chunks.  Chunk c (layers [cG, cG + G)) goes to ring
+        // entry c % n_ring as one keys copy and one values copy (the host
+        // arrays are layer-major, so a chunk is contiguous in each); its
+        // copy waits until the re-encode of chunk c - n_ring has released
+        // the entry, and its re-encode (one launch for the chunk's layers)
+        // waits for its copy.  Few large copies: each copy and each
+        // cross-stream wait carries a fixed cost.
+        constexpr size_t kMinCopyBytes = 64u << 20;
+        const int cap = (int)std::min<size_t>((size_t)n_layers, stage_bytes / slot_bytes);
+        const int G = std::max(1, std::min<int>(
+                                      (int)((kMinCopyBytes + layer_bytes - 1) / layer_bytes),
+                                      cap / 2));
+        const int n_ring = cap / G;
+        const size_t chunk_bytes = (size_t)G * layer_bytes;   // keys (or values) of a chunk
+        const int64_t ls = (int64_t)n_kv_heads * stored_rows * head_dim;
         auto layer_of = [&](const kvlink_kv_view& v, int l) {
             kvlink::View d = to_view(v);
             d.base += (int64_t)l * v.layer_stride * (int64_t)es;
@@ -492,34 +501,36 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
         };
         const bool two = cs != ks;
         hipEvent_t* ev = nullptr;
-        hipError_t e = two ? stage_events(n_slots, &ev) : hipSuccess;
-        // the first copies reuse slots that the re-encodes of an earlier call
-        // on compute_stream may still be reading
+        hipError_t e = two ? stage_events(n_ring, &ev) : hipSuccess;
+        // the first copies reuse entries that the re-encodes of an earlier
+        // call on compute_stream may still be reading
         if (two && e == hipSuccess) e = hipEventRecord(ev[0], ks);
         if (two && e == hipSuccess) e = hipStreamWaitEvent(cs, ev[0], 0);
-        for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
-            const int slot = l % n_slots;
+        const int n_chunks = (n_layers + G - 1) / G;
+        for (int c = 0; c < n_chunks && e == hipSuccess; ++c) {
+            const int l0 = c * G, nl = std::min(G, n_layers - l0);
+            const int slot = c % n_ring;
             hipEvent_t loaded = two ? ev[1 + 2 * slot] : nullptr;
             hipEvent_t freed = two ? ev[2 + 2 * slot] : nullptr;
-            char* k_slot = reinterpret_cast<char*>(d_stage) + (size_t)slot * slot_bytes;
-            char* v_slot = k_slot + layer_bytes;
-            if (two && l >= n_slots) e = hipStreamWaitEvent(cs, freed, 0);
+            char* k_slot = reinterpret_cast<char*>(d_stage) + (size_t)slot * 2 * chunk_bytes;
+            char* v_slot = k_slot + chunk_bytes;
+            if (two && c >= n_ring) e = hipStreamWaitEvent(cs, freed, 0);
             if (e == hipSuccess)
-                e = hipMemcpyAsync(k_slot, reinterpret_cast<const char*>(h_k) + l * layer_bytes,
-                                   layer_bytes, hipMemcpyHostToDevice, cs);
+                e = hipMemcpyAsync(k_slot, reinterpret_cast<const char*>(h_k) + l0 * layer_bytes,
+                                   (size_t)nl * layer_bytes, hipMemcpyHostToDevice, cs);
             if (e == hipSuccess)
-                e = hipMemcpyAsync(v_slot, reinterpret_cast<const char*>(h_v) + l * layer_bytes,
-                                   layer_bytes, hipMemcpyHostToDevice, cs);
+                e = hipMemcpyAsync(v_slot, reinterpret_cast<const char*>(h_v) + l0 * layer_bytes,
+                                   (size_t)nl * layer_bytes, hipMemcpyHostToDevice, cs);
             if (two && e == hipSuccess) e = hipEventRecord(loaded, cs);
             if (two && e == hipSuccess) e = hipStreamWaitEvent(ks, loaded, 0);
             if (e == hipSuccess && work)
-                e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
-                                            d_spans, max_span_len, slot_view(k_slot),
-                                            layer_of(k_dst, l), rot, ks);
+                e = kvlink::launch_reencode(dtype, head_dim, nl, n_kv_heads, freqs, n_spans,
+                                            d_spans, max_span_len, stored_view(k_slot, ls),
+                                            layer_of(k_dst, l0), rot, ks);
             if (e == hipSuccess && work)
-                e = kvlink::launch_reencode(dtype, head_dim, 1, n_kv_heads, freqs, n_spans,
-                                            d_spans, max_span_len, slot_view(v_slot),
-                                            layer_of(v_dst, l), kvlink::kReencodeCopy, ks);
+                e = kvlink::launch_reencode(dtype, head_dim, nl, n_kv_heads, freqs, n_spans,
+                                            d_spans, max_span_len, stored_view(v_slot, ls),
+                                            layer_of(v_dst, l0), kvlink::kReencodeCopy, ks);
             if (two && e == hipSuccess) e = hipEventRecord(freed, ks);
         }
         if (e != hipSuccess)
