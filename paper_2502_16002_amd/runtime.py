@@ -170,19 +170,21 @@ class Batch:
                                     self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
                                     d_stored_pos, stored_pos_stride, src_view, dst_view, stream)
 
-    def load_stage_bytes(self, stored_rows, n_slots=2):
-        """Bytes of a staging ring of n_slots one-layer slots."""
+    def load_stage_bytes(self, stored_rows, n_slots=None):
+        """Bytes of a staging area of n_slots layers (default: every layer,
+        so the load runs as two large chunks; two slots make every layer a
+        chunk, several times slower)."""
         return kvlink_load_stage_bytes(self.dtype, self.n_kv_heads, self.head_dim, stored_rows,
-                                       n_slots)
+                                       self.n_layers if n_slots is None else n_slots)
 
     def load_and_reencode(self, h_k, h_v, stored_rows, stage, k_view, v_view, literal=False,
                           copy_stream=None, compute_stream=None):
         """Stored caches in pinned host memory, [n_layers][H_kv][stored_rows][d]:
         with stage None the kernels read them directly (one re-encode and one
-        value-gather launch for all layers); with a staging tensor (a ring
-        of as many one-layer slots as it holds) they are copied layer by
-        layer on copy_stream while compute_stream (torch's current stream
-        when None) re-encodes the layers already copied."""
+        value-gather launch for all layers); with a staging tensor they are
+        copied in chunks of consecutive layers (a ring over the layers it
+        holds) on copy_stream while compute_stream (torch's current stream
+        when None) re-encodes the chunks already copied."""
         kvlink_load_and_reencode(self.dtype, self.n_layers, self.n_kv_heads, self.head_dim,
                                  self.rope_theta, self.n_docs, self.d_spans, self.max_doc_len,
                                  h_k, h_v, stored_rows, stage,

@@ -271,11 +271,15 @@ def _load(run, h_k, h_v, way, literal, n_slots=2, k2=None, v2=None, copy=None):
 
 @pytest.mark.parametrize("literal,way,n_slots", [(0, "direct", 2), (1, "direct", 2),
                                                  (0, "staged", 2), (1, "staged", 2),
-                                                 (0, "staged", 5), (0, "staged_one_stream", 2)])
+                                                 (0, "staged", 5), (0, "staged", 7),
+                                                 (1, "staged", 32),
+                                                 (0, "staged_one_stream", 2)])
 def test_load_and_reencode_from_host(literal, way, n_slots):
     """All 32 layers of the 10-document workload loaded from pinned host
     memory, read directly by the kernels or copied through a staging ring
-    (copies on one stream, re-encodes on another, or both on one): the keys
+    (copies on one stream, re-encodes on another, or both on one; staging
+    areas of 2, 5, 7 and 32 layers: chunks of 1, 2, 3 and 16 layers, the
+    ring wrapping and the last chunk short for 7): the keys
     against the oracle (every key of four layers: R(delta_i), or R(g_i + t)
     for keys cached without rotation), bit for bit equal to the
     device-resident entry point on every layer; the values equal the stored
