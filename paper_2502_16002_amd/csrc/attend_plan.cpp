@@ -99,8 +99,10 @@ struct CostModel {
 // loads and stores per 64 rows (about 0.9 us each).
 //
 // 128- and 64-row units: a segment's record and prologue (queries and the
-// first tile) take about 5.1 and 3.6 us; a tile about 1.5 and 1.1 us when all
-// its steps are live.  A split segment merged in the launch adds its
+// first tile) take about 5.1 and 3.6 us; a tile about 1.5 and 0.86 us, with
+// little dependence on how many of its steps are live (a per-workgroup
+// timeline fit over the 10-document workload: loop = 0.15 + 1.51 x tiles and
+// 1.9 + 0.86 x tiles, residual sd 0.6 and 0.5 us).  A split segment merged in the launch adds its
 // partial's coherent stores and the arrival (about 4.2 and 2.6 us; 3 us for
 // 256 rows); the last arrival's merge reads the unit's partials at about
 // 0.1 MB/us after 2 us.  Merged by the combine launch instead, a split
@@ -123,9 +125,9 @@ CostModel cost_model(AttendPath path, int head_dim, int row_block, bool in_launc
         if (row_block == 256)
             cm = {0.8, 3.67 * f, 1.61 * f, 0.65 * f, 1.97 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
         else if (row_block == 128)
-            cm = {5.1, 0.0, 0.9 * f, 0.6 * f, 0.5 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
+            cm = {5.1, 0.0, 1.4 * f, 0.1 * f, 0.0, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
         else
-            cm = {3.6, 0.0, 0.7 * f, 0.4 * f, 0.3 * f, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
+            cm = {3.6, 0.0, 0.8 * f, 0.06 * f, 0.0, 0.0, 1, 0.9 * f, 0, 0, 0, 0};
         if (in_launch) {
             cm.split_us = row_block == 256 ? 3.0 : row_block == 128 ? 4.2 : 2.6;
             cm.merge_us = 2.0;
