@@ -156,6 +156,26 @@ class Setup:
         self.batch.attend(l, self.q[l], self.kn[l], self.vn[l], self.dst_views[i],
                           self.v_views[i], self.out, self.lse, stages=stages, workspace=workspace)
 
+    def time_fused_reencode(self, iters):
+        """The re-encode folded into the split attention: each copy's cache
+        gets the stored keys at the request's rows (its re-encoded rows
+        overwritten), and every layer's attention re-encodes them as its
+        tiles are staged.  Microseconds per layer, the attention of every
+        layer over every copy captured in one HIP graph, as the separate
+        path's attention is timed."""
+        import torch
+        L, C = self.w.n_layers, self.n_copies
+        for i in range(C):
+            self.k_dst[i][:, :, 0, :self.R] = self.k_src[i]
+
+        def attend_fused(l, i):
+            self.batch.attend(l, self.q[l], self.kn[l], self.vn[l], self.dst_views[i],
+                              self.v_views[i], self.out, self.lse, fused_reencode=True)
+        g = capture(lambda: [attend_fused(l, i) for i in range(C) for l in range(L)])
+        g.replay()
+        torch.cuda.synchronize()
+        return time_region(lambda i: g.replay(), max(1, iters // C)) / (L * C) * 1000.0
+
     def step(self, i=0):
         # the batch's RoPE table (one launch; a no-op with the separate RoPE)
         self.batch.build_rope_table()
@@ -188,7 +208,12 @@ class Setup:
             self.attend(l, workspace=self.ws_layers[l])
         out = {"rope": None}
         # with the fused RoPE the RoPE stage launches nothing
-        names = [("split", 2), ("combine", 4)]
+        names = [("split", 2)]
+        plan = self.batch.plan
+        if plan.n_split_units > 0 and not (plan.flags & PLAN_IN_LAUNCH):
+            names.append(("combine", 4))    # else the combine stage launches nothing
+        else:
+            out["combine"] = 0.0
         if self.batch.rope_table is None:
             names.insert(0, ("rope", 1))
         for name, stage in names:
@@ -630,6 +655,18 @@ def measure(w, args, headline):
             "us_per_launch": round(lit_ms * 1000, 2),
             "gbps": round(alg["reencode_bytes"] / (lit_ms * 1e-3) / 1e9, 1),
             "frac": round(alg["reencode_bytes"] / (lit_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+    # the re-encode folded into the attention (wide bf16 kernel), against the
+    # separate re-encode plus attention, per layer
+    from paper_2502_16002_amd import KVLINK_FUSED_MAX_SPANS
+    if (not w.pool and not w.decode and w.dtype == "bf16" and b.plan.row_block in (256, 128, 64)
+            and b.max_spans_per_seq <= KVLINK_FUSED_MAX_SPANS):
+        fused_us = st.time_fused_reencode(it)
+        sep_us = re_ms * 1000 / L + at_ms * 1000
+        res["fused_reencode"] = {
+            "us_per_layer_fused_attention": round(fused_us, 2),
+            "us_per_layer_separate": round(sep_us, 2),
+            "separate_parts": "re-encode per layer + attention (all stages, one call)",
+            "selected": "fused" if fused_us < sep_us else "separate"}
     if headline and not w.pool and not w.decode and not args.no_host_load:
         res["host_load"] = host_load(st)
     if not args.no_cpu_baseline and (headline or w.pool):

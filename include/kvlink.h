@@ -622,6 +622,48 @@ kvlink_status kvlink_attend_new_tokens_noalloc(
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
     void* stream);
 
+/*
+ * kvlink_attend_new_tokens_fused — kvlink_attend_new_tokens with the
+ * positional re-encode of the cached keys (Sec. 2.2) folded into the split
+ * launch: k_cache holds, at every request's cached rows, the keys as stored
+ * (rotated at their documents' own positions, not yet re-encoded), and the
+ * kernel rotates each cached key of span i by R(delta_i) in LDS, once per
+ * workgroup, as its 64-key tile arrives and before any product reads it.
+ * The rotation uses the re-encode launch's routine and angles, so out and lse
+ * equal, bit for bit, kvlink_reencode_keys over the same spans into a cache
+ * of the same layout followed by kvlink_attend_new_tokens with the same plan.
+ * The cached rows of k_cache are only read; the new tokens' rows are handled
+ * (appended, with the RoPE inside the split launch when the plan has a rope
+ * table) as by kvlink_attend_new_tokens.  The separate re-encode's write of
+ * the re-encoded keys is skipped; every call rotates again.
+ *
+ *   d_spans, d_seq_span_ptr  device: request s's spans are d_spans[
+ *                            d_seq_span_ptr[s] .. d_seq_span_ptr[s + 1]),
+ *                            in increasing dst_row, not overlapping (as
+ *                            kvlink_build_layout makes them); a cached row
+ *                            of request s in none of them is used as stored.
+ *                            dst_row, len and delta are read (dst rows are
+ *                            request s's rows of k_cache)
+ *   max_spans_per_seq        the most spans of any request, at most
+ *                            KVLINK_FUSED_MAX_SPANS (the (cos, sin) tables of
+ *                            a request's spans are held in LDS)
+ * Other arguments, layouts and errors as kvlink_attend_new_tokens; also
+ * KVLINK_ERR_UNSUPPORTED for a plan not on the wide bf16 kernel (row_block
+ * 256, 128 or 64) or more than KVLINK_FUSED_MAX_SPANS spans per request,
+ * and KVLINK_ERR_INVALID_ARG for NULL span arrays or a negative count.
+ */
+#define KVLINK_FUSED_MAX_SPANS 48
+
+kvlink_status kvlink_attend_new_tokens_fused(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
+    const kvlink_span* d_spans, const int32_t* d_seq_span_ptr, int32_t max_spans_per_seq,
+    void* workspace, size_t workspace_bytes, void* stream);
+
 /* Message of the last non-OK status on the calling thread ("" if none). */
 const char* kvlink_last_error(void);
 

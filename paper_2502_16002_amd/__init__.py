@@ -111,6 +111,9 @@ def _load():
     lib.kvlink_attend_new_tokens.restype = ctypes.c_int
     lib.kvlink_attend_new_tokens_noalloc.argtypes = lib.kvlink_attend_new_tokens.argtypes[:-3] + [vp]
     lib.kvlink_attend_new_tokens_noalloc.restype = ctypes.c_int
+    lib.kvlink_attend_new_tokens_fused.argtypes = (lib.kvlink_attend_new_tokens.argtypes[:-3] +
+                                                   [vp, vp, i32, vp, sz, vp])
+    lib.kvlink_attend_new_tokens_fused.restype = ctypes.c_int
     lib.kvlink_attend_stages.argtypes = lib.kvlink_attend_new_tokens.argtypes + [ctypes.c_uint32]
     lib.kvlink_attend_stages.restype = ctypes.c_int
     lib.kvlink_attend_rope_table.argtypes = [i32, f64, i32, vp, vp, vp]
@@ -314,6 +317,22 @@ def kvlink_attend_new_tokens(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta,
 
 
 KVLINK_NOALLOC_SCRATCH_BYTES = 32 << 20   # as include/kvlink.h
+KVLINK_FUSED_MAX_SPANS = 48                # as include/kvlink.h
+
+
+def kvlink_attend_new_tokens_fused(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta,
+                                   softmax_scale, n_seqs, n_new_total, max_new, max_cached,
+                                   d_seq_new_ptr, d_seq_cached, d_new_pos, d_new_visible, q_new,
+                                   k_new, v_new, k_cache, v_cache, layer, out, lse, plan, d_spans,
+                                   d_seq_span_ptr, max_spans_per_seq, workspace, workspace_bytes,
+                                   stream=None):
+    _check(_lib.kvlink_attend_new_tokens_fused(
+        int(dtype), int(n_q_heads), int(n_kv_heads), int(head_dim), float(rope_theta),
+        float(softmax_scale), int(n_seqs), int(n_new_total), int(max_new), int(max_cached),
+        _ptr(d_seq_new_ptr), _ptr(d_seq_cached), _ptr(d_new_pos), _ptr(d_new_visible),
+        _ptr(q_new), _ptr(k_new), _ptr(v_new), k_cache, v_cache, int(layer), _ptr(out),
+        _ptr(lse), plan, _ptr(d_spans), _ptr(d_seq_span_ptr), int(max_spans_per_seq),
+        _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
 def kvlink_attend_new_tokens_noalloc(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta,

@@ -512,6 +512,9 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
     p.q_new = a.q_new;
     p.k_new = a.k_new;
     p.v_new = a.v_new;
+    p.fuse_spans = pl.path == kPathWide ? a.fuse_spans : nullptr;
+    p.fuse_span_ptr = a.fuse_span_ptr;
+    p.freqs = a.freqs;
 
     hipError_t e = hipSuccess;
     if ((stages & KVLINK_STAGE_ROPE) && !fused) {

@@ -23,27 +23,6 @@ __device__ __forceinline__ int seq_of(const int32_t* seq_new_ptr, int n_seqs, in
     return lo;
 }
 
-// RoPE of 16 bytes of each half of a head vector (Sec. 2.2; dims j and
-// j + D/2 form a pair): lo holds dims j.., hi dims j + D/2.., c and s the
-// cos/sin of their angles.  Every kernel that rotates new tokens goes
-// through this one routine, so the fused and the separate RoPE produce the
-// same bytes.
-template <typename T>
-__device__ __forceinline__ void rope_rotate16(const uint4& lo, const uint4& hi, const float* c,
-                                              const float* s, uint4& x_out, uint4& y_out) {
-    constexpr int E = 16 / (int)sizeof(T);
-    float a[E], b[E], x[E], y[E];
-    unpack16<T>(lo, a);
-    unpack16<T>(hi, b);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        x[e] = __builtin_fmaf(a[e], c[e], -(b[e] * s[e]));
-        y[e] = __builtin_fmaf(a[e], s[e], b[e] * c[e]);
-    }
-    x_out = pack16<T>(x);
-    y_out = pack16<T>(y);
-}
-
 // Eight (cos, sin) pairs of a rope table row from entry j (64 bytes).
 __device__ __forceinline__ void rope_table8(const float2* row, int j, float* c, float* s) {
     const float4* t = reinterpret_cast<const float4*>(row + j);
@@ -108,7 +87,19 @@ struct KParams {
     const void* q_new;
     const void* k_new;
     const void* v_new;
+    // With fuse_spans (wide kernel), the cached keys are read as stored and
+    // re-encoded as their tiles are staged: request s's spans are
+    // fuse_spans[fuse_span_ptr[s] .. fuse_span_ptr[s + 1]) (dst_row order,
+    // at most kMaxFuseSpans used), and a cached key in span i is rotated by
+    // R(delta_i) (angles from freqs); NULL: the keys are used as read.
+    const kvlink_span* fuse_spans;
+    const int32_t* fuse_span_ptr;
+    RopeFreqs freqs;
 };
+
+// Spans of one request the fused re-encode holds (their cos/sin tables sit
+// in LDS beside the wide kernel's ring).
+constexpr int kMaxFuseSpans = KVLINK_FUSED_MAX_SPANS;
 
 static_assert(kSegRecord == 16, "segment records are read as four int4");
 static_assert(kUnitRecord == 8, "unit records are read as two int4");

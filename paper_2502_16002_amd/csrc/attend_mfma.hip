@@ -86,6 +86,18 @@ struct Smem {
     static constexpr int bytes = base + kStages * stage;
 };
 
+// LDS of the fused re-encode, after the ring: the (cos, sin) table of every
+// span of the request ([kMaxFuseSpans][D/2]) and the spans' first and end
+// rows and deltas.
+template <int D>
+struct FuseSmem {
+    static constexpr int cs = 0;
+    static constexpr int start = cs + kMaxFuseSpans * (D / 2) * 8;
+    static constexpr int end = start + kMaxFuseSpans * 4;
+    static constexpr int delta = end + kMaxFuseSpans * 4;
+    static constexpr int bytes = delta + kMaxFuseSpans * 4;
+};
+
 // Shape of a unit: kRT 16-row tiles per wavefront and kKG key groups; the
 // wavefronts of a group own kRB rows between them.
 template <int kRT_, int kKG_>
@@ -102,7 +114,7 @@ struct Shape {
 // One segment of a unit: tiles [tile_a, tile_b) of the key range of KV head
 // h's rows [rho0, rho0 + rows) of request s, from its schedule record.
 // Every early return is uniform over the workgroup.
-template <int D, class S>
+template <int D, class S, bool kFuse>
 __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem,
                                                const int4 (&rec)[4]) {
     constexpr int kRT = S::kRT, kKG = S::kKG, kRW = S::kRW, kRB = S::kRB;
@@ -230,6 +242,19 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // issued, so that when every workgroup starts at once tile 0 is not
     // queued behind them (its products are what the loop waits for; issuing
     // tiles 1..3 with tile 0 measured no faster on any workload).
+    // Fused re-encode: the request's spans are read first (one per thread),
+    // so that waiting for them never waits for tile 0
+    unsigned char* fsm = smem + Smem<D>::bytes;
+    int f_n = 0;
+    int4 f_sp = {0, 0, 0, 0};
+    if constexpr (kFuse) {
+        const int b0 = load_uniform(p.fuse_span_ptr + s);
+        f_n = min(max(load_uniform(p.fuse_span_ptr + s + 1) - b0, 0), kMaxFuseSpans);
+        if ((int)threadIdx.x < f_n) {
+            const kvlink_span sp = p.fuse_spans[b0 + threadIdx.x];
+            f_sp = int4{sp.dst_row, sp.dst_row + sp.len, sp.delta, 0};
+        }
+    }
     int tok[kRT];
     QRow<D> qrow[kRT];
 #pragma unroll
@@ -239,6 +264,26 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         qrow[rt].load(p, n0 + max(tok[rt], 0), h * G + rho % G, lg);
     }
     issue_tile(0);
+    // ... and their (cos, sin) tables built while tile 0 is in flight (the
+    // previous segment's rotations are done with the area: its last tile's
+    // rotation ended in a barrier)
+    if constexpr (kFuse) {
+        int* f_start = reinterpret_cast<int*>(fsm + FuseSmem<D>::start);
+        int* f_end = reinterpret_cast<int*>(fsm + FuseSmem<D>::end);
+        int* f_delta = reinterpret_cast<int*>(fsm + FuseSmem<D>::delta);
+        if ((int)threadIdx.x < f_n) {
+            f_start[threadIdx.x] = f_sp.x;
+            f_end[threadIdx.x] = f_sp.y;
+            f_delta[threadIdx.x] = f_sp.z;
+        }
+        __syncthreads();
+        float2* f_cs = reinterpret_cast<float2*>(fsm + FuseSmem<D>::cs);
+        for (int i = threadIdx.x; i < f_n * (D / 2); i += 64 * kWaves) {
+            float c, sn;
+            rope_cos_sin((int64_t)f_delta[i / (D / 2)], i % (D / 2), p.freqs, &c, &sn);
+            f_cs[i] = float2{c, sn};
+        }
+    }
     int vis[kRT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) vis[rt] = p.new_visible[n0 + max(tok[rt], 0)];
@@ -542,8 +587,56 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     auto stage_of = [&](int t) { return smem + Smem<D>::base + (t % kStages) * Smem<D>::stage; };
     constexpr std::integral_constant<int, 0> K0{};
     constexpr std::integral_constant<int, 1> K1{};
+
+    // Fused re-encode of tile t, resident and visible in its stage, before
+    // any product reads it: each cached key of a span is rotated by
+    // R(delta) of the span, through the same routine and (cos, sin) values
+    // as the re-encode launch, so the stage then holds the re-encoded cache's
+    // bytes.  Item (block pair, lane): the K blocks of dims 32d.. and
+    // 32d + D/2.. of one 16-key group hold a pair's two halves in the same
+    // lane slot (key 16 sckt + lane % 16, dims 8 (lane / 16)..).  A
+    // barrier ends it.  f_cur: the last span starting at or before the
+    // tile's first key (tiles come in key order).
+    int f_cur = 0;
+    auto rotate_tile = [&](int t) {
+        if constexpr (kFuse) {
+            constexpr int PAIRS = KB / 2;
+            const int* f_start = reinterpret_cast<const int*>(fsm + FuseSmem<D>::start);
+            const int* f_end = reinterpret_cast<const int*>(fsm + FuseSmem<D>::end);
+            const float2* f_cs = reinterpret_cast<const float2*>(fsm + FuseSmem<D>::cs);
+            const int tb = kbeg + t * kTile;
+            while (f_cur + 1 < f_n && f_start[f_cur + 1] <= tb) ++f_cur;
+            if ((int)threadIdx.x < PAIRS * 64) {
+                const int pi = threadIdx.x >> 6, ln = threadIdx.x & 63;
+                const int sckt = pi / (DS / 2), dlo = pi % (DS / 2);
+                unsigned char* st = stage_of(t);
+                uint4* plo = reinterpret_cast<uint4*>(st + (sckt * DS + dlo) * 1024 + ln * 16);
+                uint4* phi =
+                    reinterpret_cast<uint4*>(st + (sckt * DS + dlo + DS / 2) * 1024 + ln * 16);
+                const int v = tb + 16 * sckt + (ln & 15);
+                int k = f_cur;
+                while (k + 1 < f_n && f_start[k + 1] <= v) ++k;
+                if (f_n > 0 && v < bk.cmax && v < kend && v >= f_start[k] && v < f_end[k]) {
+                    const float2* row = f_cs + k * (D / 2) + 32 * dlo + 8 * (ln >> 4);
+                    float c[8], sn[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        c[e] = row[e].x;
+                        sn[e] = row[e].y;
+                    }
+                    uint4 x, y;
+                    rope_rotate16<bf16_t>(*plo, *phi, c, sn, x, y);
+                    *plo = x;
+                    *phi = y;
+                }
+            }
+            __syncthreads();
+        }
+    };
+
     wait_vm_all();
     __syncthreads();
+    rotate_tile(0);
 
     // a step whose current and next sub-tiles are both dead for the wave is
     // skipped; a step that runs on a dead sub-tile's never-computed S masks
@@ -563,6 +656,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         if (t + 2 < n_tiles) wait_vm<LPW>(); else wait_vm<0>();
         __syncthreads();
         if (t + 3 < n_tiles) issue_tile(t + 3);
+        rotate_tile(t + 1);
     };
     if constexpr (kKG == 1) {
         const int n_sub = (kend - kbeg + 31) / 32;
@@ -716,29 +810,38 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
 // A persistent workgroup runs its chain of segments of the schedule: record
 // blockIdx.x first, then the records its `next` fields name.
-template <int D, class S>
+template <int D, class S, bool kFuse>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<D>::bytes];
+    __shared__ __attribute__((aligned(1024)))
+    unsigned char smem[Smem<D>::bytes + (kFuse ? FuseSmem<D>::bytes : 0)];
     for (int g = blockIdx.x, first = 1; g >= 0 && g < p.n_segments; first = 0) {
         int4 rec[4];
         load_record(p, g, rec);
         if (!record_ok(p, rec, g)) break;
         // the previous segment's waves are done with every LDS stage
         if (!first) __syncthreads();
-        attend_segment<D, S>(p, smem, rec);
+        attend_segment<D, S, kFuse>(p, smem, rec);
         g = rec[3].y;
     }
 }
 
-template <int D>
-void launch_d(const KParams& p, int n_wg, hipStream_t stream) {
+template <int D, bool kFuse>
+void launch_df(const KParams& p, int n_wg, hipStream_t stream) {
     const dim3 grid(n_wg), block(64 * kWaves);
     if (p.row_block == Shape<2, 1>::kRB)
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 1>>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 1>, kFuse>), grid, block, 0, stream, p);
     else if (p.row_block == Shape<2, 2>::kRB)
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 2>>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 2>, kFuse>), grid, block, 0, stream, p);
     else
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<1, 2>>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<1, 2>, kFuse>), grid, block, 0, stream, p);
+}
+
+template <int D>
+void launch_d(const KParams& p, int n_wg, hipStream_t stream) {
+    if (p.fuse_spans)
+        launch_df<D, true>(p, n_wg, stream);
+    else
+        launch_df<D, false>(p, n_wg, stream);
 }
 
 }  // namespace

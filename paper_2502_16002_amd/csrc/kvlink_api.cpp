@@ -651,7 +651,8 @@ kvlink_status attend_impl(
     const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
     const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
     kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan sched,
-    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages, bool noalloc) {
+    void* workspace, size_t workspace_bytes, void* stream, uint32_t stages, bool noalloc,
+    const kvlink_span* fuse_spans = nullptr, const int32_t* fuse_span_ptr = nullptr) {
     try {
         const uint32_t all = KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE;
         if (stages == 0 || (stages & ~all))
@@ -736,6 +737,8 @@ kvlink_status attend_impl(
         a.lse = lse;
         a.workspace = workspace;
         a.rope_table = sched.rope_table;
+        a.fuse_spans = fuse_spans;
+        a.fuse_span_ptr = fuse_span_ptr;
         hipError_t e =
             kvlink::launch_attend(dtype, plan, a, reinterpret_cast<hipStream_t>(stream), stages);
         if (e != hipSuccess) return fail(KVLINK_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
@@ -792,6 +795,32 @@ kvlink_status kvlink_attend_new_tokens_noalloc(
                        d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer, out, lse,
                        plan, nullptr, 0, stream,
                        KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE, true);
+}
+
+kvlink_status kvlink_attend_new_tokens_fused(
+    kvlink_dtype dtype, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+    double rope_theta, float softmax_scale, int32_t n_seqs, int32_t n_new_total,
+    int32_t max_new, int32_t max_cached, const int32_t* d_seq_new_ptr,
+    const int32_t* d_seq_cached, const int32_t* d_new_pos, const int32_t* d_new_visible,
+    const void* q_new, const void* k_new, const void* v_new, kvlink_kv_view k_cache,
+    kvlink_kv_view v_cache, int32_t layer, void* out, float* lse, kvlink_attend_plan plan,
+    const kvlink_span* d_spans, const int32_t* d_seq_span_ptr, int32_t max_spans_per_seq,
+    void* workspace, size_t workspace_bytes, void* stream) {
+    if (max_spans_per_seq < 0) return fail(KVLINK_ERR_INVALID_ARG, "max_spans_per_seq < 0");
+    if (max_spans_per_seq > KVLINK_FUSED_MAX_SPANS)
+        return fail(KVLINK_ERR_UNSUPPORTED, "%d spans in a request (the fused re-encode holds %d)",
+                    max_spans_per_seq, KVLINK_FUSED_MAX_SPANS);
+    if (dtype != KVLINK_BF16 || !kvlink::attend_row_block_ok(kvlink::kPathWide, plan.row_block))
+        return fail(KVLINK_ERR_UNSUPPORTED,
+                    "the fused re-encode runs on the wide bf16 kernel (row_block 256, 128 or 64)");
+    if (n_new_total > 0 && (!d_spans || !d_seq_span_ptr))
+        return fail(KVLINK_ERR_INVALID_ARG, "d_spans and d_seq_span_ptr are required");
+    return attend_impl(dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, softmax_scale, n_seqs,
+                       n_new_total, max_new, max_cached, d_seq_new_ptr, d_seq_cached, d_new_pos,
+                       d_new_visible, q_new, k_new, v_new, k_cache, v_cache, layer, out, lse,
+                       plan, workspace, workspace_bytes, stream,
+                       KVLINK_STAGE_ROPE | KVLINK_STAGE_SPLIT | KVLINK_STAGE_COMBINE, false,
+                       d_spans, d_seq_span_ptr);
 }
 
 kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int32_t n_new_total,

@@ -164,6 +164,28 @@ struct RopeFreqs {
 
 RopeFreqs make_rope_freqs(double theta, int head_dim);
 
+// RoPE of 16 bytes of each half of a head vector (Sec. 2.2; dims j and
+// j + D/2 form a pair): lo holds dims j.., hi dims j + D/2.., c and s the
+// cos/sin of their angles.  Every kernel that rotates keys or queries goes
+// through this one routine (the re-encode, the new tokens' RoPE, fused or
+// not, and the re-encode fused into the split attention), so each pair of
+// forms produces the same bytes.
+template <typename T>
+__device__ __forceinline__ void rope_rotate16(const uint4& lo, const uint4& hi, const float* c,
+                                              const float* s, uint4& x_out, uint4& y_out) {
+    constexpr int E = 16 / (int)sizeof(T);
+    float a[E], b[E], x[E], y[E];
+    unpack16<T>(lo, a);
+    unpack16<T>(hi, b);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        x[e] = __builtin_fmaf(a[e], c[e], -(b[e] * s[e]));
+        y[e] = __builtin_fmaf(a[e], s[e], b[e] * c[e]);
+    }
+    x_out = pack16<T>(x);
+    y_out = pack16<T>(y);
+}
+
 // cos and sin of the RoPE angle pos * w[j] (Sec. 2.2), computed in double
 // precision in registers, then rounded to float: Cody-Waite reduction of the
 // angle by pi/2, Taylor series of sin and cos on the reduced argument
@@ -302,6 +324,10 @@ struct AttendArgs {
     float* lse;
     void* workspace;
     const float* rope_table;   // the batch's cos/sin table, or NULL
+    // re-encode fused into the split launch (wide kernel): the requests'
+    // spans and their offsets [n_seqs + 1], or NULL
+    const kvlink_span* fuse_spans = nullptr;
+    const int32_t* fuse_span_ptr = nullptr;
 };
 
 hipError_t launch_attend(kvlink_dtype dt, const AttendPlan& p, const AttendArgs& a,

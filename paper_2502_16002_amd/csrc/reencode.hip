@@ -70,21 +70,14 @@ __device__ __forceinline__ void store_stream(const uint4& v, void* p) {
 // Rotation of one 16-byte slice pair (dims j.. and j + D/2..) by (c, s) and
 // its non-temporal store at q (the slice) and q + D/2 (its partner); the
 // per-span and the shared kernels both go through it, so they write the same
-// bytes.
+// bytes (and the same as the re-encode fused into the split attention).
 template <typename T, int D>
 __device__ __forceinline__ void rotate_store(const uint4& lo, const uint4& hi, const float* c,
                                              const float* s, T* q) {
-    constexpr int E = 16 / (int)sizeof(T);
-    float a[E], b[E], x[E], y[E];
-    unpack16<T>(lo, a);
-    unpack16<T>(hi, b);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        x[e] = a[e] * c[e] - b[e] * s[e];
-        y[e] = a[e] * s[e] + b[e] * c[e];
-    }
-    store_stream(pack16<T>(x), q);
-    store_stream(pack16<T>(y), q + D / 2);
+    uint4 x, y;
+    rope_rotate16<T>(lo, hi, c, s, x, y);
+    store_stream(x, q);
+    store_stream(y, q + D / 2);
 }
 
 // Modes: kDelta rotates every row of a span by R(delta); kPerToken rotates

@@ -24,6 +24,7 @@ from . import (KVLINK_BF16, KVLINK_F32, KVLINK_PLAN_XCD,
                KVLINK_STAGE_ALL, SPAN_FIELDS, kv_view,
                kvlink_attend_make_plan, kvlink_attend_new_tokens, kvlink_attend_rope_table,
                kvlink_attend_stages, kvlink_group_spans, kvlink_reencode_keys_shared,
+               kvlink_attend_new_tokens_fused,
                kvlink_attend_workspace_bytes, kvlink_build_layout,
                kvlink_encode_keys_at_positions, kvlink_load_and_reencode,
                kvlink_load_stage_bytes, kvlink_reencode_keys, kvlink_reencode_keys_mapped)
@@ -68,6 +69,7 @@ class Batch:
         self.n_layers, self.n_q_heads, self.n_kv_heads = n_layers, n_q_heads, n_kv_heads
         self.head_dim, self.rope_theta, self.softmax_scale = head_dim, rope_theta, softmax_scale
         self.device = device
+        self.seq_doc_ptr = np.asarray(seq_doc_ptr, dtype=np.int32)
         self.layout = kvlink_build_layout(seq_doc_ptr, doc_len, link_count, n_query, doc_src_seq,
                                           doc_src_row, doc_src_pos0)
         t = self.layout["totals"]
@@ -79,6 +81,10 @@ class Batch:
         def up(a):
             return torch.from_numpy(np.ascontiguousarray(a)).to(device)
         self.d_spans = up(self.layout["spans"].reshape(-1, SPAN_FIELDS))
+        # each request's spans (documents), for the re-encode fused into the
+        # attention
+        self.d_seq_span_ptr = up(self.seq_doc_ptr)
+        self.max_spans_per_seq = int(np.max(np.diff(self.seq_doc_ptr))) if self.n_seqs else 0
         # documents reused within the batch: their stored rows are re-encoded
         # document-major (read once per group of at most SHARED_MAX_GROUP of
         # their spans)
@@ -192,11 +198,13 @@ class Batch:
                                  k_view, v_view, int(bool(literal)), copy_stream, compute_stream)
 
     def attend(self, layer, q_new, k_new, v_new, k_view, v_view, out, lse=None, stream=None,
-               stages=KVLINK_STAGE_ALL, workspace=None):
+               stages=KVLINK_STAGE_ALL, workspace=None, fused_reencode=False):
         """RoPE + append of the new tokens and their attention, one layer
         (all stages, or the ones named by the stage mask).  `workspace`
         replaces the batch's own (at least ws_bytes, 256-byte aligned, zeroed
-        before its first use)."""
+        before its first use).  fused_reencode: k_view's cached rows hold the
+        keys as stored, re-encoded inside the split launch (all stages, wide
+        bf16 kernel only)."""
         ws = self.workspace if workspace is None else workspace
         if ws.numel() * ws.element_size() < self.ws_bytes:
             raise ValueError("workspace smaller than ws_bytes")
@@ -205,7 +213,12 @@ class Batch:
                 self.d_seq_new_ptr, self.d_seq_cached, self.d_new_pos, self.d_new_visible, q_new,
                 k_new, v_new, k_view, v_view, layer, out, lse, self.plan, ws,
                 self.ws_bytes, stream)
-        if stages == KVLINK_STAGE_ALL:
+        if fused_reencode:
+            if stages != KVLINK_STAGE_ALL:
+                raise ValueError("the fused re-encode runs all stages in one call")
+            kvlink_attend_new_tokens_fused(*args[:23], self.d_spans, self.d_seq_span_ptr,
+                                           self.max_spans_per_seq, ws, self.ws_bytes, stream)
+        elif stages == KVLINK_STAGE_ALL:
             kvlink_attend_new_tokens(*args)
         else:
             kvlink_attend_stages(*args, stages=stages)

@@ -652,3 +652,46 @@ def test_attend_noalloc_refuses_calls_beyond_its_scratch(kv):
 
 def test_attend_noalloc_no_new_tokens_is_a_no_op(kv):
     _call_noalloc(kv, _attend_args(kv, n_new=0, max_new=0))
+
+
+# ------------------------------------------------ re-encode fused into attention
+
+
+def _call_fused(kv, a, spans=4096, span_ptr=4096, max_spans=10):
+    kv.kvlink_attend_new_tokens_fused(
+        a["dtype"], a["hq"], a["hkv"], a["d"], a["theta"], a["scale"], a["n_seqs"], a["n_new"],
+        a["max_new"], a["max_cached"], a["snp"], a["sc"], a["pos"], a["vis"], a["q"], a["k"],
+        a["v"], a["kview"], a["vview"], a["layer"], a["out"], a["lse"], a["plan"], spans,
+        span_ptr, max_spans, a["ws"], a["ws_bytes"], stream=0)
+
+
+@pytest.mark.parametrize("case,status", [
+    ("too_many_spans", 2),      # more spans per request than the LDS tables hold
+    ("negative_spans", 1),
+    ("no_spans", 1),
+    ("no_span_ptr", 1),
+    ("decode_plan", 2),         # 16-row units: the decode kernel has no fused form
+    ("f32", 2),
+])
+def test_attend_fused_validation(kv, case, status):
+    """The fused entry point refuses, before any HIP call, what the wide bf16
+    kernel's fused re-encode cannot run."""
+    a = _attend_args(kv)
+    kw = {}
+    if case == "too_many_spans":
+        kw = dict(max_spans=kv.KVLINK_FUSED_MAX_SPANS + 1)
+    elif case == "negative_spans":
+        kw = dict(max_spans=-1)
+    elif case == "no_spans":
+        kw = dict(spans=None)
+    elif case == "no_span_ptr":
+        kw = dict(span_ptr=None)
+    elif case == "decode_plan":
+        a = _attend_args(kv, plan=_plan(kv, snp=(0, 2), vis=(100, 100)), n_new=2, max_new=2)
+        assert a["plan"].row_block == 16
+    elif case == "f32":
+        a = _attend_args(kv, dtype=kv.KVLINK_F32)
+    with pytest.raises(kv.KVLinkError) as e:
+        _call_fused(kv, a, **kw)
+    assert e.value.status == status
+    assert kv.kvlink_last_error()

@@ -1047,3 +1047,173 @@ def test_wide_unit_shapes_paged_pool(row_block):
         assert float(np.max(np.abs(lse_all[n0:n1] - ref_lse))) <= 2e-2
     _counters_zero(run)
     _print(f"paged pool row block {row_block}: worst {worst:.3e}")
+
+
+# -------------------------------------------- re-encode fused into attention
+
+
+def _fused_equals_separate(batch, layers, separate, fused, k_fused, stored_rows):
+    """Run the separate path (re-encode, then every layer's attention) and
+    the fused one (every layer's attention over the stored keys); the fused
+    outputs and LSE must equal the separate ones bit for bit, the stored
+    rows must be unchanged and the appended new rows equal.
+    separate(): returns {layer: (out, lse)} and the separate cache;
+    fused(): returns {layer: (out, lse)}; stored_rows(k) -> (stored part,
+    new part) of a cache for comparison."""
+    import torch
+    ref, k_sep = separate()
+    before = stored_rows(k_fused)[0].clone()
+    got = fused()
+    torch.cuda.synchronize()
+    for l in layers:
+        assert torch.equal(got[l][0].view(torch.int16), ref[l][0].view(torch.int16)), l
+        assert torch.equal(got[l][1], ref[l][1]), l
+    st_f, new_f = stored_rows(k_fused)
+    assert torch.equal(st_f.view(torch.int16), before.view(torch.int16)), "stored rows written"
+    assert torch.equal(new_f.view(torch.int16), stored_rows(k_sep)[1].view(torch.int16))
+
+
+def _fused_contiguous(w, layers, **kw):
+    import torch
+    from paper_2502_16002_amd.runtime import contiguous_view
+    run = ContiguousRun(w, layers, **kw)
+    b = run.batch
+    H, d = w.n_kv_heads, w.head_dim
+    Tc = int(b.layout["seq_cached"][0])
+    assert Tc == run.R                                # documents stored in request order
+    k_f = torch.zeros_like(run.k_dst)
+    k_f[:, :, 0, :run.R] = run.k_src
+    view = contiguous_view(k_f, H, 1, run.cap, d)
+
+    def separate():
+        run.run()
+        return {l: (run.out[l], run.lse[l]) for l in layers}, run.k_dst
+
+    def fused():
+        res = {}
+        for l in layers:
+            out, lse = b.new_out(), b.new_lse()
+            b.attend(l, run.q[l], run.kn[l], run.vn[l], view, run.v_view, out, lse,
+                     fused_reencode=True)
+            res[l] = (out, lse)
+        return res
+    rows = lambda k: (k[:, :, 0, :Tc], k[layers][:, :, 0, Tc:Tc + b.n_new])
+    _fused_equals_separate(b, layers, separate, fused, k_f, rows)
+    return run
+
+
+@pytest.mark.parametrize("row_block,flags", [(0, None), (256, 1 | 4), (128, 1 | 8), (128, 1 | 4),
+                                             (64, 1 | 8), (64, 1 | 4)])
+def test_fused_reencode_llama1b(row_block, flags):
+    """head_dim 64, ten documents: the fused re-encode gives the separate
+    path's bytes for every unit shape and merge, and several workgroup
+    counts; the outputs against the oracle."""
+    w = workloads.llama1b_layer()
+    for n_wg in [0, 1, 7]:
+        run = _fused_contiguous(w, [0], n_workgroups=n_wg, row_block=row_block, plan_flags=flags)
+        _check_attend(run, 0, tag=f"fused 1b rb{row_block} {flags} {n_wg}")
+
+
+def test_fused_reencode_llama8b_two_layers():
+    """head_dim 128, the 10-document batch, two layers, the default plan."""
+    w = workloads.llama8b_10doc(n_layers=2)
+    run = _fused_contiguous(w, [0, 1])
+    _check_attend(run, 1, tag="fused 8b")
+
+
+def test_fused_reencode_long_context():
+    """The 40-document, 20,480-row cache (40 spans per request), two layers:
+    the fused bytes equal the separate path's on every output row."""
+    w = workloads.llama8b_long(n_layers=2)
+    _fused_contiguous(w, [0, 1])
+
+
+@pytest.mark.parametrize("doc_len,link_count,n_query", [
+    ([1, 1, 3, 1], [1, 0, 1, 1], 17),        # documents shorter than a key group
+    ([63, 64, 65], [2, 2, 2], 30),            # documents ending around tile edges
+    ([130, 5, 260], [1, 0, 1], 20),
+    ([700, 2000], [0, 0], 9),                 # long documents, many tiles each
+])
+def test_fused_reencode_edge_layouts(doc_len, link_count, n_query):
+    w = workloads.custom(doc_len, link_count, n_query, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                         dtype="bf16", rope_theta=5e5, seed=41)
+    for n_wg in [0, 3]:
+        run = _fused_contiguous(w, [0], n_workgroups=n_wg)
+        assert run.batch.plan.row_block in (256, 128, 64)
+        _check_attend(run, 0, tag=f"fused edge {doc_len} {n_wg}")
+
+
+def test_fused_reencode_paged_pool():
+    """The shared pool: the fused path reads every request's keys straight
+    from the pool pages through the values' block table (no per-request key
+    copies at all) and matches the per-request re-encoded copies bit for
+    bit; every request against the oracle."""
+    import torch
+    from harness import PagedRun
+    from paper_2502_16002_amd.runtime import paged_view
+    w = workloads.llama8b_paged()
+    run = PagedRun(w)
+    b = run.batch
+    L, H, d, P = w.n_layers, w.n_kv_heads, w.head_dim, w.page_size
+    n_pool = run.k_pool.shape[1]
+    k_all = torch.zeros_like(run.v_all)
+    k_all[:, :n_pool] = run.k_pool
+    view = paged_view(k_all, run.v_all.shape[1], H, P, d, run.v_table, run.max_pages)
+
+    def separate():
+        run.run()
+        return {l: (run.out[l], run.lse[l]) for l in range(L)}, None
+
+    def fused():
+        res = {}
+        for l in range(L):
+            out, lse = b.new_out(), b.new_lse()
+            b.attend(l, run.q[l], run.kn[l], run.vn[l], view, run.v_view, out, lse,
+                     fused_reencode=True)
+            res[l] = (out, lse)
+        return res
+    ref, _ = separate()
+    pool_before = k_all[:, :n_pool].clone()
+    got = fused()
+    torch.cuda.synchronize()
+    for l in range(L):
+        assert torch.equal(got[l][0].view(torch.int16), ref[l][0].view(torch.int16)), l
+        assert torch.equal(got[l][1], ref[l][1]), l
+    assert torch.equal(k_all[:, :n_pool].view(torch.int16), pool_before.view(torch.int16))
+    got_all = to_f64(got[0][0])
+    for s in [0, 7, 15]:
+        kc, vc, q, kn, vn = run.oracle_inputs(0, s)
+        ref_o, _ = oracle.attend(w.doc_len(s), w.link_count[s], w.n_query[s], q, kn, vn, kc, vc,
+                                 w.rope_theta, w.scale)
+        n0 = int(b.layout["seq_new_ptr"][s])
+        check_close(w, got_all[n0:n0 + w.n_new(s)], ref_o, f"fused paged request {s}")
+
+
+def test_fused_reencode_batch_of_requests():
+    """Four requests over one stored sequence (a document reused by two
+    requests, one request without documents): each request's spans rotate
+    its own rows; bytes equal to the separate path's."""
+    import torch
+    from paper_2502_16002_amd.runtime import contiguous_view
+    table = [130, 7, 64, 300, 1, 45]
+    w = workloads.Workload(name="batch4", dtype="bf16", n_layers=1, n_q_heads=8, n_kv_heads=2,
+                           head_dim=128, rope_theta=5e5, seed=37, doc_table_len=table,
+                           docs=[[], [3], [0, 1, 2], [4, 5, 0]],
+                           link_count=[[], [5], [2, 0, 3], [1, 1, 4]], n_query=[9, 33, 1, 17])
+    run = _BatchRun(w)
+    b = run.batch
+    H, d = w.n_kv_heads, w.head_dim
+    k_f = torch.zeros_like(run.k_dst)
+    for sp in b.layout["spans"].reshape(-1, 6):
+        src_row, dst_seq, dst_row, n = int(sp[1]), int(sp[2]), int(sp[3]), int(sp[4])
+        k_f[:, :, dst_seq, dst_row:dst_row + n] = run.k_src[:, :, 0, src_row:src_row + n]
+    S, cap = w.n_seqs, k_f.shape[3]
+    view = contiguous_view(k_f, H, S, cap, d)
+    run.run()
+    ref_out, ref_lse = run.out[0].clone(), run.lse[0].clone()
+    out, lse = b.new_out(), b.new_lse()
+    b.attend(0, run.q, run.kn, run.vn, view, run.v_view, out, lse, fused_reencode=True)
+    torch.cuda.synchronize()
+    assert b.plan.row_block in (256, 128, 64)
+    assert torch.equal(out.view(torch.int16), ref_out.view(torch.int16))
+    assert torch.equal(lse, ref_lse)
