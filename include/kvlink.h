@@ -17,12 +17,16 @@
  *                             K' = R(g_i + t - p_t) K for compressed caches
  *                             (kept tokens at original positions p_t, GPU)
  *   kvlink_load_and_reencode  the same, from caches held in host memory: read
- *                             by the kernels over the bus, or copied layer by
- *                             layer through a device staging ring (GPU)
+ *                             by the kernels over the bus, or copied in
+ *                             chunks of layers through a device staging
+ *                             ring (GPU)
  *   kvlink_attend_make_plan   balanced split-K schedule of a batch (host)
  *   kvlink_attend_new_tokens  RoPE of the new tokens at their global positions,
  *                             append of their keys/values to the cache and
  *                             split-K GQA attention over the cache (GPU)
+ *   kvlink_attend_new_tokens_fused
+ *                             the same over the stored keys, re-encoded as
+ *                             the attention stages them (GPU)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -362,9 +366,8 @@ kvlink_status kvlink_load_and_reencode(kvlink_dtype dtype, int32_t n_layers, int
  * cost, one per workgroup, or equal-cost ranges over all units in order;
  * each piece of a unit that one workgroup covers is a segment.  A unit with
  * several segments has its partial results merged by a log-sum-exp merge:
- * by a combine launch, or (row blocks 256, 128 and 64: batches with more than
- * 16 rows per request and KV head, when the schedule chooses it) inside the
- * split launch by the unit's last-arriving workgroup.
+ * by a combine launch, or (row blocks 128, 64 and 16, when the schedule
+ * chooses it) inside the split launch by the unit's last-arriving workgroup.
  *
  * The table (int32, built on the host by kvlink_attend_make_plan, then
  * copied to the device by the caller) holds, in order:
@@ -450,9 +453,10 @@ kvlink_status kvlink_attend_rope_table(int32_t head_dim, double rope_theta, int3
  *                      sharing one L2;
  *                    KVLINK_PLAN_COMBINE or KVLINK_PLAN_IN_LAUNCH (not
  *                      both): merge split units by the combine launch, or
- *                      inside the split launch (wide kernel only); without
- *                      either the cost model chooses, and plan->flags
- *                      reports the choice;
+ *                      inside the split launch (row blocks 128, 64 and 16;
+ *                      IN_LAUNCH with row_block 256 is KVLINK_ERR_UNSUPPORTED);
+ *                      without either the cost model chooses, and
+ *                      plan->flags reports the choice;
  *                    none changes the result beyond float rounding order
  *   table, table_capacity  host array for the table; with table == NULL
  *                    only *plan is filled (to size the array)
