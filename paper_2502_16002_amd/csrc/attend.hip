@@ -538,7 +538,7 @@ hipError_t launch_typed(const AttendPlan& pl, const AttendArgs& a, hipStream_t s
         }
         if (e != hipSuccess) return e;
     }
-    // the wide kernel may merge its split units itself
+    // the split kernel may merge its split units itself
     if (!(stages & KVLINK_STAGE_COMBINE) || !pl.partials || pl.merge_in_launch) return hipSuccess;
 
     constexpr int rpb = combine_rows_per_block<T, D>();

@@ -71,11 +71,12 @@ struct KParams {
     int n_split;
     void* part_o;     // split partials O / l, in the workload dtype
     float* part_ml;   // their (running max in log2 units, sum) pairs
-    // arrival counters of the units whose segments the wide kernel merges in
-    // the same launch, one per unit; zero before the launch and after it
+    // arrival counters of the units whose segments the split kernel merges
+    // in the same launch, one per unit; zero before the launch and after it
     uint32_t* counters;
-    // wide kernel, 128- and 64-row units: split units merged in the launch by
-    // their last-arriving workgroup (1), or left to the combine launch (0)
+    // wide kernel's 128- and 64-row units and the decode kernel: split units
+    // merged in the launch by their last-arriving workgroup (1), or left to
+    // the combine launch (0)
     int merge_in_launch;
     void* out;
     float* lse;

@@ -271,8 +271,9 @@ AttendPath attend_path(kvlink_dtype dt, int group, int max_new);
 // decode and vector: 16)
 bool attend_row_block_ok(AttendPath path, int row_block);
 
-// The workspace starts with the arrival counters of the units the wide
-// kernel merges in its own launch (one uint32 per unit, at most kMaxUnits):
+// The workspace starts with the arrival counters of the units a split
+// kernel (wide or decode) merges in its own launch (one uint32 per unit, at
+// most kMaxUnits):
 // they must be zero before a workspace's first use, and every completed call
 // leaves them zero.  The rotated queries and the split partials follow.
 constexpr size_t kCounterBytes = 64 * 1024;
