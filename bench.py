@@ -45,8 +45,9 @@ CSRC = os.path.join(ROOT, "paper_2502_16002_amd", "csrc")
 # sources that decide each kernel's memory traffic (hashed to tell whether
 # the committed counter figures still describe the kernel that runs)
 KERNEL_SOURCES = {
-    "attend_mfma_kernel": ["attend_mfma.hip", "mfma_ops.h", "attend_common.h", "kvlink_internal.h"],
-    "attend_decode_kernel": ["attend_decode.hip", "mfma_ops.h", "attend_common.h",
+    "attend_mfma_kernel": ["attend_mfma.hip", "merge_launch.h", "mfma_ops.h", "attend_common.h",
+                           "kvlink_internal.h"],
+    "attend_decode_kernel": ["attend_decode.hip", "merge_launch.h", "mfma_ops.h", "attend_common.h",
                              "kvlink_internal.h"],
     "reencode_kernel": ["reencode.hip", "kvlink_internal.h"],
     "reencode_shared_kernel": ["reencode.hip", "kvlink_internal.h"],
