@@ -21,10 +21,12 @@
 //
 //   * the tiles are loaded straight from global memory into a four-stage
 //     LDS ring with 16-byte direct-to-LDS loads (each wave issues an eighth
-//     of a tile), at no register cost.  The workgroup barrier of each tile
-//     waits for every load in flight (its fence covers the direct-to-LDS
-//     writes), so one tile is in flight while the next is used; a barrier
-//     that left two in flight measured the same;
+//     of a tile), at no register cost.  At the barrier of tile t each wave
+//     has waited for its own loads of tile t+1 only (the loads of a wave
+//     complete in issue order; a direct-to-LDS load counts as complete once
+//     its bytes are in LDS), so tiles t+2 and t+3 stay in flight across it;
+//     with the fused re-encode, which rewrites a tile in LDS after its
+//     barrier, the barrier is a full one;
 //   * K is stored in MFMA operand order (for each 16-key x 32-dim block,
 //     lane l's 16 bytes at l*16): the A operand of S^T = K Q^T is one
 //     conflict-free ds_read_b128 per lane;
@@ -654,7 +656,8 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         // this wave's loads of tile t+1 are done when at most those of
         // tile t+2 are outstanding
         if (t + 2 < n_tiles) wait_vm<LPW>(); else wait_vm<0>();
-        __syncthreads();
+        if constexpr (kFuse) __syncthreads();
+        else barrier_keep_loads();
         if (t + 3 < n_tiles) issue_tile(t + 3);
         rotate_tile(t + 1);
     };

@@ -180,6 +180,15 @@ __device__ __forceinline__ void load_lds16(const void* src, void* lds) {
 #endif
 }
 
+// Workgroup barrier that leaves this wave's vector-memory loads in flight
+// (__syncthreads waits for all of them): the wave's LDS accesses complete
+// first, and the compiler keeps memory accesses on their side of it.
+__device__ __forceinline__ void barrier_keep_loads() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#endif
+}
+
 // Wait until at most n of this wave's vector-memory loads are outstanding.
 template <int n>
 __device__ __forceinline__ void wait_vm() {
