@@ -326,13 +326,14 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     // A 32-key sub-tile from v0 is dead for this wave when no row of it sees
     // any of its keys: all cached keys at or past the last row's prefix and
     // all new keys past the last row's token (always, for a wave without
-    // rows).
-    auto dead = [&](int v0) {
-        if (!wave_active || v0 >= kend) return true;
-        const bool cached_seen = v0 < wave_vis_max && v0 < bk.cmax;
-        const bool new_seen = v0 + 32 > bk.cmax && max(v0, bk.cmax) <= bk.cmax + tok_max;
-        return !cached_seen && !new_seen;
-    };
+    // rows).  It is live iff v0 < live_a (it starts below the segment end,
+    // the cached region's end and the widest prefix) or live_b < v0 <= live_c
+    // (it reaches past cmax and starts at or before the last row's new key
+    // and the segment end): three scalar compares per test.
+    const int live_a = wave_active ? min(min(wave_vis_max, bk.cmax), kend) : -1;
+    const int live_b = bk.cmax - 32;
+    const int live_c = wave_active ? min(bk.cmax + tok_max, kend - 1) : -1;
+    auto dead = [&](int v0) { return !(v0 < live_a || (v0 > live_b && v0 <= live_c)); };
 
     floatx4 o[DT][kRT];
 #pragma unroll
