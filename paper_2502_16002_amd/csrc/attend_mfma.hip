@@ -116,7 +116,7 @@ struct Shape {
 // One segment of a unit: tiles [tile_a, tile_b) of the key range of KV head
 // h's rows [rho0, rho0 + rows) of request s, from its schedule record.
 // Every early return is uniform over the workgroup.
-template <int D, class S, bool kFuse>
+template <int D, class S, bool kFuse, bool kPaged>
 __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* smem,
                                                const int4 (&rec)[4]) {
     constexpr int kRT = S::kRT, kKG = S::kKG, kRW = S::kRW, kRB = S::kRB;
@@ -148,8 +148,15 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     const int rw = wave % kRW, kg = wave / kRW;    // row wave and key group
     const int rho_w = rho0 + rw * kRT * 16;        // first row of this wave
 
-    const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
-    const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
+    // (contiguous caches: the launch picks kPaged = false only when neither
+    // view has a block table, and the null tables below fold every paged
+    // branch away)
+    RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
+    RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
+    if constexpr (!kPaged) {
+        kp.table = nullptr;
+        vp.table = nullptr;
+    }
 
     // virtual key -> cache row, clamped into the segment so that every load
     // reads a real row (keys past the segment end are masked)
@@ -181,15 +188,35 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         v_off[i] = 16 * (pc ^ (key & (CH - 1)));          // logical chunk stored at slot pc
     }
     // rows below fast_end are the keys themselves; tiles there take their
-    // rows by 16-row groups (one page each, when paged)
-    const bool grouped = kp.groups_of_16() && vp.groups_of_16();
+    // rows by 16-row groups (one page each, when paged): a load's address is
+    // its group's first row (the same in every lane, or the tile's first row
+    // when contiguous) plus a 32-bit lane offset fixed for the segment
+    const bool grouped = kp.groups_of_16() && vp.groups_of_16() &&
+                         kp.row_bytes < (1 << 24) && vp.row_bytes < (1 << 24);
     const int fast_end = grouped ? min(kend, bk.cmax) : 0;
+    uint32_t k_lane[KI], v_lane[VJ];
+#pragma unroll
+    for (int i = 0; i < KI; ++i) k_lane[i] = (uint32_t)(lr * kp.row_bytes + k_off[i]);
+#pragma unroll
+    for (int i = 0; i < VJ; ++i) v_lane[i] = (uint32_t)((v_key[i] & 15) * vp.row_bytes + v_off[i]);
 
     // this wave's share of tile t, straight into LDS stage t % kStages
     auto issue_tile = [&](int t) {
         unsigned char* st = smem + Smem<D>::base + (t % kStages) * Smem<D>::stage;
         const int tb = kbeg + t * kTile;
-        if (tb + kTile <= fast_end) {
+        if (!kPaged && tb + kTile <= fast_end) {
+            // contiguous rows: one base per tile
+            const char* kb = kp.base + (int64_t)tb * kp.row_bytes;
+            const char* vb = vp.base + (int64_t)tb * vp.row_bytes;
+#pragma unroll
+            for (int i = 0; i < KI; ++i)
+                load_lds16(kb + (k_lane[i] + (uint32_t)(k_key0[i] * kp.row_bytes)),
+                           st + (wave + kWaves * i) * 1024);
+#pragma unroll
+            for (int i = 0; i < VJ; ++i)
+                load_lds16(vb + (v_lane[i] + (uint32_t)((v_key0[i] & ~15) * vp.row_bytes)),
+                           st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
+        } else if (tb + kTile <= fast_end) {
             // a K block covers keys g..g+15 and a V load keys within one
             // aligned 16-key group g, so one page per load; the page reads
             // of the tile go out together, ahead of the address arithmetic
@@ -204,14 +231,12 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             }
 #pragma unroll
             for (int i = 0; i < KI; ++i)
-                load_lds16(kp.in_page(kpg[i], tb + k_key0[i]) + lr * kp.row_bytes + k_off[i],
+                load_lds16(kp.in_page(kpg[i], tb + k_key0[i]) + k_lane[i],
                            st + (wave + kWaves * i) * 1024);
 #pragma unroll
-            for (int i = 0; i < VJ; ++i) {
-                const int g = tb + (v_key0[i] & ~15);
-                load_lds16(vp.in_page(vpg[i], g) + (v_key[i] & 15) * vp.row_bytes + v_off[i],
+            for (int i = 0; i < VJ; ++i)
+                load_lds16(vp.in_page(vpg[i], tb + (v_key0[i] & ~15)) + v_lane[i],
                            st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
-            }
         } else {
 #pragma unroll
             for (int i = 0; i < KI; ++i)
@@ -814,7 +839,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 
 // A persistent workgroup runs its chain of segments of the schedule: record
 // blockIdx.x first, then the records its `next` fields name.
-template <int D, class S, bool kFuse>
+template <int D, class S, bool kFuse, bool kPaged>
 __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) {
     __shared__ __attribute__((aligned(1024)))
     unsigned char smem[Smem<D>::bytes + (kFuse ? FuseSmem<D>::bytes : 0)];
@@ -824,28 +849,33 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attend_mfma_kernel(KParams p) 
         if (!record_ok(p, rec, g)) break;
         // the previous segment's waves are done with every LDS stage
         if (!first) __syncthreads();
-        attend_segment<D, S, kFuse>(p, smem, rec);
+        attend_segment<D, S, kFuse, kPaged>(p, smem, rec);
         g = rec[3].y;
     }
 }
 
-template <int D, bool kFuse>
-void launch_df(const KParams& p, int n_wg, hipStream_t stream) {
+template <int D, bool kFuse, bool kPaged>
+void launch_dfp(const KParams& p, int n_wg, hipStream_t stream) {
     const dim3 grid(n_wg), block(64 * kWaves);
     if (p.row_block == Shape<2, 1>::kRB)
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 1>, kFuse>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 1>, kFuse, kPaged>), grid, block, 0,
+                           stream, p);
     else if (p.row_block == Shape<2, 2>::kRB)
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 2>, kFuse>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<2, 2>, kFuse, kPaged>), grid, block, 0,
+                           stream, p);
     else
-        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<1, 2>, kFuse>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((attend_mfma_kernel<D, Shape<1, 2>, kFuse, kPaged>), grid, block, 0,
+                           stream, p);
 }
 
 template <int D>
 void launch_d(const KParams& p, int n_wg, hipStream_t stream) {
+    const bool paged = p.k.block_table || p.v.block_table;
     if (p.fuse_spans)
-        launch_df<D, true>(p, n_wg, stream);
+        paged ? launch_dfp<D, true, true>(p, n_wg, stream) : launch_dfp<D, true, false>(p, n_wg, stream);
     else
-        launch_df<D, false>(p, n_wg, stream);
+        paged ? launch_dfp<D, false, true>(p, n_wg, stream)
+              : launch_dfp<D, false, false>(p, n_wg, stream);
 }
 
 }  // namespace
