@@ -118,11 +118,19 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
         return v0 < kend ? v0 : -1;
     };
 
-    const RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
-    const RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
+    // (the policies follow the views: a streamed view is contiguous, and its
+    // null table folds the paged branches away)
+    RowPtr kp = row_ptr<bf16_t>(p.k, p.layer, h, s);
+    RowPtr vp = row_ptr<bf16_t>(p.v, p.layer, h, s);
+    if constexpr (kPolK == kStream) kp.table = nullptr;
+    if constexpr (kPolV == kStream) vp.table = nullptr;
     // below fast_end keys are cached rows taken by 16-row groups (one page
-    // each when paged); elsewhere each lane maps its key on its own
-    const bool grouped = kp.groups_of_16() && vp.groups_of_16();
+    // each when paged): a load's address is its group's first row (the same
+    // in every lane; the step's first row when contiguous) plus a 32-bit
+    // lane offset fixed for the segment; elsewhere each lane maps its key on
+    // its own
+    const bool grouped = kp.groups_of_16() && vp.groups_of_16() &&
+                         kp.row_bytes < (1 << 24) && vp.row_bytes < (1 << 24);
     const int fast_end = grouped ? min(kend, cmax) : 0;
     auto key_row = [&](int v) {
         v = min(v, kend - 1);
@@ -134,12 +142,24 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     // chunk (lane % CH) ^ (key % CH)
     auto v_key = [&](int i) { return (64 * i + lane) / CH; };
     auto v_off = [&](int i) { return 16 * ((lane % CH) ^ (v_key(i) & (CH - 1))); };
+    const uint32_t k_lane = (uint32_t)(lr * kp.row_bytes + 16 * lg);
+    uint32_t v_lane[VL];
+#pragma unroll
+    for (int i = 0; i < VL; ++i) v_lane[i] = (uint32_t)((v_key(i) & 15) * vp.row_bytes + v_off(i));
 
     // Loads of the step at v0: K into r, then V into LDS stage st, with the
     // cache policies the launch chose for the two views.
     auto issue_k_as = [&](int v0, StepRegs<D>& r, auto policy) {
         constexpr int pol = decltype(policy)::value;
-        if (v0 + kStep <= fast_end) {
+        if (kPolK == kStream && v0 + kStep <= fast_end) {
+            const char* b = kp.base + (int64_t)v0 * kp.row_bytes;
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh) {
+                const char* g = b + (k_lane + (uint32_t)(16 * kh * kp.row_bytes));
+#pragma unroll
+                for (int ds = 0; ds < DS; ++ds) r.k[kh][ds] = load16<pol>(g + 64 * ds);
+            }
+        } else if (v0 + kStep <= fast_end) {
             int pg[2] = {0, 0};
             if (kp.table) {
                 pg[0] = kp.page_of(v0);
@@ -147,7 +167,7 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
             }
 #pragma unroll
             for (int kh = 0; kh < 2; ++kh) {
-                const char* g = kp.in_page(pg[kh], v0 + 16 * kh) + lr * kp.row_bytes + 16 * lg;
+                const char* g = kp.in_page(pg[kh], v0 + 16 * kh) + k_lane;
 #pragma unroll
                 for (int ds = 0; ds < DS; ++ds) r.k[kh][ds] = load16<pol>(g + 64 * ds);
             }
@@ -162,7 +182,14 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
     };
     auto issue_v_as = [&](int v0, unsigned char* st, auto policy) {
         constexpr int pol = decltype(policy)::value;
-        if (v0 + kStep <= fast_end) {
+        if (kPolV == kStream && v0 + kStep <= fast_end) {
+            const char* b = vp.base + (int64_t)v0 * vp.row_bytes;
+#pragma unroll
+            for (int i = 0; i < VL; ++i) {
+                const int kh = (64 * i / CH) >> 4;          // the load's 16-key group
+                load_lds16<pol>(b + (v_lane[i] + (uint32_t)(16 * kh * vp.row_bytes)), st + i * 1024);
+            }
+        } else if (v0 + kStep <= fast_end) {
             int pg[2] = {0, 0};
             if (vp.table) {
                 pg[0] = vp.page_of(v0);
@@ -171,9 +198,7 @@ __device__ __forceinline__ void decode_segment(const KParams& p, unsigned char* 
 #pragma unroll
             for (int i = 0; i < VL; ++i) {
                 const int kh = (64 * i / CH) >> 4;          // the load's 16-key group
-                load_lds16<pol>(vp.in_page(pg[kh], v0 + 16 * kh) + (v_key(i) & 15) * vp.row_bytes +
-                                    v_off(i),
-                                st + i * 1024);
+                load_lds16<pol>(vp.in_page(pg[kh], v0 + 16 * kh) + v_lane[i], st + i * 1024);
             }
         } else {
 #pragma unroll
