@@ -22,6 +22,7 @@
 // virtual key range: first the cached rows its last token sees (cmax), then
 // the new rows up to its last token; each key is masked per row.
 #include <algorithm>
+#include <type_traits>
 
 #include "attend_common.h"
 
@@ -402,34 +403,43 @@ __global__ __launch_bounds__(256, 4) void combine_kernel(KParams p) {
 #pragma unroll
         for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
         const int n_mine = valid ? nseg : 0;
-        for (int cb = phase * CAP; cb < n_mine; cb += S * CAP) {
-            const int nb = min(CAP, nseg - cb);
-            const float2 mine = ml[cb + min(gl, nb - 1)];
-            uint4 v[CAP];
+        auto rounds = [&](auto cap_c) {
+            constexpr int C = decltype(cap_c)::value;
+            for (int cb = phase * C; cb < n_mine; cb += S * C) {
+                const int nb = min(C, nseg - cb);
+                const float2 mine = ml[cb + min(gl, nb - 1)];
+                uint4 v[C];
 #pragma unroll
-            for (int i = 0; i < CAP; ++i) v[i] = po[(int64_t)(cb + min(i, nb - 1)) * LPS + gl];
-            float mb = gl < nb ? mine.x : kNoMax;
+                for (int i = 0; i < C; ++i) v[i] = po[(int64_t)(cb + min(i, nb - 1)) * LPS + gl];
+                float mb = gl < nb ? mine.x : kNoMax;
 #pragma unroll
-            for (int off = 1; off < LPS; off *= 2) mb = fmaxf(mb, __shfl_xor(mb, off));
-            const float Mn = fmaxf(M, mb);
-            const float a = __builtin_amdgcn_exp2f(M - Mn);
-            const float w_mine = gl < nb ? __builtin_amdgcn_exp2f(mine.x - Mn) * mine.y : 0.f;
-            float ws = w_mine;
+                for (int off = 1; off < LPS; off *= 2) mb = fmaxf(mb, __shfl_xor(mb, off));
+                const float Mn = fmaxf(M, mb);
+                const float a = __builtin_amdgcn_exp2f(M - Mn);
+                const float w_mine = gl < nb ? __builtin_amdgcn_exp2f(mine.x - Mn) * mine.y : 0.f;
+                float ws = w_mine;
 #pragma unroll
-            for (int off = 1; off < LPS; off *= 2) ws += __shfl_xor(ws, off);
-            L = L * a + ws;
+                for (int off = 1; off < LPS; off *= 2) ws += __shfl_xor(ws, off);
+                L = L * a + ws;
 #pragma unroll
-            for (int e = 0; e < EPL; ++e) acc[e] *= a;
+                for (int e = 0; e < EPL; ++e) acc[e] *= a;
 #pragma unroll
-            for (int i = 0; i < CAP; ++i) {
-                const float w = __shfl(w_mine, grp * LPS + i);   // 0 past the last segment
-                float x[EPL];
-                unpack16<T>(v[i], x);
+                for (int i = 0; i < C; ++i) {
+                    const float w = __shfl(w_mine, grp * LPS + i);   // 0 past the last segment
+                    float x[EPL];
+                    unpack16<T>(v[i], x);
 #pragma unroll
-                for (int e = 0; e < EPL; ++e) acc[e] += w * x[e];
+                    for (int e = 0; e < EPL; ++e) acc[e] += w * x[e];
+                }
+                M = Mn;
             }
-            M = Mn;
-        }
+        };
+        // units of at most four or eight segments (the split units of a
+        // prefill) take rounds of that many: a lane then issues four or eight
+        // partial loads per round, not sixteen
+        if (!kShare && nseg <= 4) rounds(std::integral_constant<int, 4>{});
+        else if (!kShare && nseg <= 8) rounds(std::integral_constant<int, 8>{});
+        else rounds(std::integral_constant<int, CAP>{});
         if constexpr (kShare) {
             if (S > 1) {   // uniform over the workgroup
                 if (gl == 0) {
