@@ -112,11 +112,13 @@ __device__ void merge_unit(const KParams& p, int part, int rows, int nseg, int h
             for (int e = 0; e < 8; ++e) acc[k][e] *= a;
 #pragma unroll
             for (int i = 0; i < SC; ++i) {
-                const float w = __shfl(w_mine, lane0 + i);   // 0 past the chunk's last segment
-                float x[8];
-                unpack16<bf16_t>(v[k][i], x);
+                if (i < nb) {                                 // uniform
+                    const float w = __shfl(w_mine, lane0 + i);
+                    float x[8];
+                    unpack16<bf16_t>(v[k][i], x);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) acc[k][e] += w * x[e];
+                    for (int e = 0; e < 8; ++e) acc[k][e] += w * x[e];
+                }
             }
             M[k] = Mn;
         }
