@@ -361,9 +361,12 @@ __global__ __launch_bounds__(256) void attend_valu_kernel(KParams p) {
 // of segments, S groups share a row, each taking every S-th run of LPS
 // segments, and merge their states through LDS.
 // (Four workgroups per compute unit, i.e. at most 128 registers per lane:
-// the partial loads in flight are what the kernel's speed depends on.)
+// the partial loads in flight are what the kernel's speed depends on; two,
+// at most 256, for the shared-row and fp32 forms, which would otherwise
+// spill to scratch, whose setup costs a launch far more than the lower
+// occupancy.)
 template <typename T, int D, bool kShare>
-__global__ __launch_bounds__(256, 4) void combine_kernel(KParams p) {
+__global__ __launch_bounds__(256, (kShare || sizeof(T) == 4) ? 2 : 4) void combine_kernel(KParams p) {
     constexpr int EPL = 16 / (int)sizeof(T);   // elements per 16-byte load
     constexpr int LPS = D / EPL;               // lanes per row
     constexpr int RPW = 64 / LPS;              // lane groups (rows) per wavefront
