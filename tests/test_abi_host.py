@@ -39,6 +39,64 @@ def test_library_exports_every_declared_symbol(kv):
     assert kv.kvlink_version().startswith("kvlink")
 
 
+def _kernel_metadata(so_path):
+    """(name, private segment bytes, spilled VGPRs) of every gfx950 kernel in
+    the library: its offload bundles (one per source file) unbundled and their
+    AMDGPU metadata notes read with the ROCm LLVM tools."""
+    import shutil
+    import subprocess
+    import tempfile
+    import yaml
+    llvm = "/opt/rocm/llvm/bin"
+    tools = [os.path.join(llvm, t) for t in ("llvm-objcopy", "clang-offload-bundler", "llvm-readobj")]
+    if not all(os.path.exists(t) for t in tools):
+        pytest.skip("ROCm LLVM tools not found")
+    out = []
+    with tempfile.TemporaryDirectory() as d:
+        fat = os.path.join(d, "fatbin")
+        subprocess.run([tools[0], "--dump-section", ".hip_fatbin=" + fat, so_path], check=True)
+        data = open(fat, "rb").read()
+        magic = b"__CLANG_OFFLOAD_BUNDLE__"
+        starts = [m.start() for m in re.finditer(re.escape(magic), data)] + [len(data)]
+        for k in range(len(starts) - 1):
+            b, co = os.path.join(d, f"b{k}"), os.path.join(d, f"c{k}")
+            open(b, "wb").write(data[starts[k]:starts[k + 1]])
+            subprocess.run([tools[1], "--unbundle", "--type=o",
+                            "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", "--input=" + b,
+                            "--output=" + co], check=True)
+            notes = subprocess.run([tools[2], "--notes", co], check=True, capture_output=True,
+                                   text=True).stdout
+            if "amdhsa.kernels:" not in notes:
+                continue
+            text = notes[notes.index("amdhsa.kernels:"):]
+            text = text[:text.index("\n...")] if "\n..." in text else text
+            for kern in yaml.safe_load(text)["amdhsa.kernels"]:
+                out.append((kern[".name"], kern[".private_segment_fixed_size"],
+                            kern[".vgpr_spill_count"]))
+    return out
+
+
+def test_hot_path_kernels_use_no_scratch(kv):
+    """A kernel with a private (scratch) segment pays for it at every launch
+    (a 64-byte stack array cost the split attention 5 to 17 us per layer), so
+    every kernel the default path launches stays free of one.  Exempt: the
+    fused re-encode's instances and the 128-row units, which the schedule
+    does not pick by default."""
+    kernels = _kernel_metadata(kv.LIB_PATH)
+    assert len(kernels) > 50
+    names = [n for n, _, _ in kernels]
+    for k in ["reencode_kernel", "reencode_shared_kernel", "attend_mfma_kernel",
+              "attend_decode_kernel", "combine_kernel", "rope_table_kernel"]:
+        assert any(k in n for n in names), k
+
+    def exempt(n):
+        return "attend_mfma_kernel" in n and (re.search(r"ShapeILi\dELi\dEEELb1E", n) is not None
+                                              or "ShapeILi2ELi2E" in n)
+
+    bad = [(n, p) for n, p, _ in kernels if p > 0 and not exempt(n)]
+    assert not bad, bad
+
+
 def test_struct_sizes_match_header(kv):
     assert ctypes.sizeof(kv.kvlink_span) == 24
     assert ctypes.sizeof(kv.kvlink_kv_view) == 64
