@@ -133,7 +133,9 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 // of one row, NT threads).  Workgroups whose key ranges overlap write the
 // same rows with the same bytes.  The caller makes the stores visible
 // (wait_vm_all, then a workgroup barrier) before loading those rows.
-template <int D, int NT>
+// kV = false appends the keys only (for a kernel that reads the new values
+// straight from v_new and copies them into the cache by itself).
+template <int D, int NT, bool kV = true>
 __device__ __forceinline__ void append_new_rows(const KParams& p, const RowPtr& kp,
                                                 const RowPtr& vp, int h, int n0, int Tc, int na,
                                                 int nb) {
@@ -146,18 +148,23 @@ __device__ __forceinline__ void append_new_rows(const KParams& p, const RowPtr& 
         const int64_t src = (n * p.n_kv_heads + h) * D + c;
         const uint4 a = *reinterpret_cast<const uint4*>(kn + src);
         const uint4 b = *reinterpret_cast<const uint4*>(kn + src + Hh);
-        const uint4 va = *reinterpret_cast<const uint4*>(vn + src);
-        const uint4 vb = *reinterpret_cast<const uint4*>(vn + src + Hh);
+        uint4 va, vb;
+        if constexpr (kV) {
+            va = *reinterpret_cast<const uint4*>(vn + src);
+            vb = *reinterpret_cast<const uint4*>(vn + src + Hh);
+        }
         float cs[8], sn[8];
         rope_table8(p.rope + n * Hh, c, cs, sn);
         uint4 x, y;
         rope_rotate16<bf16_t>(a, b, cs, sn, x, y);
         char* kd = const_cast<char*>(kp.row(Tc + r)) + 2 * c;
-        char* vd = const_cast<char*>(vp.row(Tc + r)) + 2 * c;
         *reinterpret_cast<uint4*>(kd) = x;
         *reinterpret_cast<uint4*>(kd + 2 * Hh) = y;
-        *reinterpret_cast<uint4*>(vd) = va;
-        *reinterpret_cast<uint4*>(vd + 2 * Hh) = vb;
+        if constexpr (kV) {
+            char* vd = const_cast<char*>(vp.row(Tc + r)) + 2 * c;
+            *reinterpret_cast<uint4*>(vd) = va;
+            *reinterpret_cast<uint4*>(vd + 2 * Hh) = vb;
+        }
     }
 }
 

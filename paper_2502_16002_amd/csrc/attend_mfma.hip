@@ -164,6 +164,18 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
         v = min(v, kend - 1);
         return v < bk.cmax ? v : Tc + (v - bk.cmax);
     };
+    // With the fused RoPE the tiles take the new rows' values straight from
+    // v_new (new row r of the request, this KV head): only the keys go
+    // through the cache, which the segment appends them to first.  256-row
+    // units only: with many segments appending the same new rows it saves
+    // 1.4% on the shared-pool batch; 64-row units measured no gain (and the
+    // fused re-encode's instances have no register to spare).
+    constexpr bool kVDirect = !kFuse && S::kRB == 256;
+    const bool v_direct = kVDirect && p.rope != nullptr;
+    auto v_new_row = [&](int r) {
+        return reinterpret_cast<const char*>(p.v_new) +
+               ((int64_t)(n0 + r) * p.n_kv_heads + h) * (D * (int64_t)sizeof(bf16_t));
+    };
     // Per-lane parts of the direct-load addresses, fixed for the whole
     // segment: this wave loads K blocks wave + kWaves*i and V slots
     // (wave + kWaves*i)*64 + lane of every tile.
@@ -242,9 +254,11 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
             for (int i = 0; i < KI; ++i)
                 load_lds16(kp.row(key_row(tb + k_key[i])) + k_off[i], st + (wave + kWaves * i) * 1024);
 #pragma unroll
-            for (int i = 0; i < VJ; ++i)
-                load_lds16(vp.row(key_row(tb + v_key[i])) + v_off[i],
-                           st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
+            for (int i = 0; i < VJ; ++i) {
+                const int v = min(tb + v_key[i], kend - 1);
+                const char* src = v_direct && v >= bk.cmax ? v_new_row(v - bk.cmax) : vp.row(key_row(v));
+                load_lds16(src + v_off[i], st + Smem<D>::k_bytes + (wave + kWaves * i) * 1024);
+            }
         }
     };
 
@@ -257,7 +271,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
     const bool has_new = p.rope != nullptr && nb > na;
     const bool tile0_new = has_new && kbeg + kTile > bk.cmax;
     if (tile0_new) {
-        append_new_rows<D, 64 * kWaves>(p, kp, vp, h, n0, Tc, na, nb);
+        append_new_rows<D, 64 * kWaves, !kVDirect>(p, kp, vp, h, n0, Tc, na, nb);
         wait_vm_all();
         __syncthreads();
     }
@@ -336,7 +350,7 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) qB[rt][ds] = as_bf16x8(q[ds]);
     }
-    if (has_new && !tile0_new) append_new_rows<D, 64 * kWaves>(p, kp, vp, h, n0, Tc, na, nb);
+    if (has_new && !tile0_new) append_new_rows<D, 64 * kWaves, !kVDirect>(p, kp, vp, h, n0, Tc, na, nb);
 
     const float c2 = p.scale_log2;   // > 0
     // Row r may see virtual key v iff v < lo (cached rows up to its document,
@@ -815,6 +829,26 @@ __device__ __forceinline__ void attend_segment(const KParams& p, unsigned char* 
                 }
             }
         }
+    }
+    // This segment's share of the new values for the cache: the tokens whose
+    // first row is in the unit's block, dealt over the unit's segments, so
+    // the request's new values are written once per head (no tile of this
+    // launch reads them back), stored with the partials
+    constexpr int VC_TPR = D / 8;
+    const int vc_t0 = (rho0 + G - 1) / G, vc_t1 = (rho_end - 1) / G + 1;
+    const int vc_n = v_direct && vc_t1 - vc_t0 > seg_local
+                         ? (vc_t1 - vc_t0 - seg_local + nseg - 1) / nseg * VC_TPR
+                         : 0;
+    auto vc_token = [&](int i) { return vc_t0 + seg_local + (i / VC_TPR) * nseg; };
+    auto vc_src = [&](int i) {
+        return reinterpret_cast<const uint4*>(
+            reinterpret_cast<const bf16_t*>(p.v_new) +
+            ((int64_t)(n0 + vc_token(i)) * p.n_kv_heads + h) * D + 8 * (i % VC_TPR));
+    };
+    for (int i = threadIdx.x; i < vc_n; i += 64 * kWaves) {
+        const uint4 x = *vc_src(i);
+        *reinterpret_cast<uint4*>(const_cast<char*>(vp.row(Tc + vc_token(i))) +
+                                  16 * (i % VC_TPR)) = x;
     }
     // (256-row units always leave their partials to the combine launch: the
     // merge's registers would crowd the eight-wavefront loop)
