@@ -415,8 +415,11 @@ typedef struct {
  * new tokens inside the split-attention launch: the RoPE stage launches
  * nothing, and the split stage rotates the queries it loads and appends the
  * rotated keys and the values to the cache rows T_c + r itself (every
- * workgroup whose keys include new rows writes the ones it reads; all write
- * identical bytes).  fp32 batches always use the separate RoPE launch.
+ * workgroup whose keys include new rows writes the keys it reads, all with
+ * identical bytes; values likewise, except that 256-row units read the new
+ * values from v_new and write each one once).  The cache holds every new
+ * row when the launch completes.  fp32 batches always use the separate RoPE
+ * launch.
  *
  *   d_new_pos   device int32 [n_new_total] (the layout's new_pos)
  *   d_table     device float [n_new_total][head_dim / 2][2]
