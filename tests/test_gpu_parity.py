@@ -991,7 +991,9 @@ def test_wide_unit_shapes_against_oracle(row_block, flags):
     launch or inside the split launch: the 10-document Llama-8B workload (two
     layers, every row) and the Llama-1B one (head_dim 64) under the
     schedule's own cut and under forced workgroup counts that split every
-    unit into one-tile segments; the merge counters are zero afterwards."""
+    unit into one-tile segments; the appended rows of every layer (the
+    256-row units copy each new value once, dealt over a unit's segments);
+    the merge counters are zero afterwards."""
     worst = 0.0
     for w, n_wgs in [(workloads.llama8b_10doc(n_layers=2), [0]),
                      (workloads.llama1b_layer(), [0, 1, 7, 1 << 20])]:
@@ -1002,13 +1004,14 @@ def test_wide_unit_shapes_against_oracle(row_block, flags):
             run.run()
             for l in range(w.n_layers):
                 worst = max(worst, _check_attend(run, l, tag=f"rb{row_block}/{n_wg}/{flags}")[0])
+                _check_append(run, l)
             _counters_zero(run)
             if n_wg == 1 << 20:
                 assert run.batch.plan.n_split_units == run.batch.plan.n_units
     _print(f"row block {row_block} flags {flags}: worst row rel {worst:.3e}")
 
 
-@pytest.mark.parametrize("row_block", [128, 64])
+@pytest.mark.parametrize("row_block", [256, 128, 64])
 @pytest.mark.parametrize("doc_len,link_count,n_query", [
     ([5], [0], 7),                          # K = 0: causal queries
     ([1, 1, 1], [3, 3, 3], 0),              # 1-token documents, no queries
