@@ -579,6 +579,20 @@ def _check_schedule(kv, w, n_wg_req, row_block=0, flags=0):
         for r in mine:
             assert tuple(r[[0, 1, 2, 3, 8, 9, 10, 11]]) == tuple(units[u, :8])
             assert r[6] == len(mine) and r[12] == unit_seg[u] and r[15] == 0
+    # the wide kernel's 256-row units write the new values once: a segment
+    # copies the tokens whose first GQA row lies in its unit's block, every
+    # nseg-th from its own index on; over all segments that is every new
+    # token of every (request, KV head) exactly once
+    copies = {}
+    for r in recs:
+        s_, h_, rho0, rows, nseg_r, loc = (int(x) for x in r[[0, 1, 2, 3, 6, 7]])
+        t0, t1 = -(-rho0 // G), (rho0 + rows - 1) // G + 1
+        for t in range(t0 + loc, t1, nseg_r):
+            copies[(s_, h_, t)] = copies.get((s_, h_, t), 0) + 1
+    snp = L["seq_new_ptr"]
+    want = {(s_, h_, t) for s_ in range(len(snp) - 1) for h_ in range(w.n_kv_heads)
+            for t in range(int(snp[s_ + 1] - snp[s_]))}
+    assert set(copies) == want and all(c == 1 for c in copies.values())
     return plan
 
 
